@@ -1,0 +1,80 @@
+/*
+ * hccl_oracle.h -- plain CPU oracle for the collective semantics (TEST INFRASTRUCTURE).
+ *
+ * This header and hccl_oracle.c are the checker, not the product. Only the test suite,
+ * the smoke entry point and the CPU-baseline leg of the benchmark may load or call them.
+ * They share no code, header, table or helper with the GPU library: every conversion and
+ * every fold below is written out again here on purpose.
+ *
+ * What is computed (paper: Section III-B "Data Path" names the collectives, Section II-A-2
+ * "Near Memory Compute" fixes the arithmetic):
+ *   - element types BF16, FP16 and FP32 are reduced with FP32 arithmetic and re-quantised
+ *     once to the buffer type (round to nearest, ties to even); INT32 is added with two's
+ *     complement wrap-around.
+ *   - the reduction visits contributors in a fixed order: ascending rank (group == 0), or
+ *     the two-level order (group == L > 0): ranks are cut into consecutive groups of L,
+ *     each group is folded in ascending rank order into an FP32 partial that is NOT
+ *     re-quantised, then the partials are folded in ascending group order (rack-contiguous
+ *     rank placement, Section V-D).
+ *   - the accumulator is seeded with the first contributor itself (never with +0.0), so a
+ *     column of negative zeros reduces to a negative zero.
+ *
+ * All buffers are host memory owned by the caller. Functions return 0 on success and a
+ * negative value on a bad argument; they never abort.
+ */
+#ifndef HCCL_ORACLE_H
+#define HCCL_ORACLE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element types and reduction operators of the oracle (its own numbering). */
+enum { ORC_BF16 = 0, ORC_FP16 = 1, ORC_FP32 = 2, ORC_INT32 = 3 };
+enum { ORC_SUM = 0, ORC_MAX = 1, ORC_MIN = 2 };
+
+/* Scalar conversions, written from the IEEE-754 binary16 / bfloat16 definitions. */
+float    orc_bf16_to_f32(uint16_t h);
+uint16_t orc_f32_to_bf16(float f);
+float    orc_f16_to_f32(uint16_t h);
+uint16_t orc_f32_to_f16(float f);
+
+/* Array forms of the conversions (used by the pins). */
+void orc_f32_to_bf16_array(const float* in, uint16_t* out, size_t n);
+void orc_f32_to_f16_array(const float* in, uint16_t* out, size_t n);
+void orc_f16_to_f32_array(const uint16_t* in, float* out, size_t n);
+
+/*
+ * AllReduce: recv[r][i] = R(send[0][i], ..., send[P-1][i]) for every rank r and i < count.
+ * recv[r] may equal send[r] (in place).
+ */
+int orc_allreduce(int P, size_t count, int dtype, int op, int group,
+                  const void* const* send, void* const* recv);
+
+/*
+ * ReduceScatter: recv[c][j] = R(send[0][c*recvcount + j], ..., send[P-1][c*recvcount + j]).
+ */
+int orc_reduce_scatter(int P, size_t recvcount, int dtype, int op, int group,
+                       const void* const* send, void* const* recv);
+
+/* AllGather: recv[r][q*sendcount + j] = send[q][j] for every r, q and j < sendcount. */
+int orc_allgather(int P, size_t sendcount, size_t elem_size,
+                  const void* const* send, void* const* recv);
+
+/*
+ * AllToAllv: for every source s and destination d, the counts[s*P+d] elements that start at
+ * element sdispls[s*P+d] of send[s] land at element rdispls[d*P+s] of recv[d]. Send arrays
+ * are indexed [src*P + dst], receive arrays [dst*P + src]. recvcounts[d*P+s] must equal
+ * sendcounts[s*P+d]. Receive elements outside every written range are left untouched.
+ */
+int orc_alltoallv(int P, size_t elem_size,
+                  const void* const* send, const size_t* sendcounts, const size_t* sdispls,
+                  void* const* recv, const size_t* recvcounts, const size_t* rdispls);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

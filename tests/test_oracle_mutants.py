@@ -1,0 +1,113 @@
+"""The oracle's pins must reject plausible mistakes in the oracle.
+
+Each case copies the oracle's C source, plants one mistake by a textual edit, compiles the
+copy with the same flags into a temporary directory (CPU only), points the oracle module at
+it and runs a subset of the pins. A mutant that every pin accepts would mean the pins do
+not constrain that part of the oracle, so the test fails.
+"""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import test_oracle_pins as pins
+
+_SRC = os.path.join(os.path.dirname(oracle.__file__), "hccl_oracle.c")
+
+MUTANTS = {
+    "fold_descending": (
+        "float acc = load_as_f32(src[0], dtype, i);\n"
+        "        for (int r = 1; r < P; ++r) acc = combine_f32(op, acc, load_as_f32(src[r], dtype, i));",
+        "float acc = load_as_f32(src[P - 1], dtype, i);\n"
+        "        for (int r = P - 2; r >= 0; --r) acc = combine_f32(op, acc, load_as_f32(src[r], dtype, i));",
+    ),
+    "seed_with_positive_zero": (
+        "float acc = load_as_f32(src[0], dtype, i);\n        for (int r = 1; r < P; ++r)",
+        "float acc = 0.0f;\n        for (int r = 0; r < P; ++r)",
+    ),
+    "drop_last_contributor": (
+        "for (int r = 1; r < P; ++r) acc = combine_f32(op, acc, load_as_f32(src[r], dtype, i));",
+        "for (int r = 1; r < P - 1; ++r) acc = combine_f32(op, acc, load_as_f32(src[r], dtype, i));",
+    ),
+    "bf16_ties_round_down": (
+        "if (r > 0x8000u || (r == 0x8000u && (t & 1u))) t += 1u;",
+        "if (r > 0x8000u) t += 1u;",
+    ),
+    "fp16_subnormal_shift_off_by_one": (
+        "int shift = 14 - he;",
+        "int shift = 13 - he;",
+    ),
+    "reduce_scatter_wrong_block": (
+        "block[r] = (const char*)send[r] + (size_t)c * recvcount * es;",
+        "block[r] = (const char*)send[r] + (size_t)r * recvcount * es;",
+    ),
+    "allgather_wrong_block": (
+        "memcpy((char*)recv[r] + (size_t)q * bytes, send[q], bytes);",
+        "memcpy((char*)recv[r] + (size_t)r * bytes, send[q], bytes);",
+    ),
+    "alltoallv_transposed_rdispls": (
+        "char* to = (char*)recv[d] + rdispls[(size_t)d * P + s] * elem_size;",
+        "char* to = (char*)recv[d] + rdispls[(size_t)s * P + d] * elem_size;",
+    ),
+    "two_level_partials_requantised": (
+        "total = (g == 0) ? part : combine_f32(op, total, part);",
+        "part = orc_bf16_to_f32(orc_f32_to_bf16(part));\n"
+        "        total = (g == 0) ? part : combine_f32(op, total, part);",
+    ),
+    "int32_sum_saturates": (
+        "if (op == ORC_SUM) return (int32_t)((uint32_t)acc + (uint32_t)x);",
+        "if (op == ORC_SUM) { long long s = (long long)acc + x; "
+        "return s > 2147483647LL ? 2147483647 : (s < -2147483648LL ? (int32_t)-2147483648LL : (int32_t)s); }",
+    ),
+}
+
+# The pins run against every mutant (cheap ones, CPU only).
+PIN_CALLS = [
+    ("bf16 ties", lambda: pins.test_bf16_narrowing_matches_torch_on_every_tie_class()),
+    ("bf16 hand", lambda: pins.test_bf16_hand_values()),
+    ("fp16 ties", lambda: pins.test_fp16_narrowing_matches_numpy_on_every_tie_class()),
+    ("fp16 subnormal", lambda: pins.test_fp16_narrowing_subnormal_ties()),
+    ("fp32 fold", lambda: pins.test_allreduce_fp32_is_the_ascending_numpy_fold(5)),
+    ("order", lambda: pins.test_fold_order_is_ascending_rank_not_any_other()),
+    ("seed", lambda: pins.test_accumulator_is_seeded_with_the_first_contributor()),
+    ("two level", lambda: pins.test_two_level_is_group_folds_then_partial_fold(4, 2)),
+    ("triangular", lambda: pins.test_allreduce_of_rank_plus_one_is_triangular_number("fp32", 7)),
+    ("int32 wrap", lambda: pins.test_int32_sum_wraps_like_uint32_arithmetic()),
+    ("rs brute", lambda: pins.test_reduce_scatter_brute_force(4, 7)),
+    ("ag brute", lambda: pins.test_allgather_brute_force(3, 1)),
+    ("a2av brute", lambda: pins.test_alltoallv_brute_force_with_gaps_and_zero_blocks()),
+]
+
+
+def _build_mutant(tmpdir, name):
+    before, after = MUTANTS[name]
+    src = open(_SRC).read()
+    assert src.count(before) == 1, f"mutation site for {name} not found exactly once"
+    mutated = src.replace(before, after)
+    c_path = os.path.join(tmpdir, f"{name}.c")
+    so_path = os.path.join(tmpdir, f"{name}.so")
+    with open(c_path, "w") as f:
+        f.write(mutated)
+    inc = os.path.dirname(_SRC)
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+                    "-fno-fast-math", "-I", inc, "-o", so_path, c_path], check=True)
+    return so_path
+
+
+def test_unmutated_source_passes_every_pin():
+    for _, call in PIN_CALLS:
+        call()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_every_planted_mistake_fails_a_pin(name, tmp_path):
+    so = _build_mutant(str(tmp_path), name)
+    caught = []
+    with oracle.use_library(so):
+        for label, call in PIN_CALLS:
+            try:
+                call()
+            except (AssertionError, ValueError):
+                caught.append(label)
+    assert caught, f"mutant {name} passed every pin"
