@@ -1,0 +1,175 @@
+/*
+ * hccl.h -- C ABI of the MI355X copy/reduce collective library.
+ *
+ * The library follows the compiled communication model of the paper "HCCL: Collective
+ * Communication for Meta Training and Inference Accelerators": for every collective the
+ * host lowers the call into a complete program of chunked copy / reduce steps with
+ * dependency ids (Section III-B "Data Path": work packets, subgraphs, WQEs and their
+ * dependency kinds), and one device-resident executor runs that program (Section II-A-2:
+ * the message engine's control core unrolls the graph and evaluates dependencies; the
+ * near-memory compute unit performs copies and sums with FP32 arithmetic).
+ *
+ * On one GPU the P ranks of a collective are P buffers in the same HBM: every call takes
+ * arrays of P device pointers. Device buffers belong to the caller and must stay valid
+ * until the work enqueued on `stream` has completed; the library never frees them. Host
+ * arrays (pointer lists, counts, displacements, config) are read during the call only.
+ *
+ * Every call is enqueue-only: it returns once the work is on `stream` (a hipStream_t
+ * passed as void*, NULL = the null stream). Errors are reported by return code; on any
+ * error nothing is enqueued. hccl_get_last_error() returns a thread-local description of
+ * the last failure. No call aborts or throws across this boundary.
+ *
+ * Limits: 1 <= nranks <= HCCL_MAX_RANKS. Element counts are in elements of `dtype`.
+ * Buffers must be aligned to their element size; 16-byte aligned buffers take the
+ * 128-bit vector path, other alignments are handled element by element.
+ *
+ * Calls on one communicator must not run concurrently from several host threads. Calls
+ * may be issued on different streams: the library orders a program's launches by itself.
+ */
+#ifndef HCCL_H
+#define HCCL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HCCL_MAX_RANKS 64
+#define HCCL_NO_DEVICE (-1)
+
+typedef enum {
+    hcclSuccess = 0,
+    hcclInvalidArgument = 1, /* a pointer, size, count, displacement or enum is invalid */
+    hcclUnsupported = 2,     /* valid request this build does not implement */
+    hcclHipError = 3,        /* a HIP runtime call failed */
+    hcclOutOfMemory = 4,     /* device allocation for a program or scratch failed */
+    hcclTimeout = 5,         /* a device dependency wait exceeded the watchdog limit */
+    hcclInternalError = 6,   /* a compiled program failed validation (library bug) */
+} hcclResult_t;
+
+/* Element types of the near-memory compute unit (BF16, FP16, FP32; Section II-A-2),
+ * plus INT32 for exact integer reductions and id payloads. */
+typedef enum { hcclBf16 = 0, hcclFp16 = 1, hcclFp32 = 2, hcclInt32 = 3 } hcclDataType_t;
+
+/* Reduction operators. SUM is the paper's operator; MAX / MIN are extensions. Floating
+ * types are combined in FP32 and rounded once to the buffer type (nearest, ties to even);
+ * INT32 SUM wraps modulo 2^32. */
+typedef enum { hcclSum = 0, hcclMax = 1, hcclMin = 2 } hcclRedOp_t;
+
+/* Schedules (Section III-B ring AllReduce; Section V-D topology-aware algorithms).
+ * All of them fold the contributors of an element in ascending rank order, except
+ * TWO_LEVEL, which folds ascending inside each group of `group_size` consecutive ranks
+ * into FP32 partials and then folds the partials in ascending group order. */
+typedef enum {
+    hcclAlgoAuto = 0,     /* TWO_LEVEL when group_size splits nranks, else RING */
+    hcclAlgoDirect = 1,   /* one step per chunk: read all contributors, write all destinations */
+    hcclAlgoRing = 2,     /* ring pipeline: P-1 reduce steps per chunk, then P-1 forwarding hops */
+    hcclAlgoTwoLevel = 3, /* group reduce-scatter, inter-group all-reduce of shards, group all-gather */
+} hcclAlgo_t;
+
+typedef struct {
+    int32_t algo;          /* hcclAlgo_t */
+    int32_t group_size;    /* ranks per group for TWO_LEVEL; 0 = none */
+    uint64_t chunk_bytes;  /* pipeline chunk, bytes of the input type per rank (0 = 1 MiB) */
+    int32_t fuse;          /* 1 = fuse chained steps into multi-operand steps (default);
+                              0 = run every lowered step as its own dependent descriptor */
+    int32_t max_workers;   /* upper bound on executor wavefronts (0 = size from the device) */
+    uint32_t tile_bytes;   /* work claimed per ticket, bytes read per tile (0 = default) */
+    uint32_t timeout_ms;   /* watchdog for one dependency wait on the device (0 = 2000) */
+    int32_t validate;      /* 1 = run the program validator on every compile */
+    int32_t reserved[5];
+} hcclConfig_t;
+
+typedef struct hcclComm* hcclComm_t;
+
+/* Fills *cfg with the defaults. */
+hcclResult_t hccl_config_init(hcclConfig_t* cfg);
+
+/*
+ * Creates a communicator of `nranks` virtual ranks on HIP device `device`. With
+ * device == HCCL_NO_DEVICE the communicator is host-only: collective calls validate their
+ * arguments and compile (and validate) the program, then return hcclSuccess without
+ * touching any buffer or device; hccl_comm_last_program() describes what was compiled.
+ * cfg may be NULL (defaults). The communicator owns its program cache, device program
+ * copies, dependency counters, FP32 scratch and error word.
+ */
+hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, hcclComm_t* comm);
+
+/* Waits for the communicator's outstanding work, then frees everything it owns. */
+hcclResult_t hccl_comm_destroy(hcclComm_t comm);
+
+/* Replaces the configuration used by later calls (cached programs stay valid). */
+hcclResult_t hccl_comm_set_config(hcclComm_t comm, const hcclConfig_t* cfg);
+
+/*
+ * AllReduce: recvbufs[r][i] = R(sendbufs[0][i], ..., sendbufs[P-1][i]) for every rank r
+ * and i < count. In place (sendbufs[r] == recvbufs[r] for every r) is allowed; any other
+ * overlap between buffers is not.
+ */
+hcclResult_t hccl_allreduce(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,
+                            size_t count, hcclDataType_t dtype, hcclRedOp_t op, void* stream);
+
+/*
+ * ReduceScatter: sendbufs[r] holds P * recvcount elements; recvbufs[c][j] =
+ * R(sendbufs[0][c*recvcount + j], ..., sendbufs[P-1][c*recvcount + j]). Receive buffers
+ * must not overlap any send buffer.
+ */
+hcclResult_t hccl_reduce_scatter(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,
+                                 size_t recvcount, hcclDataType_t dtype, hcclRedOp_t op, void* stream);
+
+/* AllGather: recvbufs[r][q*sendcount + j] = sendbufs[q][j]. A byte copy for every dtype. */
+hcclResult_t hccl_allgather(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,
+                            size_t sendcount, hcclDataType_t dtype, void* stream);
+
+/*
+ * AllToAllv (Section I: embedding exchange; Section IV-A: spread over parallel engines).
+ * For every source s and destination d, n = sendcounts[s*P + d] elements starting at
+ * element sdispls[s*P + d] of sendbufs[s] are copied to element rdispls[d*P + s] of
+ * recvbufs[d]. Requires recvcounts[d*P + s] == sendcounts[s*P + d] and non-overlapping
+ * receive ranges per destination. Receive elements outside every range are untouched.
+ * Zero counts are allowed. Count and displacement arrays are host memory, P*P entries.
+ */
+hcclResult_t hccl_alltoallv(hcclComm_t comm,
+                            const void* const* sendbufs, const size_t* sendcounts, const size_t* sdispls,
+                            void* const* recvbufs, const size_t* recvcounts, const size_t* rdispls,
+                            hcclDataType_t dtype, void* stream);
+
+/* Thread-local text of the last error returned on this thread ("" if none). */
+const char* hccl_get_last_error(void);
+
+/* Name of a result code. */
+const char* hccl_result_string(hcclResult_t r);
+
+/*
+ * Synchronises the communicator's device and reports a device-side failure recorded since
+ * the previous call (hcclTimeout when a dependency wait hit the watchdog), then clears it.
+ */
+hcclResult_t hccl_get_async_error(hcclComm_t comm);
+
+/* Description of the most recently compiled or reused program of a communicator. */
+typedef struct {
+    int32_t collective;          /* 0 allreduce, 1 reduce_scatter, 2 allgather, 3 alltoallv */
+    int32_t algo;                /* hcclAlgo_t actually lowered */
+    int32_t fused;               /* fusion pass applied */
+    int32_t cache_hit;           /* 1 if the program came from the cache */
+    uint32_t num_descs;          /* descriptors (steps) in the program */
+    uint32_t num_tiles;          /* work tickets */
+    uint32_t num_deps;           /* dependency edges */
+    uint32_t num_operands;       /* operand entries */
+    uint32_t workers;            /* wavefronts of the last launch (0 on host-only comms) */
+    uint32_t max_srcs;           /* most sources of one step */
+    uint64_t bytes_read;         /* bytes the program's steps read */
+    uint64_t bytes_written;      /* bytes the program's steps write */
+    uint64_t scratch_bytes;      /* FP32 scratch the program needs */
+    uint64_t program_bytes;      /* size of the device copy of the program */
+    double compile_us;           /* host time to lower, fuse, validate and pack */
+} hcclProgramInfo_t;
+
+hcclResult_t hccl_comm_last_program(hcclComm_t comm, hcclProgramInfo_t* info);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HCCL_H */

@@ -1,0 +1,540 @@
+// api.cpp -- the C ABI: argument checks, program cache, upload and launch.
+//
+// Mirrors the host side of the paper's compiled model (Section III-B "Data Path"; Section V-B
+// "Host-side Performance"): a collective call is validated, lowered into a complete program
+// (or found in the cache of compiled work packets, which then costs only a re-enqueue),
+// copied to device memory once, and enqueued as one executor launch on the caller's stream.
+#include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <list>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "compiler.h"
+#include "hccl.h"
+#include "program.h"
+
+namespace hccl {
+hipError_t launch_executor(const LaunchArgs& a, uint32_t blocks, int kind, hipStream_t stream);
+hipError_t launch_fill_u32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t stream);
+hipError_t executor_occupancy(int kind, int* blocks_per_cu);
+int executor_waves_per_block();
+}  // namespace hccl
+
+using namespace hccl;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hcclResult_t fail(hcclResult_t code, const std::string& msg) {
+    g_last_error = msg;
+    return code;
+}
+
+hcclResult_t hip_fail(hipError_t e, const char* what) {
+    return fail(hcclHipError, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+struct DeviceProgram {
+    CollectiveSpec spec;
+    HostProgram prog;
+    uint8_t* d_image = nullptr;
+    uint32_t* d_state = nullptr;
+    hipEvent_t done = nullptr;       // recorded after each launch
+    hipStream_t last_stream = nullptr;
+    bool launched = false;
+    double compile_us = 0;
+};
+
+}  // namespace
+
+struct hcclComm {
+    int nranks = 0;
+    int device = HCCL_NO_DEVICE;
+    hcclConfig_t cfg;
+    int cus = 0;
+    int blocks_per_cu[kNumKinds] = {0};
+    uint64_t wall_clock_khz = 100000;
+    ErrorRecord* d_error = nullptr;
+    void* d_scratch = nullptr;
+    uint64_t scratch_bytes = 0;
+    std::list<std::unique_ptr<DeviceProgram>> cache;  // most recently used first
+    size_t cache_limit = 64;
+    hcclProgramInfo_t last{};
+};
+
+namespace {
+
+bool env_flag(const char* name) {
+    const char* v = std::getenv(name);
+    return v && *v && std::strcmp(v, "0") != 0;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    bool changed = false;
+    explicit DeviceGuard(int dev) {
+        if (dev < 0) return;
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) changed = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (changed) (void)hipSetDevice(prev);
+    }
+};
+
+void free_program(DeviceProgram* p) {
+    if (p->done) (void)hipEventSynchronize(p->done);
+    if (p->d_image) (void)hipFree(p->d_image);
+    if (p->d_state) (void)hipFree(p->d_state);
+    if (p->done) (void)hipEventDestroy(p->done);
+    p->d_image = nullptr;
+    p->d_state = nullptr;
+    p->done = nullptr;
+}
+
+hcclResult_t check_dtype(hcclDataType_t dt) {
+    if (dt != hcclBf16 && dt != hcclFp16 && dt != hcclFp32 && dt != hcclInt32)
+        return fail(hcclInvalidArgument, "unknown data type");
+    return hcclSuccess;
+}
+
+hcclResult_t check_op(hcclRedOp_t op) {
+    if (op != hcclSum && op != hcclMax && op != hcclMin) return fail(hcclInvalidArgument, "unknown reduction operator");
+    return hcclSuccess;
+}
+
+struct Range {
+    uintptr_t lo, hi;
+    int id;
+};
+
+// Buffers must be non-null (when non-empty), aligned to the element size, and must not
+// overlap each other except where `allow` accepts the pair.
+template <typename Allow>
+hcclResult_t check_buffers(const std::vector<Range>& v, size_t es, Allow allow) {
+    for (const Range& r : v) {
+        if (r.hi == r.lo) continue;
+        if (r.lo == 0) return fail(hcclInvalidArgument, "null buffer pointer");
+        if (r.lo % es) return fail(hcclInvalidArgument, "buffer not aligned to its element size");
+    }
+    std::vector<Range> s;
+    for (const Range& r : v)
+        if (r.hi > r.lo) s.push_back(r);
+    std::sort(s.begin(), s.end(), [](const Range& a, const Range& b) { return a.lo < b.lo; });
+    for (size_t i = 0; i < s.size(); ++i)
+        for (size_t j = i + 1; j < s.size() && s[j].lo < s[i].hi; ++j)
+            if (!allow(s[i], s[j])) return fail(hcclInvalidArgument, "buffers overlap");
+    return hcclSuccess;
+}
+
+hcclResult_t compile_program(hcclComm* c, const CollectiveSpec& spec, DeviceProgram*& out, bool& hit) {
+    for (auto it = c->cache.begin(); it != c->cache.end(); ++it) {
+        if ((*it)->spec == spec) {
+            if (it != c->cache.begin()) c->cache.splice(c->cache.begin(), c->cache, it);
+            out = c->cache.front().get();
+            hit = true;
+            return hcclSuccess;
+        }
+    }
+    hit = false;
+    auto t0 = std::chrono::steady_clock::now();
+    auto dp = std::make_unique<DeviceProgram>();
+    dp->spec = spec;
+    std::string err;
+    if (!lower(spec, dp->prog, err)) return fail(hcclInvalidArgument, err);
+    if (spec.fuse) fuse(dp->prog);
+    if (!finalize(dp->prog, spec.tile_bytes, err)) return fail(hcclInternalError, err);
+    if (c->cfg.validate || c->device == HCCL_NO_DEVICE || env_flag("HCCL_VALIDATE")) {
+        if (!validate(dp->prog, spec, err)) return fail(hcclInternalError, "program validation failed: " + err);
+    }
+    dp->compile_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+
+    if (c->device != HCCL_NO_DEVICE) {
+        const auto& img = dp->prog.image;
+        hipError_t e = hipMalloc(&dp->d_image, img.size());
+        if (e != hipSuccess) return fail(hcclOutOfMemory, "program image allocation failed");
+        e = hipMemcpy(dp->d_image, img.data(), img.size(), hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            free_program(dp.get());
+            return hip_fail(e, "program upload");
+        }
+        e = hipMalloc(&dp->d_state, (size_t)dp->prog.nstate * sizeof(uint32_t));
+        if (e != hipSuccess) {
+            free_program(dp.get());
+            return fail(hcclOutOfMemory, "program state allocation failed");
+        }
+        e = launch_fill_u32(dp->d_state, dp->prog.nstate, 0u, nullptr);
+        if (e == hipSuccess) e = hipDeviceSynchronize();
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&dp->done, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            free_program(dp.get());
+            return hip_fail(e, "program state setup");
+        }
+    }
+    c->cache.push_front(std::move(dp));
+    while (c->cache.size() > c->cache_limit) {
+        free_program(c->cache.back().get());
+        c->cache.pop_back();
+    }
+    out = c->cache.front().get();
+    return hcclSuccess;
+}
+
+hcclResult_t ensure_scratch(hcclComm* c, uint64_t bytes) {
+    if (bytes <= c->scratch_bytes) return hcclSuccess;
+    hipError_t e = hipDeviceSynchronize();  // the old scratch may still be in use
+    if (e != hipSuccess) return hip_fail(e, "synchronize before scratch growth");
+    if (c->d_scratch) (void)hipFree(c->d_scratch);
+    c->d_scratch = nullptr;
+    c->scratch_bytes = 0;
+    e = hipMalloc(&c->d_scratch, bytes);
+    if (e != hipSuccess) return fail(hcclOutOfMemory, "scratch allocation failed");
+    c->scratch_bytes = bytes;
+    return hcclSuccess;
+}
+
+uint32_t stream_cu_count(hcclComm* c, hipStream_t s) {
+    if (!s) return (uint32_t)c->cus;
+    uint32_t mask[16] = {0};
+    if (hipExtStreamGetCUMask(s, 16, mask) != hipSuccess) return (uint32_t)c->cus;
+    uint32_t n = 0;
+    for (uint32_t w : mask) n += (uint32_t)__builtin_popcount(w);
+    if (n == 0 || n > (uint32_t)c->cus) return (uint32_t)c->cus;
+    return n;
+}
+
+hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* send, void* const* recv, void* stream) {
+    DeviceProgram* dp = nullptr;
+    bool hit = false;
+    DeviceGuard guard(c->device);
+    hcclResult_t r = compile_program(c, spec, dp, hit);
+    if (r != hcclSuccess) return r;
+
+    hcclProgramInfo_t& info = c->last;
+    std::memset(&info, 0, sizeof info);
+    info.collective = spec.coll;
+    info.algo = dp->prog.algo;
+    info.fused = dp->prog.fused ? 1 : 0;
+    info.cache_hit = hit ? 1 : 0;
+    info.num_descs = (uint32_t)dp->prog.descs.size();
+    info.num_tiles = dp->prog.ntiles;
+    info.num_deps = dp->prog.ndeps;
+    info.num_operands = dp->prog.noperands;
+    info.max_srcs = dp->prog.max_srcs;
+    info.bytes_read = dp->prog.bytes_read;
+    info.bytes_written = dp->prog.bytes_written;
+    info.scratch_bytes = dp->prog.scratch_bytes;
+    info.program_bytes = dp->prog.image.size();
+    info.compile_us = dp->compile_us;
+
+    if (c->device == HCCL_NO_DEVICE || dp->prog.ntiles == 0) return hcclSuccess;
+
+    r = ensure_scratch(c, dp->prog.scratch_bytes);
+    if (r != hcclSuccess) return r;
+
+    hipStream_t s = (hipStream_t)stream;
+    LaunchArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.prog = dp->d_image;
+    a.state = dp->d_state;
+    a.error = c->d_error;
+    const int P = c->nranks;
+    for (int i = 0; i < P; ++i) {
+        a.bufs[send_buf(i)] = (char*)send[i];
+        a.bufs[recv_buf(P, i)] = (char*)recv[i];
+    }
+    a.bufs[scratch_buf(P)] = (char*)c->d_scratch;
+    const bool has_deps = (dp->prog.flags & PF_HAS_DEPS) != 0;
+    a.dynamic = has_deps ? 1u : 0u;
+    const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
+    a.timeout_ticks = ms * c->wall_clock_khz;
+
+    const uint32_t wpb = (uint32_t)executor_waves_per_block();
+    uint32_t cus = stream_cu_count(c, s);
+    const int kind = dp->prog.kind;
+    uint32_t slots = cus * (uint32_t)std::max(1, c->blocks_per_cu[kind]) * wpb;
+    if (c->cfg.max_workers > 0) slots = std::min<uint32_t>(slots, (uint32_t)c->cfg.max_workers);
+    uint32_t workers = std::min<uint32_t>(slots, dp->prog.ntiles);
+    uint32_t blocks = (workers + wpb - 1) / wpb;
+    if (blocks == 0) blocks = 1;
+    a.nworkers = blocks * wpb;
+    info.workers = a.nworkers;
+
+    // a program's counters serve one launch at a time: order launches across streams
+    if (has_deps && dp->launched && dp->last_stream != s) {
+        hipError_t e = hipStreamWaitEvent(s, dp->done, 0);
+        if (e != hipSuccess) return hip_fail(e, "cross-stream ordering");
+    }
+    hipError_t e = launch_executor(a, blocks, kind, s);
+    if (e != hipSuccess) return hip_fail(e, "executor launch");
+    if (has_deps) {
+        e = hipEventRecord(dp->done, s);
+        if (e != hipSuccess) return hip_fail(e, "completion event");
+        dp->last_stream = s;
+        dp->launched = true;
+    }
+    return hcclSuccess;
+}
+
+hcclResult_t fill_spec(hcclComm* c, CollectiveSpec& s, int coll, hcclDataType_t dt, hcclRedOp_t op) {
+    s.coll = coll;
+    s.P = c->nranks;
+    s.dtype = (int)dt;
+    s.redop = (int)op;
+    s.algo = c->cfg.algo;
+    s.group_size = c->cfg.group_size;
+    s.chunk_bytes = c->cfg.chunk_bytes;
+    s.fuse = c->cfg.fuse != 0;
+    s.tile_bytes = c->cfg.tile_bytes;
+    if (s.algo < hcclAlgoAuto || s.algo > hcclAlgoTwoLevel) return fail(hcclInvalidArgument, "unknown algorithm");
+    return hcclSuccess;
+}
+
+hcclResult_t check_comm(hcclComm_t comm) {
+    if (!comm) return fail(hcclInvalidArgument, "null communicator");
+    return hcclSuccess;
+}
+
+hcclResult_t check_ptr_arrays(const void* a, const void* b) {
+    if (!a || !b) return fail(hcclInvalidArgument, "null buffer array");
+    return hcclSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+hcclResult_t hccl_config_init(hcclConfig_t* cfg) {
+    if (!cfg) return fail(hcclInvalidArgument, "null config");
+    std::memset(cfg, 0, sizeof *cfg);
+    cfg->algo = hcclAlgoAuto;
+    cfg->fuse = 1;
+    return hcclSuccess;
+}
+
+hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, hcclComm_t* out) {
+    if (!out) return fail(hcclInvalidArgument, "null output pointer");
+    *out = nullptr;
+    if (nranks < 1 || nranks > HCCL_MAX_RANKS) return fail(hcclInvalidArgument, "nranks must be in [1, 64]");
+    auto c = std::make_unique<hcclComm>();
+    c->nranks = nranks;
+    c->device = device < 0 ? HCCL_NO_DEVICE : device;
+    if (cfg) c->cfg = *cfg;
+    else hccl_config_init(&c->cfg);
+    if (c->device != HCCL_NO_DEVICE) {
+        int n = 0;
+        hipError_t e = hipGetDeviceCount(&n);
+        if (e != hipSuccess || device >= n) return fail(hcclInvalidArgument, "no such HIP device");
+        DeviceGuard guard(c->device);
+        e = hipDeviceGetAttribute(&c->cus, hipDeviceAttributeMultiprocessorCount, c->device);
+        if (e != hipSuccess) return hip_fail(e, "device attributes");
+        int khz = 0;
+        if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->device) == hipSuccess && khz > 0)
+            c->wall_clock_khz = (uint64_t)khz;
+        const char* bpc = std::getenv("HCCL_BLOCKS_PER_CU");
+        for (int k = 0; k < kNumKinds; ++k) {
+            if (k > SIG_INT32 && k < kKindCopyOnly) continue;  // no kernel of its own
+            e = executor_occupancy(k, &c->blocks_per_cu[k]);
+            if (e != hipSuccess) return hip_fail(e, "executor occupancy");
+            if (bpc && std::atoi(bpc) > 0) c->blocks_per_cu[k] = std::min(c->blocks_per_cu[k], std::atoi(bpc));
+        }
+        e = hipMalloc(&c->d_error, sizeof(ErrorRecord));
+        if (e != hipSuccess) return fail(hcclOutOfMemory, "error record allocation failed");
+        e = hipMemset(c->d_error, 0, sizeof(ErrorRecord));
+        if (e != hipSuccess) return hip_fail(e, "error record init");
+    }
+    *out = c.release();
+    return hcclSuccess;
+}
+
+hcclResult_t hccl_comm_destroy(hcclComm_t comm) {
+    if (!comm) return hcclSuccess;
+    {
+        DeviceGuard guard(comm->device);
+        if (comm->device != HCCL_NO_DEVICE) (void)hipDeviceSynchronize();
+        for (auto& p : comm->cache) free_program(p.get());
+        comm->cache.clear();
+        if (comm->d_scratch) (void)hipFree(comm->d_scratch);
+        if (comm->d_error) (void)hipFree(comm->d_error);
+    }
+    delete comm;
+    return hcclSuccess;
+}
+
+hcclResult_t hccl_comm_set_config(hcclComm_t comm, const hcclConfig_t* cfg) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (!cfg) return fail(hcclInvalidArgument, "null config");
+    comm->cfg = *cfg;
+    return hcclSuccess;
+}
+
+hcclResult_t hccl_allreduce(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs, size_t count,
+                            hcclDataType_t dtype, hcclRedOp_t op, void* stream) {
+    hcclResult_t r;
+    if ((r = check_comm(comm)) || (r = check_ptr_arrays(sendbufs, recvbufs)) || (r = check_dtype(dtype)) ||
+        (r = check_op(op)))
+        return r;
+    const int P = comm->nranks;
+    const size_t es = dtype_size((uint32_t)dtype);
+    bool in_place = true;
+    std::vector<Range> v;
+    for (int i = 0; i < P; ++i) {
+        v.push_back({(uintptr_t)sendbufs[i], (uintptr_t)sendbufs[i] + count * es, i});
+        v.push_back({(uintptr_t)recvbufs[i], (uintptr_t)recvbufs[i] + count * es, P + i});
+        in_place &= (sendbufs[i] == recvbufs[i]);
+    }
+    if (count) {
+        if (!in_place)
+            for (int i = 0; i < P; ++i)
+                if (sendbufs[i] == recvbufs[i])
+                    return fail(hcclInvalidArgument, "allreduce in place must be in place on every rank");
+        r = check_buffers(v, es, [&](const Range& a, const Range& b) {
+            return in_place && (a.id % P == b.id % P) && a.lo == b.lo && a.hi == b.hi;
+        });
+        if (r) return r;
+    }
+    CollectiveSpec s;
+    if ((r = fill_spec(comm, s, COLL_ALLREDUCE, dtype, op))) return r;
+    s.count = count;
+    s.in_place = in_place && count > 0;
+    return run(comm, s, sendbufs, recvbufs, stream);
+}
+
+hcclResult_t hccl_reduce_scatter(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,
+                                 size_t recvcount, hcclDataType_t dtype, hcclRedOp_t op, void* stream) {
+    hcclResult_t r;
+    if ((r = check_comm(comm)) || (r = check_ptr_arrays(sendbufs, recvbufs)) || (r = check_dtype(dtype)) ||
+        (r = check_op(op)))
+        return r;
+    const int P = comm->nranks;
+    const size_t es = dtype_size((uint32_t)dtype);
+    std::vector<Range> v;
+    for (int i = 0; i < P; ++i) {
+        v.push_back({(uintptr_t)sendbufs[i], (uintptr_t)sendbufs[i] + (size_t)P * recvcount * es, i});
+        v.push_back({(uintptr_t)recvbufs[i], (uintptr_t)recvbufs[i] + recvcount * es, P + i});
+    }
+    if (recvcount && (r = check_buffers(v, es, [](const Range&, const Range&) { return false; }))) return r;
+    CollectiveSpec s;
+    if ((r = fill_spec(comm, s, COLL_REDUCE_SCATTER, dtype, op))) return r;
+    if (s.algo == hcclAlgoTwoLevel) return fail(hcclUnsupported, "the two-level schedule is for allreduce");
+    s.count = recvcount;
+    return run(comm, s, sendbufs, recvbufs, stream);
+}
+
+hcclResult_t hccl_allgather(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs, size_t sendcount,
+                            hcclDataType_t dtype, void* stream) {
+    hcclResult_t r;
+    if ((r = check_comm(comm)) || (r = check_ptr_arrays(sendbufs, recvbufs)) || (r = check_dtype(dtype))) return r;
+    const int P = comm->nranks;
+    const size_t es = dtype_size((uint32_t)dtype);
+    std::vector<Range> v;
+    for (int i = 0; i < P; ++i) {
+        v.push_back({(uintptr_t)sendbufs[i], (uintptr_t)sendbufs[i] + sendcount * es, i});
+        v.push_back({(uintptr_t)recvbufs[i], (uintptr_t)recvbufs[i] + (size_t)P * sendcount * es, P + i});
+    }
+    if (sendcount && (r = check_buffers(v, es, [](const Range&, const Range&) { return false; }))) return r;
+    CollectiveSpec s;
+    if ((r = fill_spec(comm, s, COLL_ALLGATHER, dtype, hcclSum))) return r;
+    if (s.algo == hcclAlgoTwoLevel) return fail(hcclUnsupported, "the two-level schedule is for allreduce");
+    s.count = sendcount;
+    return run(comm, s, sendbufs, recvbufs, stream);
+}
+
+hcclResult_t hccl_alltoallv(hcclComm_t comm, const void* const* sendbufs, const size_t* sendcounts,
+                            const size_t* sdispls, void* const* recvbufs, const size_t* recvcounts,
+                            const size_t* rdispls, hcclDataType_t dtype, void* stream) {
+    hcclResult_t r;
+    if ((r = check_comm(comm)) || (r = check_ptr_arrays(sendbufs, recvbufs)) || (r = check_dtype(dtype))) return r;
+    if (!sendcounts || !sdispls || !recvcounts || !rdispls) return fail(hcclInvalidArgument, "null count array");
+    const int P = comm->nranks;
+    const size_t es = dtype_size((uint32_t)dtype);
+    const size_t PP = (size_t)P * P;
+    CollectiveSpec s;
+    if ((r = fill_spec(comm, s, COLL_ALLTOALLV, dtype, hcclSum))) return r;
+    s.sendcounts.assign(sendcounts, sendcounts + PP);
+    s.sdispls.assign(sdispls, sdispls + PP);
+    s.recvcounts.assign(recvcounts, recvcounts + PP);
+    s.rdispls.assign(rdispls, rdispls + PP);
+    const uint64_t kLimit = (1ull << 62) / 8;
+    for (int src = 0; src < P; ++src) {
+        for (int dst = 0; dst < P; ++dst) {
+            uint64_t n = sendcounts[(size_t)src * P + dst];
+            if (recvcounts[(size_t)dst * P + src] != n)
+                return fail(hcclInvalidArgument, "recvcounts[dst*P+src] must equal sendcounts[src*P+dst]");
+            if (n > kLimit || sdispls[(size_t)src * P + dst] > kLimit || rdispls[(size_t)dst * P + src] > kLimit)
+                return fail(hcclInvalidArgument, "count or displacement out of range");
+        }
+    }
+    // receive ranges of one destination must not overlap
+    for (int dst = 0; dst < P; ++dst) {
+        std::vector<std::pair<uint64_t, uint64_t>> rr;
+        for (int src = 0; src < P; ++src) {
+            uint64_t n = recvcounts[(size_t)dst * P + src];
+            if (n) rr.push_back({rdispls[(size_t)dst * P + src], rdispls[(size_t)dst * P + src] + n});
+        }
+        std::sort(rr.begin(), rr.end());
+        for (size_t i = 1; i < rr.size(); ++i)
+            if (rr[i].first < rr[i - 1].second) return fail(hcclInvalidArgument, "receive ranges overlap");
+    }
+    // every send / receive buffer span must be disjoint from every other
+    BufferSizes sizes = buffer_sizes(s, 0);
+    std::vector<Range> v;
+    for (int i = 0; i < P; ++i) {
+        v.push_back({(uintptr_t)sendbufs[i], (uintptr_t)sendbufs[i] + sizes.bytes[send_buf(i)], i});
+        v.push_back({(uintptr_t)recvbufs[i], (uintptr_t)recvbufs[i] + sizes.bytes[recv_buf(P, i)], P + i});
+    }
+    // send buffers may alias each other (read-only); nothing may alias a receive buffer
+    if ((r = check_buffers(v, es, [&](const Range& a, const Range& b) { return a.id < P && b.id < P; })))
+        return r;
+    return run(comm, s, sendbufs, recvbufs, stream);
+}
+
+const char* hccl_get_last_error(void) { return g_last_error.c_str(); }
+
+const char* hccl_result_string(hcclResult_t r) {
+    switch (r) {
+        case hcclSuccess: return "hcclSuccess";
+        case hcclInvalidArgument: return "hcclInvalidArgument";
+        case hcclUnsupported: return "hcclUnsupported";
+        case hcclHipError: return "hcclHipError";
+        case hcclOutOfMemory: return "hcclOutOfMemory";
+        case hcclTimeout: return "hcclTimeout";
+        case hcclInternalError: return "hcclInternalError";
+    }
+    return "unknown hcclResult_t";
+}
+
+hcclResult_t hccl_get_async_error(hcclComm_t comm) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (comm->device == HCCL_NO_DEVICE) return hcclSuccess;
+    DeviceGuard guard(comm->device);
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "synchronize");
+    ErrorRecord rec;
+    e = hipMemcpy(&rec, comm->d_error, sizeof rec, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "read error record");
+    if (rec.code == 0) return hcclSuccess;
+    std::memset(&rec, 0, sizeof rec);
+    (void)hipMemcpy(comm->d_error, &rec, sizeof rec, hipMemcpyHostToDevice);
+    char buf[160];
+    std::snprintf(buf, sizeof buf, "a dependency wait of step %u (tile %u) exceeded the watchdog limit",
+                  rec.desc, rec.tile);
+    return fail(hcclTimeout, buf);
+}
+
+hcclResult_t hccl_comm_last_program(hcclComm_t comm, hcclProgramInfo_t* info) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (!info) return fail(hcclInvalidArgument, "null info");
+    *info = comm->last;
+    return hcclSuccess;
+}
+
+}  // extern "C"

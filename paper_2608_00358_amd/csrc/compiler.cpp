@@ -1,0 +1,704 @@
+// compiler.cpp -- lowering, fusion and packing of descriptor programs (host only).
+//
+// Lowerings write out the schedules the paper describes (Section III-B: the ring AllReduce
+// built from per-hop receive/compute/send steps with dependencies; Section V-D: topology-
+// aware two-level schedules that keep most traffic inside a group of consecutive ranks).
+// On one GPU a "send" from rank a to rank b is a read of a's buffer by the step that writes
+// b's buffer, so a hop becomes a COPY or REDUCE descriptor with a dependency id on the step
+// that produced its input.
+//
+// Every reduction visits contributors in ascending rank order (two-level: ascending inside
+// each group, then ascending over groups), so results never depend on the schedule.
+#include "compiler.h"
+
+#include <algorithm>
+#include <cstring>
+#include <unordered_map>
+
+namespace hccl {
+
+namespace {
+
+constexpr uint64_t kDefaultChunkBytes = 1ull << 20;
+constexpr uint32_t kDefaultTileBytes = 128u * 1024u;
+constexpr uint32_t kWaveStepElems = kWaveSize * kVecElems;  // 512: one vector per lane
+constexpr uint64_t kShardAlignElems = 64;                      // 128 B of bf16, 256 B of fp32
+
+uint32_t acc_dtype(int dtype, int redop) {
+    if (dtype == DT_INT32) return DT_INT32;
+    // MAX / MIN are exact in any floating type: partials keep the buffer type.
+    if (redop != RO_SUM) return (uint32_t)dtype;
+    return DT_FP32;
+}
+
+uint64_t chunk_elems(const CollectiveSpec& s) {
+    uint64_t bytes = s.chunk_bytes ? s.chunk_bytes : kDefaultChunkBytes;
+    uint64_t c = bytes / dtype_size(s.dtype);
+    c = (c / kShardAlignElems) * kShardAlignElems;
+    return std::max<uint64_t>(c, kShardAlignElems);
+}
+
+uint64_t shard_size(uint64_t n, int parts) {
+    uint64_t q = (n + parts - 1) / parts;
+    return ((q + kShardAlignElems - 1) / kShardAlignElems) * kShardAlignElems;
+}
+
+Operand opnd(uint32_t buf, uint32_t dtype, uint64_t elem_offset) {
+    Operand o;
+    o.buf = buf;
+    o.dtype = dtype;
+    o.offset = elem_offset * dtype_size(dtype);
+    return o;
+}
+
+struct Builder {
+    HostProgram& prog;
+    uint32_t add(uint8_t op, uint8_t redop, uint64_t nelem, std::vector<Operand> srcs,
+                 std::vector<Operand> dsts, std::vector<Dep> deps = {}, uint16_t group = 0) {
+        HostDesc d;
+        d.op = op;
+        d.redop = redop;
+        d.nelem = nelem;
+        d.group = group;
+        d.srcs = std::move(srcs);
+        d.dsts = std::move(dsts);
+        d.deps = std::move(deps);
+        prog.descs.push_back(std::move(d));
+        return (uint32_t)(prog.descs.size() - 1);
+    }
+};
+
+Dep tile_dep(uint32_t d) { return Dep{d, DEP_TILE, 0, 0}; }
+
+template <typename F>
+void for_chunks(uint64_t begin, uint64_t end, uint64_t C, F&& f) {
+    uint32_t j = 0;
+    for (uint64_t o = begin; o < end; o += C, ++j) f(j, o, std::min(C, end - o));
+}
+
+// ---------------------------------------------------------------------------- DIRECT
+// One step per chunk: read every contributor, write every destination (the one-shot,
+// all-to-all style schedule used for small messages, Section V-E).
+void lower_direct(const CollectiveSpec& s, HostProgram& p) {
+    Builder b{p};
+    const int P = s.P;
+    const uint64_t C = chunk_elems(s);
+    const uint32_t dt = (uint32_t)s.dtype;
+    if (s.coll == COLL_ALLREDUCE) {
+        for_chunks(0, s.count, C, [&](uint32_t, uint64_t o, uint64_t n) {
+            std::vector<Operand> src, dst;
+            for (int r = 0; r < P; ++r) src.push_back(opnd(send_buf(r), dt, o));
+            for (int r = 0; r < P; ++r) dst.push_back(opnd(recv_buf(P, r), dt, o));
+            b.add(OP_REDUCE, (uint8_t)s.redop, n, src, dst);
+        });
+    } else if (s.coll == COLL_REDUCE_SCATTER) {
+        const uint64_t M = s.count;
+        for (int c = 0; c < P; ++c) {
+            for_chunks(0, M, C, [&](uint32_t, uint64_t o, uint64_t n) {
+                std::vector<Operand> src;
+                for (int r = 0; r < P; ++r) src.push_back(opnd(send_buf(r), dt, (uint64_t)c * M + o));
+                b.add(OP_REDUCE, (uint8_t)s.redop, n, src, {opnd(recv_buf(P, c), dt, o)});
+            });
+        }
+    } else if (s.coll == COLL_ALLGATHER) {
+        const uint64_t M = s.count;
+        for (int q = 0; q < P; ++q) {
+            for_chunks(0, M, C, [&](uint32_t, uint64_t o, uint64_t n) {
+                std::vector<Operand> dst;
+                for (int r = 0; r < P; ++r) dst.push_back(opnd(recv_buf(P, r), dt, (uint64_t)q * M + o));
+                b.add(OP_COPY, RO_SUM, n, {opnd(send_buf(q), dt, o)}, dst);
+            });
+        }
+    }
+    p.algo = ALGO_DIRECT;
+}
+
+// ------------------------------------------------------------------------------ RING
+// Reduce chain of one chunk: step t (t = 1 .. P-1) folds contributor t into the partial of
+// contributors 0 .. t-1. Partials live in scratch in the accumulation type; the last step
+// rounds into `final_dst`. Steps of all chunks are emitted step-major so every chunk's step
+// t is available while step t+1 waits only for the same tile of its own chain.
+struct Chain {
+    uint64_t src_elem;    // element offset of the chunk in every send buffer
+    uint64_t nelem;
+    Operand final_dst;
+    uint64_t scratch_elem;  // element offset of the partial in scratch (accumulation type)
+    uint32_t last = 0;      // descriptor of the final step
+    uint32_t prev = 0;
+};
+
+void emit_reduce_chains(const CollectiveSpec& s, HostProgram& p, std::vector<Chain>& chains) {
+    Builder b{p};
+    const int P = s.P;
+    const uint32_t dt = (uint32_t)s.dtype;
+    const uint32_t acc = acc_dtype(s.dtype, s.redop);
+    if (P == 1) {
+        for (auto& ch : chains)
+            ch.last = b.add(OP_REDUCE, (uint8_t)s.redop, ch.nelem, {opnd(send_buf(0), dt, ch.src_elem)},
+                            {ch.final_dst});
+        return;
+    }
+    for (int t = 1; t < P; ++t) {
+        for (auto& ch : chains) {
+            Operand partial = opnd(scratch_buf(P), acc, ch.scratch_elem);
+            std::vector<Operand> src;
+            if (t == 1) src.push_back(opnd(send_buf(0), dt, ch.src_elem));
+            else src.push_back(partial);
+            src.push_back(opnd(send_buf(t), dt, ch.src_elem));
+            Operand dst = (t == P - 1) ? ch.final_dst : partial;
+            std::vector<Dep> deps;
+            if (t > 1) deps.push_back(tile_dep(ch.prev));
+            ch.prev = b.add(OP_REDUCE, (uint8_t)s.redop, ch.nelem, src, {dst}, deps);
+            if (t == P - 1) ch.last = ch.prev;
+        }
+    }
+}
+
+void lower_ring(const CollectiveSpec& s, HostProgram& p) {
+    Builder b{p};
+    const int P = s.P;
+    const uint64_t C = chunk_elems(s);
+    const uint32_t dt = (uint32_t)s.dtype;
+    const uint32_t acc = acc_dtype(s.dtype, s.redop);
+
+    if (s.coll == COLL_ALLGATHER) {
+        // hop 0 places block q in rank q's output; hop h forwards it from rank q+h-1 to q+h.
+        const uint64_t M = s.count;
+        struct Hop { int q; uint64_t o, n; uint32_t prev; };
+        std::vector<Hop> hops;
+        for (int q = 0; q < P; ++q)
+            for_chunks(0, M, C, [&](uint32_t, uint64_t o, uint64_t n) { hops.push_back({q, o, n, 0}); });
+        for (auto& h : hops)
+            h.prev = b.add(OP_COPY, RO_SUM, h.n, {opnd(send_buf(h.q), dt, h.o)},
+                           {opnd(recv_buf(P, h.q), dt, (uint64_t)h.q * M + h.o)});
+        for (int step = 1; step < P; ++step) {
+            for (auto& h : hops) {
+                int from = (h.q + step - 1) % P, to = (h.q + step) % P;
+                uint64_t at = (uint64_t)h.q * M + h.o;
+                h.prev = b.add(OP_COPY, RO_SUM, h.n, {opnd(recv_buf(P, from), dt, at)},
+                               {opnd(recv_buf(P, to), dt, at)}, {tile_dep(h.prev)});
+            }
+        }
+        p.algo = ALGO_RING;
+        return;
+    }
+
+    std::vector<Chain> chains;
+    std::vector<int> owner;
+    if (s.coll == COLL_REDUCE_SCATTER) {
+        const uint64_t M = s.count;
+        for (int c = 0; c < P; ++c)
+            for_chunks(0, M, C, [&](uint32_t, uint64_t o, uint64_t n) {
+                Chain ch;
+                ch.src_elem = (uint64_t)c * M + o;
+                ch.nelem = n;
+                ch.final_dst = opnd(recv_buf(P, c), dt, o);
+                ch.scratch_elem = (uint64_t)c * M + o;
+                chains.push_back(ch);
+                owner.push_back(c);
+            });
+        p.scratch_bytes = (P > 2) ? (uint64_t)P * M * dtype_size(acc) : 0;
+    } else {  // allreduce: owner c reduces shard c, then the result travels around the ring
+        const uint64_t q = shard_size(s.count, P);
+        for (int c = 0; c < P; ++c) {
+            uint64_t lo = std::min(s.count, (uint64_t)c * q), hi = std::min(s.count, lo + q);
+            for_chunks(lo, hi, C, [&](uint32_t, uint64_t o, uint64_t n) {
+                Chain ch;
+                ch.src_elem = o;
+                ch.nelem = n;
+                ch.final_dst = opnd(recv_buf(P, c), dt, o);
+                ch.scratch_elem = o;
+                chains.push_back(ch);
+                owner.push_back(c);
+            });
+        }
+        p.scratch_bytes = (P > 2) ? s.count * dtype_size(acc) : 0;
+    }
+    emit_reduce_chains(s, p, chains);
+
+    if (s.coll == COLL_ALLREDUCE) {
+        for (int step = 1; step < P; ++step) {
+            for (size_t i = 0; i < chains.size(); ++i) {
+                Chain& ch = chains[i];
+                int from = (owner[i] + step - 1) % P, to = (owner[i] + step) % P;
+                ch.last = b.add(OP_COPY, RO_SUM, ch.nelem, {opnd(recv_buf(P, from), dt, ch.src_elem)},
+                                {opnd(recv_buf(P, to), dt, ch.src_elem)}, {tile_dep(ch.last)});
+            }
+        }
+    }
+    p.algo = ALGO_RING;
+}
+
+// ------------------------------------------------------------------------- TWO_LEVEL
+// P = G groups x L consecutive ranks. Shard k of the vector is owned by local rank k of
+// every group. Phase 1 (inside each group): the L contributors of shard k are folded into
+// an FP32 partial per group. Phase 2 (across groups): the G partials of shard k are folded
+// in ascending group order, rounded, and written to local rank k of every group. Phase 3
+// (inside each group): local rank k forwards shard k to the other L-1 ranks of its group.
+void lower_two_level(const CollectiveSpec& s, HostProgram& p) {
+    Builder b{p};
+    const int P = s.P, L = s.group_size, G = P / L;
+    const uint64_t N = s.count, C = chunk_elems(s);
+    const uint32_t dt = (uint32_t)s.dtype;
+    const uint32_t acc = acc_dtype(s.dtype, s.redop);
+    const uint64_t q = shard_size(N, L);
+    struct Piece { int k; uint64_t o, n; };
+    std::vector<Piece> pieces;
+    for (int k = 0; k < L; ++k) {
+        uint64_t lo = std::min(N, (uint64_t)k * q), hi = std::min(N, lo + q);
+        for_chunks(lo, hi, C, [&](uint32_t, uint64_t o, uint64_t n) { pieces.push_back({k, o, n}); });
+    }
+    std::vector<std::vector<uint32_t>> rs(pieces.size(), std::vector<uint32_t>(G));
+    for (int g = 0; g < G; ++g) {
+        for (size_t i = 0; i < pieces.size(); ++i) {
+            const Piece& pc = pieces[i];
+            std::vector<Operand> src;
+            for (int m = 0; m < L; ++m) src.push_back(opnd(send_buf(g * L + m), dt, pc.o));
+            rs[i][g] = b.add(OP_REDUCE, (uint8_t)s.redop, pc.n, src,
+                             {opnd(scratch_buf(P), acc, (uint64_t)g * N + pc.o)});
+        }
+    }
+    std::vector<uint32_t> inter(pieces.size());
+    for (size_t i = 0; i < pieces.size(); ++i) {
+        const Piece& pc = pieces[i];
+        std::vector<Operand> src, dst;
+        std::vector<Dep> deps;
+        for (int g = 0; g < G; ++g) {
+            src.push_back(opnd(scratch_buf(P), acc, (uint64_t)g * N + pc.o));
+            deps.push_back(tile_dep(rs[i][g]));
+        }
+        for (int g = 0; g < G; ++g) dst.push_back(opnd(recv_buf(P, g * L + pc.k), dt, pc.o));
+        inter[i] = b.add(OP_REDUCE, (uint8_t)s.redop, pc.n, src, dst, deps);
+    }
+    if (L > 1) {
+        for (int g = 0; g < G; ++g) {
+            for (size_t i = 0; i < pieces.size(); ++i) {
+                const Piece& pc = pieces[i];
+                std::vector<Operand> dst;
+                for (int m = 0; m < L; ++m)
+                    if (m != pc.k) dst.push_back(opnd(recv_buf(P, g * L + m), dt, pc.o));
+                b.add(OP_COPY, RO_SUM, pc.n, {opnd(recv_buf(P, g * L + pc.k), dt, pc.o)}, dst,
+                      {tile_dep(inter[i])});
+            }
+        }
+    }
+    p.scratch_bytes = (uint64_t)G * N * dtype_size(acc);
+    p.algo = ALGO_TWO_LEVEL;
+}
+
+// ------------------------------------------------------------------------- ALLTOALLV
+// Every non-empty (source, destination) block becomes COPY steps of at most one chunk; the
+// steps are ordered largest first so the long blocks start early (Section IV-A: AllToAllv
+// spread across parallel engines).
+void lower_alltoallv(const CollectiveSpec& s, HostProgram& p) {
+    Builder b{p};
+    const int P = s.P;
+    const uint32_t dt = (uint32_t)s.dtype;
+    const uint64_t C = chunk_elems(s);
+    struct Piece { int src, dst; uint64_t so, ro, n; };
+    std::vector<Piece> pieces;
+    for (int src = 0; src < P; ++src) {
+        for (int dst = 0; dst < P; ++dst) {
+            uint64_t n = s.sendcounts[(size_t)src * P + dst];
+            uint64_t so = s.sdispls[(size_t)src * P + dst];
+            uint64_t ro = s.rdispls[(size_t)dst * P + src];
+            for (uint64_t o = 0; o < n; o += C) pieces.push_back({src, dst, so + o, ro + o, std::min(C, n - o)});
+        }
+    }
+    std::stable_sort(pieces.begin(), pieces.end(), [](const Piece& a, const Piece& c) { return a.n > c.n; });
+    for (const Piece& pc : pieces)
+        b.add(OP_COPY, RO_SUM, pc.n, {opnd(send_buf(pc.src), dt, pc.so)}, {opnd(recv_buf(P, pc.dst), dt, pc.ro)});
+    p.algo = ALGO_DIRECT;
+}
+
+void dedupe_deps(HostDesc& d, uint32_t self) {
+    std::vector<Dep> out;
+    for (const Dep& e : d.deps) {
+        if (e.desc == self) continue;
+        bool merged = false;
+        for (Dep& o : out) {
+            if (o.desc == e.desc) {
+                if (e.kind == DEP_ALL) o.kind = DEP_ALL;  // the stronger wait wins
+                merged = true;
+                break;
+            }
+        }
+        if (!merged) out.push_back(e);
+    }
+    d.deps = std::move(out);
+}
+
+struct OperandKey {
+    uint32_t buf;
+    uint64_t offset;
+    bool operator==(const OperandKey& o) const { return buf == o.buf && offset == o.offset; }
+};
+struct OperandKeyHash {
+    size_t operator()(const OperandKey& k) const { return std::hash<uint64_t>()(k.offset * 131 + k.buf); }
+};
+
+}  // namespace
+
+bool CollectiveSpec::operator==(const CollectiveSpec& o) const {
+    return coll == o.coll && P == o.P && dtype == o.dtype && redop == o.redop && count == o.count &&
+           sendcounts == o.sendcounts && sdispls == o.sdispls && recvcounts == o.recvcounts &&
+           rdispls == o.rdispls && in_place == o.in_place && algo == o.algo && group_size == o.group_size &&
+           chunk_bytes == o.chunk_bytes && fuse == o.fuse && tile_bytes == o.tile_bytes;
+}
+
+int resolve_algo(const CollectiveSpec& s) {
+    if (s.coll == COLL_ALLTOALLV) return ALGO_DIRECT;
+    if (s.algo != ALGO_AUTO) return s.algo;
+    if (s.coll == COLL_ALLREDUCE && s.group_size > 1 && s.group_size < s.P && s.P % s.group_size == 0)
+        return ALGO_TWO_LEVEL;
+    return ALGO_RING;
+}
+
+BufferSizes buffer_sizes(const CollectiveSpec& s, uint64_t scratch_bytes) {
+    BufferSizes b;
+    const int P = s.P;
+    const uint64_t es = dtype_size(s.dtype);
+    b.bytes.assign((size_t)2 * P + 1, 0);
+    for (int r = 0; r < P; ++r) {
+        uint64_t sb = 0, rb = 0;
+        switch (s.coll) {
+            case COLL_ALLREDUCE: sb = rb = s.count * es; break;
+            case COLL_REDUCE_SCATTER: sb = (uint64_t)P * s.count * es; rb = s.count * es; break;
+            case COLL_ALLGATHER: sb = s.count * es; rb = (uint64_t)P * s.count * es; break;
+            default:
+                for (int q = 0; q < P; ++q) {
+                    sb = std::max(sb, (s.sdispls[(size_t)r * P + q] + s.sendcounts[(size_t)r * P + q]) * es);
+                    rb = std::max(rb, (s.rdispls[(size_t)r * P + q] + s.recvcounts[(size_t)r * P + q]) * es);
+                }
+        }
+        b.bytes[send_buf(r)] = sb;
+        b.bytes[recv_buf(P, r)] = rb;
+    }
+    b.bytes[scratch_buf(P)] = scratch_bytes;
+    return b;
+}
+
+bool lower(const CollectiveSpec& s, HostProgram& p, std::string& err) {
+    p = HostProgram();
+    p.P = s.P;
+    if (s.coll == COLL_ALLTOALLV) {
+        lower_alltoallv(s, p);
+        return true;
+    }
+    int algo = resolve_algo(s);
+    if (algo == ALGO_TWO_LEVEL) {
+        if (s.coll != COLL_ALLREDUCE) {
+            err = "the two-level schedule is defined for allreduce only";
+            return false;
+        }
+        if (s.group_size < 1 || s.P % s.group_size != 0) {
+            err = "group_size must divide nranks for the two-level schedule";
+            return false;
+        }
+        lower_two_level(s, p);
+    } else if (algo == ALGO_RING) {
+        lower_ring(s, p);
+    } else if (algo == ALGO_DIRECT) {
+        lower_direct(s, p);
+    } else {
+        err = "unknown algorithm";
+        return false;
+    }
+    return true;
+}
+
+// ---------------------------------------------------------------------------- fusion
+//
+// Rule 1 (chain): B = REDUCE(partial, x...) where partial is the scratch output of REDUCE A
+//   (its only destination) and B is the only step that reads that value  ->  B = REDUCE(A's
+//   sources, x...). The fold is the same sequence of operations on the same values: A's
+//   result was never rounded (it is in the accumulation type), B continued from it.
+// Rule 2 (groups): E = REDUCE(p_0, ..., p_{G-1}) where every p_g is the scratch output of a
+//   flat REDUCE D_g of L sources that only E reads  ->  E = REDUCE(all D_g sources,
+//   group = L): fold each run of L into a partial, then fold the partials, as before.
+// Rule 3 (forwarding): F = COPY(x -> y...) where x is the value a step E wrote (same
+//   location and element count) and F waits for E  ->  E also writes y... .
+//
+// Values are tracked by version: the producer of a source is the last step, in program
+// order, that wrote exactly that location. Merged steps forward to the step that absorbed
+// them, so later lookups and dependencies resolve to the surviving step.
+void fuse(HostProgram& p) {
+    const uint32_t scratch = scratch_buf(p.P);
+    const uint32_t D = (uint32_t)p.descs.size();
+    std::vector<uint32_t> fwd(D);
+    for (uint32_t i = 0; i < D; ++i) fwd[i] = i;
+    auto find = [&](uint32_t x) {
+        while (fwd[x] != x) {
+            fwd[x] = fwd[fwd[x]];
+            x = fwd[x];
+        }
+        return x;
+    };
+
+    // producer of every source operand, and how many sources read each written value
+    std::vector<std::vector<int64_t>> prod(D);
+    std::vector<std::vector<uint32_t>> nread(D);
+    {
+        std::unordered_map<OperandKey, std::pair<uint32_t, uint32_t>, OperandKeyHash> last;
+        for (uint32_t i = 0; i < D; ++i) {
+            const HostDesc& d = p.descs[i];
+            nread[i].assign(d.dsts.size(), 0);
+            prod[i].assign(d.srcs.size(), -1);
+            for (size_t k = 0; k < d.srcs.size(); ++k) {
+                auto it = last.find({d.srcs[k].buf, d.srcs[k].offset});
+                if (it == last.end()) continue;
+                const HostDesc& w = p.descs[it->second.first];
+                if (w.dsts[it->second.second].dtype != d.srcs[k].dtype || w.nelem != d.nelem) continue;
+                prod[i][k] = it->second.first;
+                nread[it->second.first][it->second.second] += 1;
+            }
+            for (size_t k = 0; k < d.dsts.size(); ++k) last[{d.dsts[k].buf, d.dsts[k].offset}] = {i, (uint32_t)k};
+        }
+    }
+    auto depends_on = [&](const HostDesc& d, uint32_t target) {
+        for (const Dep& e : d.deps)
+            if (find(e.desc) == target) return true;
+        return false;
+    };
+    // A is a partial-sum step whose single value only `consumer` reads
+    auto private_partial = [&](int64_t a, const HostDesc& B) {
+        if (a < 0) return false;
+        const HostDesc& A = p.descs[a];
+        return A.alive && A.op == OP_REDUCE && A.group == 0 && A.dsts.size() == 1 && A.dsts[0].buf == scratch &&
+               A.redop == B.redop && A.nelem == B.nelem && nread[a][0] == 1 && depends_on(B, (uint32_t)a);
+    };
+    auto absorb_deps = [&](HostDesc& into, const HostDesc& from) {
+        into.deps.insert(into.deps.end(), from.deps.begin(), from.deps.end());
+    };
+
+    for (uint32_t i = 0; i < D; ++i) {
+        HostDesc& B = p.descs[i];
+        if (!B.alive) continue;
+        if (B.op == OP_REDUCE && B.group == 0 && !B.srcs.empty()) {
+            // Rule 2: every source is a private partial of an equally sized flat reduction.
+            bool groups = B.srcs.size() >= 2;
+            size_t L = 0, total = 0;
+            for (size_t k = 0; groups && k < B.srcs.size(); ++k) {
+                int64_t a = prod[i][k];
+                if (!private_partial(a, B) || (L && p.descs[a].srcs.size() != L)) {
+                    groups = false;
+                    break;
+                }
+                L = p.descs[a].srcs.size();
+                total += L;
+            }
+            if (groups && total <= (size_t)kMaxOperands) {
+                std::vector<Operand> srcs;
+                std::vector<int64_t> sprod;
+                size_t G = B.srcs.size();
+                for (size_t k = 0; k < G; ++k) {
+                    uint32_t a = (uint32_t)prod[i][k];
+                    HostDesc& A = p.descs[a];
+                    srcs.insert(srcs.end(), A.srcs.begin(), A.srcs.end());
+                    sprod.insert(sprod.end(), prod[a].begin(), prod[a].end());
+                    absorb_deps(B, A);
+                    A.alive = false;
+                    fwd[a] = i;
+                }
+                B.srcs = std::move(srcs);
+                prod[i] = std::move(sprod);
+                B.group = (G == 1 || L == 1) ? 0 : (uint16_t)L;
+                continue;
+            }
+            // Rule 1: the first source is a private partial.
+            int64_t a = prod[i][0];
+            if (private_partial(a, B) && p.descs[a].srcs.size() + B.srcs.size() - 1 <= (size_t)kMaxOperands) {
+                HostDesc& A = p.descs[a];
+                std::vector<Operand> srcs = A.srcs;
+                srcs.insert(srcs.end(), B.srcs.begin() + 1, B.srcs.end());
+                std::vector<int64_t> sprod = prod[a];
+                sprod.insert(sprod.end(), prod[i].begin() + 1, prod[i].end());
+                B.srcs = std::move(srcs);
+                prod[i] = std::move(sprod);
+                absorb_deps(B, A);
+                A.alive = false;
+                fwd[a] = i;
+            }
+            continue;
+        }
+        if (B.op == OP_COPY && B.srcs.size() == 1 && prod[i][0] >= 0) {
+            // Rule 3: a forwarding copy of a value becomes more destinations of its producer.
+            uint32_t e = find((uint32_t)prod[i][0]);
+            HostDesc& E = p.descs[e];
+            if (!E.alive || E.nelem != B.nelem || !depends_on(B, e)) continue;
+            if (E.dsts.size() + B.dsts.size() > (size_t)kMaxOperands) continue;
+            bool deps_ok = true;
+            for (const Dep& d : B.deps) {
+                uint32_t t = find(d.desc);
+                if (t != e && t > e) deps_ok = false;
+            }
+            if (!deps_ok) continue;
+            E.dsts.insert(E.dsts.end(), B.dsts.begin(), B.dsts.end());
+            nread[e].resize(E.dsts.size(), 0);
+            for (const Dep& d : B.deps)
+                if (find(d.desc) != e) E.deps.push_back(d);
+            B.alive = false;
+            fwd[i] = e;
+        }
+    }
+    // resolve every dependency to the step that survived
+    for (uint32_t i = 0; i < D; ++i) {
+        HostDesc& d = p.descs[i];
+        if (!d.alive) continue;
+        for (Dep& e : d.deps) e.desc = find(e.desc);
+        dedupe_deps(d, i);
+    }
+    p.fused = true;
+    // scratch is needed only if some live step still touches it
+    bool uses_scratch = false;
+    for (const auto& d : p.descs) {
+        if (!d.alive) continue;
+        for (const Operand& o : d.srcs) uses_scratch |= (o.buf == scratch);
+        for (const Operand& o : d.dsts) uses_scratch |= (o.buf == scratch);
+    }
+    if (!uses_scratch) p.scratch_bytes = 0;
+}
+
+// ---------------------------------------------------------------------------- packing
+bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
+    // compact
+    std::vector<int64_t> remap(p.descs.size(), -1);
+    std::vector<HostDesc> live;
+    for (size_t i = 0; i < p.descs.size(); ++i) {
+        if (!p.descs[i].alive) continue;
+        remap[i] = (int64_t)live.size();
+        live.push_back(std::move(p.descs[i]));
+    }
+    for (size_t i = 0; i < live.size(); ++i) {
+        for (Dep& d : live[i].deps) {
+            if (remap[d.desc] < 0) {
+                err = "dependency on a removed step";
+                return false;
+            }
+            d.desc = (uint32_t)remap[d.desc];
+        }
+        dedupe_deps(live[i], (uint32_t)i);
+    }
+    p.descs = std::move(live);
+
+    // one tile size for the whole program, so per-tile dependencies line up
+    uint64_t max_bpe = 1;
+    for (const auto& d : p.descs) {
+        uint64_t bpe = 0;
+        for (const Operand& o : d.srcs) bpe += dtype_size(o.dtype);
+        max_bpe = std::max(max_bpe, bpe);
+    }
+    uint64_t tb = tile_bytes ? tile_bytes : kDefaultTileBytes;
+    uint64_t te = (tb / max_bpe) / kWaveStepElems * kWaveStepElems;
+    te = std::max<uint64_t>(te, kWaveStepElems);
+    te = std::min<uint64_t>(te, 1ull << 30);
+    p.tile_elems = (uint32_t)te;
+
+    const uint32_t nd = (uint32_t)p.descs.size();
+    std::vector<Desc> out(nd);
+    std::vector<Operand> ops;
+    std::vector<Dep> deps;
+    std::vector<uint32_t> tile_owner;
+    uint64_t ntiles = 0;
+    p.bytes_read = p.bytes_written = 0;
+    p.max_srcs = 0;
+    bool has_deps = false;
+    for (uint32_t i = 0; i < nd; ++i) {
+        const HostDesc& h = p.descs[i];
+        Desc& d = out[i];
+        std::memset(&d, 0, sizeof d);
+        d.op = h.op;
+        d.redop = h.redop;
+        d.group = h.group;
+        d.nsrc = (uint16_t)h.srcs.size();
+        d.ndst = (uint16_t)h.dsts.size();
+        d.nelem = h.nelem;
+        d.tile_elems = p.tile_elems;
+        uint64_t nt = (h.op == OP_NOOP) ? 1 : (h.nelem + te - 1) / te;
+        if (nt == 0) nt = 1;
+        d.ntiles = (uint32_t)nt;
+        d.tile0 = (uint32_t)ntiles;
+        ntiles += nt;
+        if (ntiles >= (1ull << 31)) {
+            err = "program has too many tiles";
+            return false;
+        }
+        d.sig = SIG_INVALID;
+        if (h.op == OP_REDUCE && !h.srcs.empty() && !h.dsts.empty()) {
+            uint32_t tr = h.srcs.size() > 1 ? h.srcs[1].dtype : h.srcs[0].dtype;
+            d.sig = reduce_signature(h.srcs[0].dtype, tr, h.dsts[0].dtype);
+        }
+        d.src = (uint32_t)ops.size();
+        ops.insert(ops.end(), h.srcs.begin(), h.srcs.end());
+        d.dst = (uint32_t)ops.size();
+        ops.insert(ops.end(), h.dsts.begin(), h.dsts.end());
+        d.dep = (uint32_t)deps.size();
+        d.ndep = (uint16_t)h.deps.size();
+        deps.insert(deps.end(), h.deps.begin(), h.deps.end());
+        has_deps |= !h.deps.empty();
+        p.max_srcs = std::max<uint32_t>(p.max_srcs, d.nsrc);
+        for (const Operand& o : h.srcs) p.bytes_read += h.nelem * dtype_size(o.dtype);
+        for (const Operand& o : h.dsts) p.bytes_written += h.nelem * dtype_size(o.dtype);
+        for (uint64_t t = 0; t < nt; ++t) tile_owner.push_back(i);
+    }
+    p.ntiles = (uint32_t)ntiles;
+    p.nstate = has_deps ? (uint32_t)(kStateDescBase + nd + ntiles) : kStateDescBase;
+    p.flags = has_deps ? PF_HAS_DEPS : 0;
+    // dependency targets: expected values, state words, signal flags
+    for (uint32_t i = 0; i < nd; ++i) {
+        for (uint32_t k = 0; k < out[i].ndep; ++k) {
+            Dep& e = deps[out[i].dep + k];
+            Desc& t = out[e.desc];
+            if (e.kind == DEP_ALL) {
+                e.expected = t.ntiles;
+                e.state = kStateDescBase + e.desc;
+                t.flags |= DF_SIGNAL_DESC;
+            } else {
+                e.expected = 1;
+                e.state = kStateDescBase + nd + t.tile0;
+                t.flags |= DF_SIGNAL_TILE;
+            }
+        }
+    }
+    p.ndeps = (uint32_t)deps.size();
+    p.noperands = (uint32_t)ops.size();
+
+    // the leanest executor kernel that covers every step
+    int kind = kKindCopyOnly;
+    for (uint32_t i = 0; i < nd; ++i) {
+        if (out[i].op != OP_REDUCE) continue;
+        const bool plain = out[i].sig <= SIG_INT32 && out[i].redop == RO_SUM;
+        if (!plain) { kind = kKindGeneric; break; }
+        if (kind == kKindCopyOnly) kind = out[i].sig;
+        else if (kind != out[i].sig) { kind = kKindGeneric; break; }
+    }
+    p.kind = kind;
+
+    auto align16 = [](uint64_t x) { return (x + 15) & ~uint64_t(15); };
+    ProgramHeader hdr;
+    std::memset(&hdr, 0, sizeof hdr);
+    hdr.magic = kProgramMagic;
+    hdr.version = kProgramVersion;
+    hdr.ndesc = nd;
+    hdr.ntiles = p.ntiles;
+    hdr.noperand = p.noperands;
+    hdr.ndep = p.ndeps;
+    hdr.flags = p.flags;
+    hdr.nstate = p.nstate;
+    hdr.off_desc = align16(sizeof(ProgramHeader));
+    hdr.off_operand = align16(hdr.off_desc + (uint64_t)nd * sizeof(Desc));
+    hdr.off_dep = align16(hdr.off_operand + ops.size() * sizeof(Operand));
+    hdr.off_tile_desc = align16(hdr.off_dep + deps.size() * sizeof(Dep));
+    hdr.total_bytes = align16(hdr.off_tile_desc + tile_owner.size() * sizeof(uint32_t));
+    hdr.scratch_bytes = p.scratch_bytes;
+    p.image.assign(hdr.total_bytes, 0);
+    std::memcpy(p.image.data(), &hdr, sizeof hdr);
+    if (nd) std::memcpy(p.image.data() + hdr.off_desc, out.data(), (size_t)nd * sizeof(Desc));
+    if (!ops.empty()) std::memcpy(p.image.data() + hdr.off_operand, ops.data(), ops.size() * sizeof(Operand));
+    if (!deps.empty()) std::memcpy(p.image.data() + hdr.off_dep, deps.data(), deps.size() * sizeof(Dep));
+    if (!tile_owner.empty())
+        std::memcpy(p.image.data() + hdr.off_tile_desc, tile_owner.data(), tile_owner.size() * sizeof(uint32_t));
+    return true;
+}
+
+}  // namespace hccl

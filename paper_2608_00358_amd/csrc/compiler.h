@@ -1,0 +1,102 @@
+// compiler.h -- host-side lowering of collectives into descriptor programs.
+//
+// The host builds the complete description of a collective, dependencies included, before
+// anything runs on the device (paper, Section III-B "Data Path"; host-side generation,
+// Section V-B). Lowerings emit the schedule step by step (ring reduce chains and forwarding
+// hops, two-level group phases); the fusion pass then merges chained steps whose
+// intermediate only feeds the next step, which keeps the arithmetic (same operations in
+// the same order) and removes the intermediate traffic.
+#pragma once
+
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "program.h"
+
+namespace hccl {
+
+enum Collective : int { COLL_ALLREDUCE = 0, COLL_REDUCE_SCATTER = 1, COLL_ALLGATHER = 2, COLL_ALLTOALLV = 3 };
+enum Algo : int { ALGO_AUTO = 0, ALGO_DIRECT = 1, ALGO_RING = 2, ALGO_TWO_LEVEL = 3 };
+
+struct CollectiveSpec {
+    int coll = COLL_ALLREDUCE;
+    int P = 1;
+    int dtype = DT_FP32;
+    int redop = RO_SUM;
+    uint64_t count = 0;          // allreduce: count; reduce_scatter: recvcount; allgather: sendcount
+    std::vector<uint64_t> sendcounts, sdispls, recvcounts, rdispls;  // alltoallv, P*P each
+    bool in_place = false;       // allreduce with send[r] == recv[r]
+    int algo = ALGO_AUTO;
+    int group_size = 0;
+    uint64_t chunk_bytes = 0;
+    bool fuse = true;
+    uint32_t tile_bytes = 0;
+
+    bool operator==(const CollectiveSpec& o) const;
+};
+
+struct HostDesc {
+    uint8_t op = OP_REDUCE;
+    uint8_t redop = RO_SUM;
+    uint16_t group = 0;
+    uint64_t nelem = 0;
+    std::vector<Operand> srcs;
+    std::vector<Operand> dsts;
+    std::vector<Dep> deps;
+    bool alive = true;
+};
+
+struct HostProgram {
+    int P = 0;
+    int algo = ALGO_DIRECT;      // schedule actually lowered
+    bool fused = false;
+    uint64_t scratch_bytes = 0;
+    std::vector<HostDesc> descs;
+
+    // filled by finalize()
+    uint32_t tile_elems = 0;
+    uint32_t ntiles = 0;
+    uint32_t ndeps = 0;
+    uint32_t noperands = 0;
+    uint32_t max_srcs = 0;
+    uint64_t bytes_read = 0;
+    uint64_t bytes_written = 0;
+    std::vector<uint8_t> image;  // ProgramHeader + arrays, uploaded to the device as is
+    uint32_t nstate = 0;
+    uint32_t flags = 0;
+    int kind = kKindGeneric;     // executor specialisation that can run this program
+};
+
+// Buffer ids used by lowerings.
+inline uint32_t send_buf(int r) { return (uint32_t)r; }
+inline uint32_t recv_buf(int P, int r) { return (uint32_t)(P + r); }
+inline uint32_t scratch_buf(int P) { return (uint32_t)(2 * P); }
+
+// Byte size of every buffer id a program may touch (for bounds checks and coverage).
+struct BufferSizes {
+    std::vector<uint64_t> bytes;  // indexed by buffer id, 2P + 1 entries
+};
+BufferSizes buffer_sizes(const CollectiveSpec& spec, uint64_t scratch_bytes);
+
+// Picks the schedule for ALGO_AUTO.
+int resolve_algo(const CollectiveSpec& spec);
+
+// Lowers `spec` into `prog` (unfused steps). Returns false and sets err on bad input.
+bool lower(const CollectiveSpec& spec, HostProgram& prog, std::string& err);
+
+// Merges chained steps: reduce chains into multi-source reductions, group partial folds into
+// grouped reductions, forwarding copies into extra destinations of their producer.
+void fuse(HostProgram& prog);
+
+// Removes dead descriptors, renumbers dependencies, cuts tiles, sets signal flags and packs
+// the device image. tile_bytes = 0 selects the default.
+bool finalize(HostProgram& prog, uint32_t tile_bytes, std::string& err);
+
+// Structural checks of a finalized program: dependency order, operand bounds, per-tile
+// dependency shape, data races between steps not ordered by dependencies (with send and
+// receive buffers aliased when in_place), and exact coverage of the collective's output.
+bool validate(const HostProgram& prog, const CollectiveSpec& spec, std::string& err);
+
+}  // namespace hccl

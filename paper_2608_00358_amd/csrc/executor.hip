@@ -1,0 +1,620 @@
+// executor.hip -- the persistent descriptor executor for gfx950 (MI355X).
+//
+// One launch runs one program (the single-GPU form of a work packet; paper, Section III-B).
+// Every wavefront is an independent worker, the analogue of a message engine's control core
+// (Section II-A-2: fetch the graph, evaluate dependencies, issue the work): it takes a tile
+// ticket, waits for the tile's dependencies, performs the copy or reduction of the tile with
+// 128-bit coalesced loads and stores (the near-memory-compute analogue: FP32 arithmetic,
+// one rounding to the buffer type), and signals completion with monotonically growing
+// counters (the signal pairs of Section III-B).
+//
+// Memory model: dependency counters are written with agent-scope release and read with
+// agent-scope acquire, so a consumer on another XCD (each XCD has its own L2) sees the
+// producer's data. Programs without dependencies use no counters at all: wavefront w runs
+// tiles w, w + W, ... and nothing is shared between wavefronts.
+#include <hip/hip_runtime.h>
+
+#include <stddef.h>
+
+#include <type_traits>
+
+#include "program.h"
+
+namespace hccl {
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlockThreads = kWavesPerBlock * kWaveSize;
+constexpr int kSrcBatch = 8;  // sources whose loads are issued together
+
+template <int DT> struct DtInfo;
+template <> struct DtInfo<DT_BF16> { static constexpr int size = 2; typedef float acc; };
+template <> struct DtInfo<DT_FP16> { static constexpr int size = 2; typedef float acc; };
+template <> struct DtInfo<DT_FP32> { static constexpr int size = 4; typedef float acc; };
+template <> struct DtInfo<DT_INT32> { static constexpr int size = 4; typedef int32_t acc; };
+
+// ------------------------------------------------------------------ wave-uniform values
+__device__ __forceinline__ uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ uint64_t uni64(uint64_t x) {
+    uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// value held by lane j (j wave-uniform) of a lane-distributed 64-bit value
+__device__ __forceinline__ uint64_t from_lane(uint64_t v, uint32_t j) {
+    uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, j);
+    uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), j);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t elem_bytes(uint32_t dt) { return (dt == DT_BF16 || dt == DT_FP16) ? 2u : 4u; }
+
+// ----------------------------------------------------------------------- conversions
+// bf16 -> fp32 is exact: the bf16 bits are the upper half of the fp32 encoding.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// fp32 -> bf16, round to nearest, ties to even: adding 0x7FFF plus the lowest kept bit to
+// the encoding carries into the kept half exactly when the dropped half is above one half,
+// or equal to one half with an odd kept half. NaNs keep sign and top payload, quiet bit set.
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ float f16_lo(uint32_t w) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xFFFFu));
+}
+__device__ __forceinline__ float f16_hi(uint32_t w) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
+}
+// fp32 -> fp16 with the hardware conversion in the default round-to-nearest-even mode
+// (overflow to infinity, subnormal results kept).
+__device__ __forceinline__ uint32_t f16_bits(float f) {
+    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
+// --------------------------------------------------------------- reduction operators
+// SUM: one binary32 addition (never fused). MAX / MIN: a NaN running value stays, a NaN
+// contributor replaces a number, otherwise the strictly larger / smaller value wins.
+template <int OPR>
+__device__ __forceinline__ float comb(float a, float x) {
+    if (OPR == RO_SUM) return a + x;
+    if (a != a) return a;
+    if (x != x) return x;
+    if (OPR == RO_MAX) return (x > a) ? x : a;
+    return (x < a) ? x : a;
+}
+template <int OPR>
+__device__ __forceinline__ int32_t comb(int32_t a, int32_t x) {
+    if (OPR == RO_SUM) return (int32_t)((uint32_t)a + (uint32_t)x);
+    if (OPR == RO_MAX) return (x > a) ? x : a;
+    return (x < a) ? x : a;
+}
+
+// ------------------------------------------------------- 8-element vectors per lane
+template <int DT> struct Raw8 { u32x4 v[DtInfo<DT>::size / 2]; };
+
+template <int DT>
+__device__ __forceinline__ Raw8<DT> load8(const char* p) {
+    Raw8<DT> r;
+#pragma unroll
+    for (int q = 0; q < DtInfo<DT>::size / 2; ++q) r.v[q] = *(const u32x4*)(p + 16 * q);
+    return r;
+}
+
+template <int DT, typename A>
+__device__ __forceinline__ void widen8(const Raw8<DT>& r, A (&x)[8]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if constexpr (DT == DT_BF16) {
+            x[2 * i] = bf16_lo(r.v[0][i]);
+            x[2 * i + 1] = bf16_hi(r.v[0][i]);
+        } else if constexpr (DT == DT_FP16) {
+            x[2 * i] = f16_lo(r.v[0][i]);
+            x[2 * i + 1] = f16_hi(r.v[0][i]);
+        } else if constexpr (DT == DT_FP32) {
+            x[i] = __uint_as_float(r.v[0][i]);
+            x[4 + i] = __uint_as_float(r.v[1][i]);
+        } else {
+            x[i] = (int32_t)r.v[0][i];
+            x[4 + i] = (int32_t)r.v[1][i];
+        }
+    }
+}
+
+template <int DT, typename A>
+__device__ __forceinline__ void store8(char* p, const A (&x)[8]) {
+    if constexpr (DT == DT_BF16 || DT == DT_FP16) {
+        u32x4 w;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (DT == DT_BF16) w[i] = bf16_bits(x[2 * i]) | (bf16_bits(x[2 * i + 1]) << 16);
+            else w[i] = f16_bits(x[2 * i]) | (f16_bits(x[2 * i + 1]) << 16);
+        }
+        *(u32x4*)p = w;
+    } else {
+        u32x4 a, b;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (DT == DT_FP32) {
+                a[i] = __float_as_uint(x[i]);
+                b[i] = __float_as_uint(x[4 + i]);
+            } else {
+                a[i] = (uint32_t)x[i];
+                b[i] = (uint32_t)x[4 + i];
+            }
+        }
+        *(u32x4*)p = a;
+        *(u32x4*)(p + 16) = b;
+    }
+}
+
+// single elements (tails and misaligned operands)
+template <int DT, typename A>
+__device__ __forceinline__ A load1(const char* p) {
+    if constexpr (DT == DT_BF16) return bf16_lo(*(const uint16_t*)p);
+    else if constexpr (DT == DT_FP16) return f16_lo(*(const uint16_t*)p);
+    else if constexpr (DT == DT_FP32) return *(const float*)p;
+    else return *(const int32_t*)p;
+}
+
+template <int DT, typename A>
+__device__ __forceinline__ void store1(char* p, A v) {
+    if constexpr (DT == DT_BF16) *(uint16_t*)p = (uint16_t)bf16_bits(v);
+    else if constexpr (DT == DT_FP16) *(uint16_t*)p = (uint16_t)f16_bits(v);
+    else if constexpr (DT == DT_FP32) *(float*)p = v;
+    else *(int32_t*)p = v;
+}
+
+// ---------------------------------------------------------------------------- REDUCE
+struct TileOps {
+    uint64_t src;     // lane j: address of source j at the tile's first element
+    uint64_t dst;     // lane j: address of destination j at the tile's first element
+    uint32_t nsrc, ndst, group;
+};
+
+// Fold the sources of `count` elements starting at tile element `first`, one element per
+// lane, contributors in list order (grouped when group > 0), and store to every destination.
+template <int T0, int TR, int TO, int OPR>
+__device__ __forceinline__ void reduce_elems(const TileOps& t, uint32_t first, uint32_t count, uint32_t lane) {
+    typedef typename DtInfo<TO>::acc A;
+    const uint32_t L = t.group ? t.group : t.nsrc;
+    for (uint32_t e = first + lane; e < first + count; e += kWaveSize) {
+        A tot = A(0);
+        for (uint32_t g0 = 0; g0 < t.nsrc; g0 += L) {
+            A part;
+            const char* b0 = (const char*)from_lane(t.src, g0);
+            if (g0 == 0) part = load1<T0, A>(b0 + (uint64_t)e * DtInfo<T0>::size);
+            else part = load1<TR, A>(b0 + (uint64_t)e * DtInfo<TR>::size);
+            const uint32_t gend = (g0 + L < t.nsrc) ? g0 + L : t.nsrc;
+            for (uint32_t s = g0 + 1; s < gend; ++s) {
+                const char* b = (const char*)from_lane(t.src, s);
+                part = comb<OPR>(part, load1<TR, A>(b + (uint64_t)e * DtInfo<TR>::size));
+            }
+            tot = (g0 == 0) ? part : comb<OPR>(tot, part);
+        }
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* b = (char*)from_lane(t.dst, j);
+            store1<TO, A>(b + (uint64_t)e * DtInfo<TO>::size, tot);
+        }
+    }
+}
+
+// U vectors of 8 elements per lane: elements [base, base + U*512) of the tile, all in range.
+template <int T0, int TR, int TO, int OPR, int U>
+__device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, uint32_t lane) {
+    typedef typename DtInfo<TO>::acc A;
+    const uint32_t L = t.group ? t.group : t.nsrc;
+    A tot[U][8], part[U][8];
+    for (uint32_t g0 = 0; g0 < t.nsrc; g0 += L) {
+        const uint32_t gend = (g0 + L < t.nsrc) ? g0 + L : t.nsrc;
+        {
+            const char* b = (const char*)from_lane(t.src, g0);
+            if (g0 == 0) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
+                    widen8<T0, A>(load8<T0>(b + (uint64_t)e * DtInfo<T0>::size), part[u]);
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
+                    widen8<TR, A>(load8<TR>(b + (uint64_t)e * DtInfo<TR>::size), part[u]);
+                }
+            }
+        }
+        for (uint32_t s = g0 + 1; s < gend; s += kSrcBatch) {
+            Raw8<TR> raw[kSrcBatch][U];
+#pragma unroll
+            for (int j = 0; j < kSrcBatch; ++j) {
+                if (s + j < gend) {
+                    const char* b = (const char*)from_lane(t.src, s + j);
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
+                        raw[j][u] = load8<TR>(b + (uint64_t)e * DtInfo<TR>::size);
+                    }
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kSrcBatch; ++j) {
+                if (s + j < gend) {
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        A x[8];
+                        widen8<TR, A>(raw[j][u], x);
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) part[u][i] = comb<OPR>(part[u][i], x[i]);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) tot[u][i] = (g0 == 0) ? part[u][i] : comb<OPR>(tot[u][i], part[u][i]);
+    }
+    for (uint32_t j = 0; j < t.ndst; ++j) {
+        char* b = (char*)from_lane(t.dst, j);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
+            store8<TO, A>(b + (uint64_t)e * DtInfo<TO>::size, tot[u]);
+        }
+    }
+}
+
+template <int T0, int TR, int TO, int OPR>
+__device__ __forceinline__ void reduce_tile(const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
+    if (!aligned) {
+        reduce_elems<T0, TR, TO, OPR>(t, 0, n, lane);
+        return;
+    }
+    constexpr int U = (DtInfo<TR>::size == 2) ? 2 : 1;
+    constexpr uint32_t kBlock = (uint32_t)U * kWaveSize * kVecElems;
+    uint32_t base = 0;
+    for (; base + kBlock <= n; base += kBlock) reduce_block<T0, TR, TO, OPR, U>(t, base, lane);
+    // remaining whole 512-element steps, then single elements
+    for (; base + kWaveSize * kVecElems <= n; base += kWaveSize * kVecElems)
+        reduce_block<T0, TR, TO, OPR, 1>(t, base, lane);
+    if (base < n) {
+        // lanes whose 8 elements are all in range take one more vector step
+        const uint32_t whole = (n - base) / kVecElems;
+        if (lane < whole) reduce_block<T0, TR, TO, OPR, 1>(t, base, lane);
+        base += whole * kVecElems;
+    }
+    if (base < n) reduce_elems<T0, TR, TO, OPR>(t, base, n - base, lane);
+}
+
+template <int T0, int TR, int TO>
+__device__ __forceinline__ void reduce_dispatch_op(uint32_t op, const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
+    if (op == RO_SUM) reduce_tile<T0, TR, TO, RO_SUM>(t, n, aligned, lane);
+    else if constexpr (T0 == TR && TR == TO) {
+        if (op == RO_MAX) reduce_tile<T0, TR, TO, RO_MAX>(t, n, aligned, lane);
+        else reduce_tile<T0, TR, TO, RO_MIN>(t, n, aligned, lane);
+    }
+}
+
+__device__ __forceinline__ void run_reduce(uint32_t sig, uint32_t op, const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
+    switch (sig) {
+        case SIG_BF16: reduce_dispatch_op<DT_BF16, DT_BF16, DT_BF16>(op, t, n, aligned, lane); break;
+        case SIG_FP16: reduce_dispatch_op<DT_FP16, DT_FP16, DT_FP16>(op, t, n, aligned, lane); break;
+        case SIG_FP32: reduce_dispatch_op<DT_FP32, DT_FP32, DT_FP32>(op, t, n, aligned, lane); break;
+        case SIG_INT32: reduce_dispatch_op<DT_INT32, DT_INT32, DT_INT32>(op, t, n, aligned, lane); break;
+        case SIG_BF16_TO_F32: reduce_dispatch_op<DT_BF16, DT_BF16, DT_FP32>(op, t, n, aligned, lane); break;
+        case SIG_F32_BF16_TO_F32: reduce_dispatch_op<DT_FP32, DT_BF16, DT_FP32>(op, t, n, aligned, lane); break;
+        case SIG_F32_BF16_TO_BF16: reduce_dispatch_op<DT_FP32, DT_BF16, DT_BF16>(op, t, n, aligned, lane); break;
+        case SIG_F32_TO_BF16: reduce_dispatch_op<DT_FP32, DT_FP32, DT_BF16>(op, t, n, aligned, lane); break;
+        case SIG_FP16_TO_F32: reduce_dispatch_op<DT_FP16, DT_FP16, DT_FP32>(op, t, n, aligned, lane); break;
+        case SIG_F32_FP16_TO_F32: reduce_dispatch_op<DT_FP32, DT_FP16, DT_FP32>(op, t, n, aligned, lane); break;
+        case SIG_F32_FP16_TO_FP16: reduce_dispatch_op<DT_FP32, DT_FP16, DT_FP16>(op, t, n, aligned, lane); break;
+        case SIG_F32_TO_FP16: reduce_dispatch_op<DT_FP32, DT_FP32, DT_FP16>(op, t, n, aligned, lane); break;
+        default: break;
+    }
+}
+
+// ------------------------------------------------------------------------------ COPY
+// Byte copy of one source to every destination. 16-byte vectors when source and all
+// destinations share their offset modulo 16 (a head and a tail of whole elements go one
+// element per lane); element by element otherwise.
+template <int ES>
+__device__ __forceinline__ void copy_elems(const char* src, const TileOps& t, uint64_t first, uint64_t count, uint32_t lane) {
+    typedef typename std::conditional<ES == 2, uint16_t, uint32_t>::type W;
+    constexpr int U = 8;
+    uint64_t e = first;
+    for (; e + (uint64_t)U * kWaveSize <= first + count; e += (uint64_t)U * kWaveSize) {
+        W v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = *(const W*)(src + (e + (uint64_t)u * kWaveSize + lane) * ES);
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* d = (char*)from_lane(t.dst, j);
+#pragma unroll
+            for (int u = 0; u < U; ++u) *(W*)(d + (e + (uint64_t)u * kWaveSize + lane) * ES) = v[u];
+        }
+    }
+    for (uint64_t x = e + lane; x < first + count; x += kWaveSize) {
+        W v = *(const W*)(src + x * ES);
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* d = (char*)from_lane(t.dst, j);
+            *(W*)(d + x * ES) = v;
+        }
+    }
+}
+
+template <int ES>
+__device__ __forceinline__ void copy_tile(const TileOps& t, uint32_t n, uint32_t lane) {
+    const char* src = (const char*)from_lane(t.src, 0);
+    const uint32_t mis = (uint32_t)((uint64_t)src & 15u);
+    // every destination must share the source's offset modulo 16 for the vector path
+    const bool congruent =
+        __ballot(lane < t.ndst && (uint32_t)(t.dst & 15u) != mis) == 0ull;
+    if (!congruent) {
+        copy_elems<ES>(src, t, 0, n, lane);
+        return;
+    }
+    const uint64_t nbytes = (uint64_t)n * ES;
+    uint64_t head = mis ? (16u - mis) : 0u;   // bytes before the first 16-byte boundary
+    if (head > nbytes) head = nbytes;
+    if (head) copy_elems<ES>(src, t, 0, head / ES, lane);
+    constexpr int U = 4;
+    constexpr uint64_t kStep = (uint64_t)U * kWaveSize * 16;
+    uint64_t off = head;
+    for (; off + kStep <= nbytes; off += kStep) {
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = *(const u32x4*)(src + off + ((uint64_t)u * kWaveSize + lane) * 16);
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* d = (char*)from_lane(t.dst, j);
+#pragma unroll
+            for (int u = 0; u < U; ++u) *(u32x4*)(d + off + ((uint64_t)u * kWaveSize + lane) * 16) = v[u];
+        }
+    }
+    for (; off + 16 * kWaveSize <= nbytes; off += 16 * kWaveSize) {
+        u32x4 v = *(const u32x4*)(src + off + (uint64_t)lane * 16);
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* d = (char*)from_lane(t.dst, j);
+            *(u32x4*)(d + off + (uint64_t)lane * 16) = v;
+        }
+    }
+    {
+        uint64_t x = off + (uint64_t)lane * 16;
+        if (x + 16 <= nbytes) {
+            u32x4 v = *(const u32x4*)(src + x);
+            for (uint32_t j = 0; j < t.ndst; ++j) {
+                char* d = (char*)from_lane(t.dst, j);
+                *(u32x4*)(d + x) = v;
+            }
+        }
+        off += (nbytes - off) / 16 * 16;
+    }
+    if (off < nbytes) copy_elems<ES>(src, t, off / ES, (nbytes - off) / ES, lane);
+}
+
+// ---------------------------------------------------------------------- dependencies
+__device__ __forceinline__ uint32_t load_relaxed(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waits until every dependency of the tile is satisfied. Returns false if the watchdog
+// fired here or another wavefront recorded an error.
+__device__ __forceinline__ bool wait_deps(const Dep* deps, uint32_t ndep, uint32_t k, uint32_t* state, ErrorRecord* err,
+                          uint64_t timeout, uint32_t desc, uint32_t tile) {
+    for (uint32_t i = 0; i < ndep; ++i) {
+        const uint32_t kind = uni(deps[i].kind);
+        const uint32_t expected = uni(deps[i].expected);
+        const uint32_t word = uni(deps[i].state) + (kind == DEP_TILE ? k : 0u);
+        const uint32_t* w = state + word;
+        if (load_relaxed(w) >= expected) continue;
+        const uint64_t t0 = wall_clock64();
+        while (load_relaxed(w) < expected) {
+            if (load_relaxed(&err->code) != 0u) return false;
+            if (wall_clock64() - t0 > timeout) {
+                if (__lane_id() == 0) {
+                    uint32_t zero = 0;
+                    if (__hip_atomic_compare_exchange_strong(&err->code, &zero, 1u, __ATOMIC_RELAXED,
+                                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                        __hip_atomic_store(&err->desc, desc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(&err->tile, tile, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                }
+                return false;
+            }
+            __builtin_amdgcn_s_sleep(2);
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    return true;
+}
+
+// ----------------------------------------------------------------------- the kernel
+// Runs tile `t`. Returns false when a dependency wait failed.
+struct Shared {
+    uint32_t* state;
+    ErrorRecord* error;
+    uint64_t timeout;
+};
+
+// Kernel specialisations: a program whose reductions all share one plain signature with SUM
+// runs on the kernel built for that signature (only that path is compiled in, so registers
+// are allocated for it alone); copy-only programs, and everything else, have their own.
+template <int KIND>
+__device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, const ProgramHeader& h, uint32_t t,
+                                         uint32_t lane, const uint64_t* bufs) {
+    const uint32_t d = uni(((const uint32_t*)(prog + h.off_tile_desc))[t]);
+    const Desc* D = (const Desc*)(prog + h.off_desc) + d;
+    const uint32_t op = uni(D->op);
+    const uint32_t flags = uni(D->flags);
+    const uint32_t ndep = uni(D->ndep);
+    const uint32_t k = t - uni(D->tile0);
+    const uint64_t te = uni(D->tile_elems);
+    const uint64_t nelem = uni64(D->nelem);
+    const uint64_t e0 = (uint64_t)k * te;
+    const uint32_t n = (uint32_t)((nelem - e0 < te) ? (nelem - e0) : te);
+
+    if (ndep) {
+        const Dep* deps = (const Dep*)(prog + h.off_dep) + uni(D->dep);
+        if (!wait_deps(deps, ndep, k, a.state, a.error, a.timeout, d, t)) return false;
+    }
+
+    if (op != OP_NOOP) {
+        TileOps ops;
+        ops.nsrc = uni(D->nsrc);
+        ops.ndst = uni(D->ndst);
+        ops.group = uni(D->group);
+        const Operand* opl = (const Operand*)(prog + h.off_operand);
+        ops.src = 0;
+        ops.dst = 0;
+        bool misaligned = false;
+        if (lane < ops.nsrc) {
+            Operand o = opl[uni(D->src) + lane];
+            ops.src = bufs[o.buf] + o.offset + e0 * elem_bytes(o.dtype);
+            misaligned |= (ops.src & 15u) != 0;
+        }
+        if (lane < ops.ndst) {
+            Operand o = opl[uni(D->dst) + lane];
+            ops.dst = bufs[o.buf] + o.offset + e0 * elem_bytes(o.dtype);
+            misaligned |= (ops.dst & 15u) != 0;
+        }
+        if (op == OP_REDUCE) {
+            const bool aligned = __ballot(misaligned) == 0ull;
+            if constexpr (KIND == kKindGeneric) {
+                run_reduce(uni(D->sig), uni(D->redop), ops, n, aligned, lane);
+            } else if constexpr (KIND == SIG_BF16) {
+                reduce_tile<DT_BF16, DT_BF16, DT_BF16, RO_SUM>(ops, n, aligned, lane);
+            } else if constexpr (KIND == SIG_FP16) {
+                reduce_tile<DT_FP16, DT_FP16, DT_FP16, RO_SUM>(ops, n, aligned, lane);
+            } else if constexpr (KIND == SIG_FP32) {
+                reduce_tile<DT_FP32, DT_FP32, DT_FP32, RO_SUM>(ops, n, aligned, lane);
+            } else if constexpr (KIND == SIG_INT32) {
+                reduce_tile<DT_INT32, DT_INT32, DT_INT32, RO_SUM>(ops, n, aligned, lane);
+            }
+        } else {
+            const uint32_t es = elem_bytes(uni(opl[uni(D->src)].dtype));
+            if (es == 2) copy_tile<2>(ops, n, lane);
+            else copy_tile<4>(ops, n, lane);
+        }
+    }
+
+    if (flags) {
+        // make this tile's stores visible device-wide before the signal
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        if (lane == 0) {
+            if (flags & DF_SIGNAL_DESC)
+                __hip_atomic_fetch_add(a.state + kStateDescBase + d, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (flags & DF_SIGNAL_TILE)
+                __hip_atomic_store(a.state + kStateDescBase + h.ndesc + t, 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    return true;
+}
+
+template <int KIND>
+__global__ void __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(4))) hccl_executor(LaunchArgs a) {
+    const uint32_t lane = __lane_id();
+    const uint32_t wave = uni(blockIdx.x * kWavesPerBlock + (threadIdx.x / kWaveSize));
+    const uint8_t* prog = a.prog;
+    ProgramHeader h;
+    h.ndesc = uni(((const ProgramHeader*)prog)->ndesc);
+    h.ntiles = uni(((const ProgramHeader*)prog)->ntiles);
+    h.nstate = uni(((const ProgramHeader*)prog)->nstate);
+    h.off_desc = uni64(((const ProgramHeader*)prog)->off_desc);
+    h.off_operand = uni64(((const ProgramHeader*)prog)->off_operand);
+    h.off_dep = uni64(((const ProgramHeader*)prog)->off_dep);
+    h.off_tile_desc = uni64(((const ProgramHeader*)prog)->off_tile_desc);
+    // the buffer table is indexed per lane, so it is read from the kernel-argument segment
+    const uint64_t* bufs = (const uint64_t*)((const char*)__builtin_amdgcn_kernarg_segment_ptr() +
+                                             offsetof(LaunchArgs, bufs));
+
+    Shared sh;
+    sh.state = a.state;
+    sh.error = a.error;
+    sh.timeout = a.timeout_ticks;
+    const uint32_t nworkers = a.nworkers;
+
+    if (!a.dynamic) {
+        for (uint32_t t = wave; t < h.ntiles; t += nworkers) run_tile<KIND>(sh, prog, h, t, lane, bufs);
+        return;
+    }
+
+    uint32_t* ticket = a.state + kStateTicket;
+    uint32_t mine = 0;
+    if (lane == 0) mine = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t t = uni(__shfl(mine, 0));
+    while (t < h.ntiles) {
+        if (load_relaxed(&a.error->code) != 0u) break;
+        // claim the next ticket now; its latency hides behind this tile's work
+        uint32_t next = 0;
+        if (lane == 0) next = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (!run_tile<KIND>(sh, prog, h, t, lane, bufs)) break;
+        t = uni(__shfl(next, 0));
+    }
+
+    // The last wavefront to finish clears the counters for the next launch.
+    uint32_t prev = 0;
+    if (lane == 0)
+        prev = __hip_atomic_fetch_add(a.state + kStateDone, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    prev = uni(__shfl(prev, 0));
+    if (prev == nworkers - 1) {
+        for (uint32_t i = lane; i < h.nstate; i += kWaveSize)
+            __hip_atomic_store(a.state + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+__global__ void hccl_fill_u32(uint32_t* p, uint64_t n, uint32_t v) {
+    uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; i < n; i += (uint64_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+}  // namespace
+
+int executor_block_threads() { return kBlockThreads; }
+int executor_waves_per_block() { return kWavesPerBlock; }
+
+// kind: a plain signature (SIG_BF16 .. SIG_INT32) for SUM-only programs of that signature,
+// kKindCopyOnly, or anything else for the generic kernel.
+hipError_t launch_executor(const LaunchArgs& a, uint32_t blocks, int kind, hipStream_t stream) {
+    switch (kind) {
+        case SIG_BF16: hipLaunchKernelGGL(hccl_executor<SIG_BF16>, dim3(blocks), dim3(kBlockThreads), 0, stream, a); break;
+        case SIG_FP16: hipLaunchKernelGGL(hccl_executor<SIG_FP16>, dim3(blocks), dim3(kBlockThreads), 0, stream, a); break;
+        case SIG_FP32: hipLaunchKernelGGL(hccl_executor<SIG_FP32>, dim3(blocks), dim3(kBlockThreads), 0, stream, a); break;
+        case SIG_INT32: hipLaunchKernelGGL(hccl_executor<SIG_INT32>, dim3(blocks), dim3(kBlockThreads), 0, stream, a); break;
+        case kKindCopyOnly:
+            hipLaunchKernelGGL(hccl_executor<kKindCopyOnly>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
+            break;
+        default:
+            hipLaunchKernelGGL(hccl_executor<kKindGeneric>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
+            break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_u32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    uint64_t blocks = (n + 255) / 256;
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(hccl_fill_u32, dim3((uint32_t)blocks), dim3(256), 0, stream, p, n, v);
+    return hipGetLastError();
+}
+
+// Resident blocks per CU of the kernel of one kind.
+hipError_t executor_occupancy(int kind, int* blocks_per_cu) {
+    switch (kind) {
+        case SIG_BF16: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<SIG_BF16>, kBlockThreads, 0);
+        case SIG_FP16: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<SIG_FP16>, kBlockThreads, 0);
+        case SIG_FP32: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<SIG_FP32>, kBlockThreads, 0);
+        case SIG_INT32: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<SIG_INT32>, kBlockThreads, 0);
+        case kKindCopyOnly: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindCopyOnly>, kBlockThreads, 0);
+        default: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindGeneric>, kBlockThreads, 0);
+    }
+}
+
+}  // namespace hccl

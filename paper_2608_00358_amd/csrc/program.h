@@ -1,0 +1,164 @@
+// program.h -- the descriptor program shared by the host compiler and the device executor.
+//
+// A program is the single-GPU form of a work packet (paper, Section III-B "Data Path"):
+// a topologically ordered list of steps (descriptors, the analogue of WQEs) with explicit
+// dependency ids. Descriptors refer to buffers by id, never by address, so a compiled
+// program is reused for any buffers of the same shape (work packet caching, Section V-B);
+// the addresses arrive in the kernel arguments of each launch.
+//
+// Buffer ids: 0..P-1 = send buffers, P..2P-1 = receive buffers, 2P = the communicator's
+// FP32 scratch.
+//
+// Each descriptor is cut into tiles of `tile_elems` elements; tiles are numbered globally
+// in descriptor order and handed out to wavefronts by ticket. A tile only waits for tiles
+// with lower numbers, so the wavefront holding the lowest unfinished ticket can always run.
+#pragma once
+
+#include <stdint.h>
+
+namespace hccl {
+
+constexpr uint32_t kProgramMagic = 0x4C434348u;  // "HCCL"
+constexpr uint32_t kProgramVersion = 1;
+constexpr int kMaxOperands = 64;   // sources or destinations of one descriptor (one per lane)
+constexpr int kMaxRanks = 64;
+constexpr int kMaxBuffers = 2 * kMaxRanks + 1;
+constexpr int kVecElems = 8;       // elements per lane per vector step
+constexpr int kWaveSize = 64;
+
+enum Op : uint8_t {
+    OP_COPY = 0,    // byte copy of src[0] to every destination (NMC "A = B")
+    OP_REDUCE = 1,  // fold of all sources in list order, rounded once, to every destination
+    OP_NOOP = 2,    // carries only dependencies (a join)
+};
+
+enum DType : uint8_t { DT_BF16 = 0, DT_FP16 = 1, DT_FP32 = 2, DT_INT32 = 3 };
+enum RedOp : uint8_t { RO_SUM = 0, RO_MAX = 1, RO_MIN = 2 };
+
+enum DepKind : uint32_t {
+    DEP_ALL = 0,   // wait until every tile of the named descriptor has completed
+    DEP_TILE = 1,  // wait until the tile with the same index of the named descriptor has completed
+};
+
+enum DescFlags : uint8_t {
+    DF_SIGNAL_DESC = 1,  // count completed tiles in the descriptor counter (someone waits for DEP_ALL)
+    DF_SIGNAL_TILE = 2,  // set the per-tile flag (someone waits for DEP_TILE)
+};
+
+enum ProgramFlags : uint32_t {
+    PF_HAS_DEPS = 1,     // some descriptor waits; counters must be reset after each launch
+};
+
+inline uint32_t dtype_size(uint32_t dt) { return (dt == DT_BF16 || dt == DT_FP16) ? 2u : 4u; }
+
+struct Operand {        // 16 bytes
+    uint32_t buf;       // buffer id
+    uint32_t dtype;     // element type of this operand
+    uint64_t offset;    // byte offset of element 0 of the descriptor in that buffer
+};
+
+struct Dep {            // 16 bytes
+    uint32_t desc;      // descriptor waited for (lower index than the waiter)
+    uint32_t kind;      // DepKind
+    uint32_t expected;  // counter value that means "done": ntiles of desc (DEP_ALL) or 1 (DEP_TILE)
+    uint32_t state;     // state word: kStateDescBase + desc (DEP_ALL) or the flag of tile 0 of
+                        // desc (DEP_TILE; the waiter adds its own tile index)
+};
+
+// Element-type signatures a REDUCE may have: (type of source 0, type of the other sources,
+// type of the destinations). Chained steps carry FP32 partials next to 16-bit inputs; the
+// two-level schedule folds FP32 partials into a 16-bit result.
+enum Signature : uint8_t {
+    SIG_BF16 = 0, SIG_FP16, SIG_FP32, SIG_INT32,        // (T, T, T)
+    SIG_BF16_TO_F32, SIG_F32_BF16_TO_F32, SIG_F32_BF16_TO_BF16, SIG_F32_TO_BF16,
+    SIG_FP16_TO_F32, SIG_F32_FP16_TO_F32, SIG_F32_FP16_TO_FP16, SIG_F32_TO_FP16,
+    SIG_COUNT,
+    SIG_INVALID = 255,
+};
+
+// Executor kernel specialisations ("kinds"): a plain signature id for programs whose
+// reductions all have that signature and SUM, or one of these two.
+constexpr int kKindCopyOnly = SIG_COUNT;     // no reductions at all
+constexpr int kKindGeneric = SIG_COUNT + 1;  // anything else
+constexpr int kNumKinds = SIG_COUNT + 2;
+
+inline uint8_t reduce_signature(uint32_t t0, uint32_t tr, uint32_t to) {
+    if (t0 == tr && tr == to) return (uint8_t)t0;  // DT_* and SIG_* plain ids coincide
+    for (uint32_t h = DT_BF16; h <= DT_FP16; ++h) {
+        uint8_t base = (h == DT_BF16) ? SIG_BF16_TO_F32 : SIG_FP16_TO_F32;
+        if (t0 == h && tr == h && to == DT_FP32) return base;
+        if (t0 == DT_FP32 && tr == h && to == DT_FP32) return base + 1;
+        if (t0 == DT_FP32 && tr == h && to == h) return base + 2;
+        if (t0 == DT_FP32 && tr == DT_FP32 && to == h) return base + 3;
+    }
+    return SIG_INVALID;
+}
+
+struct Desc {           // 64 bytes
+    uint8_t op;
+    uint8_t redop;
+    uint8_t flags;
+    uint8_t sig;        // Signature of a REDUCE
+    uint16_t nsrc;
+    uint16_t ndst;
+    uint16_t group;     // fold order: 0 = ascending over all sources; L = ascending inside
+                        // each run of L sources into an FP32 partial, then over the partials
+    uint16_t ndep;
+    uint32_t src;       // index of the first source operand
+    uint32_t dst;       // index of the first destination operand
+    uint32_t dep;       // index of the first dependency
+    uint32_t tile0;     // global number of this descriptor's first tile
+    uint32_t ntiles;
+    uint32_t tile_elems;
+    uint64_t nelem;
+    uint32_t pad1[4];
+};
+static_assert(sizeof(Desc) == 64, "descriptor layout");
+static_assert(sizeof(Operand) == 16, "operand layout");
+static_assert(sizeof(Dep) == 16, "dependency layout");
+
+// Device image: header, then the arrays at the offsets the header records (16-byte aligned).
+struct ProgramHeader {
+    uint32_t magic;
+    uint32_t version;
+    uint32_t ndesc;
+    uint32_t ntiles;
+    uint32_t noperand;
+    uint32_t ndep;
+    uint32_t flags;
+    uint32_t nstate;       // u32 words of device state (2 + ndesc + ntiles when PF_HAS_DEPS)
+    uint64_t off_desc;
+    uint64_t off_operand;
+    uint64_t off_dep;
+    uint64_t off_tile_desc;  // u32 per tile: the descriptor that owns it
+    uint64_t total_bytes;
+    uint64_t scratch_bytes;
+};
+
+// Device state words: [0] ticket counter, [1] finished-wavefront counter, then one tile
+// counter per descriptor, then one flag per tile. All zero between launches.
+constexpr uint32_t kStateTicket = 0;
+constexpr uint32_t kStateDone = 1;
+constexpr uint32_t kStateDescBase = 2;
+
+// Device-side error record (per communicator).
+struct ErrorRecord {
+    uint32_t code;   // 0 = none, 1 = dependency wait timed out
+    uint32_t desc;
+    uint32_t tile;
+    uint32_t pad;
+};
+
+// Kernel arguments of one executor launch.
+struct LaunchArgs {
+    const uint8_t* prog;     // device image (ProgramHeader first)
+    uint32_t* state;         // nstate words
+    ErrorRecord* error;
+    uint32_t nworkers;       // wavefronts in the grid
+    uint32_t dynamic;        // 1 = tiles by atomic ticket (always when PF_HAS_DEPS);
+                             // 0 = wavefront w runs tiles w, w + nworkers, ... (no state used)
+    uint64_t timeout_ticks;  // watchdog for one dependency wait, in wall-clock counter ticks
+    char* bufs[kMaxBuffers];
+};
+
+}  // namespace hccl

@@ -1,0 +1,250 @@
+"""ctypes binding of libhccl.so: argument marshalling only.
+
+Every function here has the name of the C entry point it calls and turns Python arguments
+(torch tensors or raw device addresses, strings for enums) into the C arguments. All
+collective work runs in the HIP library; if the library is not built, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "lib", "libhccl.so")
+
+DTYPES = {"bf16": 0, "fp16": 1, "fp32": 2, "int32": 3}
+OPS = {"sum": 0, "max": 1, "min": 2}
+ALGOS = {"auto": 0, "direct": 1, "ring": 2, "two_level": 3}
+RESULTS = {0: "hcclSuccess", 1: "hcclInvalidArgument", 2: "hcclUnsupported", 3: "hcclHipError",
+           4: "hcclOutOfMemory", 5: "hcclTimeout", 6: "hcclInternalError"}
+NO_DEVICE = -1
+MAX_RANKS = 64
+
+# Every symbol include/hccl.h declares.
+EXPORTS = [
+    "hccl_config_init", "hccl_comm_create", "hccl_comm_destroy", "hccl_comm_set_config",
+    "hccl_allreduce", "hccl_reduce_scatter", "hccl_allgather", "hccl_alltoallv",
+    "hccl_get_last_error", "hccl_result_string", "hccl_get_async_error", "hccl_comm_last_program",
+]
+
+
+class HcclError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{RESULTS.get(code, code)}: {message}")
+        self.code = code
+
+
+class hcclConfig_t(ctypes.Structure):
+    _fields_ = [
+        ("algo", ctypes.c_int32), ("group_size", ctypes.c_int32), ("chunk_bytes", ctypes.c_uint64),
+        ("fuse", ctypes.c_int32), ("max_workers", ctypes.c_int32), ("tile_bytes", ctypes.c_uint32),
+        ("timeout_ms", ctypes.c_uint32), ("validate", ctypes.c_int32), ("reserved", ctypes.c_int32 * 5),
+    ]
+
+
+class hcclProgramInfo_t(ctypes.Structure):
+    _fields_ = [
+        ("collective", ctypes.c_int32), ("algo", ctypes.c_int32), ("fused", ctypes.c_int32),
+        ("cache_hit", ctypes.c_int32), ("num_descs", ctypes.c_uint32), ("num_tiles", ctypes.c_uint32),
+        ("num_deps", ctypes.c_uint32), ("num_operands", ctypes.c_uint32), ("workers", ctypes.c_uint32),
+        ("max_srcs", ctypes.c_uint32), ("bytes_read", ctypes.c_uint64), ("bytes_written", ctypes.c_uint64),
+        ("scratch_bytes", ctypes.c_uint64), ("program_bytes", ctypes.c_uint64), ("compile_us", ctypes.c_double),
+    ]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Loads libhccl.so (built by ``__graft_entry__.build()``); raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run __graft_entry__.build() first "
+                           "(the collectives exist only as HIP code)")
+    lib = ctypes.CDLL(path)
+    vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+    vpp = ctypes.POINTER(ctypes.c_void_p)
+    szp = ctypes.POINTER(ctypes.c_size_t)
+    res = ctypes.c_int
+    lib.hccl_config_init.argtypes = [ctypes.POINTER(hcclConfig_t)]
+    lib.hccl_comm_create.argtypes = [i32, i32, ctypes.POINTER(hcclConfig_t), ctypes.POINTER(vp)]
+    lib.hccl_comm_destroy.argtypes = [vp]
+    lib.hccl_comm_set_config.argtypes = [vp, ctypes.POINTER(hcclConfig_t)]
+    lib.hccl_allreduce.argtypes = [vp, vpp, vpp, sz, i32, i32, vp]
+    lib.hccl_reduce_scatter.argtypes = [vp, vpp, vpp, sz, i32, i32, vp]
+    lib.hccl_allgather.argtypes = [vp, vpp, vpp, sz, i32, vp]
+    lib.hccl_alltoallv.argtypes = [vp, vpp, szp, szp, vpp, szp, szp, i32, vp]
+    lib.hccl_get_last_error.argtypes = []
+    lib.hccl_get_last_error.restype = ctypes.c_char_p
+    lib.hccl_result_string.argtypes = [i32]
+    lib.hccl_result_string.restype = ctypes.c_char_p
+    lib.hccl_get_async_error.argtypes = [vp]
+    lib.hccl_comm_last_program.argtypes = [vp, ctypes.POINTER(hcclProgramInfo_t)]
+    for name in EXPORTS:
+        if name not in ("hccl_get_last_error", "hccl_result_string"):
+            getattr(lib, name).restype = res
+    _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise HcclError(rc, load().hccl_get_last_error().decode())
+
+
+def _addr(x) -> int:
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _ptr_array(bufs: Sequence) -> ctypes.Array:
+    return (ctypes.c_void_p * len(bufs))(*[_addr(b) for b in bufs])
+
+
+def _size_array(a) -> ctypes.Array:
+    flat = [int(v) for v in (a.reshape(-1).tolist() if hasattr(a, "reshape") else a)]
+    return (ctypes.c_size_t * len(flat))(*flat)
+
+
+def _dtype_code(dtype) -> int:
+    if isinstance(dtype, str):
+        return DTYPES[dtype]
+    if isinstance(dtype, int):
+        return dtype
+    import torch
+
+    table = {torch.bfloat16: 0, torch.float16: 1, torch.float32: 2, torch.int32: 3}
+    if dtype not in table:
+        raise TypeError(f"unsupported element type {dtype}")
+    return table[dtype]
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+
+        if torch.cuda.is_available():
+            return torch.cuda.current_stream().cuda_stream
+        return None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def hccl_config_init(**kw) -> hcclConfig_t:
+    cfg = hcclConfig_t()
+    _check(load().hccl_config_init(ctypes.byref(cfg)))
+    for k, v in kw.items():
+        if k == "algo" and isinstance(v, str):
+            v = ALGOS[v]
+        setattr(cfg, k, int(v))
+    return cfg
+
+
+def hccl_comm_create(nranks: int, device: int = 0, cfg: Optional[hcclConfig_t] = None) -> ctypes.c_void_p:
+    comm = ctypes.c_void_p()
+    _check(load().hccl_comm_create(nranks, device, ctypes.byref(cfg) if cfg is not None else None,
+                                   ctypes.byref(comm)))
+    return comm
+
+
+def hccl_comm_destroy(comm) -> None:
+    _check(load().hccl_comm_destroy(comm))
+
+
+def hccl_comm_set_config(comm, cfg: hcclConfig_t) -> None:
+    _check(load().hccl_comm_set_config(comm, ctypes.byref(cfg)))
+
+
+def hccl_allreduce(comm, sendbufs, recvbufs, count: int, dtype, op: str = "sum", stream=None) -> None:
+    _check(load().hccl_allreduce(comm, _ptr_array(sendbufs), _ptr_array(recvbufs), count, _dtype_code(dtype),
+                                 OPS[op], _stream_handle(stream)))
+
+
+def hccl_reduce_scatter(comm, sendbufs, recvbufs, recvcount: int, dtype, op: str = "sum", stream=None) -> None:
+    _check(load().hccl_reduce_scatter(comm, _ptr_array(sendbufs), _ptr_array(recvbufs), recvcount,
+                                      _dtype_code(dtype), OPS[op], _stream_handle(stream)))
+
+
+def hccl_allgather(comm, sendbufs, recvbufs, sendcount: int, dtype, stream=None) -> None:
+    _check(load().hccl_allgather(comm, _ptr_array(sendbufs), _ptr_array(recvbufs), sendcount,
+                                 _dtype_code(dtype), _stream_handle(stream)))
+
+
+def hccl_alltoallv(comm, sendbufs, sendcounts, sdispls, recvbufs, recvcounts, rdispls, dtype, stream=None) -> None:
+    _check(load().hccl_alltoallv(comm, _ptr_array(sendbufs), _size_array(sendcounts), _size_array(sdispls),
+                                 _ptr_array(recvbufs), _size_array(recvcounts), _size_array(rdispls),
+                                 _dtype_code(dtype), _stream_handle(stream)))
+
+
+def hccl_get_last_error() -> str:
+    return load().hccl_get_last_error().decode()
+
+
+def hccl_result_string(code: int) -> str:
+    return load().hccl_result_string(code).decode()
+
+
+def hccl_get_async_error(comm) -> int:
+    """Returns the result code (0 = no device-side error since the last call)."""
+    return int(load().hccl_get_async_error(comm))
+
+
+def hccl_comm_last_program(comm) -> dict:
+    info = hcclProgramInfo_t()
+    _check(load().hccl_comm_last_program(comm, ctypes.byref(info)))
+    return {name: getattr(info, name) for name, _ in hcclProgramInfo_t._fields_}
+
+
+class Comm:
+    """Convenience owner of one communicator; methods take lists of torch tensors."""
+
+    def __init__(self, nranks: int, device: int = 0, **cfg):
+        self.nranks = nranks
+        self.device = device
+        self.cfg = hccl_config_init(**cfg)
+        self.handle = hccl_comm_create(nranks, device, self.cfg)
+
+    def close(self):
+        if self.handle is not None:
+            hccl_comm_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+        return False
+
+    def set_config(self, **cfg):
+        self.cfg = hccl_config_init(**cfg)
+        hccl_comm_set_config(self.handle, self.cfg)
+
+    def allreduce(self, send, recv, op="sum", stream=None):
+        hccl_allreduce(self.handle, send, recv, send[0].numel(), send[0].dtype, op, stream)
+
+    def reduce_scatter(self, send, recv, op="sum", stream=None):
+        hccl_reduce_scatter(self.handle, send, recv, recv[0].numel(), send[0].dtype, op, stream)
+
+    def allgather(self, send, recv, stream=None):
+        hccl_allgather(self.handle, send, recv, send[0].numel(), send[0].dtype, stream)
+
+    def alltoallv(self, send, sendcounts, sdispls, recv, recvcounts, rdispls, stream=None):
+        hccl_alltoallv(self.handle, send, sendcounts, sdispls, recv, recvcounts, rdispls, send[0].dtype, stream)
+
+    def last_program(self) -> dict:
+        return hccl_comm_last_program(self.handle)
+
+    def async_error(self) -> int:
+        return hccl_get_async_error(self.handle)

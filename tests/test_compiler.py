@@ -1,0 +1,210 @@
+"""Host logic: lowering, fusion, packing and validation of descriptor programs.
+
+These run on host-only communicators (device = HCCL_NO_DEVICE): a collective call checks its
+arguments, compiles the program and runs the validator (dependency order, bounds, races under
+the dependency closure, scratch read-after-write, exact output coverage), then returns
+without touching memory. No GPU is needed.
+"""
+import numpy as np
+import pytest
+
+import paper_2608_00358_amd as H
+from workloads import alltoallv_layout, zipf_counts
+
+ES = {"bf16": 2, "fp16": 2, "fp32": 4, "int32": 4}
+GiB = 1 << 30
+
+
+def fake_bufs(P, base):
+    # distinct, 4 KiB aligned, far apart: never dereferenced on a host-only communicator
+    return [base + i * (1 << 36) for i in range(P)]
+
+
+def comm(P, **cfg):
+    return H.Comm(P, device=H.NO_DEVICE, **cfg)
+
+
+def info_of(c):
+    return c.last_program()
+
+
+def ceil_div(a, b):
+    return -(-a // b)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "fp32", "int32", "fp16"])
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_reduce_scatter_ring_structure(dt, P, fuse):
+    M = 3 * 4096 + 17
+    chunk = 8192
+    with comm(P, algo="ring", fuse=fuse, chunk_bytes=chunk) as c:
+        H.hccl_reduce_scatter(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), M, dt)
+        info = info_of(c)
+    C = chunk // ES[dt]
+    chains = P * ceil_div(M, C)
+    if fuse or P <= 2:
+        assert info["num_descs"] == chains * (1 if P <= 2 or fuse else P - 1)
+    else:
+        assert info["num_descs"] == chains * (P - 1)
+    if fuse:
+        assert info["num_deps"] == 0 and info["max_srcs"] == P
+        assert info["bytes_read"] == P * P * M * ES[dt]
+        assert info["bytes_written"] == P * M * ES[dt]
+        assert info["scratch_bytes"] == 0
+
+
+@pytest.mark.parametrize("algo", ["direct", "ring"])
+@pytest.mark.parametrize("P", [1, 2, 4, 5])
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_allreduce_structure_and_minimal_traffic_when_fused(algo, P, fuse):
+    N = 100003
+    dt = "bf16"
+    with comm(P, algo=algo, fuse=fuse, chunk_bytes=65536) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, dt)
+        info = info_of(c)
+    if fuse or algo == "direct":
+        assert info["num_deps"] == 0
+        assert info["bytes_read"] == P * N * 2 and info["bytes_written"] == P * N * 2
+    elif P > 1:
+        assert info["num_deps"] > 0 and info["bytes_read"] > P * N * 2
+
+
+def test_allreduce_in_place_is_validated_with_aliasing():
+    P, N = 4, 50000
+    bufs = fake_bufs(P, 1 << 40)
+    for fuse in (0, 1):
+        with comm(P, algo="ring", fuse=fuse, chunk_bytes=16384) as c:
+            H.hccl_allreduce(c.handle, bufs, bufs, N, "fp32")
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_allgather_ring_fuses_to_one_copy_per_chunk(P, fuse):
+    M = 70001
+    with comm(P, algo="ring", fuse=fuse, chunk_bytes=65536) as c:
+        H.hccl_allgather(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), M, "bf16")
+        info = info_of(c)
+    chunks = ceil_div(M, 65536 // 2)
+    if fuse:
+        assert info["num_descs"] == P * chunks and info["num_deps"] == 0
+        assert info["bytes_read"] == P * M * 2 and info["bytes_written"] == P * P * M * 2
+    else:
+        assert info["num_descs"] == P * P * chunks
+
+
+@pytest.mark.parametrize("L,G", [(8, 8), (2, 4), (4, 2), (1, 4), (4, 1)])
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_two_level_structure(L, G, fuse):
+    P = L * G
+    N = 1 << 16
+    with comm(P, algo="two_level", group_size=L, fuse=fuse, chunk_bytes=16384) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "bf16")
+        info = info_of(c)
+    assert info["algo"] == 3
+    if fuse:
+        assert info["num_deps"] == 0 and info["scratch_bytes"] == 0
+        assert info["bytes_read"] == P * N * 2 and info["bytes_written"] == P * N * 2
+        assert info["max_srcs"] == P
+    else:
+        assert info["scratch_bytes"] == G * N * 4
+
+
+def test_auto_picks_two_level_when_group_size_splits_ranks():
+    with comm(16, group_size=4) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(16, 1 << 40), fake_bufs(16, 1 << 44), 4096, "bf16")
+        assert info_of(c)["algo"] == 3
+    with comm(16, group_size=5) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(16, 1 << 40), fake_bufs(16, 1 << 44), 4096, "bf16")
+        assert info_of(c)["algo"] == 2
+
+
+def test_alltoallv_zipf_layout_compiles_and_counts_bytes():
+    P, R, D = 8, 1 << 12, 128
+    counts = zipf_counts(P, R, 1.1, seed=0)
+    lay = alltoallv_layout(counts, D)
+    chunk = 1 << 16
+    with comm(P, chunk_bytes=chunk) as c:
+        H.hccl_alltoallv(c.handle, fake_bufs(P, 1 << 40), lay["sendcounts"], lay["sdispls"],
+                         fake_bufs(P, 1 << 44), lay["recvcounts"], lay["rdispls"], "bf16")
+        info = info_of(c)
+    total = int(lay["sendcounts"].sum()) * 2
+    assert info["bytes_read"] == total and info["bytes_written"] == total
+    pieces = sum(ceil_div(int(n) * 2, chunk) for n in lay["sendcounts"].reshape(-1) if n)
+    assert info["num_descs"] == pieces
+
+
+def test_program_cache_reuses_compiled_programs():
+    with comm(4) as c:
+        s, r = fake_bufs(4, 1 << 40), fake_bufs(4, 1 << 44)
+        H.hccl_allreduce(c.handle, s, r, 1000, "fp32")
+        assert info_of(c)["cache_hit"] == 0
+        H.hccl_allreduce(c.handle, fake_bufs(4, 1 << 41), fake_bufs(4, 1 << 45), 1000, "fp32")
+        assert info_of(c)["cache_hit"] == 1       # other buffers, same shape: cached
+        H.hccl_allreduce(c.handle, s, r, 1001, "fp32")
+        assert info_of(c)["cache_hit"] == 0
+
+
+# ----------------------------------------------------------------------- error paths
+def _expect(code, fn, *args):
+    with pytest.raises(H.HcclError) as e:
+        fn(*args)
+    assert e.value.code == code, str(e.value)
+
+
+def test_rejects_overlapping_buffers_and_partial_in_place():
+    P = 4
+    with comm(P) as c:
+        s = fake_bufs(P, 1 << 40)
+        r = list(s)
+        r[1] = s[1] + 8
+        _expect(1, H.hccl_allreduce, c.handle, s, r, 1000, "fp32")
+        r2 = fake_bufs(P, 1 << 44)
+        r2[2] = s[2]
+        _expect(1, H.hccl_allreduce, c.handle, s, r2, 1000, "fp32")
+        _expect(1, H.hccl_reduce_scatter, c.handle, s, s, 1000, "fp32")
+
+
+def test_rejects_misaligned_and_null_buffers():
+    P = 2
+    with comm(P) as c:
+        s, r = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+        s[0] += 2
+        _expect(1, H.hccl_allreduce, c.handle, s, r, 100, "fp32")
+        s, r = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+        r[1] = 0
+        _expect(1, H.hccl_allreduce, c.handle, s, r, 100, "fp32")
+
+
+def test_rejects_bad_enums():
+    with comm(2) as c:
+        s, r = fake_bufs(2, 1 << 40), fake_bufs(2, 1 << 44)
+        _expect(1, H.hccl_allreduce, c.handle, s, r, 100, 7)
+
+
+def test_alltoallv_rejects_inconsistent_counts_and_overlapping_receive_ranges():
+    P = 3
+    counts = np.array([[1, 2, 3], [4, 5, 6], [7, 8, 9]])
+    lay = alltoallv_layout(counts)
+    with comm(P) as c:
+        s, r = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+        bad = lay["recvcounts"].copy()
+        bad[0, 2] += 1
+        _expect(1, H.hccl_alltoallv, c.handle, s, lay["sendcounts"], lay["sdispls"], r, bad, lay["rdispls"], "fp32")
+        rd = lay["rdispls"].copy()
+        rd[1, 1] = rd[1, 0]
+        _expect(1, H.hccl_alltoallv, c.handle, s, lay["sendcounts"], lay["sdispls"], r, lay["recvcounts"], rd, "fp32")
+
+
+def test_two_level_rejected_for_reduce_scatter():
+    with comm(4, algo="two_level", group_size=2) as c:
+        _expect(2, H.hccl_reduce_scatter, c.handle, fake_bufs(4, 1 << 40), fake_bufs(4, 1 << 44), 10, "fp32")
+
+
+def test_empty_collectives_compile_to_nothing():
+    with comm(4) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(4, 1 << 40), fake_bufs(4, 1 << 44), 0, "bf16")
+        assert info_of(c)["num_tiles"] == 0
+        z = np.zeros((4, 4), dtype=np.int64)
+        H.hccl_alltoallv(c.handle, fake_bufs(4, 1 << 40), z, z, fake_bufs(4, 1 << 44), z, z, "bf16")
+        assert info_of(c)["num_tiles"] == 0

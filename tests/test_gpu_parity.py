@@ -1,0 +1,260 @@
+"""GPU parity: the HIP executor against the CPU oracle, bit for bit, through the C-ABI.
+
+Inputs come from the seeded generators; expected values come from the oracle only. Sizes span
+several tiles (small tiles are forced where needed) and ragged tails; every output buffer has
+poison guard bands that must survive.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_00358_amd as H
+from gpu_helpers import Guarded, same_bits, first_mismatch, to_device, to_host
+from workloads import alltoallv_layout, normal_bf16, normal_f32, row_ids_int32, uniform_f32, zipf_counts
+
+pytestmark = pytest.mark.gpu
+
+DT_ES = {"bf16": 2, "fp16": 2, "fp32": 4, "int32": 4}
+
+
+def inputs(P, N, dt, seed):
+    if dt == "fp32":
+        return uniform_f32(P, N, seed=seed)
+    if dt == "bf16":
+        return normal_bf16(P, N, std=2.0, seed=seed)
+    if dt == "fp16":
+        return normal_f32(P, N, std=8.0, seed=seed).astype(np.float16).view(np.uint16)
+    rng = np.random.default_rng(seed)
+    return rng.integers(-2 ** 31, 2 ** 31, size=(P, N), dtype=np.int64).astype(np.int32)
+
+
+def run_allreduce(P, N, dt, op="sum", in_place=False, seed=0, **cfg):
+    x = inputs(P, N, dt, seed)
+    print(f"allreduce P={P} N={N} dt={dt} op={op} in_place={in_place} cfg={cfg}", flush=True)
+    with H.Comm(P, device=0, **cfg) as c:
+        if in_place:
+            bufs = [Guarded(N, dt, fill=x[r]) for r in range(P)]
+            H.hccl_allreduce(c.handle, [b.view for b in bufs], [b.view for b in bufs], N, dt, op)
+            outs = bufs
+        else:
+            send = [to_device(x[r], dt) for r in range(P)]
+            outs = [Guarded(N, dt) for _ in range(P)]
+            H.hccl_allreduce(c.handle, send, [o.view for o in outs], N, dt, op)
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+        info = c.last_program()
+    want = oracle.allreduce(x, dt, op=op, group=cfg.get("group_size", 0) if cfg.get("algo") == "two_level" else 0)
+    for r in range(P):
+        got = outs[r].result()
+        assert same_bits(got, want[r], dt), f"rank {r}: {first_mismatch(got, want[r])}"
+        assert outs[r].guards_intact(), f"rank {r}: guard band overwritten"
+    return info
+
+
+@pytest.mark.parametrize("dt", ["fp32", "bf16", "fp16", "int32"])
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("algo,fuse", [("direct", 1), ("ring", 1), ("ring", 0)])
+def test_allreduce_matches_oracle(dt, P, algo, fuse):
+    # 12345 elements with 4 KiB tiles: many tiles, a ragged vector tail and single elements
+    run_allreduce(P, 12345, dt, algo=algo, fuse=fuse, chunk_bytes=8192, tile_bytes=4096)
+
+
+@pytest.mark.parametrize("N", [1, 7, 8, 9, 511, 513, 4096])
+def test_allreduce_small_and_ragged_sizes(N):
+    run_allreduce(4, N, "bf16", algo="ring", fuse=1, tile_bytes=4096)
+    run_allreduce(3, N, "fp32", algo="ring", fuse=0, chunk_bytes=256, tile_bytes=4096)
+
+
+@pytest.mark.parametrize("fuse", [0, 1])
+@pytest.mark.parametrize("dt", ["bf16", "fp32"])
+def test_allreduce_in_place(fuse, dt):
+    run_allreduce(5, 20011, dt, in_place=True, algo="ring", fuse=fuse, chunk_bytes=4096, tile_bytes=4096)
+
+
+@pytest.mark.parametrize("op", ["max", "min"])
+@pytest.mark.parametrize("dt", ["fp32", "bf16", "int32"])
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_allreduce_max_min(op, dt, fuse):
+    run_allreduce(6, 9999, dt, op=op, algo="ring", fuse=fuse, chunk_bytes=4096, tile_bytes=4096)
+
+
+@pytest.mark.parametrize("L,G", [(4, 4), (8, 8), (2, 3), (1, 4), (4, 1)])
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_two_level_allreduce_matches_tree_order_oracle(L, G, fuse):
+    run_allreduce(L * G, 20000, "bf16", algo="two_level", group_size=L, fuse=fuse, chunk_bytes=8192,
+                  tile_bytes=8192)
+
+
+def run_reduce_scatter(P, M, dt, op="sum", seed=1, **cfg):
+    x = inputs(P, P * M, dt, seed)
+    print(f"reduce_scatter P={P} M={M} dt={dt} cfg={cfg}", flush=True)
+    with H.Comm(P, device=0, **cfg) as c:
+        send = [to_device(x[r], dt) for r in range(P)]
+        outs = [Guarded(M, dt) for _ in range(P)]
+        H.hccl_reduce_scatter(c.handle, send, [o.view for o in outs], M, dt, op)
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+    want = oracle.reduce_scatter(x, dt, op=op)
+    for r in range(P):
+        got = outs[r].result()
+        assert same_bits(got, want[r], dt), f"rank {r}: {first_mismatch(got, want[r])}"
+        assert outs[r].guards_intact()
+
+
+@pytest.mark.parametrize("dt", ["fp32", "bf16", "fp16", "int32"])
+@pytest.mark.parametrize("P", [1, 2, 5, 8])
+@pytest.mark.parametrize("algo,fuse", [("direct", 1), ("ring", 1), ("ring", 0)])
+def test_reduce_scatter_matches_oracle(dt, P, algo, fuse):
+    run_reduce_scatter(P, 3001, dt, algo=algo, fuse=fuse, chunk_bytes=2048, tile_bytes=4096)
+
+
+def run_allgather(P, M, dt, seed=2, **cfg):
+    x = inputs(P, M, dt, seed)
+    print(f"allgather P={P} M={M} dt={dt} cfg={cfg}", flush=True)
+    with H.Comm(P, device=0, **cfg) as c:
+        send = [to_device(x[r], dt) for r in range(P)]
+        outs = [Guarded(P * M, dt) for _ in range(P)]
+        H.hccl_allgather(c.handle, send, [o.view for o in outs], M, dt)
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+    want = oracle.allgather(x)
+    for r in range(P):
+        got = outs[r].result()
+        assert np.array_equal(got.view(np.uint8), want[r].view(np.uint8)), f"rank {r}"
+        assert outs[r].guards_intact()
+
+
+@pytest.mark.parametrize("dt", ["bf16", "fp32"])
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("M", [1, 5, 1000, 40001])
+@pytest.mark.parametrize("algo,fuse", [("direct", 1), ("ring", 0)])
+def test_allgather_matches_oracle(dt, P, M, algo, fuse):
+    run_allgather(P, M, dt, algo=algo, fuse=fuse, chunk_bytes=8192, tile_bytes=4096)
+
+
+def run_alltoallv(P, counts, elems_per_row, dt, seed=3, gap=0, **cfg):
+    lay = alltoallv_layout(counts, elems_per_row)
+    rdispls = lay["rdispls"].copy()
+    recv_len = lay["recv_len"].copy()
+    if gap:
+        # receive blocks separated by `gap` untouched elements
+        for d in range(P):
+            off = gap
+            for s in range(P):
+                rdispls[d, s] = off
+                off += lay["recvcounts"][d, s] + gap
+            recv_len[d] = off
+    rng = np.random.default_rng(seed)
+    send_host = []
+    for s in range(P):
+        n = int(lay["send_len"][s])
+        if dt == "int32":
+            send_host.append(rng.integers(-2 ** 31, 2 ** 31, size=n, dtype=np.int64).astype(np.int32))
+        else:
+            send_host.append(rng.integers(0, 2 ** 16, size=n, dtype=np.int64).astype(np.uint16))
+    print(f"alltoallv P={P} rows={counts.sum()} elems/row={elems_per_row} dt={dt} gap={gap} cfg={cfg}", flush=True)
+    with H.Comm(P, device=0, **cfg) as c:
+        send = [to_device(send_host[s], dt) for s in range(P)]
+        outs = [Guarded(int(recv_len[d]), dt) for d in range(P)]
+        H.hccl_alltoallv(c.handle, send, lay["sendcounts"], lay["sdispls"], [o.view for o in outs],
+                         lay["recvcounts"], rdispls, dt)
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+    expect = [o.host_init[64:64 + o.n].copy() for o in outs]
+    oracle.alltoallv(send_host, lay["sendcounts"], lay["sdispls"], expect, lay["recvcounts"], rdispls)
+    for d in range(P):
+        got = outs[d].result()
+        assert np.array_equal(got.view(np.uint8), expect[d].view(np.uint8)), f"dst {d}"
+        assert outs[d].guards_intact()
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("gap", [0, 3])
+def test_alltoallv_embedding_rows_and_ids(P, gap):
+    counts = zipf_counts(P, 3000, 1.1, seed=P)
+    run_alltoallv(P, counts, 128, "bf16", gap=gap, chunk_bytes=65536, tile_bytes=16384)
+    run_alltoallv(P, counts, 1, "int32", gap=gap, chunk_bytes=4096, tile_bytes=4096)
+
+
+def test_alltoallv_zero_blocks_and_odd_row_widths():
+    P = 5
+    rng = np.random.default_rng(7)
+    counts = rng.integers(0, 40, size=(P, P))
+    counts[0, :] = 0
+    counts[:, 3] = 0
+    for elems in (1, 3, 7, 8, 9):
+        run_alltoallv(P, counts, elems, "bf16", gap=1, chunk_bytes=512, tile_bytes=4096)
+        run_alltoallv(P, counts, elems, "int32", gap=2, chunk_bytes=512, tile_bytes=4096)
+
+
+def test_special_values_follow_the_oracle():
+    P, N = 4, 4096
+    rng = np.random.default_rng(11)
+    specials = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 1e-45, -1e-45, 1.17549435e-38,
+                         3.4028235e38, -3.4028235e38, 65504.0, 65520.0, 6e-8, 1.0, -1.0], np.float32)
+    x32 = specials[rng.integers(0, specials.size, size=(P, N))]
+    print("special values fp32/bf16/fp16", flush=True)
+    for dt, bits in (("fp32", x32), ("bf16", oracle.f32_to_bf16(x32)), ("fp16", oracle.f32_to_f16(x32))):
+        with H.Comm(P, device=0, algo="direct", tile_bytes=4096) as c:
+            send = [to_device(bits[r], dt) for r in range(P)]
+            outs = [Guarded(N, dt) for _ in range(P)]
+            H.hccl_allreduce(c.handle, send, [o.view for o in outs], N, dt)
+            torch.cuda.synchronize()
+        want = oracle.allreduce(bits, dt)
+        for r in range(P):
+            got = outs[r].result()
+            assert same_bits(got, want[r], dt), f"{dt} rank {r}: {first_mismatch(got, want[r])}"
+
+
+def test_fp16_rounding_boundaries_of_the_hardware_conversion():
+    # sums that land on fp16 ties, overflow thresholds and subnormals
+    P = 2
+    rng = np.random.default_rng(12)
+    halves = rng.integers(0, 1 << 16, size=(P, 1 << 16)).astype(np.uint16)
+    halves[0, :] = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    with H.Comm(P, device=0, algo="direct") as c:
+        send = [to_device(halves[r], "fp16") for r in range(P)]
+        outs = [Guarded(1 << 16, "fp16") for _ in range(P)]
+        H.hccl_allreduce(c.handle, send, [o.view for o in outs], 1 << 16, "fp16")
+        torch.cuda.synchronize()
+    want = oracle.allreduce(halves, "fp16")
+    got = outs[0].result()
+    assert same_bits(got, want[0], "fp16"), first_mismatch(got, want[0])
+
+
+def test_repeated_launches_of_a_dependent_program_reset_their_counters():
+    # the unfused ring uses per-tile counters; ten launches in a row must all be right
+    P, N = 8, 65536
+    x = inputs(P, N, "bf16", 21)
+    with H.Comm(P, device=0, algo="ring", fuse=0, chunk_bytes=16384, tile_bytes=8192) as c:
+        send = [to_device(x[r], "bf16") for r in range(P)]
+        outs = [Guarded(N, "bf16") for _ in range(P)]
+        want = oracle.allreduce(x, "bf16")
+        for it in range(10):
+            for o in outs:
+                o.view.zero_()
+            H.hccl_allreduce(c.handle, send, [o.view for o in outs], N, "bf16")
+            torch.cuda.synchronize()
+            assert c.async_error() == 0
+            for r in range(P):
+                assert same_bits(outs[r].result(), want[r], "bf16"), f"launch {it} rank {r}"
+
+
+def test_launches_on_two_streams_are_ordered():
+    P, N = 4, 100000
+    x = inputs(P, N, "fp32", 22)
+    want = oracle.allreduce(x, "fp32")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    with H.Comm(P, device=0, algo="ring", fuse=0, chunk_bytes=16384, tile_bytes=8192) as c:
+        send = [to_device(x[r], "fp32") for r in range(P)]
+        o1 = [Guarded(N, "fp32") for _ in range(P)]
+        o2 = [Guarded(N, "fp32") for _ in range(P)]
+        torch.cuda.synchronize()
+        H.hccl_allreduce(c.handle, send, [o.view for o in o1], N, "fp32", stream=s1)
+        H.hccl_allreduce(c.handle, send, [o.view for o in o2], N, "fp32", stream=s2)
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+    for r in range(P):
+        assert same_bits(o1[r].result(), want[r], "fp32")
+        assert same_bits(o2[r].result(), want[r], "fp32")
