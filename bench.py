@@ -1,0 +1,489 @@
+#!/usr/bin/env python3
+"""Benchmark of the HCCL copy/reduce hot path on one MI355X.
+
+A step is one AllToAllv of recommendation-shaped data over P = 8 virtual ranks: every rank
+sends 2^18 embedding rows (128 bf16 = 256 B each, 64 MiB) split across destinations by a
+Zipf(1.1) law, then the int32 row ids ride along in a second call. The metric is effective
+HBM GB/s = algorithmic bytes / time, algorithmic bytes = 2 x payload (each byte read once,
+written once). Inputs are resident in HBM before timing starts.
+
+The same JSON line carries the roofline of the dominant kernel (the embedding-row launch,
+timed with HIP events on its stream), the CPU oracle timed on the host, and the other
+collective workloads measured the same way (ring all-reduce, ring reduce-scatter, two-level
+all-reduce, small-message latency, GEMM overlap on a CU-masked stream).
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--headline-only] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MiB = 1 << 20
+
+
+def _log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def _time_events(fn, iters: int, stream=None):
+    """Runs fn() iters times back to back; returns per-iteration ms from one event pair."""
+    import torch
+
+    s = stream or torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(s)
+    for _ in range(iters):
+        fn()
+    b.record(s)
+    b.synchronize()
+    return a.elapsed_time(b) / iters
+
+
+# ------------------------------------------------------------------------- headline
+def alltoallv_workload(device):
+    import numpy as np
+
+    from workloads import alltoallv_layout, device_normal_bf16, row_ids_int32, zipf_counts
+
+    P, R, D = 8, 1 << 18, 128
+    counts = zipf_counts(P, R, 1.1, seed=0)
+    rows = alltoallv_layout(counts, D)
+    ids = alltoallv_layout(counts, 1)
+    t0 = time.time()
+    send_rows = device_normal_bf16(P, R * D, seed=0, device=device)   # each rank sends exactly R rows
+    id_vals = row_ids_int32(P, R, seed=1)
+    _log(f"alltoallv inputs generated in {time.time() - t0:.1f}s")
+    return {"P": P, "R": R, "D": D, "counts": counts, "rows": rows, "ids": ids,
+            "send_rows": send_rows, "id_vals": id_vals}
+
+
+def run_headline(args, device):
+    import numpy as np
+    import torch
+
+    import paper_2608_00358_amd as H
+
+    w = alltoallv_workload(device)
+    P = w["P"]
+    rows, ids = w["rows"], w["ids"]
+    send_rows = w["send_rows"]
+    send_ids = [torch.from_numpy(w["id_vals"][s].copy()).to(device) for s in range(P)]
+    recv_rows = [torch.empty(int(rows["recv_len"][d]), dtype=torch.bfloat16, device=device) for d in range(P)]
+    recv_ids = [torch.empty(int(ids["recv_len"][d]), dtype=torch.int32, device=device) for d in range(P)]
+    row_bytes = int(rows["sendcounts"].sum()) * 2
+    id_bytes = int(ids["sendcounts"].sum()) * 4
+    comm = H.Comm(P, device=0)
+
+    def step():
+        comm.alltoallv(send_rows, rows["sendcounts"], rows["sdispls"], recv_rows, rows["recvcounts"], rows["rdispls"])
+        comm.alltoallv(send_ids, ids["sendcounts"], ids["sdispls"], recv_ids, ids["recvcounts"], ids["rdispls"])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    info_ids = comm.last_program()
+    comm.alltoallv(send_rows, rows["sendcounts"], rows["sdispls"], recv_rows, rows["recvcounts"], rows["rdispls"])
+    info_rows = comm.last_program()
+    torch.cuda.synchronize()
+
+    s = torch.cuda.current_stream()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(s)
+        comm.alltoallv(send_rows, rows["sendcounts"], rows["sdispls"], recv_rows, rows["recvcounts"], rows["rdispls"])
+        ends[i].record(s)
+        comm.alltoallv(send_ids, ids["sendcounts"], ids["sdispls"], recv_ids, ids["recvcounts"], ids["rdispls"])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    if comm.async_error() != 0:
+        raise RuntimeError(H.hccl_get_last_error())
+    ms_step = elapsed * 1e3 / args.steps
+    row_ms = [a.elapsed_time(b) for a, b in zip(starts, ends)]
+    row_ms_avg = statistics.mean(row_ms)
+    algo_step = 2 * (row_bytes + id_bytes)
+    algo_rows = 2 * row_bytes
+    recv_counts = w["counts"].sum(axis=0)
+    result = {
+        "ms_per_step": ms_step,
+        "value": algo_step / (ms_step * 1e-3) / 1e9,
+        "row_launch_ms": row_ms_avg,
+        "row_launch_ms_min": min(row_ms),
+        "algo_bytes_rows": algo_rows,
+        "algo_bytes_step": algo_step,
+        "recv_imbalance": float(recv_counts.max() / recv_counts.mean()),
+        "program_rows": info_rows,
+        "program_ids": info_ids,
+    }
+    comm.close()
+    return result, w
+
+
+# --------------------------------------------------------------------- other configs
+def bench_allreduce_ring_c1(device, iters=200, cold_sets=40):
+    """All-reduce P=4 x 2^20 fp32 U[-1,1), ring reduce-scatter + all-gather, 64 KiB chunks."""
+    import torch
+
+    import paper_2608_00358_amd as H
+    from workloads import uniform_f32
+
+    P, N = 4, 1 << 20
+    x = uniform_f32(P, N, seed=0)
+    send = [torch.from_numpy(x[r].copy()).to(device) for r in range(P)]
+    recv = [torch.empty(N, dtype=torch.float32, device=device) for _ in range(P)]
+    algo = 2 * P * N * 4
+    out = {}
+    with H.Comm(P, device=0, algo="ring", chunk_bytes=64 * 1024) as c:
+        ms = _time_events(lambda: c.allreduce(send, recv), iters)
+        info = c.last_program()
+        out["warm_us"] = ms * 1e3
+        out["warm_gbs"] = algo / (ms * 1e-3) / 1e9
+        # cold: rotate through enough buffer sets to defeat the 256 MiB infinity cache
+        sets = [([torch.empty(N, dtype=torch.float32, device=device).copy_(t) for t in send],
+                 [torch.empty(N, dtype=torch.float32, device=device) for _ in range(P)]) for _ in range(cold_sets)]
+        k = [0]
+
+        def cold():
+            s, r = sets[k[0] % cold_sets]
+            k[0] += 1
+            c.allreduce(s, r)
+
+        ms = _time_events(cold, iters)
+        out["cold_us"] = ms * 1e3
+        out["cold_gbs"] = algo / (ms * 1e-3) / 1e9
+        # the same program with every ring step as its own dependent descriptor
+        c.set_config(algo="ring", chunk_bytes=64 * 1024, fuse=0)
+        ms = _time_events(lambda: c.allreduce(send, recv), iters)
+        out["unfused_warm_gbs"] = algo / (ms * 1e-3) / 1e9
+    out.update({"workload": "allreduce ring P=4 N=2^20 fp32 chunk=64KiB", "algo_bytes": algo,
+                "descs": info["num_descs"], "tiles": info["num_tiles"]})
+    return out
+
+
+def bench_reduce_scatter_c3(device, iters=20):
+    """Reduce-scatter P=8 x 256 MiB bf16 N(0, 0.02), ascending fp32 fold, 1 MiB ring chunks."""
+    import torch
+
+    import paper_2608_00358_amd as H
+    from workloads import device_normal_bf16
+
+    P = 8
+    M = (256 * MiB // 2) // P
+    send = device_normal_bf16(P, P * M, std=0.02, seed=0, device=device)
+    recv = [torch.empty(M, dtype=torch.bfloat16, device=device) for _ in range(P)]
+    algo = (P + 1) * P * M * 2
+    with H.Comm(P, device=0, algo="ring", chunk_bytes=MiB) as c:
+        c.reduce_scatter(send, recv)
+        ms = _time_events(lambda: c.reduce_scatter(send, recv), iters)
+        info = c.last_program()
+    res = {"workload": "reduce_scatter ring P=8 256MiB/rank bf16 chunk=1MiB", "us": ms * 1e3,
+           "gbs": algo / (ms * 1e-3) / 1e9, "algo_bytes": algo, "descs": info["num_descs"],
+           "tiles": info["num_tiles"], "workers": info["workers"]}
+    res["frac"] = res["gbs"] / HBM_PEAK_GBS
+    return res, send, recv
+
+
+def bench_two_level_c4(device, iters=10):
+    """Two-level all-reduce P=64 (8 groups x 8) x 32 MiB bf16 N(0,1)."""
+    import torch
+
+    import paper_2608_00358_amd as H
+    from workloads import device_normal_bf16
+
+    P, L = 64, 8
+    N = 32 * MiB // 2
+    send = device_normal_bf16(P, N, seed=0, device=device)
+    recv = [torch.empty(N, dtype=torch.bfloat16, device=device) for _ in range(P)]
+    algo = 2 * P * N * 2
+    out = {"workload": "allreduce two-level P=64 (8x8) 32MiB/rank bf16", "algo_bytes": algo}
+    with H.Comm(P, device=0, algo="two_level", group_size=L) as c:
+        c.allreduce(send, recv)
+        ms = _time_events(lambda: c.allreduce(send, recv), iters)
+        info = c.last_program()
+        out.update({"us": ms * 1e3, "gbs": algo / (ms * 1e-3) / 1e9, "descs": info["num_descs"]})
+        c.set_config(algo="two_level", group_size=L, fuse=0)
+        c.allreduce(send, recv)
+        ms = _time_events(lambda: c.allreduce(send, recv), iters)
+        info = c.last_program()
+        out.update({"unfused_us": ms * 1e3, "unfused_gbs": algo / (ms * 1e-3) / 1e9,
+                    "unfused_schedule_bytes": info["bytes_read"] + info["bytes_written"]})
+    out["frac"] = out["gbs"] / HBM_PEAK_GBS
+    del send, recv
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_latency_c5b(device, warmup=100, iters=1000, isolated=200):
+    """All-reduce P=8 x 64 KiB fp32, one-shot schedule: back-to-back and isolated latency."""
+    import torch
+
+    import paper_2608_00358_amd as H
+    from workloads import uniform_f32
+
+    P, N = 8, 1 << 14
+    x = uniform_f32(P, N, seed=5)
+    send = [torch.from_numpy(x[r].copy()).to(device) for r in range(P)]
+    recv = [torch.empty(N, dtype=torch.float32, device=device) for _ in range(P)]
+    with H.Comm(P, device=0, algo="direct") as c:
+        for _ in range(warmup):
+            c.allreduce(send, recv)
+        ms = _time_events(lambda: c.allreduce(send, recv), iters)
+        s = torch.cuda.current_stream()
+        samples = []
+        for _ in range(isolated):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record(s)
+            c.allreduce(send, recv)
+            b.record(s)
+            b.synchronize()
+            samples.append(a.elapsed_time(b) * 1e3)
+        t_host = []
+        for _ in range(isolated):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            c.allreduce(send, recv)
+            torch.cuda.synchronize()
+            t_host.append((time.perf_counter() - t0) * 1e6)
+        info = c.last_program()
+    return {"workload": "allreduce direct P=8 64KiB/rank fp32", "back_to_back_us": ms * 1e3,
+            "isolated_median_us": statistics.median(samples),
+            "host_roundtrip_median_us": statistics.median(t_host), "workers": info["workers"],
+            "tiles": info["num_tiles"]}
+
+
+def _cu_masked_stream(mask_words):
+    """hipExtStreamCreateWithCUMask on the current device (default priority)."""
+    import torch
+
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
+                                                 ctypes.POINTER(ctypes.c_uint32)]
+    s = ctypes.c_void_p()
+    arr = (ctypes.c_uint32 * len(mask_words))(*mask_words)
+    rc = hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), len(mask_words), arr)
+    if rc != 0:
+        raise RuntimeError(f"hipExtStreamCreateWithCUMask failed ({rc})")
+    return torch.cuda.ExternalStream(s.value), s.value
+
+
+def bench_overlap_c5a(device, rs_send, rs_recv, n_rs=100, rs_cus=16):
+    """Reduce-scatter (c3 shape) on a stream masked to 16 CUs while a bf16 8192^3 GEMM runs on
+    a second stream (all CUs, and the 240 complementary CUs)."""
+    import torch
+
+    import paper_2608_00358_amd as H
+
+    props = torch.cuda.get_device_properties(0)
+    ncu = props.multi_processor_count
+    words = (ncu + 31) // 32
+    rs_bits = [0] * words
+    for i in range(rs_cus):
+        rs_bits[i // 32] |= 1 << (i % 32)
+    rest_bits = [((~rs_bits[w]) & 0xFFFFFFFF) for w in range(words)]
+    if ncu % 32:
+        rest_bits[-1] &= (1 << (ncu % 32)) - 1
+    rs_stream, _ = _cu_masked_stream(rs_bits)
+    rest_stream, _ = _cu_masked_stream(rest_bits)
+    gemm_stream = torch.cuda.Stream()
+    n = 8192
+    g = torch.Generator(device=device).manual_seed(0)
+    A = torch.randn(n, n, device=device, dtype=torch.bfloat16, generator=g)
+    B = torch.randn(n, n, device=device, dtype=torch.bfloat16, generator=g)
+    C = torch.empty(n, n, device=device, dtype=torch.bfloat16)
+    flop = 2.0 * n ** 3
+
+    def gemm_time(stream, iters=20):
+        with torch.cuda.stream(stream):
+            for _ in range(3):
+                torch.matmul(A, B, out=C)
+            return _time_events(lambda: torch.matmul(A, B, out=C), iters, stream)
+
+    t_all = gemm_time(gemm_stream)
+    t_240 = gemm_time(rest_stream)
+    P = len(rs_send)
+    M = rs_recv[0].numel()
+    algo = (P + 1) * P * M * 2
+    comm = H.Comm(P, device=0, algo="ring", chunk_bytes=MiB)
+    rs_ms = _time_events(lambda: comm.reduce_scatter(rs_send, rs_recv, stream=rs_stream), 3, rs_stream)
+    workers = comm.last_program()["workers"]
+    # overlap: n_rs back-to-back reduce-scatters on the masked stream, GEMMs alongside
+    n_gemm = max(5, int(0.9 * n_rs * rs_ms / t_all))
+    results = {}
+    for label, gstream in (("all_cus", gemm_stream), ("complement_cus", rest_stream)):
+        torch.cuda.synchronize()
+        ev = {k: torch.cuda.Event(enable_timing=True) for k in ("rs0", "rs1", "g0", "g1")}
+        ev["rs0"].record(rs_stream)
+        for _ in range(n_rs):
+            comm.reduce_scatter(rs_send, rs_recv, stream=rs_stream)
+        ev["rs1"].record(rs_stream)
+        with torch.cuda.stream(gstream):
+            ev["g0"].record(gstream)
+            for _ in range(n_gemm):
+                torch.matmul(A, B, out=C)
+            ev["g1"].record(gstream)
+        torch.cuda.synchronize()
+        g_ms = ev["g0"].elapsed_time(ev["g1"]) / n_gemm
+        r_ms = ev["rs0"].elapsed_time(ev["rs1"]) / n_rs
+        base = t_all if label == "all_cus" else t_240
+        results[label] = {"gemm_ms": g_ms, "gemm_tflops": flop / (g_ms * 1e-3) / 1e12,
+                          "gemm_slowdown_pct": (g_ms / base - 1.0) * 100.0,
+                          "rs_ms": r_ms, "rs_gbs": algo / (r_ms * 1e-3) / 1e9}
+    if comm.async_error() != 0:
+        raise RuntimeError(H.hccl_get_last_error())
+    comm.close()
+    return {"workload": "reduce_scatter P=8 256MiB/rank bf16 on 16 CUs || bf16 8192^3 GEMM",
+            "gemm_alone_all_cus_ms": t_all, "gemm_alone_all_cus_tflops": flop / (t_all * 1e-3) / 1e12,
+            "gemm_alone_240_cus_ms": t_240, "rs_alone_16cu_ms": rs_ms,
+            "rs_alone_16cu_gbs": algo / (rs_ms * 1e-3) / 1e9, "rs_workers": workers,
+            "n_rs": n_rs, "n_gemm": n_gemm, "overlap": results}
+
+
+# ---------------------------------------------------------------------- CPU baseline
+def cpu_baseline(w, budget_s=12.0):
+    """The oracle's AllToAllv on the host cores (single-threaded C), same inputs."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    P = w["P"]
+    rows = w["rows"]
+    send = [t.view(torch.int16).cpu().numpy().view(np.uint16) for t in w["send_rows"]]
+    recv = [np.empty(int(rows["recv_len"][d]), np.uint16) for d in range(P)]
+    oracle.build(force=False)
+    reps, t = 0, 0.0
+    while t < budget_s and reps < 50:
+        t0 = time.perf_counter()
+        oracle.alltoallv(send, rows["sendcounts"], rows["sdispls"], recv, rows["recvcounts"], rows["rdispls"])
+        t += time.perf_counter() - t0
+        reps += 1
+    algo = 2 * int(rows["sendcounts"].sum()) * 2
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": algo * reps / t / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"embedding-row AllToAllv of the same workload (8 ranks x 64 MiB bf16), "
+                      f"{reps} full repetitions in {t:.1f}s, single-threaded C oracle",
+            "cpu_model": model, "host_threads_available": os.cpu_count()}
+
+
+# ------------------------------------------------------------------------ roofline
+def traffic_record(kernel: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were taken on
+    the current executor source (otherwise null)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except ValueError:
+        return None
+    src = os.path.join(ROOT, "paper_2608_00358_amd", "csrc", "executor.hip")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    entry = rec.get(kernel)
+    if not entry or entry.get("executor_sha256_16") != digest:
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--headline-only", action="store_true", help="only the timed AllToAllv steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-overlap", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the P ranks are buffers in one MI355X's HBM; "
+              "multi-GPU runs are not part of this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    import paper_2608_00358_amd as H
+
+    H.load()
+    device = "cuda:0"
+    torch.cuda.set_device(0)
+
+    head, w = run_headline(args, device)
+    _log(f"alltoallv step {head['ms_per_step']:.3f} ms, {head['value']:.1f} GB/s; "
+         f"row launch {head['row_launch_ms'] * 1e3:.1f} us")
+    achieved = head["algo_bytes_rows"] / (head["row_launch_ms"] * 1e-3) / 1e9
+    traffic = traffic_record("alltoallv_rows_p8_zipf")
+    line = {
+        "metric": "effective HBM GB/s per collective (% of MI355X HBM peak); small-msg latency us",
+        "value": round(head["value"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(head["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "alltoallv P=8 virtual ranks, 2^18 rows/rank of 128 bf16 (64 MiB/rank), "
+                               "Zipf(1.1) destination split, int32 row ids in a second call",
+                   "ranks": 8, "rows_per_rank": 1 << 18, "row_elems": 128,
+                   "recv_imbalance_max_over_mean": round(head["recv_imbalance"], 3),
+                   "descs_rows": head["program_rows"]["num_descs"],
+                   "workers": head["program_rows"]["workers"]},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "kernel": "hccl_executor<copy, 16-byte aligned> (embedding-row launch)",
+                     "algo_bytes_per_launch": head["algo_bytes_rows"],
+                     "avg_launch_us": round(head["row_launch_ms"] * 1e3, 2)},
+    }
+    if not args.headline_only:
+        extras = {}
+        _log("c1 ring all-reduce")
+        extras["allreduce_ring_p4_fp32"] = bench_allreduce_ring_c1(device)
+        _log("c3 ring reduce-scatter")
+        c3, rs_send, rs_recv = bench_reduce_scatter_c3(device)
+        extras["reduce_scatter_ring_p8_bf16"] = c3
+        _log(f"c3 {c3['gbs']:.1f} GB/s")
+        if not args.no_overlap:
+            _log("c5a overlap")
+            extras["overlap_rs16cu_gemm"] = bench_overlap_c5a(device, rs_send, rs_recv)
+        del rs_send, rs_recv
+        torch.cuda.empty_cache()
+        _log("c4 two-level all-reduce")
+        extras["allreduce_two_level_p64_bf16"] = bench_two_level_c4(device)
+        _log("c5b latency")
+        extras["latency_allreduce_p8_64KiB_fp32"] = bench_latency_c5b(device)
+        line["collectives"] = extras
+    if not args.no_cpu_baseline:
+        _log("cpu baseline")
+        line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

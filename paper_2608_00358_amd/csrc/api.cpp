@@ -259,7 +259,11 @@ hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* sen
 
     const uint32_t wpb = (uint32_t)executor_waves_per_block();
     uint32_t cus = stream_cu_count(c, s);
-    const int kind = dp->prog.kind;
+    int kind = dp->prog.kind;
+    if (kind == kKindCopyAligned) {
+        for (int i = 0; i < 2 * P; ++i)
+            if ((uintptr_t)a.bufs[i] % 16) kind = kKindCopyOnly;
+    }
     uint32_t slots = cus * (uint32_t)std::max(1, c->blocks_per_cu[kind]) * wpb;
     if (c->cfg.max_workers > 0) slots = std::min<uint32_t>(slots, (uint32_t)c->cfg.max_workers);
     uint32_t workers = std::min<uint32_t>(slots, dp->prog.ntiles);

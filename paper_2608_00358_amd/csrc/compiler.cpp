@@ -672,6 +672,11 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
         if (kind == kKindCopyOnly) kind = out[i].sig;
         else if (kind != out[i].sig) { kind = kKindGeneric; break; }
     }
+    if (kind == kKindCopyOnly) {
+        bool aligned = true;
+        for (const Operand& o : ops) aligned &= (o.offset % 16) == 0;
+        if (aligned) kind = kKindCopyAligned;  // the launch falls back if a buffer is not aligned
+    }
     p.kind = kind;
 
     auto align16 = [](uint64_t x) { return (x + 15) & ~uint64_t(15); };

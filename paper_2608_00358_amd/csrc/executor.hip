@@ -398,6 +398,35 @@ __device__ __forceinline__ void copy_tile(const TileOps& t, uint32_t n, uint32_t
     if (off < nbytes) copy_elems<ES>(src, t, off / ES, (nbytes - off) / ES, lane);
 }
 
+// Copy of a tile whose source and destinations are all 16-byte aligned.
+template <int ES>
+__device__ __forceinline__ void copy_tile_aligned(const TileOps& t, uint32_t n, uint32_t lane) {
+    const char* src = (const char*)from_lane(t.src, 0);
+    const uint64_t nbytes = (uint64_t)n * ES;
+    constexpr int U = 4;
+    constexpr uint64_t kStep = (uint64_t)U * kWaveSize * 16;
+    uint64_t off = 0;
+    for (; off + kStep <= nbytes; off += kStep) {
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = *(const u32x4*)(src + off + ((uint64_t)u * kWaveSize + lane) * 16);
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* d = (char*)from_lane(t.dst, j);
+#pragma unroll
+            for (int u = 0; u < U; ++u) *(u32x4*)(d + off + ((uint64_t)u * kWaveSize + lane) * 16) = v[u];
+        }
+    }
+    for (uint64_t x = off + (uint64_t)lane * 16; x + 16 <= nbytes; x += 16 * kWaveSize) {
+        u32x4 v = *(const u32x4*)(src + x);
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* d = (char*)from_lane(t.dst, j);
+            *(u32x4*)(d + x) = v;
+        }
+    }
+    off = nbytes / 16 * 16;
+    if (off < nbytes) copy_elems<ES>(src, t, off / ES, (nbytes - off) / ES, lane);
+}
+
 // ---------------------------------------------------------------------- dependencies
 __device__ __forceinline__ uint32_t load_relaxed(const uint32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -498,8 +527,13 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
             }
         } else {
             const uint32_t es = elem_bytes(uni(opl[uni(D->src)].dtype));
-            if (es == 2) copy_tile<2>(ops, n, lane);
-            else copy_tile<4>(ops, n, lane);
+            if constexpr (KIND == kKindCopyAligned) {
+                if (es == 2) copy_tile_aligned<2>(ops, n, lane);
+                else copy_tile_aligned<4>(ops, n, lane);
+            } else {
+                if (es == 2) copy_tile<2>(ops, n, lane);
+                else copy_tile<4>(ops, n, lane);
+            }
         }
     }
 
@@ -590,6 +624,9 @@ hipError_t launch_executor(const LaunchArgs& a, uint32_t blocks, int kind, hipSt
         case kKindCopyOnly:
             hipLaunchKernelGGL(hccl_executor<kKindCopyOnly>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
             break;
+        case kKindCopyAligned:
+            hipLaunchKernelGGL(hccl_executor<kKindCopyAligned>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
+            break;
         default:
             hipLaunchKernelGGL(hccl_executor<kKindGeneric>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
             break;
@@ -613,6 +650,7 @@ hipError_t executor_occupancy(int kind, int* blocks_per_cu) {
         case SIG_FP32: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<SIG_FP32>, kBlockThreads, 0);
         case SIG_INT32: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<SIG_INT32>, kBlockThreads, 0);
         case kKindCopyOnly: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindCopyOnly>, kBlockThreads, 0);
+        case kKindCopyAligned: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindCopyAligned>, kBlockThreads, 0);
         default: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindGeneric>, kBlockThreads, 0);
     }
 }

@@ -78,9 +78,10 @@ enum Signature : uint8_t {
 
 // Executor kernel specialisations ("kinds"): a plain signature id for programs whose
 // reductions all have that signature and SUM, or one of these two.
-constexpr int kKindCopyOnly = SIG_COUNT;     // no reductions at all
-constexpr int kKindGeneric = SIG_COUNT + 1;  // anything else
-constexpr int kNumKinds = SIG_COUNT + 2;
+constexpr int kKindCopyOnly = SIG_COUNT;         // no reductions at all
+constexpr int kKindGeneric = SIG_COUNT + 1;      // anything else
+constexpr int kKindCopyAligned = SIG_COUNT + 2;  // copies only, every operand 16-byte aligned
+constexpr int kNumKinds = SIG_COUNT + 3;
 
 inline uint8_t reduce_signature(uint32_t t0, uint32_t tr, uint32_t to) {
     if (t0 == tr && tr == to) return (uint8_t)t0;  // DT_* and SIG_* plain ids coincide

@@ -7,6 +7,8 @@ oracle's callers take their inputs from here, so neither side depends on the oth
 from .generators import (  # noqa: F401
     alltoallv_layout,
     bf16_bits_from_f32,
+    device_normal_bf16,
+    device_uniform_f32,
     normal_bf16,
     normal_f32,
     row_ids_int32,

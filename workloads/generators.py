@@ -1,6 +1,6 @@
 """Seeded input generators (numpy PCG64). No collective arithmetic lives here.
 
-Recipe, shared by every consumer:
+Recipe, shared by every consumer (host generators, used up to tens of millions of values):
   * one ``numpy.random.SeedSequence(seed)`` is spawned into P child sequences; rank r draws
     its values from ``Generator(PCG64(child[r]))``, so ranks can be generated in parallel and
     a rank's data does not depend on P's other ranks being drawn;
@@ -8,6 +8,12 @@ Recipe, shared by every consumer:
     conversion (element bits are returned as uint16);
   * uniform [-1, 1) float32 values are ``random(float32) * 2 - 1``: random() yields k * 2^-24,
     so the affine map is exact and never reaches 1.0.
+
+Device generators (full-size workloads of hundreds of millions of values, where host
+generation would take minutes): rank r draws from ``torch.Generator(device)`` seeded with
+``seed * 1_000_003 + r`` (torch's Philox counter-based generator), in float32, then rounds to
+bf16 with torch. Callers that need the values on the host copy the device tensor back; the
+values are the same bits on both sides.
 """
 from __future__ import annotations
 
@@ -149,3 +155,39 @@ def alltoallv_layout(row_counts: np.ndarray, elems_per_row: int = 1) -> dict:
         "recv_len": c.sum(axis=0),
         "P": P,
     }
+
+
+def device_rank_seed(seed: int, r: int) -> int:
+    return seed * 1_000_003 + r
+
+
+def device_normal_bf16(P: int, N: int, mean: float = 0.0, std: float = 1.0, seed: int = 0,
+                       device: str = "cuda:0"):
+    """List of P device tensors (bfloat16, N elements) of N(mean, std) draws."""
+    import torch
+
+    out = []
+    for r in range(P):
+        g = torch.Generator(device=device)
+        g.manual_seed(device_rank_seed(seed, r))
+        x = torch.randn(N, generator=g, device=device, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(std)
+        if mean != 0.0:
+            x.add_(mean)
+        out.append(x.to(torch.bfloat16))
+        del x
+    return out
+
+
+def device_uniform_f32(P: int, N: int, seed: int = 0, device: str = "cuda:0"):
+    """List of P device tensors (float32, N elements), uniform in [-1, 1)."""
+    import torch
+
+    out = []
+    for r in range(P):
+        g = torch.Generator(device=device)
+        g.manual_seed(device_rank_seed(seed, r))
+        x = torch.rand(N, generator=g, device=device, dtype=torch.float32)
+        out.append(x.mul_(2.0).sub_(1.0))
+    return out
