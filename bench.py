@@ -414,6 +414,9 @@ def main():
     ap.add_argument("--headline-only", action="store_true", help="only the timed AllToAllv steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run torch's device copy of 1 GiB (the known-size kernel that scales "
+                         "the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the P ranks are buffers in one MI355X's HBM; "
@@ -430,6 +433,14 @@ def main():
     H.load()
     device = "cuda:0"
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=device)
+        a.fill_(1)
+        b = torch.empty_like(a)
+        ms = _time_events(lambda: b.copy_(a), 5)
+        print(json.dumps({"calibration": "torch copy_ 1 GiB", "bytes_read": 1 << 30, "bytes_written": 1 << 30,
+                          "us": ms * 1e3}), flush=True)
+        return
 
     head, w = run_headline(args, device)
     _log(f"alltoallv step {head['ms_per_step']:.3f} ms, {head['value']:.1f} GB/s; "

@@ -68,6 +68,7 @@ struct hcclComm {
     uint64_t scratch_bytes = 0;
     std::list<std::unique_ptr<DeviceProgram>> cache;  // most recently used first
     size_t cache_limit = 64;
+    bool dynamic_dispatch = false;  // tickets also for programs without dependencies
     hcclProgramInfo_t last{};
 };
 
@@ -253,7 +254,7 @@ hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* sen
     }
     a.bufs[scratch_buf(P)] = (char*)c->d_scratch;
     const bool has_deps = (dp->prog.flags & PF_HAS_DEPS) != 0;
-    a.dynamic = has_deps ? 1u : 0u;
+    a.dynamic = (has_deps || c->dynamic_dispatch) ? 1u : 0u;
     const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
     a.timeout_ticks = ms * c->wall_clock_khz;
 
@@ -273,13 +274,14 @@ hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* sen
     info.workers = a.nworkers;
 
     // a program's counters serve one launch at a time: order launches across streams
-    if (has_deps && dp->launched && dp->last_stream != s) {
+    const bool stateful = a.dynamic != 0;
+    if (stateful && dp->launched && dp->last_stream != s) {
         hipError_t e = hipStreamWaitEvent(s, dp->done, 0);
         if (e != hipSuccess) return hip_fail(e, "cross-stream ordering");
     }
     hipError_t e = launch_executor(a, blocks, kind, s);
     if (e != hipSuccess) return hip_fail(e, "executor launch");
-    if (has_deps) {
+    if (stateful) {
         e = hipEventRecord(dp->done, s);
         if (e != hipSuccess) return hip_fail(e, "completion event");
         dp->last_stream = s;
@@ -343,6 +345,8 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
         int khz = 0;
         if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->device) == hipSuccess && khz > 0)
             c->wall_clock_khz = (uint64_t)khz;
+        const char* disp = std::getenv("HCCL_DISPATCH");
+        c->dynamic_dispatch = disp && std::strcmp(disp, "dynamic") == 0;
         const char* bpc = std::getenv("HCCL_BLOCKS_PER_CU");
         for (int k = 0; k < kNumKinds; ++k) {
             if (k > SIG_INT32 && k < kKindCopyOnly) continue;  // no kernel of its own

@@ -30,6 +30,41 @@ constexpr int kWavesPerBlock = 4;
 constexpr int kBlockThreads = kWavesPerBlock * kWaveSize;
 constexpr int kSrcBatch = 8;  // sources whose loads are issued together
 
+// 128-bit global accesses. Every byte of a collective is read once and written once, so the
+// nontemporal hint streams it past the caches instead of evicting the program, the counters
+// and other waves' lines. Copies store nontemporally too; reductions keep ordinary stores
+// (measured faster for their small write share).
+#ifndef HCCL_NT_LOAD
+#define HCCL_NT_LOAD 1
+#endif
+#ifndef HCCL_NT_STORE_COPY
+#define HCCL_NT_STORE_COPY 1
+#endif
+#ifndef HCCL_NT_STORE_REDUCE
+#define HCCL_NT_STORE_REDUCE 0
+#endif
+#ifndef HCCL_COPY_UNROLL
+#define HCCL_COPY_UNROLL 4
+#endif
+#ifndef HCCL_REDUCE_UNROLL16
+#define HCCL_REDUCE_UNROLL16 2
+#endif
+
+__device__ __forceinline__ u32x4 vld(const char* p) {
+    if constexpr (HCCL_NT_LOAD) return __builtin_nontemporal_load((const u32x4*)p);
+    else return *(const u32x4*)p;
+}
+// store of reduction results
+__device__ __forceinline__ void vst(char* p, u32x4 v) {
+    if constexpr (HCCL_NT_STORE_REDUCE) __builtin_nontemporal_store(v, (u32x4*)p);
+    else *(u32x4*)p = v;
+}
+// store of copied data
+__device__ __forceinline__ void vst_copy(char* p, u32x4 v) {
+    if constexpr (HCCL_NT_STORE_COPY) __builtin_nontemporal_store(v, (u32x4*)p);
+    else *(u32x4*)p = v;
+}
+
 template <int DT> struct DtInfo;
 template <> struct DtInfo<DT_BF16> { static constexpr int size = 2; typedef float acc; };
 template <> struct DtInfo<DT_FP16> { static constexpr int size = 2; typedef float acc; };
@@ -105,7 +140,7 @@ template <int DT>
 __device__ __forceinline__ Raw8<DT> load8(const char* p) {
     Raw8<DT> r;
 #pragma unroll
-    for (int q = 0; q < DtInfo<DT>::size / 2; ++q) r.v[q] = *(const u32x4*)(p + 16 * q);
+    for (int q = 0; q < DtInfo<DT>::size / 2; ++q) r.v[q] = vld(p + 16 * q);
     return r;
 }
 
@@ -138,7 +173,7 @@ __device__ __forceinline__ void store8(char* p, const A (&x)[8]) {
             if constexpr (DT == DT_BF16) w[i] = bf16_bits(x[2 * i]) | (bf16_bits(x[2 * i + 1]) << 16);
             else w[i] = f16_bits(x[2 * i]) | (f16_bits(x[2 * i + 1]) << 16);
         }
-        *(u32x4*)p = w;
+        vst(p, w);
     } else {
         u32x4 a, b;
 #pragma unroll
@@ -151,8 +186,8 @@ __device__ __forceinline__ void store8(char* p, const A (&x)[8]) {
                 b[i] = (uint32_t)x[4 + i];
             }
         }
-        *(u32x4*)p = a;
-        *(u32x4*)(p + 16) = b;
+        vst(p, a);
+        vst(p + 16, b);
     }
 }
 
@@ -211,31 +246,32 @@ __device__ __forceinline__ void reduce_elems(const TileOps& t, uint32_t first, u
 template <int T0, int TR, int TO, int OPR, int U>
 __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, uint32_t lane) {
     typedef typename DtInfo<TO>::acc A;
+    // a first source of another type (a chained step's FP32 partial) needs its own registers
+    constexpr bool kMixed = (T0 != TR);
+    constexpr int SB = kMixed ? kSrcBatch / 2 : kSrcBatch;
     const uint32_t L = t.group ? t.group : t.nsrc;
     A tot[U][8], part[U][8];
     for (uint32_t g0 = 0; g0 < t.nsrc; g0 += L) {
         const uint32_t gend = (g0 + L < t.nsrc) ? g0 + L : t.nsrc;
-        {
-            const char* b = (const char*)from_lane(t.src, g0);
-            if (g0 == 0) {
+        // Sources are visited in batches; every load of a batch is issued before the first
+        // of them is folded, so one memory round trip serves the whole batch.
+        for (uint32_t s = g0; s < gend; s += SB) {
+            Raw8<T0> raw0[kMixed ? U : 1];
+            Raw8<TR> raw[SB][U];
+            const bool first_mixed = kMixed && s == 0;  // source 0 is typed T0
+            if constexpr (kMixed) {
+                if (first_mixed) {
+                    const char* b = (const char*)from_lane(t.src, 0);
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
-                    widen8<T0, A>(load8<T0>(b + (uint64_t)e * DtInfo<T0>::size), part[u]);
-                }
-            } else {
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
-                    widen8<TR, A>(load8<TR>(b + (uint64_t)e * DtInfo<TR>::size), part[u]);
+                    for (int u = 0; u < U; ++u) {
+                        uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
+                        raw0[u] = load8<T0>(b + (uint64_t)e * DtInfo<T0>::size);
+                    }
                 }
             }
-        }
-        for (uint32_t s = g0 + 1; s < gend; s += kSrcBatch) {
-            Raw8<TR> raw[kSrcBatch][U];
 #pragma unroll
-            for (int j = 0; j < kSrcBatch; ++j) {
-                if (s + j < gend) {
+            for (int j = 0; j < SB; ++j) {
+                if ((j > 0 || !first_mixed) && s + j < gend) {
                     const char* b = (const char*)from_lane(t.src, s + j);
 #pragma unroll
                     for (int u = 0; u < U; ++u) {
@@ -244,15 +280,26 @@ __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, ui
                     }
                 }
             }
+            if constexpr (kMixed) {
+                if (first_mixed) {
 #pragma unroll
-            for (int j = 0; j < kSrcBatch; ++j) {
-                if (s + j < gend) {
+                    for (int u = 0; u < U; ++u) widen8<T0, A>(raw0[u], part[u]);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < SB; ++j) {
+                if ((j > 0 || !first_mixed) && s + j < gend) {
 #pragma unroll
                     for (int u = 0; u < U; ++u) {
                         A x[8];
                         widen8<TR, A>(raw[j][u], x);
+                        if (s + j == g0) {
 #pragma unroll
-                        for (int i = 0; i < 8; ++i) part[u][i] = comb<OPR>(part[u][i], x[i]);
+                            for (int i = 0; i < 8; ++i) part[u][i] = x[i];
+                        } else {
+#pragma unroll
+                            for (int i = 0; i < 8; ++i) part[u][i] = comb<OPR>(part[u][i], x[i]);
+                        }
                     }
                 }
             }
@@ -278,7 +325,7 @@ __device__ __forceinline__ void reduce_tile(const TileOps& t, uint32_t n, bool a
         reduce_elems<T0, TR, TO, OPR>(t, 0, n, lane);
         return;
     }
-    constexpr int U = (DtInfo<TR>::size == 2) ? 2 : 1;
+    constexpr int U = (DtInfo<TR>::size == 2) ? HCCL_REDUCE_UNROLL16 : 1;
     constexpr uint32_t kBlock = (uint32_t)U * kWaveSize * kVecElems;
     uint32_t base = 0;
     for (; base + kBlock <= n; base += kBlock) reduce_block<T0, TR, TO, OPR, U>(t, base, lane);
@@ -364,33 +411,33 @@ __device__ __forceinline__ void copy_tile(const TileOps& t, uint32_t n, uint32_t
     uint64_t head = mis ? (16u - mis) : 0u;   // bytes before the first 16-byte boundary
     if (head > nbytes) head = nbytes;
     if (head) copy_elems<ES>(src, t, 0, head / ES, lane);
-    constexpr int U = 4;
+    constexpr int U = HCCL_COPY_UNROLL;
     constexpr uint64_t kStep = (uint64_t)U * kWaveSize * 16;
     uint64_t off = head;
     for (; off + kStep <= nbytes; off += kStep) {
         u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = *(const u32x4*)(src + off + ((uint64_t)u * kWaveSize + lane) * 16);
+        for (int u = 0; u < U; ++u) v[u] = vld(src + off + ((uint64_t)u * kWaveSize + lane) * 16);
         for (uint32_t j = 0; j < t.ndst; ++j) {
             char* d = (char*)from_lane(t.dst, j);
 #pragma unroll
-            for (int u = 0; u < U; ++u) *(u32x4*)(d + off + ((uint64_t)u * kWaveSize + lane) * 16) = v[u];
+            for (int u = 0; u < U; ++u) vst_copy(d + off + ((uint64_t)u * kWaveSize + lane) * 16, v[u]);
         }
     }
     for (; off + 16 * kWaveSize <= nbytes; off += 16 * kWaveSize) {
-        u32x4 v = *(const u32x4*)(src + off + (uint64_t)lane * 16);
+        u32x4 v = vld(src + off + (uint64_t)lane * 16);
         for (uint32_t j = 0; j < t.ndst; ++j) {
             char* d = (char*)from_lane(t.dst, j);
-            *(u32x4*)(d + off + (uint64_t)lane * 16) = v;
+            vst_copy(d + off + (uint64_t)lane * 16, v);
         }
     }
     {
         uint64_t x = off + (uint64_t)lane * 16;
         if (x + 16 <= nbytes) {
-            u32x4 v = *(const u32x4*)(src + x);
+            u32x4 v = vld(src + x);
             for (uint32_t j = 0; j < t.ndst; ++j) {
                 char* d = (char*)from_lane(t.dst, j);
-                *(u32x4*)(d + x) = v;
+                vst_copy(d + x, v);
             }
         }
         off += (nbytes - off) / 16 * 16;
@@ -403,24 +450,24 @@ template <int ES>
 __device__ __forceinline__ void copy_tile_aligned(const TileOps& t, uint32_t n, uint32_t lane) {
     const char* src = (const char*)from_lane(t.src, 0);
     const uint64_t nbytes = (uint64_t)n * ES;
-    constexpr int U = 4;
+    constexpr int U = HCCL_COPY_UNROLL;
     constexpr uint64_t kStep = (uint64_t)U * kWaveSize * 16;
     uint64_t off = 0;
     for (; off + kStep <= nbytes; off += kStep) {
         u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = *(const u32x4*)(src + off + ((uint64_t)u * kWaveSize + lane) * 16);
+        for (int u = 0; u < U; ++u) v[u] = vld(src + off + ((uint64_t)u * kWaveSize + lane) * 16);
         for (uint32_t j = 0; j < t.ndst; ++j) {
             char* d = (char*)from_lane(t.dst, j);
 #pragma unroll
-            for (int u = 0; u < U; ++u) *(u32x4*)(d + off + ((uint64_t)u * kWaveSize + lane) * 16) = v[u];
+            for (int u = 0; u < U; ++u) vst_copy(d + off + ((uint64_t)u * kWaveSize + lane) * 16, v[u]);
         }
     }
     for (uint64_t x = off + (uint64_t)lane * 16; x + 16 <= nbytes; x += 16 * kWaveSize) {
-        u32x4 v = *(const u32x4*)(src + x);
+        u32x4 v = vld(src + x);
         for (uint32_t j = 0; j < t.ndst; ++j) {
             char* d = (char*)from_lane(t.dst, j);
-            *(u32x4*)(d + x) = v;
+            vst_copy(d + x, v);
         }
     }
     off = nbytes / 16 * 16;
