@@ -160,6 +160,8 @@ typedef struct {
     uint32_t num_operands;       /* operand entries */
     uint32_t workers;            /* wavefronts of the last launch (0 on host-only comms) */
     uint32_t max_srcs;           /* most sources of one step */
+    uint32_t inline_launch;      /* 1 if the one-step program travelled in the launch packet */
+    uint32_t pad;
     uint64_t bytes_read;         /* bytes the program's steps read */
     uint64_t bytes_written;      /* bytes the program's steps write */
     uint64_t scratch_bytes;      /* FP32 scratch the program needs */

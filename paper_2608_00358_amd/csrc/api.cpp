@@ -23,6 +23,7 @@
 
 namespace hccl {
 hipError_t launch_executor(const LaunchArgs& a, uint32_t blocks, int kind, hipStream_t stream);
+hipError_t launch_executor_inline(const InlineArgs& a, uint32_t blocks, int kind, hipStream_t stream);
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t stream);
 hipError_t executor_occupancy(int kind, int* blocks_per_cu);
 int executor_waves_per_block();
@@ -69,6 +70,7 @@ struct hcclComm {
     std::list<std::unique_ptr<DeviceProgram>> cache;  // most recently used first
     size_t cache_limit = 64;
     bool dynamic_dispatch = false;  // tickets also for programs without dependencies
+    bool inline_single_step = true;  // one-step programs travel in the launch packet
     hcclProgramInfo_t last{};
 };
 
@@ -273,6 +275,32 @@ hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* sen
     a.nworkers = blocks * wpb;
     info.workers = a.nworkers;
 
+    if (c->inline_single_step && dp->prog.descs.size() == 1 && !has_deps && !c->dynamic_dispatch) {
+        const HostDesc& d = dp->prog.descs[0];
+        InlineArgs ia;
+        std::memset(&ia, 0, sizeof ia);
+        ia.nelem = d.nelem;
+        ia.tile_elems = dp->prog.tile_elems;
+        ia.ntiles = dp->prog.ntiles;
+        ia.nworkers = a.nworkers;
+        ia.op = d.op;
+        ia.redop = d.redop;
+        ia.nsrc = (uint32_t)d.srcs.size();
+        ia.ndst = (uint32_t)d.dsts.size();
+        ia.group = d.group;
+        ia.es_first = dtype_size(d.srcs[0].dtype);
+        ia.es_rest = dtype_size(d.srcs.size() > 1 ? d.srcs[1].dtype : d.srcs[0].dtype);
+        ia.es_out = dtype_size(d.dsts[0].dtype);
+        ia.sig = reduce_signature(d.srcs[0].dtype, d.srcs.size() > 1 ? d.srcs[1].dtype : d.srcs[0].dtype,
+                                  d.dsts[0].dtype);
+        for (size_t j = 0; j < d.srcs.size(); ++j) ia.src[j] = (uint64_t)(uintptr_t)a.bufs[d.srcs[j].buf] + d.srcs[j].offset;
+        for (size_t j = 0; j < d.dsts.size(); ++j) ia.dst[j] = (uint64_t)(uintptr_t)a.bufs[d.dsts[j].buf] + d.dsts[j].offset;
+        info.inline_launch = 1;
+        hipError_t e = launch_executor_inline(ia, blocks, kind, s);
+        if (e != hipSuccess) return hip_fail(e, "inline executor launch");
+        return hcclSuccess;
+    }
+
     // a program's counters serve one launch at a time: order launches across streams
     const bool stateful = a.dynamic != 0;
     if (stateful && dp->launched && dp->last_stream != s) {
@@ -345,6 +373,7 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
         int khz = 0;
         if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->device) == hipSuccess && khz > 0)
             c->wall_clock_khz = (uint64_t)khz;
+        c->inline_single_step = !(std::getenv("HCCL_INLINE") && std::strcmp(std::getenv("HCCL_INLINE"), "0") == 0);
         const char* disp = std::getenv("HCCL_DISPATCH");
         c->dynamic_dispatch = disp && std::strcmp(disp, "dynamic") == 0;
         const char* bpc = std::getenv("HCCL_BLOCKS_PER_CU");

@@ -522,6 +522,32 @@ struct Shared {
 // runs on the kernel built for that signature (only that path is compiled in, so registers
 // are allocated for it alone); copy-only programs, and everything else, have their own.
 template <int KIND>
+__device__ __forceinline__ void exec_tile(uint32_t op, uint32_t sig, uint32_t redop, uint32_t es, const TileOps& ops,
+                                          uint32_t n, bool aligned, uint32_t lane) {
+    if (op == OP_REDUCE) {
+        if constexpr (KIND == kKindGeneric) {
+            run_reduce(sig, redop, ops, n, aligned, lane);
+        } else if constexpr (KIND == SIG_BF16) {
+            reduce_tile<DT_BF16, DT_BF16, DT_BF16, RO_SUM>(ops, n, aligned, lane);
+        } else if constexpr (KIND == SIG_FP16) {
+            reduce_tile<DT_FP16, DT_FP16, DT_FP16, RO_SUM>(ops, n, aligned, lane);
+        } else if constexpr (KIND == SIG_FP32) {
+            reduce_tile<DT_FP32, DT_FP32, DT_FP32, RO_SUM>(ops, n, aligned, lane);
+        } else if constexpr (KIND == SIG_INT32) {
+            reduce_tile<DT_INT32, DT_INT32, DT_INT32, RO_SUM>(ops, n, aligned, lane);
+        }
+    } else if (op == OP_COPY) {
+        if constexpr (KIND == kKindCopyAligned) {
+            if (es == 2) copy_tile_aligned<2>(ops, n, lane);
+            else copy_tile_aligned<4>(ops, n, lane);
+        } else {
+            if (es == 2) copy_tile<2>(ops, n, lane);
+            else copy_tile<4>(ops, n, lane);
+        }
+    }
+}
+
+template <int KIND>
 __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, const ProgramHeader& h, uint32_t t,
                                          uint32_t lane, const uint64_t* bufs) {
     const uint32_t d = uni(((const uint32_t*)(prog + h.off_tile_desc))[t]);
@@ -559,29 +585,8 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
             ops.dst = bufs[o.buf] + o.offset + e0 * elem_bytes(o.dtype);
             misaligned |= (ops.dst & 15u) != 0;
         }
-        if (op == OP_REDUCE) {
-            const bool aligned = __ballot(misaligned) == 0ull;
-            if constexpr (KIND == kKindGeneric) {
-                run_reduce(uni(D->sig), uni(D->redop), ops, n, aligned, lane);
-            } else if constexpr (KIND == SIG_BF16) {
-                reduce_tile<DT_BF16, DT_BF16, DT_BF16, RO_SUM>(ops, n, aligned, lane);
-            } else if constexpr (KIND == SIG_FP16) {
-                reduce_tile<DT_FP16, DT_FP16, DT_FP16, RO_SUM>(ops, n, aligned, lane);
-            } else if constexpr (KIND == SIG_FP32) {
-                reduce_tile<DT_FP32, DT_FP32, DT_FP32, RO_SUM>(ops, n, aligned, lane);
-            } else if constexpr (KIND == SIG_INT32) {
-                reduce_tile<DT_INT32, DT_INT32, DT_INT32, RO_SUM>(ops, n, aligned, lane);
-            }
-        } else {
-            const uint32_t es = elem_bytes(uni(opl[uni(D->src)].dtype));
-            if constexpr (KIND == kKindCopyAligned) {
-                if (es == 2) copy_tile_aligned<2>(ops, n, lane);
-                else copy_tile_aligned<4>(ops, n, lane);
-            } else {
-                if (es == 2) copy_tile<2>(ops, n, lane);
-                else copy_tile<4>(ops, n, lane);
-            }
-        }
+        exec_tile<KIND>(op, uni(D->sig), uni(D->redop), elem_bytes(uni(opl[uni(D->src)].dtype)), ops, n,
+                        __ballot(misaligned) == 0ull, lane);
     }
 
     if (flags) {
@@ -650,12 +655,56 @@ __global__ void __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per
     }
 }
 
+// A program of one step needs no device image: its step travels inside the launch packet
+// with every operand already resolved to an address (the analogue of the express doorbell,
+// where the work request itself is the doorbell write and nothing is fetched first).
+template <int KIND>
+__global__ void __launch_bounds__(kBlockThreads) hccl_executor_inline(InlineArgs a) {
+    const uint32_t lane = __lane_id();
+    const uint32_t wave = uni(blockIdx.x * kWavesPerBlock + (threadIdx.x / kWaveSize));
+    const char* kargs = (const char*)__builtin_amdgcn_kernarg_segment_ptr();
+    const uint64_t* srcs = (const uint64_t*)(kargs + offsetof(InlineArgs, src));
+    const uint64_t* dsts = (const uint64_t*)(kargs + offsetof(InlineArgs, dst));
+    TileOps ops;
+    ops.nsrc = a.nsrc;
+    ops.ndst = a.ndst;
+    ops.group = a.group;
+    const uint64_t te = a.tile_elems;
+    for (uint32_t t = wave; t < a.ntiles; t += a.nworkers) {
+        const uint64_t e0 = (uint64_t)t * te;
+        const uint32_t n = (uint32_t)((a.nelem - e0 < te) ? (a.nelem - e0) : te);
+        ops.src = lane < ops.nsrc ? srcs[lane] + e0 * (lane == 0 ? a.es_first : a.es_rest) : 0;
+        ops.dst = lane < ops.ndst ? dsts[lane] + e0 * a.es_out : 0;
+        const bool misaligned = (lane < ops.nsrc && (ops.src & 15u)) || (lane < ops.ndst && (ops.dst & 15u));
+        exec_tile<KIND>(a.op, a.sig, a.redop, a.es_first, ops, n, __ballot(misaligned) == 0ull, lane);
+    }
+}
+
 __global__ void hccl_fill_u32(uint32_t* p, uint64_t n, uint32_t v) {
     uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     for (; i < n; i += (uint64_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
 }  // namespace
+
+hipError_t launch_executor_inline(const InlineArgs& a, uint32_t blocks, int kind, hipStream_t stream) {
+    switch (kind) {
+        case SIG_BF16: hipLaunchKernelGGL(hccl_executor_inline<SIG_BF16>, dim3(blocks), dim3(kBlockThreads), 0, stream, a); break;
+        case SIG_FP16: hipLaunchKernelGGL(hccl_executor_inline<SIG_FP16>, dim3(blocks), dim3(kBlockThreads), 0, stream, a); break;
+        case SIG_FP32: hipLaunchKernelGGL(hccl_executor_inline<SIG_FP32>, dim3(blocks), dim3(kBlockThreads), 0, stream, a); break;
+        case SIG_INT32: hipLaunchKernelGGL(hccl_executor_inline<SIG_INT32>, dim3(blocks), dim3(kBlockThreads), 0, stream, a); break;
+        case kKindCopyOnly:
+            hipLaunchKernelGGL(hccl_executor_inline<kKindCopyOnly>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
+            break;
+        case kKindCopyAligned:
+            hipLaunchKernelGGL(hccl_executor_inline<kKindCopyAligned>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
+            break;
+        default:
+            hipLaunchKernelGGL(hccl_executor_inline<kKindGeneric>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
+            break;
+    }
+    return hipGetLastError();
+}
 
 int executor_block_threads() { return kBlockThreads; }
 int executor_waves_per_block() { return kWavesPerBlock; }

@@ -162,4 +162,24 @@ struct LaunchArgs {
     char* bufs[kMaxBuffers];
 };
 
+// Kernel arguments of a one-step program launched inline: the step and its operands,
+// already resolved to addresses of element 0, travel in the launch packet.
+struct InlineArgs {
+    uint64_t nelem;
+    uint32_t tile_elems;
+    uint32_t ntiles;
+    uint32_t nworkers;
+    uint32_t op;
+    uint32_t sig;
+    uint32_t redop;
+    uint32_t nsrc;
+    uint32_t ndst;
+    uint32_t group;
+    uint32_t es_first;   // element bytes of source 0 (and of a copy)
+    uint32_t es_rest;    // element bytes of the other sources
+    uint32_t es_out;     // element bytes of the destinations
+    uint64_t src[kMaxOperands];
+    uint64_t dst[kMaxOperands];
+};
+
 }  // namespace hccl

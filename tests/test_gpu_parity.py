@@ -258,3 +258,40 @@ def test_launches_on_two_streams_are_ordered():
     for r in range(P):
         assert same_bits(o1[r].result(), want[r], "fp32")
         assert same_bits(o2[r].result(), want[r], "fp32")
+
+
+@pytest.mark.parametrize("dt", ["fp32", "bf16", "fp16", "int32"])
+@pytest.mark.parametrize("P,N", [(8, 1 << 14), (3, 1000), (1, 77), (64, 4099)])
+def test_single_step_programs_travel_inline(dt, P, N):
+    info = run_allreduce(P, N, dt, algo="direct")
+    assert info["inline_launch"] == 1 and info["num_descs"] == 1
+
+
+@pytest.mark.parametrize("op", ["max", "min"])
+def test_single_step_inline_max_min_and_misaligned_views(op):
+    # a buffer view that is 4-byte but not 16-byte aligned takes the element path inline
+    P, N = 4, 3001
+    x = inputs(P, N + 1, "fp32", 30)
+    with H.Comm(P, device=0, algo="direct") as c:
+        send_full = [to_device(x[r], "fp32") for r in range(P)]
+        send = [t[1:] for t in send_full]
+        outs = [Guarded(N + 1, "fp32") for _ in range(P)]
+        H.hccl_allreduce(c.handle, send, [o.view[1:] for o in outs], N, "fp32", op)
+        torch.cuda.synchronize()
+        assert c.last_program()["inline_launch"] == 1
+    want = oracle.allreduce(np.ascontiguousarray(x[:, 1:]), "fp32", op=op)
+    for r in range(P):
+        got = outs[r].result()[1:]
+        assert same_bits(got, want[r], "fp32"), f"rank {r}: {first_mismatch(got, want[r])}"
+
+
+def test_single_step_allgather_copy_inline():
+    run_allgather(1, 5000, "bf16")
+    with H.Comm(1, device=0) as c:
+        x = inputs(1, 4097, "int32", 31)
+        send = [to_device(x[0], "int32")]
+        out = Guarded(4097, "int32")
+        H.hccl_allgather(c.handle, send, [out.view], 4097, "int32")
+        torch.cuda.synchronize()
+        assert c.last_program()["inline_launch"] == 1
+        assert np.array_equal(out.result(), x[0]) and out.guards_intact()
