@@ -70,7 +70,8 @@ def alltoallv_workload(device):
 
 
 def run_headline(args, device):
-    import numpy as np
+    """Times K steps of the grouped AllToAllv (rows + ids in one work packet, one launch),
+    with HIP events around every launch; also times the two calls issued separately."""
     import torch
 
     import paper_2608_00358_amd as H
@@ -85,18 +86,21 @@ def run_headline(args, device):
     row_bytes = int(rows["sendcounts"].sum()) * 2
     id_bytes = int(ids["sendcounts"].sum()) * 4
     comm = H.Comm(P, device=0)
+    rows_call = comm.bind_alltoallv(send_rows, rows["sendcounts"], rows["sdispls"], recv_rows,
+                                    rows["recvcounts"], rows["rdispls"])
+    ids_call = comm.bind_alltoallv(send_ids, ids["sendcounts"], ids["sdispls"], recv_ids,
+                                   ids["recvcounts"], ids["rdispls"])
 
     def step():
-        comm.alltoallv(send_rows, rows["sendcounts"], rows["sdispls"], recv_rows, rows["recvcounts"], rows["rdispls"])
-        comm.alltoallv(send_ids, ids["sendcounts"], ids["sdispls"], recv_ids, ids["recvcounts"], ids["rdispls"])
+        H.hccl_group_start(comm.handle)
+        rows_call()
+        ids_call()
+        H.hccl_group_end(comm.handle)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    info_ids = comm.last_program()
-    comm.alltoallv(send_rows, rows["sendcounts"], rows["sdispls"], recv_rows, rows["recvcounts"], rows["rdispls"])
-    info_rows = comm.last_program()
-    torch.cuda.synchronize()
+    info_step = comm.last_program()
 
     s = torch.cuda.current_stream()
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -105,29 +109,36 @@ def run_headline(args, device):
     t0 = time.perf_counter()
     for i in range(args.steps):
         starts[i].record(s)
-        comm.alltoallv(send_rows, rows["sendcounts"], rows["sdispls"], recv_rows, rows["recvcounts"], rows["rdispls"])
+        step()
         ends[i].record(s)
-        comm.alltoallv(send_ids, ids["sendcounts"], ids["sdispls"], recv_ids, ids["recvcounts"], ids["rdispls"])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     if comm.async_error() != 0:
         raise RuntimeError(H.hccl_get_last_error())
     ms_step = elapsed * 1e3 / args.steps
-    row_ms = [a.elapsed_time(b) for a, b in zip(starts, ends)]
-    row_ms_avg = statistics.mean(row_ms)
+    launch_ms = statistics.mean(a.elapsed_time(b) for a, b in zip(starts, ends))
     algo_step = 2 * (row_bytes + id_bytes)
-    algo_rows = 2 * row_bytes
+
+    # the same two collectives as two launches
+    separate = {}
+    if not args.headline_only:
+        for _ in range(3):
+            rows_call()
+            ids_call()
+        ms_rows = _time_events(rows_call, args.steps)
+        ms_sep = _time_events(lambda: (rows_call(), ids_call()), args.steps)
+        separate = {"rows_launch_us": ms_rows * 1e3, "rows_launch_gbs": 2 * row_bytes / (ms_rows * 1e-3) / 1e9,
+                    "two_launch_step_us": ms_sep * 1e3,
+                    "two_launch_step_gbs": algo_step / (ms_sep * 1e-3) / 1e9}
     recv_counts = w["counts"].sum(axis=0)
     result = {
         "ms_per_step": ms_step,
         "value": algo_step / (ms_step * 1e-3) / 1e9,
-        "row_launch_ms": row_ms_avg,
-        "row_launch_ms_min": min(row_ms),
-        "algo_bytes_rows": algo_rows,
+        "launch_ms": launch_ms,
         "algo_bytes_step": algo_step,
         "recv_imbalance": float(recv_counts.max() / recv_counts.mean()),
-        "program_rows": info_rows,
-        "program_ids": info_ids,
+        "program": info_step,
+        "separate_calls": separate,
     }
     comm.close()
     return result, w
@@ -148,26 +159,26 @@ def bench_allreduce_ring_c1(device, iters=200, cold_sets=40):
     algo = 2 * P * N * 4
     out = {}
     with H.Comm(P, device=0, algo="ring", chunk_bytes=64 * 1024) as c:
-        ms = _time_events(lambda: c.allreduce(send, recv), iters)
+        ms = _time_events(c.bind_allreduce(send, recv), iters)
         info = c.last_program()
         out["warm_us"] = ms * 1e3
         out["warm_gbs"] = algo / (ms * 1e-3) / 1e9
         # cold: rotate through enough buffer sets to defeat the 256 MiB infinity cache
         sets = [([torch.empty(N, dtype=torch.float32, device=device).copy_(t) for t in send],
                  [torch.empty(N, dtype=torch.float32, device=device) for _ in range(P)]) for _ in range(cold_sets)]
+        calls = [c.bind_allreduce(s, r) for s, r in sets]
         k = [0]
 
         def cold():
-            s, r = sets[k[0] % cold_sets]
+            calls[k[0] % cold_sets]()
             k[0] += 1
-            c.allreduce(s, r)
 
         ms = _time_events(cold, iters)
         out["cold_us"] = ms * 1e3
         out["cold_gbs"] = algo / (ms * 1e-3) / 1e9
         # the same program with every ring step as its own dependent descriptor
         c.set_config(algo="ring", chunk_bytes=64 * 1024, fuse=0)
-        ms = _time_events(lambda: c.allreduce(send, recv), iters)
+        ms = _time_events(c.bind_allreduce(send, recv), iters)
         out["unfused_warm_gbs"] = algo / (ms * 1e-3) / 1e9
     out.update({"workload": "allreduce ring P=4 N=2^20 fp32 chunk=64KiB", "algo_bytes": algo,
                 "descs": info["num_descs"], "tiles": info["num_tiles"]})
@@ -241,14 +252,16 @@ def bench_latency_c5b(device, warmup=100, iters=1000, isolated=200):
     with H.Comm(P, device=0, algo="direct") as c:
         for _ in range(warmup):
             c.allreduce(send, recv)
-        ms = _time_events(lambda: c.allreduce(send, recv), iters)
+        ms_marshal = _time_events(lambda: c.allreduce(send, recv), iters)
+        call = c.bind_allreduce(send, recv)
+        ms = _time_events(call, iters)
         s = torch.cuda.current_stream()
         samples = []
         for _ in range(isolated):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             torch.cuda.synchronize()
             a.record(s)
-            c.allreduce(send, recv)
+            call()
             b.record(s)
             b.synchronize()
             samples.append(a.elapsed_time(b) * 1e3)
@@ -256,11 +269,16 @@ def bench_latency_c5b(device, warmup=100, iters=1000, isolated=200):
         for _ in range(isolated):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            c.allreduce(send, recv)
+            call()
             torch.cuda.synchronize()
             t_host.append((time.perf_counter() - t0) * 1e6)
         info = c.last_program()
+    # floor: a one-element torch fill launched back to back on the same stream
+    tiny = torch.zeros(1, device=device)
+    empty_ms = _time_events(lambda: tiny.fill_(1.0), iters)
     return {"workload": "allreduce direct P=8 64KiB/rank fp32", "back_to_back_us": ms * 1e3,
+            "back_to_back_with_python_marshalling_us": ms_marshal * 1e3,
+            "tiny_torch_kernel_back_to_back_us": empty_ms * 1e3, "inline_launch": info["inline_launch"],
             "isolated_median_us": statistics.median(samples),
             "host_roundtrip_median_us": statistics.median(t_host), "workers": info["workers"],
             "tiles": info["num_tiles"]}
@@ -414,6 +432,7 @@ def main():
     ap.add_argument("--headline-only", action="store_true", help="only the timed AllToAllv steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true")
+    ap.add_argument("--latency-only", action="store_true", help="only the 64 KiB all-reduce latency test")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run torch's device copy of 1 GiB (the known-size kernel that scales "
                          "the FETCH_SIZE / WRITE_SIZE counters)")
@@ -442,11 +461,15 @@ def main():
                           "us": ms * 1e3}), flush=True)
         return
 
+    if args.latency_only:
+        print(json.dumps(bench_latency_c5b(device)), flush=True)
+        return
+
     head, w = run_headline(args, device)
     _log(f"alltoallv step {head['ms_per_step']:.3f} ms, {head['value']:.1f} GB/s; "
-         f"row launch {head['row_launch_ms'] * 1e3:.1f} us")
-    achieved = head["algo_bytes_rows"] / (head["row_launch_ms"] * 1e-3) / 1e9
-    traffic = traffic_record("alltoallv_rows_p8_zipf")
+         f"launch {head['launch_ms'] * 1e3:.1f} us")
+    achieved = head["algo_bytes_step"] / (head["launch_ms"] * 1e-3) / 1e9
+    traffic = traffic_record("alltoallv_rows_ids_p8_zipf_group")
     line = {
         "metric": "effective HBM GB/s per collective (% of MI355X HBM peak); small-msg latency us",
         "value": round(head["value"], 2),
@@ -461,17 +484,20 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": "alltoallv P=8 virtual ranks, 2^18 rows/rank of 128 bf16 (64 MiB/rank), "
-                               "Zipf(1.1) destination split, int32 row ids in a second call",
+                               "Zipf(1.1) destination split, int32 row ids alongside; both payloads in one "
+                               "group (one work packet, one executor launch)",
                    "ranks": 8, "rows_per_rank": 1 << 18, "row_elems": 128,
                    "recv_imbalance_max_over_mean": round(head["recv_imbalance"], 3),
-                   "descs_rows": head["program_rows"]["num_descs"],
-                   "workers": head["program_rows"]["workers"]},
+                   "descs": head["program"]["num_descs"], "tiles": head["program"]["num_tiles"],
+                   "workers": head["program"]["workers"]},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": "hccl_executor<copy, 16-byte aligned> (embedding-row launch)",
-                     "algo_bytes_per_launch": head["algo_bytes_rows"],
-                     "avg_launch_us": round(head["row_launch_ms"] * 1e3, 2)},
+                     "kernel": "hccl_executor<12> (copy-only executor; the grouped rows + ids launch)",
+                     "algo_bytes_per_launch": head["algo_bytes_step"],
+                     "avg_launch_us": round(head["launch_ms"] * 1e3, 2)},
     }
+    if head["separate_calls"]:
+        line["config"]["separate_calls"] = {k: round(v, 2) for k, v in head["separate_calls"].items()}
     if not args.headline_only:
         extras = {}
         _log("c1 ring all-reduce")

@@ -136,6 +136,19 @@ hcclResult_t hccl_alltoallv(hcclComm_t comm,
                             void* const* recvbufs, const size_t* recvcounts, const size_t* rdispls,
                             hcclDataType_t dtype, void* stream);
 
+/*
+ * Groups (one work packet for several collectives, Section III-B: a work packet holds
+ * several subgraphs). Collectives called on `comm` between hccl_group_start and the
+ * matching hccl_group_end are checked when called but only recorded; hccl_group_end
+ * compiles them into one program and enqueues it as one executor launch on the stream the
+ * calls named (all calls of a group must name the same stream). Groups nest; only the
+ * outermost end launches. The buffers of different calls in a group must not overlap, and
+ * a group may name at most 128 rank buffers in total (sum of 2 * nranks over its calls).
+ * On an error in hccl_group_end nothing of the group is enqueued.
+ */
+hcclResult_t hccl_group_start(hcclComm_t comm);
+hcclResult_t hccl_group_end(hcclComm_t comm);
+
 /* Thread-local text of the last error returned on this thread ("" if none). */
 const char* hccl_get_last_error(void);
 

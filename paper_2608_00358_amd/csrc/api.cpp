@@ -44,8 +44,15 @@ hcclResult_t hip_fail(hipError_t e, const char* what) {
     return fail(hcclHipError, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-struct DeviceProgram {
+struct Call {
     CollectiveSpec spec;
+    std::vector<const void*> send;
+    std::vector<void*> recv;
+    hipStream_t stream = nullptr;
+};
+
+struct DeviceProgram {
+    std::vector<CollectiveSpec> specs;
     HostProgram prog;
     uint8_t* d_image = nullptr;
     uint32_t* d_state = nullptr;
@@ -71,6 +78,8 @@ struct hcclComm {
     size_t cache_limit = 64;
     bool dynamic_dispatch = false;  // tickets also for programs without dependencies
     bool inline_single_step = true;  // one-step programs travel in the launch packet
+    int group_depth = 0;             // > 0 between hccl_group_start and hccl_group_end
+    std::vector<Call> pending;       // calls recorded inside a group
     hcclProgramInfo_t last{};
 };
 
@@ -138,9 +147,11 @@ hcclResult_t check_buffers(const std::vector<Range>& v, size_t es, Allow allow) 
     return hcclSuccess;
 }
 
-hcclResult_t compile_program(hcclComm* c, const CollectiveSpec& spec, DeviceProgram*& out, bool& hit) {
+// Compiles (or finds in the cache) the program of one work packet: one collective, or the
+// collectives of a group, merged into one program whose steps use disjoint buffer ids.
+hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& specs, DeviceProgram*& out, bool& hit) {
     for (auto it = c->cache.begin(); it != c->cache.end(); ++it) {
-        if ((*it)->spec == spec) {
+        if ((*it)->specs == specs) {
             if (it != c->cache.begin()) c->cache.splice(c->cache.begin(), c->cache, it);
             out = c->cache.front().get();
             hit = true;
@@ -150,14 +161,25 @@ hcclResult_t compile_program(hcclComm* c, const CollectiveSpec& spec, DeviceProg
     hit = false;
     auto t0 = std::chrono::steady_clock::now();
     auto dp = std::make_unique<DeviceProgram>();
-    dp->spec = spec;
+    dp->specs = specs;
     std::string err;
-    if (!lower(spec, dp->prog, err)) return fail(hcclInvalidArgument, err);
-    if (spec.fuse) fuse(dp->prog);
-    if (!finalize(dp->prog, spec.tile_bytes, err)) return fail(hcclInternalError, err);
-    if (c->cfg.validate || c->device == HCCL_NO_DEVICE || env_flag("HCCL_VALIDATE")) {
-        if (!validate(dp->prog, spec, err)) return fail(hcclInternalError, "program validation failed: " + err);
+    const bool check = c->cfg.validate || c->device == HCCL_NO_DEVICE || env_flag("HCCL_VALIDATE");
+    std::vector<HostProgram> parts(specs.size());
+    for (size_t k = 0; k < specs.size(); ++k) {
+        if (!lower(specs[k], parts[k], err)) return fail(hcclInvalidArgument, err);
+        if (specs[k].fuse) fuse(parts[k]);
+        if (check) {
+            HostProgram probe = parts[k];
+            if (!finalize(probe, specs[k].tile_bytes, err)) return fail(hcclInternalError, err);
+            if (!validate(probe, specs[k], err)) return fail(hcclInternalError, "program validation failed: " + err);
+        }
     }
+    if (parts.size() == 1) {
+        dp->prog = std::move(parts[0]);
+    } else if (!merge(parts, specs, dp->prog, err)) {
+        return fail(hcclUnsupported, err);
+    }
+    if (!finalize(dp->prog, specs[0].tile_bytes, err)) return fail(hcclInternalError, err);
     dp->compile_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
 
     if (c->device != HCCL_NO_DEVICE) {
@@ -214,16 +236,19 @@ uint32_t stream_cu_count(hcclComm* c, hipStream_t s) {
     return n;
 }
 
-hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* send, void* const* recv, void* stream) {
+// Compiles and enqueues one work packet (a list of collective calls on one stream).
+hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     DeviceProgram* dp = nullptr;
     bool hit = false;
     DeviceGuard guard(c->device);
-    hcclResult_t r = compile_program(c, spec, dp, hit);
+    std::vector<CollectiveSpec> specs;
+    for (const Call& k : calls) specs.push_back(k.spec);
+    hcclResult_t r = compile_program(c, specs, dp, hit);
     if (r != hcclSuccess) return r;
 
     hcclProgramInfo_t& info = c->last;
     std::memset(&info, 0, sizeof info);
-    info.collective = spec.coll;
+    info.collective = specs.size() == 1 ? specs[0].coll : -1;
     info.algo = dp->prog.algo;
     info.fused = dp->prog.fused ? 1 : 0;
     info.cache_hit = hit ? 1 : 0;
@@ -243,18 +268,23 @@ hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* sen
     r = ensure_scratch(c, dp->prog.scratch_bytes);
     if (r != hcclSuccess) return r;
 
-    hipStream_t s = (hipStream_t)stream;
+    hipStream_t s = calls[0].stream;
     LaunchArgs a;
     std::memset(&a, 0, sizeof a);
     a.prog = dp->d_image;
     a.state = dp->d_state;
     a.error = c->d_error;
-    const int P = c->nranks;
-    for (int i = 0; i < P; ++i) {
-        a.bufs[send_buf(i)] = (char*)send[i];
-        a.bufs[recv_buf(P, i)] = (char*)recv[i];
+    uint32_t base = 0;
+    for (const Call& k : calls) {
+        const int P = k.spec.P;
+        for (int i = 0; i < P; ++i) {
+            a.bufs[base + send_buf(i)] = (char*)k.send[i];
+            a.bufs[base + recv_buf(P, i)] = (char*)k.recv[i];
+        }
+        base += 2 * (uint32_t)P;
     }
-    a.bufs[scratch_buf(P)] = (char*)c->d_scratch;
+    a.bufs[base] = (char*)c->d_scratch;  // the scratch id follows every call's buffers
+    const uint32_t nuser = base;
     const bool has_deps = (dp->prog.flags & PF_HAS_DEPS) != 0;
     a.dynamic = (has_deps || c->dynamic_dispatch) ? 1u : 0u;
     const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
@@ -264,7 +294,7 @@ hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* sen
     uint32_t cus = stream_cu_count(c, s);
     int kind = dp->prog.kind;
     if (kind == kKindCopyAligned) {
-        for (int i = 0; i < 2 * P; ++i)
+        for (uint32_t i = 0; i < nuser; ++i)
             if ((uintptr_t)a.bufs[i] % 16) kind = kKindCopyOnly;
     }
     uint32_t slots = cus * (uint32_t)std::max(1, c->blocks_per_cu[kind]) * wpb;
@@ -316,6 +346,21 @@ hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* sen
         dp->launched = true;
     }
     return hcclSuccess;
+}
+
+hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* send, void* const* recv, void* stream) {
+    Call k;
+    k.spec = spec;
+    k.send.assign(send, send + spec.P);
+    k.recv.assign(recv, recv + spec.P);
+    k.stream = (hipStream_t)stream;
+    if (c->group_depth > 0) {
+        c->pending.push_back(std::move(k));
+        return hcclSuccess;
+    }
+    std::vector<Call> one;
+    one.push_back(std::move(k));
+    return run_packet(c, one);
 }
 
 hcclResult_t fill_spec(hcclComm* c, CollectiveSpec& s, int coll, hcclDataType_t dt, hcclRedOp_t op) {
@@ -532,6 +577,42 @@ hcclResult_t hccl_alltoallv(hcclComm_t comm, const void* const* sendbufs, const 
     if ((r = check_buffers(v, es, [&](const Range& a, const Range& b) { return a.id < P && b.id < P; })))
         return r;
     return run(comm, s, sendbufs, recvbufs, stream);
+}
+
+hcclResult_t hccl_group_start(hcclComm_t comm) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    comm->group_depth += 1;
+    return hcclSuccess;
+}
+
+hcclResult_t hccl_group_end(hcclComm_t comm) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (comm->group_depth == 0) return fail(hcclInvalidArgument, "hccl_group_end without hccl_group_start");
+    if (--comm->group_depth > 0) return hcclSuccess;
+    std::vector<Call> calls;
+    calls.swap(comm->pending);
+    if (calls.empty()) return hcclSuccess;
+    for (const Call& k : calls)
+        if (k.stream != calls[0].stream) return fail(hcclInvalidArgument, "calls of one group must use one stream");
+    uint32_t nbuf = 1;
+    for (const Call& k : calls) nbuf += 2 * (uint32_t)k.spec.P;
+    if (nbuf > (uint32_t)kMaxBuffers) return fail(hcclUnsupported, "a group may name at most 128 rank buffers");
+    // buffers of different calls must not overlap (each call was checked on its own)
+    if (calls.size() > 1) {
+        std::vector<Range> v;
+        int id = 0;
+        for (const Call& k : calls) {
+            BufferSizes sz = buffer_sizes(k.spec, 0);
+            for (int i = 0; i < k.spec.P; ++i) {
+                v.push_back({(uintptr_t)k.send[i], (uintptr_t)k.send[i] + sz.bytes[send_buf(i)], id});
+                v.push_back({(uintptr_t)k.recv[i], (uintptr_t)k.recv[i] + sz.bytes[recv_buf(k.spec.P, i)], id});
+            }
+            ++id;
+        }
+        hcclResult_t r = check_buffers(v, 1, [](const Range& a, const Range& b) { return a.id == b.id; });
+        if (r != hcclSuccess) return fail(hcclInvalidArgument, "buffers of different calls in a group overlap");
+    }
+    return run_packet(comm, calls);
 }
 
 const char* hccl_get_last_error(void) { return g_last_error.c_str(); }

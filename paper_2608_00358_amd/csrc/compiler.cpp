@@ -568,6 +568,71 @@ void fuse(HostProgram& p) {
     if (!uses_scratch) p.scratch_bytes = 0;
 }
 
+// ------------------------------------------------------------------------------ groups
+bool merge(std::vector<HostProgram>& parts, const std::vector<CollectiveSpec>& specs, HostProgram& out,
+           std::string& err) {
+    out = HostProgram();
+    const size_t n = parts.size();
+    std::vector<uint32_t> buf_base(n), nbuf(n);
+    std::vector<uint64_t> scratch_base(n), bytes(n);
+    uint32_t total = 0;
+    uint64_t scratch = 0;
+    for (size_t k = 0; k < n; ++k) {
+        buf_base[k] = total;
+        nbuf[k] = 2u * (uint32_t)specs[k].P;
+        total += nbuf[k];
+        scratch_base[k] = scratch;
+        scratch += (parts[k].scratch_bytes + 255) & ~uint64_t(255);
+        for (const auto& d : parts[k].descs)
+            if (d.alive) bytes[k] += d.nelem * (d.srcs.size() + d.dsts.size());
+    }
+    if (total + 1 > (uint32_t)kMaxBuffers) {
+        err = "a group may name at most 128 rank buffers";
+        return false;
+    }
+    std::vector<size_t> order(n);
+    for (size_t k = 0; k < n; ++k) order[k] = k;
+    std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return bytes[a] < bytes[b]; });
+    const uint32_t scratch_id = total;
+    bool fused = true;
+    for (size_t k : order) {
+        HostProgram& p = parts[k];
+        fused &= p.fused;
+        std::vector<int64_t> remap(p.descs.size(), -1);
+        const uint32_t first = (uint32_t)out.descs.size();
+        for (size_t i = 0; i < p.descs.size(); ++i) {
+            if (!p.descs[i].alive) continue;
+            remap[i] = (int64_t)(first + (out.descs.size() - first));
+            HostDesc d = p.descs[i];
+            for (auto* list : {&d.srcs, &d.dsts}) {
+                for (Operand& o : *list) {
+                    if (o.buf < nbuf[k]) {
+                        o.buf += buf_base[k];
+                    } else {
+                        o.buf = scratch_id;
+                        o.offset += scratch_base[k];
+                    }
+                }
+            }
+            out.descs.push_back(std::move(d));
+        }
+        for (uint32_t i = first; i < out.descs.size(); ++i) {
+            for (Dep& e : out.descs[i].deps) {
+                if (remap[e.desc] < 0) {
+                    err = "dependency on a removed step";
+                    return false;
+                }
+                e.desc = (uint32_t)remap[e.desc];
+            }
+        }
+    }
+    out.P = (int)(total / 2);
+    out.algo = parts[order[0]].algo;
+    out.fused = fused;
+    out.scratch_bytes = scratch;
+    return true;
+}
+
 // ---------------------------------------------------------------------------- packing
 bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     // compact

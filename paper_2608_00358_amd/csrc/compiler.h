@@ -90,6 +90,14 @@ bool lower(const CollectiveSpec& spec, HostProgram& prog, std::string& err);
 // grouped reductions, forwarding copies into extra destinations of their producer.
 void fuse(HostProgram& prog);
 
+// Merges the (lowered, possibly fused) programs of the collectives of one group into one
+// program: call k's buffer ids move up by the ranks of the calls before it (send and
+// receive ids of every call stay disjoint), every call's scratch gets its own region of one
+// shared scratch, and the calls' steps are laid out smallest call first (the calls are
+// independent, so their relative order is free). Returns false if the group is too large.
+bool merge(std::vector<HostProgram>& parts, const std::vector<CollectiveSpec>& specs, HostProgram& out,
+           std::string& err);
+
 // Removes dead descriptors, renumbers dependencies, cuts tiles, sets signal flags and packs
 // the device image. tile_bytes = 0 selects the default.
 bool finalize(HostProgram& prog, uint32_t tile_bytes, std::string& err);

@@ -26,6 +26,7 @@ EXPORTS = [
     "hccl_config_init", "hccl_comm_create", "hccl_comm_destroy", "hccl_comm_set_config",
     "hccl_allreduce", "hccl_reduce_scatter", "hccl_allgather", "hccl_alltoallv",
     "hccl_get_last_error", "hccl_result_string", "hccl_get_async_error", "hccl_comm_last_program",
+    "hccl_group_start", "hccl_group_end",
 ]
 
 
@@ -84,6 +85,8 @@ def load(path: str = LIB_PATH):
     lib.hccl_result_string.restype = ctypes.c_char_p
     lib.hccl_get_async_error.argtypes = [vp]
     lib.hccl_comm_last_program.argtypes = [vp, ctypes.POINTER(hcclProgramInfo_t)]
+    lib.hccl_group_start.argtypes = [vp]
+    lib.hccl_group_end.argtypes = [vp]
     for name in EXPORTS:
         if name not in ("hccl_get_last_error", "hccl_result_string"):
             getattr(lib, name).restype = res
@@ -182,6 +185,14 @@ def hccl_alltoallv(comm, sendbufs, sendcounts, sdispls, recvbufs, recvcounts, rd
                                  _dtype_code(dtype), _stream_handle(stream)))
 
 
+def hccl_group_start(comm) -> None:
+    _check(load().hccl_group_start(comm))
+
+
+def hccl_group_end(comm) -> None:
+    _check(load().hccl_group_end(comm))
+
+
 def hccl_get_last_error() -> str:
     return load().hccl_get_last_error().decode()
 
@@ -199,6 +210,13 @@ def hccl_comm_last_program(comm) -> dict:
     info = hcclProgramInfo_t()
     _check(load().hccl_comm_last_program(comm, ctypes.byref(info)))
     return {name: getattr(info, name) for name, _ in hcclProgramInfo_t._fields_}
+
+
+def _bound(fn, *args):
+    def call():
+        _check(fn(*args))
+
+    return call
 
 
 class Comm:
@@ -243,6 +261,41 @@ class Comm:
 
     def alltoallv(self, send, sendcounts, sdispls, recv, recvcounts, rdispls, stream=None):
         hccl_alltoallv(self.handle, send, sendcounts, sdispls, recv, recvcounts, rdispls, send[0].dtype, stream)
+
+    # The bind_* methods marshal the arguments once and return a no-argument callable that
+    # enqueues the collective: for loops that reuse the same buffers, where per-call ctypes
+    # marshalling would otherwise cost more than a small collective itself.
+    def bind_allreduce(self, send, recv, op="sum", stream=None):
+        return _bound(load().hccl_allreduce, self.handle, _ptr_array(send), _ptr_array(recv), send[0].numel(),
+                      _dtype_code(send[0].dtype), OPS[op], _stream_handle(stream))
+
+    def bind_reduce_scatter(self, send, recv, op="sum", stream=None):
+        return _bound(load().hccl_reduce_scatter, self.handle, _ptr_array(send), _ptr_array(recv), recv[0].numel(),
+                      _dtype_code(send[0].dtype), OPS[op], _stream_handle(stream))
+
+    def bind_allgather(self, send, recv, stream=None):
+        return _bound(load().hccl_allgather, self.handle, _ptr_array(send), _ptr_array(recv), send[0].numel(),
+                      _dtype_code(send[0].dtype), _stream_handle(stream))
+
+    def bind_alltoallv(self, send, sendcounts, sdispls, recv, recvcounts, rdispls, stream=None):
+        return _bound(load().hccl_alltoallv, self.handle, _ptr_array(send), _size_array(sendcounts),
+                      _size_array(sdispls), _ptr_array(recv), _size_array(recvcounts), _size_array(rdispls),
+                      _dtype_code(send[0].dtype), _stream_handle(stream))
+
+    def group(self):
+        """Context manager: the collectives called inside run as one launch at its end."""
+        comm = self
+
+        class _Group:
+            def __enter__(self):
+                hccl_group_start(comm.handle)
+                return comm
+
+            def __exit__(self, exc_type, *exc):
+                hccl_group_end(comm.handle)
+                return False
+
+        return _Group()
 
     def last_program(self) -> dict:
         return hccl_comm_last_program(self.handle)

@@ -208,3 +208,53 @@ def test_empty_collectives_compile_to_nothing():
         z = np.zeros((4, 4), dtype=np.int64)
         H.hccl_alltoallv(c.handle, fake_bufs(4, 1 << 40), z, z, fake_bufs(4, 1 << 44), z, z, "bf16")
         assert info_of(c)["num_tiles"] == 0
+
+
+# -------------------------------------------------------------------------- groups
+def test_group_merges_calls_into_one_program():
+    P = 4
+    with comm(P, algo="ring", fuse=0, chunk_bytes=4096) as c:
+        s1, r1 = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+        H.hccl_allreduce(c.handle, s1, r1, 5000, "bf16")
+        one = info_of(c)
+        s2, r2 = fake_bufs(P, 1 << 42), fake_bufs(P, 1 << 46)
+        H.hccl_reduce_scatter(c.handle, s2, r2, 3000, "fp32")
+        two = info_of(c)
+        H.hccl_group_start(c.handle)
+        H.hccl_allreduce(c.handle, s1, r1, 5000, "bf16")
+        H.hccl_reduce_scatter(c.handle, s2, r2, 3000, "fp32")
+        H.hccl_group_end(c.handle)
+        g = info_of(c)
+    assert g["num_descs"] == one["num_descs"] + two["num_descs"]
+    assert g["num_deps"] == one["num_deps"] + two["num_deps"]
+    assert g["bytes_read"] == one["bytes_read"] + two["bytes_read"]
+    assert g["scratch_bytes"] >= one["scratch_bytes"] + two["scratch_bytes"]
+    assert g["collective"] == -1
+
+
+def test_group_rejects_overlap_between_calls_and_unbalanced_end():
+    P = 2
+    with comm(P) as c:
+        s, r = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+        H.hccl_group_start(c.handle)
+        H.hccl_allreduce(c.handle, s, r, 100, "fp32")
+        H.hccl_allreduce(c.handle, r, fake_bufs(P, 1 << 42), 100, "fp32")   # reads what the first writes
+        _expect(1, H.hccl_group_end, c.handle)
+        _expect(1, H.hccl_group_end, c.handle)
+
+
+def test_group_rejects_too_many_buffers_and_nests():
+    with comm(64) as c:
+        H.hccl_group_start(c.handle)
+        H.hccl_group_start(c.handle)      # nested: only the outer end launches
+        for k in range(2):
+            H.hccl_allgather(c.handle, fake_bufs(64, (1 << 40) + k * (1 << 35)),
+                             fake_bufs(64, (1 << 44) + k * (1 << 35)), 10, "bf16")
+        H.hccl_group_end(c.handle)
+        _expect(2, H.hccl_group_end, c.handle)   # 2 x 128 rank buffers > 128
+
+
+def test_empty_group_is_a_no_op():
+    with comm(2) as c:
+        H.hccl_group_start(c.handle)
+        H.hccl_group_end(c.handle)

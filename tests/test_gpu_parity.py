@@ -295,3 +295,61 @@ def test_single_step_allgather_copy_inline():
         torch.cuda.synchronize()
         assert c.last_program()["inline_launch"] == 1
         assert np.array_equal(out.result(), x[0]) and out.guards_intact()
+
+
+def test_group_of_embedding_rows_and_ids_is_one_launch():
+    P = 8
+    counts = zipf_counts(P, 5000, 1.1, seed=40)
+    rows, ids = alltoallv_layout(counts, 128), alltoallv_layout(counts, 1)
+    rng = np.random.default_rng(41)
+    rows_h = [rng.integers(0, 2 ** 16, int(rows["send_len"][s]), dtype=np.int64).astype(np.uint16) for s in range(P)]
+    ids_h = [rng.integers(-2 ** 31, 2 ** 31, int(ids["send_len"][s]), dtype=np.int64).astype(np.int32) for s in range(P)]
+    print("group: alltoallv rows + ids", flush=True)
+    with H.Comm(P, device=0) as c:
+        sr = [to_device(rows_h[s], "bf16") for s in range(P)]
+        si = [to_device(ids_h[s], "int32") for s in range(P)]
+        rr = [Guarded(int(rows["recv_len"][d]), "bf16") for d in range(P)]
+        ri = [Guarded(int(ids["recv_len"][d]), "int32") for d in range(P)]
+        with c.group():
+            c.alltoallv(sr, rows["sendcounts"], rows["sdispls"], [o.view for o in rr], rows["recvcounts"], rows["rdispls"])
+            c.alltoallv(si, ids["sendcounts"], ids["sdispls"], [o.view for o in ri], ids["recvcounts"], ids["rdispls"])
+        torch.cuda.synchronize()
+        info = c.last_program()
+        assert c.async_error() == 0
+    assert info["collective"] == -1
+    want_r = [np.zeros(o.n, np.uint16) for o in rr]
+    want_i = [np.zeros(o.n, np.int32) for o in ri]
+    oracle.alltoallv(rows_h, rows["sendcounts"], rows["sdispls"], want_r, rows["recvcounts"], rows["rdispls"])
+    oracle.alltoallv(ids_h, ids["sendcounts"], ids["sdispls"], want_i, ids["recvcounts"], ids["rdispls"])
+    for d in range(P):
+        assert np.array_equal(rr[d].result(), want_r[d]) and rr[d].guards_intact(), f"rows {d}"
+        assert np.array_equal(ri[d].result(), want_i[d]) and ri[d].guards_intact(), f"ids {d}"
+
+
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_group_of_dependent_programs_with_scratch(fuse):
+    # two unfused ring collectives with FP32 scratch partials and dependency chains in one launch
+    P = 4
+    xa = inputs(P, 20000, "bf16", 42)
+    xb = inputs(P, P * 3001, "bf16", 43)
+    xc = inputs(P, 777, "fp32", 44)
+    print(f"group: allreduce + reduce_scatter + allgather, fuse={fuse}", flush=True)
+    with H.Comm(P, device=0, algo="ring", fuse=fuse, chunk_bytes=4096, tile_bytes=4096) as c:
+        sa = [to_device(xa[r], "bf16") for r in range(P)]
+        sb = [to_device(xb[r], "bf16") for r in range(P)]
+        sc = [to_device(xc[r], "fp32") for r in range(P)]
+        oa = [Guarded(20000, "bf16") for _ in range(P)]
+        ob = [Guarded(3001, "bf16") for _ in range(P)]
+        oc = [Guarded(P * 777, "fp32") for _ in range(P)]
+        for _ in range(3):
+            with c.group():
+                c.allreduce(sa, [o.view for o in oa])
+                c.reduce_scatter(sb, [o.view for o in ob])
+                c.allgather(sc, [o.view for o in oc])
+            torch.cuda.synchronize()
+            assert c.async_error() == 0
+    wa, wb, wc = oracle.allreduce(xa, "bf16"), oracle.reduce_scatter(xb, "bf16"), oracle.allgather(xc)
+    for r in range(P):
+        assert same_bits(oa[r].result(), wa[r], "bf16") and oa[r].guards_intact()
+        assert same_bits(ob[r].result(), wb[r], "bf16") and ob[r].guards_intact()
+        assert np.array_equal(oc[r].result().view(np.uint8), wc[r].view(np.uint8)) and oc[r].guards_intact()
