@@ -32,6 +32,17 @@ NP_STORAGE = {"bf16": np.uint16, "fp16": np.uint16, "fp32": np.float32, "int32":
 
 _lib = None
 
+ORDERS = {"ascending": 0, "two_level": 1, "ring": 2, "halving": 3}
+
+
+class OrderSpec(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("group", ctypes.c_int), ("shard", ctypes.c_size_t),
+                ("requant", ctypes.c_int)]
+
+
+def _order(order: str, group: int, shard: int, requant: bool) -> OrderSpec:
+    return OrderSpec(ORDERS[order], int(group), int(shard), 1 if requant else 0)
+
 
 def build(force: bool = True) -> str:
     """Compile the oracle with gcc (no fast-math, no FP contraction)."""
@@ -77,6 +88,10 @@ def _bind(lib):
     lib.orc_allgather.argtypes = [i, sz, sz, vpp, vpp]
     lib.orc_alltoallv.restype = i
     lib.orc_alltoallv.argtypes = [i, sz, vpp, szp, szp, vpp, szp, szp]
+    lib.orc_allreduce_ordered.restype = i
+    lib.orc_allreduce_ordered.argtypes = [i, sz, i, i, ctypes.POINTER(OrderSpec), vpp, vpp]
+    lib.orc_reduce_scatter_ordered.restype = i
+    lib.orc_reduce_scatter_ordered.argtypes = [i, sz, i, i, ctypes.POINTER(OrderSpec), vpp, vpp]
     return lib
 
 
@@ -168,6 +183,39 @@ def reduce_scatter(x: np.ndarray, dtype: str, op: str = "sum", group: int = 0) -
     rc = _load().orc_reduce_scatter(P, M, DTYPES[dtype], OPS[op], group, _ptrs(rows), _ptrs(out))
     if rc != 0:
         raise ValueError(f"orc_reduce_scatter rejected its arguments (rc={rc})")
+    return np.stack(out)
+
+
+def allreduce_ordered(x: np.ndarray, dtype: str, order: str = "ascending", op: str = "sum", group: int = 0,
+                      shard: int = 0, requant: bool = False) -> np.ndarray:
+    """All-reduce in an explicit fold order (see hccl_oracle.h): "ascending", "two_level"
+    (group), "ring" (rotated per shard of `shard` elements), "halving"; requant rounds every
+    partial to the buffer type."""
+    P, N = x.shape
+    rows = _rows(x, dtype)
+    out = [np.empty(N, dtype=NP_STORAGE[dtype]) for _ in range(P)]
+    spec = _order(order, group, shard, requant)
+    rc = _load().orc_allreduce_ordered(P, N, DTYPES[dtype], OPS[op], ctypes.byref(spec), _ptrs(rows), _ptrs(out))
+    if rc != 0:
+        raise ValueError(f"orc_allreduce_ordered rejected its arguments (rc={rc})")
+    return np.stack(out)
+
+
+def reduce_scatter_ordered(x: np.ndarray, dtype: str, order: str = "ascending", op: str = "sum",
+                           group: int = 0, requant: bool = False) -> np.ndarray:
+    """Reduce-scatter in an explicit fold order; for "ring", block c is folded starting at
+    contributor c+1."""
+    P, total = x.shape
+    if total % P:
+        raise ValueError("reduce_scatter input length must be a multiple of P")
+    M = total // P
+    rows = _rows(x, dtype)
+    out = [np.empty(M, dtype=NP_STORAGE[dtype]) for _ in range(P)]
+    spec = _order(order, group, 0, requant)
+    rc = _load().orc_reduce_scatter_ordered(P, M, DTYPES[dtype], OPS[op], ctypes.byref(spec), _ptrs(rows),
+                                            _ptrs(out))
+    if rc != 0:
+        raise ValueError(f"orc_reduce_scatter_ordered rejected its arguments (rc={rc})")
     return np.stack(out)
 
 

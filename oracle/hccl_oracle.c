@@ -237,8 +237,117 @@ static int check_reduce_args(int P, int dtype, int op, int group) {
 }
 
 /* ------------------------------------------------------------------------------------- */
+/* Other fold orders                                                                      */
+/* ------------------------------------------------------------------------------------- */
+
+/* Round an FP32 running value to the buffer type and widen it again. */
+static float requantize(int dtype, float v) {
+    if (dtype == ORC_BF16) return orc_bf16_to_f32(orc_f32_to_bf16(v));
+    if (dtype == ORC_FP16) return orc_f16_to_f32(orc_f32_to_f16(v));
+    return v;
+}
+
+static float comb_q(int op, int dtype, int requant, float acc, float x) {
+    float v = combine_f32(op, acc, x);
+    return requant ? requantize(dtype, v) : v;
+}
+
+/*
+ * One element of shard `c` (or any shard for the orders that ignore it), folded in the
+ * order `ord` describes. Returns the FP32 value before the final rounding.
+ */
+static float reduce_column_ordered_f32(int P, int dtype, int op, const orc_order* ord, int c,
+                                       const void* const* src, size_t i) {
+    int q = ord->requant;
+    if (ord->kind == ORC_ORDER_RING) {
+        int first = (c + 1) % P;
+        float acc = load_as_f32(src[first], dtype, i);
+        for (int k = 1; k < P; ++k) acc = comb_q(op, dtype, q, acc, load_as_f32(src[(first + k) % P], dtype, i));
+        return acc;
+    }
+    if (ord->kind == ORC_ORDER_HALVING) {
+        float v[512];
+        for (int r = 0; r < P; ++r) v[r] = load_as_f32(src[r], dtype, i);
+        for (int d = P / 2; d >= 1; d /= 2)
+            for (int r = 0; r < d; ++r) v[r] = comb_q(op, dtype, q, v[r], v[r + d]);
+        return v[0];
+    }
+    int group = (ord->kind == ORC_ORDER_TWO_LEVEL) ? ord->group : P;
+    float total = 0.0f;
+    for (int g = 0; g * group < P; ++g) {
+        int first = g * group;
+        float part = load_as_f32(src[first], dtype, i);
+        for (int r = first + 1; r < first + group; ++r)
+            part = comb_q(op, dtype, q, part, load_as_f32(src[r], dtype, i));
+        total = (g == 0) ? part : comb_q(op, dtype, q, total, part);
+    }
+    return total;
+}
+
+static int32_t reduce_column_ordered_i32(int P, int op, const orc_order* ord, int c,
+                                         const void* const* src, size_t i) {
+    if (ord->kind == ORC_ORDER_RING) {
+        int first = (c + 1) % P;
+        int32_t acc = ((const int32_t*)src[first])[i];
+        for (int k = 1; k < P; ++k) acc = combine_i32(op, acc, ((const int32_t*)src[(first + k) % P])[i]);
+        return acc;
+    }
+    if (ord->kind == ORC_ORDER_HALVING) {
+        int32_t v[512];
+        for (int r = 0; r < P; ++r) v[r] = ((const int32_t*)src[r])[i];
+        for (int d = P / 2; d >= 1; d /= 2)
+            for (int r = 0; r < d; ++r) v[r] = combine_i32(op, v[r], v[r + d]);
+        return v[0];
+    }
+    return reduce_column_i32(P, op, ord->kind == ORC_ORDER_TWO_LEVEL ? ord->group : 0, src, i);
+}
+
+static int check_order(int P, const orc_order* ord) {
+    if (!ord) return -1;
+    if (P > 512) return -1;
+    if (ord->kind == ORC_ORDER_TWO_LEVEL && (ord->group < 1 || P % ord->group)) return -1;
+    if (ord->kind == ORC_ORDER_HALVING && (P & (P - 1))) return -1;
+    if (ord->kind < ORC_ORDER_ASCENDING || ord->kind > ORC_ORDER_HALVING) return -1;
+    return 0;
+}
+
+/* ------------------------------------------------------------------------------------- */
 /* Collectives                                                                            */
 /* ------------------------------------------------------------------------------------- */
+
+int orc_allreduce_ordered(int P, size_t count, int dtype, int op, const orc_order* ord,
+                          const void* const* send, void* const* recv) {
+    if (check_reduce_args(P, dtype, op, 0) != 0 || check_order(P, ord) != 0) return -1;
+    if (ord->kind == ORC_ORDER_RING && ord->shard == 0) return -1;
+    for (size_t i = 0; i < count; ++i) {
+        int c = (ord->kind == ORC_ORDER_RING && ord->shard) ? (int)(i / ord->shard) : 0;
+        if (dtype == ORC_INT32) {
+            int32_t v = reduce_column_ordered_i32(P, op, ord, c, send, i);
+            for (int r = 0; r < P; ++r) ((int32_t*)recv[r])[i] = v;
+        } else {
+            float v = reduce_column_ordered_f32(P, dtype, op, ord, c, send, i);
+            for (int r = 0; r < P; ++r) store_from_f32(recv[r], dtype, i, v);
+        }
+    }
+    return 0;
+}
+
+int orc_reduce_scatter_ordered(int P, size_t recvcount, int dtype, int op, const orc_order* ord,
+                               const void* const* send, void* const* recv) {
+    if (check_reduce_args(P, dtype, op, 0) != 0 || check_order(P, ord) != 0) return -1;
+    size_t es = dtype_size(dtype);
+    const void* block[512];
+    for (int c = 0; c < P; ++c) {
+        for (int r = 0; r < P; ++r) block[r] = (const char*)send[r] + (size_t)c * recvcount * es;
+        for (size_t j = 0; j < recvcount; ++j) {
+            if (dtype == ORC_INT32)
+                ((int32_t*)recv[c])[j] = reduce_column_ordered_i32(P, op, ord, c, block, j);
+            else
+                store_from_f32(recv[c], dtype, j, reduce_column_ordered_f32(P, dtype, op, ord, c, block, j));
+        }
+    }
+    return 0;
+}
 
 /*
  * AllReduce. Every output element is written only after all P inputs of that element have

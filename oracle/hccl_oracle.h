@@ -36,6 +36,36 @@ extern "C" {
 enum { ORC_BF16 = 0, ORC_FP16 = 1, ORC_FP32 = 2, ORC_INT32 = 3 };
 enum { ORC_SUM = 0, ORC_MAX = 1, ORC_MIN = 2 };
 
+/*
+ * Fold orders beyond the default (paper: Section III-B ring AllReduce; Section II-A-2: the
+ * near-memory compute unit re-quantises every result to the buffer type).
+ *   ORC_ORDER_ASCENDING : contributors 0, 1, ..., P-1.
+ *   ORC_ORDER_TWO_LEVEL : `group` consecutive ranks folded ascending into a partial, then the
+ *                         partials ascending.
+ *   ORC_ORDER_RING      : the element belongs to shard c; contributors are visited
+ *                         c+1, c+2, ..., P-1, 0, ..., c (the order a ring reduce-scatter adds
+ *                         them as the partial travels towards its owner c). For all-reduce the
+ *                         shard of element i is i / shard; for reduce-scatter it is the block.
+ *   ORC_ORDER_HALVING   : recursive halving (P a power of two): level by level, value r is
+ *                         combined with value r + d for d = P/2, P/4, ..., 1; the result is
+ *                         value 0.
+ * requant != 0: after every combine the running value is rounded to the buffer type and
+ * widened again (no effect for FP32 and INT32).
+ */
+enum { ORC_ORDER_ASCENDING = 0, ORC_ORDER_TWO_LEVEL = 1, ORC_ORDER_RING = 2, ORC_ORDER_HALVING = 3 };
+
+typedef struct {
+    int kind;
+    int group;       /* ORC_ORDER_TWO_LEVEL */
+    size_t shard;    /* ORC_ORDER_RING, all-reduce: elements per shard */
+    int requant;
+} orc_order;
+
+int orc_allreduce_ordered(int P, size_t count, int dtype, int op, const orc_order* order,
+                          const void* const* send, void* const* recv);
+int orc_reduce_scatter_ordered(int P, size_t recvcount, int dtype, int op, const orc_order* order,
+                               const void* const* send, void* const* recv);
+
 /* Scalar conversions, written from the IEEE-754 binary16 / bfloat16 definitions. */
 float    orc_bf16_to_f32(uint16_t h);
 uint16_t orc_f32_to_bf16(float f);

@@ -11,6 +11,7 @@ import subprocess
 import pytest
 
 import oracle
+import test_oracle_order_pins as order_pins
 import test_oracle_pins as pins
 
 _SRC = os.path.join(os.path.dirname(oracle.__file__), "hccl_oracle.c")
@@ -39,8 +40,12 @@ MUTANTS = {
         "int shift = 13 - he;",
     ),
     "reduce_scatter_wrong_block": (
-        "block[r] = (const char*)send[r] + (size_t)c * recvcount * es;",
-        "block[r] = (const char*)send[r] + (size_t)r * recvcount * es;",
+        "\n            block[r] = (const char*)send[r] + (size_t)c * recvcount * es;",
+        "\n            block[r] = (const char*)send[r] + (size_t)r * recvcount * es;",
+    ),
+    "ordered_reduce_scatter_wrong_block": (
+        "++r) block[r] = (const char*)send[r] + (size_t)c * recvcount * es;",
+        "++r) block[r] = (const char*)send[r] + (size_t)r * recvcount * es;",
     ),
     "allgather_wrong_block": (
         "memcpy((char*)recv[r] + (size_t)q * bytes, send[q], bytes);",
@@ -60,6 +65,18 @@ MUTANTS = {
         "if (op == ORC_SUM) { long long s = (long long)acc + x; "
         "return s > 2147483647LL ? 2147483647 : (s < -2147483648LL ? (int32_t)-2147483648LL : (int32_t)s); }",
     ),
+    "halving_distances_doubling": (
+        "for (int d = P / 2; d >= 1; d /= 2)\n            for (int r = 0; r < d; ++r) v[r] = comb_q(op, dtype, q, v[r], v[r + d]);",
+        "for (int d = 1; d < P; d *= 2)\n            for (int r = 0; r + d < P; r += 2 * d) v[r] = comb_q(op, dtype, q, v[r], v[r + d]);",
+    ),
+    "ring_starts_at_the_owner": (
+        "int first = (c + 1) % P;\n        float acc",
+        "int first = c % P;\n        float acc",
+    ),
+    "requant_ignored": (
+        "return requant ? requantize(dtype, v) : v;",
+        "return v;",
+    ),
 }
 
 # The pins run against every mutant (cheap ones, CPU only).
@@ -77,6 +94,10 @@ PIN_CALLS = [
     ("rs brute", lambda: pins.test_reduce_scatter_brute_force(4, 7)),
     ("ag brute", lambda: pins.test_allgather_brute_force(3, 1)),
     ("a2av brute", lambda: pins.test_alltoallv_brute_force_with_gaps_and_zero_blocks()),
+    ("ring order", lambda: order_pins.test_ring_order_reduce_scatter_is_the_rotated_numpy_fold(5)),
+    ("halving order", lambda: order_pins.test_halving_order_is_the_distance_halving_tree(8)),
+    ("order cancellation", lambda: order_pins.test_orders_are_told_apart_by_cancellation()),
+    ("requant", lambda: order_pins.test_requant_rounds_every_partial_to_bf16("ascending")),
 ]
 
 
