@@ -63,11 +63,27 @@ typedef enum { hcclSum = 0, hcclMax = 1, hcclMin = 2 } hcclRedOp_t;
  * TWO_LEVEL, which folds ascending inside each group of `group_size` consecutive ranks
  * into FP32 partials and then folds the partials in ascending group order. */
 typedef enum {
-    hcclAlgoAuto = 0,     /* TWO_LEVEL when group_size splits nranks, else RING */
+    hcclAlgoAuto = 0,     /* TWO_LEVEL when group_size splits nranks, RHD for the HALVING order,
+                             else RING */
     hcclAlgoDirect = 1,   /* one step per chunk: read all contributors, write all destinations */
     hcclAlgoRing = 2,     /* ring pipeline: P-1 reduce steps per chunk, then P-1 forwarding hops */
     hcclAlgoTwoLevel = 3, /* group reduce-scatter, inter-group all-reduce of shards, group all-gather */
+    hcclAlgoRhd = 4,      /* recursive halving reduce-scatter (+ recursive doubling all-gather);
+                             nranks must be a power of two */
 } hcclAlgo_t;
+
+/* Order in which the contributors of an element are folded (the result depends on it).
+ * ASCENDING: ranks 0, 1, ..., P-1 (TWO_LEVEL: ascending inside each group, then over groups).
+ * RING: an element of shard c is folded starting at rank c+1: c+1, c+2, ..., P-1, 0, ..., c,
+ *   the order a ring reduce-scatter accumulates it (Section III-B ring AllReduce). For
+ *   reduce-scatter, shard c is block c; for all-reduce, element i is in shard i / q with
+ *   q = ceil(count / P) rounded up to a multiple of 64.
+ * HALVING: the recursive-halving tree: values whose rank differs in bit P/2 are combined first,
+ *   then bit P/4, ..., then bit 1 (nranks must be a power of two).
+ * With `requantize` set, every partial is rounded to the buffer type as soon as it is formed
+ * (the near-memory compute unit re-quantises each result, Section II-A-2); otherwise partials
+ * stay FP32 and the result is rounded once. */
+typedef enum { hcclOrderAscending = 0, hcclOrderRing = 1, hcclOrderHalving = 2 } hcclOrder_t;
 
 typedef struct {
     int32_t algo;          /* hcclAlgo_t */
@@ -79,7 +95,9 @@ typedef struct {
     uint32_t tile_bytes;   /* work claimed per ticket, bytes read per tile (0 = default) */
     uint32_t timeout_ms;   /* watchdog for one dependency wait on the device (0 = 2000) */
     int32_t validate;      /* 1 = run the program validator on every compile */
-    int32_t reserved[5];
+    int32_t order;         /* hcclOrder_t */
+    int32_t requantize;    /* 1 = round every partial to the buffer type */
+    int32_t reserved[3];
 } hcclConfig_t;
 
 typedef struct hcclComm* hcclComm_t;

@@ -166,7 +166,7 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
     const bool check = c->cfg.validate || c->device == HCCL_NO_DEVICE || env_flag("HCCL_VALIDATE");
     std::vector<HostProgram> parts(specs.size());
     for (size_t k = 0; k < specs.size(); ++k) {
-        if (!lower(specs[k], parts[k], err)) return fail(hcclInvalidArgument, err);
+        if (!lower(specs[k], parts[k], err)) return fail(hcclUnsupported, err);
         if (specs[k].fuse) fuse(parts[k]);
         if (check) {
             HostProgram probe = parts[k];
@@ -318,6 +318,8 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         ia.nsrc = (uint32_t)d.srcs.size();
         ia.ndst = (uint32_t)d.dsts.size();
         ia.group = d.group;
+        ia.fold = d.fold;
+        ia.requant = d.requant ? 1u : 0u;
         ia.es_first = dtype_size(d.srcs[0].dtype);
         ia.es_rest = dtype_size(d.srcs.size() > 1 ? d.srcs[1].dtype : d.srcs[0].dtype);
         ia.es_out = dtype_size(d.dsts[0].dtype);
@@ -373,7 +375,10 @@ hcclResult_t fill_spec(hcclComm* c, CollectiveSpec& s, int coll, hcclDataType_t 
     s.chunk_bytes = c->cfg.chunk_bytes;
     s.fuse = c->cfg.fuse != 0;
     s.tile_bytes = c->cfg.tile_bytes;
-    if (s.algo < hcclAlgoAuto || s.algo > hcclAlgoTwoLevel) return fail(hcclInvalidArgument, "unknown algorithm");
+    s.order = c->cfg.order;
+    s.requant = c->cfg.requantize != 0;
+    if (s.algo < hcclAlgoAuto || s.algo > hcclAlgoRhd) return fail(hcclInvalidArgument, "unknown algorithm");
+    if (s.order < hcclOrderAscending || s.order > hcclOrderHalving) return fail(hcclInvalidArgument, "unknown order");
     return hcclSuccess;
 }
 

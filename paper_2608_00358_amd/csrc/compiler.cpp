@@ -33,11 +33,33 @@ constexpr uint64_t kSmallTargetTiles = 2048;
 constexpr uint32_t kWaveStepElems = kWaveSize * kVecElems;  // 512: one vector per lane
 constexpr uint64_t kShardAlignElems = 64;                      // 128 B of bf16, 256 B of fp32
 
-uint32_t acc_dtype(int dtype, int redop) {
-    if (dtype == DT_INT32) return DT_INT32;
-    // MAX / MIN are exact in any floating type: partials keep the buffer type.
-    if (redop != RO_SUM) return (uint32_t)dtype;
+// Type of partials that leave registers: FP32 for floating sums (one rounding at the end),
+// the buffer type when every partial is re-quantised, or for MAX / MIN (exact in any type).
+uint32_t acc_dtype(const CollectiveSpec& s) {
+    if (s.dtype == DT_INT32) return DT_INT32;
+    if (s.redop != RO_SUM || s.requant) return (uint32_t)s.dtype;
     return DT_FP32;
+}
+
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+// Contributors of an element of shard (or block) c in fold order.
+std::vector<int> contributor_order(const CollectiveSpec& s, int c) {
+    const int P = s.P;
+    std::vector<int> v(P);
+    for (int k = 0; k < P; ++k) {
+        if (s.order == ORDER_RING) {
+            v[k] = (c + 1 + k) % P;
+        } else if (s.order == ORDER_HALVING) {
+            int r = 0;  // bit reversal of k: adjacent list entries differ in bit P/2, pairs of
+            for (int b = 1, t = P >> 1; b < P; b <<= 1, t >>= 1)  // pairs in bit P/4, ...
+                if (k & b) r |= t;
+            v[k] = r;
+        } else {
+            v[k] = k;
+        }
+    }
+    return v;
 }
 
 uint64_t chunk_elems(const CollectiveSpec& s) {
@@ -45,11 +67,6 @@ uint64_t chunk_elems(const CollectiveSpec& s) {
     uint64_t c = bytes / dtype_size(s.dtype);
     c = (c / kShardAlignElems) * kShardAlignElems;
     return std::max<uint64_t>(c, kShardAlignElems);
-}
-
-uint64_t shard_size(uint64_t n, int parts) {
-    uint64_t q = (n + parts - 1) / parts;
-    return ((q + kShardAlignElems - 1) / kShardAlignElems) * kShardAlignElems;
 }
 
 Operand opnd(uint32_t buf, uint32_t dtype, uint64_t elem_offset) {
@@ -93,20 +110,30 @@ void lower_direct(const CollectiveSpec& s, HostProgram& p) {
     const int P = s.P;
     const uint64_t C = chunk_elems(s);
     const uint32_t dt = (uint32_t)s.dtype;
+    const uint32_t fold = (s.order == ORDER_HALVING) ? FOLD_PAIRWISE : FOLD_LIST;
+    auto reduce_step = [&](uint64_t n, const std::vector<int>& order, uint64_t src_elem, std::vector<Operand> dst) {
+        std::vector<Operand> src;
+        for (int r : order) src.push_back(opnd(send_buf(r), dt, src_elem));
+        uint32_t i = b.add(OP_REDUCE, (uint8_t)s.redop, n, src, std::move(dst));
+        p.descs[i].fold = fold;
+    };
     if (s.coll == COLL_ALLREDUCE) {
-        for_chunks(0, s.count, C, [&](uint32_t, uint64_t o, uint64_t n) {
-            std::vector<Operand> src, dst;
-            for (int r = 0; r < P; ++r) src.push_back(opnd(send_buf(r), dt, o));
-            for (int r = 0; r < P; ++r) dst.push_back(opnd(recv_buf(P, r), dt, o));
-            b.add(OP_REDUCE, (uint8_t)s.redop, n, src, dst);
-        });
+        // the ring order rotates per shard, so chunks never straddle a shard boundary then
+        const uint64_t q = (s.order == ORDER_RING) ? shard_size(s.count, P) : s.count;
+        for (uint64_t lo = 0, c = 0; lo < s.count; lo += q, ++c) {
+            const std::vector<int> order = contributor_order(s, (int)c);
+            for_chunks(lo, std::min(s.count, lo + q), C, [&](uint32_t, uint64_t o, uint64_t n) {
+                std::vector<Operand> dst;
+                for (int r = 0; r < P; ++r) dst.push_back(opnd(recv_buf(P, r), dt, o));
+                reduce_step(n, order, o, dst);
+            });
+        }
     } else if (s.coll == COLL_REDUCE_SCATTER) {
         const uint64_t M = s.count;
         for (int c = 0; c < P; ++c) {
+            const std::vector<int> order = contributor_order(s, c);
             for_chunks(0, M, C, [&](uint32_t, uint64_t o, uint64_t n) {
-                std::vector<Operand> src;
-                for (int r = 0; r < P; ++r) src.push_back(opnd(send_buf(r), dt, (uint64_t)c * M + o));
-                b.add(OP_REDUCE, (uint8_t)s.redop, n, src, {opnd(recv_buf(P, c), dt, o)});
+                reduce_step(n, order, (uint64_t)c * M + o, {opnd(recv_buf(P, c), dt, o)});
             });
         }
     } else if (s.coll == COLL_ALLGATHER) {
@@ -128,6 +155,7 @@ void lower_direct(const CollectiveSpec& s, HostProgram& p) {
 // rounds into `final_dst`. Steps of all chunks are emitted step-major so every chunk's step
 // t is available while step t+1 waits only for the same tile of its own chain.
 struct Chain {
+    int owner = 0;        // shard / block the chain reduces (fixes the ring order's start)
     uint64_t src_elem;    // element offset of the chunk in every send buffer
     uint64_t nelem;
     Operand final_dst;
@@ -140,20 +168,23 @@ void emit_reduce_chains(const CollectiveSpec& s, HostProgram& p, std::vector<Cha
     Builder b{p};
     const int P = s.P;
     const uint32_t dt = (uint32_t)s.dtype;
-    const uint32_t acc = acc_dtype(s.dtype, s.redop);
+    const uint32_t acc = acc_dtype(s);
     if (P == 1) {
         for (auto& ch : chains)
             ch.last = b.add(OP_REDUCE, (uint8_t)s.redop, ch.nelem, {opnd(send_buf(0), dt, ch.src_elem)},
                             {ch.final_dst});
         return;
     }
+    std::vector<std::vector<int>> order(P);
+    for (int c = 0; c < P; ++c) order[c] = contributor_order(s, c);
     for (int t = 1; t < P; ++t) {
         for (auto& ch : chains) {
+            const std::vector<int>& seq = order[ch.owner];
             Operand partial = opnd(scratch_buf(P), acc, ch.scratch_elem);
             std::vector<Operand> src;
-            if (t == 1) src.push_back(opnd(send_buf(0), dt, ch.src_elem));
+            if (t == 1) src.push_back(opnd(send_buf(seq[0]), dt, ch.src_elem));
             else src.push_back(partial);
-            src.push_back(opnd(send_buf(t), dt, ch.src_elem));
+            src.push_back(opnd(send_buf(seq[t]), dt, ch.src_elem));
             Operand dst = (t == P - 1) ? ch.final_dst : partial;
             std::vector<Dep> deps;
             if (t > 1) deps.push_back(tile_dep(ch.prev));
@@ -168,7 +199,7 @@ void lower_ring(const CollectiveSpec& s, HostProgram& p) {
     const int P = s.P;
     const uint64_t C = chunk_elems(s);
     const uint32_t dt = (uint32_t)s.dtype;
-    const uint32_t acc = acc_dtype(s.dtype, s.redop);
+    const uint32_t acc = acc_dtype(s);
 
     if (s.coll == COLL_ALLGATHER) {
         // hop 0 places block q in rank q's output; hop h forwards it from rank q+h-1 to q+h.
@@ -199,6 +230,7 @@ void lower_ring(const CollectiveSpec& s, HostProgram& p) {
         for (int c = 0; c < P; ++c)
             for_chunks(0, M, C, [&](uint32_t, uint64_t o, uint64_t n) {
                 Chain ch;
+                ch.owner = c;
                 ch.src_elem = (uint64_t)c * M + o;
                 ch.nelem = n;
                 ch.final_dst = opnd(recv_buf(P, c), dt, o);
@@ -213,6 +245,7 @@ void lower_ring(const CollectiveSpec& s, HostProgram& p) {
             uint64_t lo = std::min(s.count, (uint64_t)c * q), hi = std::min(s.count, lo + q);
             for_chunks(lo, hi, C, [&](uint32_t, uint64_t o, uint64_t n) {
                 Chain ch;
+                ch.owner = c;
                 ch.src_elem = o;
                 ch.nelem = n;
                 ch.final_dst = opnd(recv_buf(P, c), dt, o);
@@ -238,6 +271,108 @@ void lower_ring(const CollectiveSpec& s, HostProgram& p) {
     p.algo = ALGO_RING;
 }
 
+// ------------------------------------------------------------------------------- RHD
+// Recursive halving reduce-scatter (and recursive doubling all-gather) for P = 2^L ranks.
+// The vector is cut into P blocks; block b ends at rank b. At halving step j (distance
+// d = P >> (j+1)) rank r keeps the blocks that agree with r on every bit handled so far; for
+// each kept block it combines its own value with the value of partner r ^ d, which kept the
+// same block one step earlier. Partials live in scratch slot (r, b) in the accumulation type;
+// the last step writes the owner's receive buffer. The tree this builds for every element
+// pairs ranks differing in bit P/2 first, then bit P/4, ..., then bit 1. Doubling step j
+// (distance d = 1 << j) copies the d blocks a rank holds to its partner r ^ d.
+void lower_rhd(const CollectiveSpec& s, HostProgram& p) {
+    Builder b{p};
+    const int P = s.P;
+    const uint64_t C = chunk_elems(s);
+    const uint32_t dt = (uint32_t)s.dtype;
+    const uint32_t acc = acc_dtype(s);
+    const bool ag_only = s.coll == COLL_ALLGATHER;
+    // block geometry: element offset of block b in a send buffer / in a receive buffer
+    const uint64_t N = s.count;
+    const uint64_t q = (s.coll == COLL_ALLREDUCE) ? shard_size(N, P) : N;
+    auto blo = [&](int blk) { return std::min<uint64_t>((uint64_t)blk * q, s.coll == COLL_ALLREDUCE ? N : (uint64_t)P * N); };
+    auto bhi = [&](int blk) { return std::min<uint64_t>(blo(blk) + q, s.coll == COLL_ALLREDUCE ? N : (uint64_t)P * N); };
+    // receive-side element offset of block b: all-reduce and all-gather keep the send layout;
+    // reduce-scatter writes its block at offset 0 of the owner's buffer
+    auto rlo = [&](int blk) { return s.coll == COLL_REDUCE_SCATTER ? 0 : blo(blk); };
+
+    // producer of the value rank r holds for (block, chunk offset), per step
+    std::vector<std::unordered_map<uint64_t, uint32_t>> prev(P), next(P);
+    auto key = [&](int blk, uint64_t o) { return ((uint64_t)blk << 40) | (o - blo(blk)); };
+
+    if (!ag_only) {
+        int steps = 0;
+        while ((1 << steps) < P) ++steps;
+        uint64_t mask = 0;
+        for (int j = 0; j < steps; ++j) {
+            const int d = P >> (j + 1);
+            mask |= (uint64_t)d;
+            for (int r = 0; r < P; ++r) next[r].clear();
+            for (int r = 0; r < P; ++r) {
+                const int partner = r ^ d;
+                for (int blk = 0; blk < P; ++blk) {
+                    if (((uint64_t)blk & mask) != ((uint64_t)r & mask)) continue;
+                    const bool last = (j == steps - 1);
+                    for_chunks(blo(blk), bhi(blk), C, [&](uint32_t, uint64_t o, uint64_t n) {
+                        const uint64_t so = (uint64_t)(r * P + blk) * q + (o - blo(blk));
+                        const uint64_t po = (uint64_t)(partner * P + blk) * q + (o - blo(blk));
+                        std::vector<Operand> src;
+                        std::vector<Dep> deps;
+                        if (j == 0) {
+                            src.push_back(opnd(send_buf(r), dt, o));
+                            src.push_back(opnd(send_buf(partner), dt, o));
+                        } else {
+                            src.push_back(opnd(scratch_buf(P), acc, so));
+                            src.push_back(opnd(scratch_buf(P), acc, po));
+                            deps.push_back(tile_dep(prev[r].at(key(blk, o))));
+                            deps.push_back(tile_dep(prev[partner].at(key(blk, o))));
+                        }
+                        Operand dst = last ? opnd(recv_buf(P, r), dt, rlo(blk) + (o - blo(blk)))
+                                           : opnd(scratch_buf(P), acc, so);
+                        next[r][key(blk, o)] = b.add(OP_REDUCE, (uint8_t)s.redop, n, src, {dst}, deps);
+                    });
+                }
+            }
+            prev.swap(next);
+        }
+        p.scratch_bytes = (steps > 1) ? (uint64_t)P * P * q * dtype_size(acc) : 0;
+        if (P == 1) {
+            for_chunks(blo(0), bhi(0), C, [&](uint32_t, uint64_t o, uint64_t n) {
+                prev[0][key(0, o)] = b.add(OP_REDUCE, (uint8_t)s.redop, n, {opnd(send_buf(0), dt, o)},
+                                           {opnd(recv_buf(P, 0), dt, rlo(0) + (o - blo(0)))});
+            });
+        }
+    } else {
+        // all-gather: every rank first places its own block
+        for (int r = 0; r < P; ++r)
+            for_chunks(0, N, C, [&](uint32_t, uint64_t o, uint64_t n) {
+                prev[r][key(r, (uint64_t)r * N + o)] =
+                    b.add(OP_COPY, RO_SUM, n, {opnd(send_buf(r), dt, o)}, {opnd(recv_buf(P, r), dt, (uint64_t)r * N + o)});
+            });
+    }
+
+    if (s.coll != COLL_REDUCE_SCATTER) {
+        // doubling: at distance d, rank r holds the d blocks of its aligned group and sends them
+        for (int d = 1; d < P; d <<= 1) {
+            for (int r = 0; r < P; ++r) next[r] = prev[r];
+            for (int r = 0; r < P; ++r) {
+                const int partner = r ^ d;
+                const int base = r & ~(d - 1);
+                for (int blk = base; blk < base + d; ++blk) {
+                    for_chunks(blo(blk), bhi(blk), C, [&](uint32_t, uint64_t o, uint64_t n) {
+                        const uint32_t src_desc = prev[r].at(key(blk, o));
+                        next[partner][key(blk, o)] =
+                            b.add(OP_COPY, RO_SUM, n, {opnd(recv_buf(P, r), dt, o)}, {opnd(recv_buf(P, partner), dt, o)},
+                                  {tile_dep(src_desc)});
+                    });
+                }
+            }
+            prev.swap(next);
+        }
+    }
+    p.algo = ALGO_RHD;
+}
+
 // ------------------------------------------------------------------------- TWO_LEVEL
 // P = G groups x L consecutive ranks. Shard k of the vector is owned by local rank k of
 // every group. Phase 1 (inside each group): the L contributors of shard k are folded into
@@ -249,7 +384,7 @@ void lower_two_level(const CollectiveSpec& s, HostProgram& p) {
     const int P = s.P, L = s.group_size, G = P / L;
     const uint64_t N = s.count, C = chunk_elems(s);
     const uint32_t dt = (uint32_t)s.dtype;
-    const uint32_t acc = acc_dtype(s.dtype, s.redop);
+    const uint32_t acc = acc_dtype(s);
     const uint64_t q = shard_size(N, L);
     struct Piece { int k; uint64_t o, n; };
     std::vector<Piece> pieces;
@@ -348,17 +483,25 @@ struct OperandKeyHash {
 
 }  // namespace
 
+uint64_t shard_size(uint64_t n, int parts) {
+    uint64_t q = (n + parts - 1) / parts;
+    return ((q + kShardAlignElems - 1) / kShardAlignElems) * kShardAlignElems;
+}
+
 bool CollectiveSpec::operator==(const CollectiveSpec& o) const {
     return coll == o.coll && P == o.P && dtype == o.dtype && redop == o.redop && count == o.count &&
            sendcounts == o.sendcounts && sdispls == o.sdispls && recvcounts == o.recvcounts &&
            rdispls == o.rdispls && in_place == o.in_place && algo == o.algo && group_size == o.group_size &&
-           chunk_bytes == o.chunk_bytes && fuse == o.fuse && tile_bytes == o.tile_bytes;
+           chunk_bytes == o.chunk_bytes && fuse == o.fuse && tile_bytes == o.tile_bytes && order == o.order &&
+           requant == o.requant;
 }
 
 int resolve_algo(const CollectiveSpec& s) {
     if (s.coll == COLL_ALLTOALLV) return ALGO_DIRECT;
     if (s.algo != ALGO_AUTO) return s.algo;
-    if (s.coll == COLL_ALLREDUCE && s.group_size > 1 && s.group_size < s.P && s.P % s.group_size == 0)
+    if (s.order == ORDER_HALVING) return ALGO_RHD;
+    if (s.coll == COLL_ALLREDUCE && s.order == ORDER_ASCENDING && s.group_size > 1 && s.group_size < s.P &&
+        s.P % s.group_size == 0)
         return ALGO_TWO_LEVEL;
     return ALGO_RING;
 }
@@ -395,7 +538,29 @@ bool lower(const CollectiveSpec& s, HostProgram& p, std::string& err) {
         return true;
     }
     int algo = resolve_algo(s);
-    if (algo == ALGO_TWO_LEVEL) {
+    if (s.order == ORDER_HALVING && !is_pow2(s.P)) {
+        err = "the recursive-halving order needs a power-of-two number of ranks";
+        return false;
+    }
+    if (s.order == ORDER_HALVING && algo != ALGO_RHD && algo != ALGO_DIRECT) {
+        err = "the recursive-halving order is produced by the RHD or DIRECT schedules";
+        return false;
+    }
+    if (algo == ALGO_RHD && s.order != ORDER_HALVING && s.coll != COLL_ALLGATHER) {
+        err = "the RHD schedule folds in the recursive-halving order (set order = HALVING)";
+        return false;
+    }
+    if (algo == ALGO_RHD && !is_pow2(s.P)) {
+        err = "the RHD schedule needs a power-of-two number of ranks";
+        return false;
+    }
+    if (algo == ALGO_TWO_LEVEL && s.order != ORDER_ASCENDING) {
+        err = "the two-level schedule has its own grouped order";
+        return false;
+    }
+    if (algo == ALGO_RHD) {
+        lower_rhd(s, p);
+    } else if (algo == ALGO_TWO_LEVEL) {
         if (s.coll != COLL_ALLREDUCE) {
             err = "the two-level schedule is defined for allreduce only";
             return false;
@@ -413,6 +578,9 @@ bool lower(const CollectiveSpec& s, HostProgram& p, std::string& err) {
         err = "unknown algorithm";
         return false;
     }
+    if (s.requant && s.redop == RO_SUM && (s.dtype == DT_BF16 || s.dtype == DT_FP16))
+        for (auto& d : p.descs)
+            if (d.op == OP_REDUCE) d.requant = true;
     return true;
 }
 
@@ -427,6 +595,10 @@ bool lower(const CollectiveSpec& s, HostProgram& p, std::string& err) {
 //   group = L): fold each run of L into a partial, then fold the partials, as before.
 // Rule 3 (forwarding): F = COPY(x -> y...) where x is the value a step E wrote (same
 //   location and element count) and F waits for E  ->  E also writes y... .
+// Rule 4 (trees): E = REDUCE(a, b) where a and b are the private partials of two binary-tree
+//   reductions over equally many sources  ->  E = binary tree over both source lists. This
+//   is what a recursive-halving level does; the tree, and so every operation, is unchanged.
+// Steps merge only if they share the operator and the re-quantisation rule.
 //
 // Values are tracked by version: the producer of a source is the last step, in program
 // order, that wrote exactly that location. Merged steps forward to the step that absorbed
@@ -469,12 +641,26 @@ void fuse(HostProgram& p) {
             if (find(e.desc) == target) return true;
         return false;
     };
-    // A is a partial-sum step whose single value only `consumer` reads
-    auto private_partial = [&](int64_t a, const HostDesc& B) {
+    // A is a partial step (scratch output, one destination) whose single value only B reads,
+    // with the same operator and rounding rule as B
+    auto partial_of = [&](int64_t a, const HostDesc& B) {
         if (a < 0) return false;
         const HostDesc& A = p.descs[a];
-        return A.alive && A.op == OP_REDUCE && A.group == 0 && A.dsts.size() == 1 && A.dsts[0].buf == scratch &&
-               A.redop == B.redop && A.nelem == B.nelem && nread[a][0] == 1 && depends_on(B, (uint32_t)a);
+        return A.alive && A.op == OP_REDUCE && A.dsts.size() == 1 && A.dsts[0].buf == scratch &&
+               A.redop == B.redop && A.requant == B.requant && A.nelem == B.nelem && nread[a][0] == 1 &&
+               depends_on(B, (uint32_t)a);
+    };
+    // ... folded ascending over its list
+    auto private_partial = [&](int64_t a, const HostDesc& B) {
+        return partial_of(a, B) && p.descs[a].group == 0 && p.descs[a].fold == FOLD_LIST;
+    };
+    // ... folded as a complete binary tree (a two-source step is one)
+    auto tree_partial = [&](int64_t a, const HostDesc& B) {
+        if (!partial_of(a, B)) return false;
+        const HostDesc& A = p.descs[a];
+        const size_t n = A.srcs.size();
+        if ((n & (n - 1)) != 0) return false;
+        return A.fold == FOLD_PAIRWISE || (n == 2 && A.group == 0);
     };
     auto absorb_deps = [&](HostDesc& into, const HostDesc& from) {
         into.deps.insert(into.deps.end(), from.deps.begin(), from.deps.end());
@@ -483,7 +669,28 @@ void fuse(HostProgram& p) {
     for (uint32_t i = 0; i < D; ++i) {
         HostDesc& B = p.descs[i];
         if (!B.alive) continue;
-        if (B.op == OP_REDUCE && B.group == 0 && !B.srcs.empty()) {
+        if (B.op == OP_REDUCE && B.group == 0 && B.fold == FOLD_LIST && !B.srcs.empty()) {
+            // Rule 4 (trees): B adds the roots of two equally sized binary trees, each a private
+            // partial -> one binary tree over both leaf lists (a recursive-halving level).
+            if (B.srcs.size() == 2 && tree_partial(prod[i][0], B) && tree_partial(prod[i][1], B) &&
+                p.descs[prod[i][0]].srcs.size() == p.descs[prod[i][1]].srcs.size() &&
+                2 * p.descs[prod[i][0]].srcs.size() <= (size_t)kMaxOperands) {
+                std::vector<Operand> srcs;
+                std::vector<int64_t> sprod;
+                for (int k = 0; k < 2; ++k) {
+                    uint32_t a = (uint32_t)prod[i][k];
+                    HostDesc& A = p.descs[a];
+                    srcs.insert(srcs.end(), A.srcs.begin(), A.srcs.end());
+                    sprod.insert(sprod.end(), prod[a].begin(), prod[a].end());
+                    absorb_deps(B, A);
+                    A.alive = false;
+                    fwd[a] = i;
+                }
+                B.srcs = std::move(srcs);
+                prod[i] = std::move(sprod);
+                B.fold = FOLD_PAIRWISE;
+                continue;
+            }
             // Rule 2: every source is a private partial of an equally sized flat reduction.
             bool groups = B.srcs.size() >= 2;
             size_t L = 0, total = 0;
@@ -695,6 +902,8 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
         d.nsrc = (uint16_t)h.srcs.size();
         d.ndst = (uint16_t)h.dsts.size();
         d.nelem = h.nelem;
+        d.fold = h.fold;
+        d.requant = h.requant ? 1u : 0u;
         d.tile_elems = p.tile_elems;
         uint64_t nt = (h.op == OP_NOOP) ? 1 : (h.nelem + te - 1) / te;
         if (nt == 0) nt = 1;
@@ -749,7 +958,8 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     int kind = kKindCopyOnly;
     for (uint32_t i = 0; i < nd; ++i) {
         if (out[i].op != OP_REDUCE) continue;
-        const bool plain = out[i].sig <= SIG_INT32 && out[i].redop == RO_SUM;
+        const bool plain = out[i].sig <= SIG_INT32 && out[i].redop == RO_SUM && out[i].fold == FOLD_LIST &&
+                           !out[i].requant;
         if (!plain) { kind = kKindGeneric; break; }
         if (kind == kKindCopyOnly) kind = out[i].sig;
         else if (kind != out[i].sig) { kind = kKindGeneric; break; }

@@ -18,7 +18,8 @@
 namespace hccl {
 
 enum Collective : int { COLL_ALLREDUCE = 0, COLL_REDUCE_SCATTER = 1, COLL_ALLGATHER = 2, COLL_ALLTOALLV = 3 };
-enum Algo : int { ALGO_AUTO = 0, ALGO_DIRECT = 1, ALGO_RING = 2, ALGO_TWO_LEVEL = 3 };
+enum Algo : int { ALGO_AUTO = 0, ALGO_DIRECT = 1, ALGO_RING = 2, ALGO_TWO_LEVEL = 3, ALGO_RHD = 4 };
+enum Order : int { ORDER_ASCENDING = 0, ORDER_RING = 1, ORDER_HALVING = 2 };
 
 struct CollectiveSpec {
     int coll = COLL_ALLREDUCE;
@@ -33,6 +34,8 @@ struct CollectiveSpec {
     uint64_t chunk_bytes = 0;
     bool fuse = true;
     uint32_t tile_bytes = 0;
+    int order = ORDER_ASCENDING;
+    bool requant = false;        // round every partial to the buffer type
 
     bool operator==(const CollectiveSpec& o) const;
 };
@@ -41,6 +44,8 @@ struct HostDesc {
     uint8_t op = OP_REDUCE;
     uint8_t redop = RO_SUM;
     uint16_t group = 0;
+    uint32_t fold = FOLD_LIST;
+    bool requant = false;
     uint64_t nelem = 0;
     std::vector<Operand> srcs;
     std::vector<Operand> dsts;
@@ -82,6 +87,9 @@ BufferSizes buffer_sizes(const CollectiveSpec& spec, uint64_t scratch_bytes);
 
 // Picks the schedule for ALGO_AUTO.
 int resolve_algo(const CollectiveSpec& spec);
+
+// Element count of one all-reduce shard: ceil(count / parts) rounded up to 64 elements.
+uint64_t shard_size(uint64_t count, int parts);
 
 // Lowers `spec` into `prog` (unfused steps). Returns false and sets err on bad input.
 bool lower(const CollectiveSpec& spec, HostProgram& prog, std::string& err);

@@ -213,11 +213,27 @@ struct TileOps {
     uint64_t src;     // lane j: address of source j at the tile's first element
     uint64_t dst;     // lane j: address of destination j at the tile's first element
     uint32_t nsrc, ndst, group;
+    uint32_t fold = FOLD_LIST;
+    uint32_t requant = 0;
 };
+
+// Re-quantisation of a partial to the destination type and back (Section II-A-2: the
+// near-memory compute unit rounds every result to the buffer type).
+template <int TO, bool REQ, typename A>
+__device__ __forceinline__ A requant(A v) {
+    if constexpr (REQ && TO == DT_BF16) return bf16_lo(bf16_bits(v));
+    else if constexpr (REQ && TO == DT_FP16) return f16_lo(f16_bits(v));
+    else return v;
+}
+
+template <int OPR, int TO, bool REQ, typename A>
+__device__ __forceinline__ A combq(A a, A x) {
+    return requant<TO, REQ>(comb<OPR>(a, x));
+}
 
 // Fold the sources of `count` elements starting at tile element `first`, one element per
 // lane, contributors in list order (grouped when group > 0), and store to every destination.
-template <int T0, int TR, int TO, int OPR>
+template <int T0, int TR, int TO, int OPR, bool REQ = false>
 __device__ __forceinline__ void reduce_elems(const TileOps& t, uint32_t first, uint32_t count, uint32_t lane) {
     typedef typename DtInfo<TO>::acc A;
     const uint32_t L = t.group ? t.group : t.nsrc;
@@ -231,9 +247,9 @@ __device__ __forceinline__ void reduce_elems(const TileOps& t, uint32_t first, u
             const uint32_t gend = (g0 + L < t.nsrc) ? g0 + L : t.nsrc;
             for (uint32_t s = g0 + 1; s < gend; ++s) {
                 const char* b = (const char*)from_lane(t.src, s);
-                part = comb<OPR>(part, load1<TR, A>(b + (uint64_t)e * DtInfo<TR>::size));
+                part = combq<OPR, TO, REQ>(part, load1<TR, A>(b + (uint64_t)e * DtInfo<TR>::size));
             }
-            tot = (g0 == 0) ? part : comb<OPR>(tot, part);
+            tot = (g0 == 0) ? part : combq<OPR, TO, REQ>(tot, part);
         }
         for (uint32_t j = 0; j < t.ndst; ++j) {
             char* b = (char*)from_lane(t.dst, j);
@@ -243,7 +259,7 @@ __device__ __forceinline__ void reduce_elems(const TileOps& t, uint32_t first, u
 }
 
 // U vectors of 8 elements per lane: elements [base, base + U*512) of the tile, all in range.
-template <int T0, int TR, int TO, int OPR, int U>
+template <int T0, int TR, int TO, int OPR, int U, bool REQ = false>
 __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, uint32_t lane) {
     typedef typename DtInfo<TO>::acc A;
     // a first source of another type (a chained step's FP32 partial) needs its own registers
@@ -298,7 +314,7 @@ __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, ui
                             for (int i = 0; i < 8; ++i) part[u][i] = x[i];
                         } else {
 #pragma unroll
-                            for (int i = 0; i < 8; ++i) part[u][i] = comb<OPR>(part[u][i], x[i]);
+                            for (int i = 0; i < 8; ++i) part[u][i] = combq<OPR, TO, REQ>(part[u][i], x[i]);
                         }
                     }
                 }
@@ -307,7 +323,8 @@ __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, ui
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int i = 0; i < 8; ++i) tot[u][i] = (g0 == 0) ? part[u][i] : comb<OPR>(tot[u][i], part[u][i]);
+            for (int i = 0; i < 8; ++i)
+                tot[u][i] = (g0 == 0) ? part[u][i] : combq<OPR, TO, REQ>(tot[u][i], part[u][i]);
     }
     for (uint32_t j = 0; j < t.ndst; ++j) {
         char* b = (char*)from_lane(t.dst, j);
@@ -319,26 +336,133 @@ __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, ui
     }
 }
 
-template <int T0, int TR, int TO, int OPR>
+template <int T0, int TR, int TO, int OPR, bool REQ = false>
 __device__ __forceinline__ void reduce_tile(const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
     if (!aligned) {
-        reduce_elems<T0, TR, TO, OPR>(t, 0, n, lane);
+        reduce_elems<T0, TR, TO, OPR, REQ>(t, 0, n, lane);
         return;
     }
     constexpr int U = (DtInfo<TR>::size == 2) ? HCCL_REDUCE_UNROLL16 : 1;
     constexpr uint32_t kBlock = (uint32_t)U * kWaveSize * kVecElems;
     uint32_t base = 0;
-    for (; base + kBlock <= n; base += kBlock) reduce_block<T0, TR, TO, OPR, U>(t, base, lane);
+    for (; base + kBlock <= n; base += kBlock) reduce_block<T0, TR, TO, OPR, U, REQ>(t, base, lane);
     // remaining whole 512-element steps, then single elements
     for (; base + kWaveSize * kVecElems <= n; base += kWaveSize * kVecElems)
-        reduce_block<T0, TR, TO, OPR, 1>(t, base, lane);
+        reduce_block<T0, TR, TO, OPR, 1, REQ>(t, base, lane);
     if (base < n) {
         // lanes whose 8 elements are all in range take one more vector step
         const uint32_t whole = (n - base) / kVecElems;
-        if (lane < whole) reduce_block<T0, TR, TO, OPR, 1>(t, base, lane);
+        if (lane < whole) reduce_block<T0, TR, TO, OPR, 1, REQ>(t, base, lane);
         base += whole * kVecElems;
     }
-    if (base < n) reduce_elems<T0, TR, TO, OPR>(t, base, n - base, lane);
+    if (base < n) reduce_elems<T0, TR, TO, OPR, REQ>(t, base, n - base, lane);
+}
+
+// ------------------------------------------------------------- binary-tree (pairwise) fold
+// The sources form the leaves of a complete binary tree in list order: (s0 s1) (s2 s3) ...,
+// then pairs of those, up to the root (the recursive-halving order once the compiler has
+// listed the ranks by bit reversal). Leaf k joins the pending subtree on each level where
+// bit `level` of k is set; the pending subtrees live in a six-level stack (64 sources).
+constexpr int kTreeLevels = 6;    // 2^6 = 64 sources
+constexpr int kTreeBatch = 4;     // sources whose loads are issued together in a tree fold
+
+template <int T, int OPR, bool REQ>
+__device__ __forceinline__ void reduce_elems_tree(const TileOps& t, uint32_t first, uint32_t count, uint32_t lane) {
+    typedef typename DtInfo<T>::acc A;
+    for (uint32_t e = first + lane; e < first + count; e += kWaveSize) {
+        A stk[kTreeLevels], root = A(0);
+        for (uint32_t k = 0; k < t.nsrc; ++k) {
+            const char* b = (const char*)from_lane(t.src, k);
+            A v = load1<T, A>(b + (uint64_t)e * DtInfo<T>::size);
+            bool placed = false;
+#pragma unroll
+            for (int l = 0; l < kTreeLevels; ++l) {
+                if (!placed) {
+                    if ((k >> l) & 1u) {
+                        v = combq<OPR, T, REQ>(stk[l], v);
+                    } else {
+                        stk[l] = v;
+                        placed = true;
+                    }
+                }
+            }
+            if (!placed) root = v;  // leaf 63 closes the 64-source tree
+        }
+#pragma unroll
+        for (int l = 0; l < kTreeLevels; ++l)
+            if ((1u << l) == t.nsrc) root = stk[l];
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* b = (char*)from_lane(t.dst, j);
+            store1<T, A>(b + (uint64_t)e * DtInfo<T>::size, root);
+        }
+    }
+}
+
+template <int T, int OPR, bool REQ>
+__device__ __forceinline__ void reduce_block_tree(const TileOps& t, uint32_t base, uint32_t lane) {
+    typedef typename DtInfo<T>::acc A;
+    A stk[kTreeLevels][8], root[8];
+    const uint32_t e = base + lane * kVecElems;
+    for (uint32_t s = 0; s < t.nsrc; s += kTreeBatch) {
+        Raw8<T> raw[kTreeBatch];
+#pragma unroll
+        for (int j = 0; j < kTreeBatch; ++j) {
+            if (s + j < t.nsrc) {
+                const char* b = (const char*)from_lane(t.src, s + j);
+                raw[j] = load8<T>(b + (uint64_t)e * DtInfo<T>::size);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kTreeBatch; ++j) {
+            if (s + j < t.nsrc) {
+                const uint32_t k = s + j;
+                A v[8];
+                widen8<T, A>(raw[j], v);
+                bool placed = false;
+#pragma unroll
+                for (int l = 0; l < kTreeLevels; ++l) {
+                    if (!placed) {
+                        if ((k >> l) & 1u) {
+#pragma unroll
+                            for (int i = 0; i < 8; ++i) v[i] = combq<OPR, T, REQ>(stk[l][i], v[i]);
+                        } else {
+#pragma unroll
+                            for (int i = 0; i < 8; ++i) stk[l][i] = v[i];
+                            placed = true;
+                        }
+                    }
+                }
+                if (!placed) {
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) root[i] = v[i];
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int l = 0; l < kTreeLevels; ++l)
+        if ((1u << l) == t.nsrc)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) root[i] = stk[l][i];
+    for (uint32_t j = 0; j < t.ndst; ++j) {
+        char* b = (char*)from_lane(t.dst, j);
+        store8<T, A>(b + (uint64_t)e * DtInfo<T>::size, root);
+    }
+}
+
+template <int T, int OPR, bool REQ>
+__device__ __forceinline__ void reduce_tile_tree(const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
+    uint32_t base = 0;
+    if (aligned) {
+        for (; base + kWaveSize * kVecElems <= n; base += kWaveSize * kVecElems)
+            reduce_block_tree<T, OPR, REQ>(t, base, lane);
+        if (base < n) {
+            const uint32_t whole = (n - base) / kVecElems;
+            if (lane < whole) reduce_block_tree<T, OPR, REQ>(t, base, lane);
+            base += whole * kVecElems;
+        }
+    }
+    if (base < n) reduce_elems_tree<T, OPR, REQ>(t, base, n - base, lane);
 }
 
 template <int T0, int TR, int TO>
@@ -350,7 +474,45 @@ __device__ __forceinline__ void reduce_dispatch_op(uint32_t op, const TileOps& t
     }
 }
 
+template <int T>
+__device__ __forceinline__ void run_tree(uint32_t op, const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
+    if (op == RO_SUM) {
+        if constexpr (T == DT_BF16 || T == DT_FP16) {
+            if (t.requant) {
+                reduce_tile_tree<T, RO_SUM, true>(t, n, aligned, lane);
+                return;
+            }
+        }
+        reduce_tile_tree<T, RO_SUM, false>(t, n, aligned, lane);
+    } else if (op == RO_MAX) {
+        reduce_tile_tree<T, RO_MAX, false>(t, n, aligned, lane);
+    } else {
+        reduce_tile_tree<T, RO_MIN, false>(t, n, aligned, lane);
+    }
+}
+
 __device__ __forceinline__ void run_reduce(uint32_t sig, uint32_t op, const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
+    if (t.fold == FOLD_PAIRWISE) {
+        switch (sig) {
+            case SIG_BF16: run_tree<DT_BF16>(op, t, n, aligned, lane); break;
+            case SIG_FP16: run_tree<DT_FP16>(op, t, n, aligned, lane); break;
+            case SIG_FP32: run_tree<DT_FP32>(op, t, n, aligned, lane); break;
+            case SIG_INT32: run_tree<DT_INT32>(op, t, n, aligned, lane); break;
+            default: break;
+        }
+        return;
+    }
+    if (t.requant && op == RO_SUM) {
+        // re-quantised partials only matter for 16-bit destinations
+        if (sig == SIG_BF16) {
+            reduce_tile<DT_BF16, DT_BF16, DT_BF16, RO_SUM, true>(t, n, aligned, lane);
+            return;
+        }
+        if (sig == SIG_FP16) {
+            reduce_tile<DT_FP16, DT_FP16, DT_FP16, RO_SUM, true>(t, n, aligned, lane);
+            return;
+        }
+    }
     switch (sig) {
         case SIG_BF16: reduce_dispatch_op<DT_BF16, DT_BF16, DT_BF16>(op, t, n, aligned, lane); break;
         case SIG_FP16: reduce_dispatch_op<DT_FP16, DT_FP16, DT_FP16>(op, t, n, aligned, lane); break;
@@ -571,6 +733,8 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
         ops.nsrc = uni(D->nsrc);
         ops.ndst = uni(D->ndst);
         ops.group = uni(D->group);
+        ops.fold = uni(D->fold);
+        ops.requant = uni(D->requant);
         const Operand* opl = (const Operand*)(prog + h.off_operand);
         ops.src = 0;
         ops.dst = 0;
@@ -603,8 +767,11 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
     return true;
 }
 
+// Four waves per SIMD for the specialised kernels; the generic kernel (every fold, mixed types)
+// may use more registers rather than spill.
 template <int KIND>
-__global__ void __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(4))) hccl_executor(LaunchArgs a) {
+__global__ void __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(KIND == kKindGeneric ? 3 : 4)))
+hccl_executor(LaunchArgs a) {
     const uint32_t lane = __lane_id();
     const uint32_t wave = uni(blockIdx.x * kWavesPerBlock + (threadIdx.x / kWaveSize));
     const uint8_t* prog = a.prog;
@@ -669,6 +836,8 @@ __global__ void __launch_bounds__(kBlockThreads) hccl_executor_inline(InlineArgs
     ops.nsrc = a.nsrc;
     ops.ndst = a.ndst;
     ops.group = a.group;
+    ops.fold = a.fold;
+    ops.requant = a.requant;
     const uint64_t te = a.tile_elems;
     for (uint32_t t = wave; t < a.ntiles; t += a.nworkers) {
         const uint64_t e0 = (uint64_t)t * te;

@@ -35,6 +35,13 @@ enum Op : uint8_t {
 enum DType : uint8_t { DT_BF16 = 0, DT_FP16 = 1, DT_FP32 = 2, DT_INT32 = 3 };
 enum RedOp : uint8_t { RO_SUM = 0, RO_MAX = 1, RO_MIN = 2 };
 
+// How a REDUCE folds its source list.
+enum Fold : uint32_t {
+    FOLD_LIST = 0,      // ascending over the list (grouped when `group` > 0)
+    FOLD_PAIRWISE = 1,  // complete binary tree over the list: (s0 s1)(s2 s3)..., then pairs of
+                        // those, ...; the list length is a power of two
+};
+
 enum DepKind : uint32_t {
     DEP_ALL = 0,   // wait until every tile of the named descriptor has completed
     DEP_TILE = 1,  // wait until the tile with the same index of the named descriptor has completed
@@ -112,7 +119,9 @@ struct Desc {           // 64 bytes
     uint32_t ntiles;
     uint32_t tile_elems;
     uint64_t nelem;
-    uint32_t pad1[4];
+    uint32_t fold;      // FOLD_LIST (grouped / flat, per `group`) or FOLD_PAIRWISE
+    uint32_t requant;   // 1 = round every partial to the destination type
+    uint32_t pad1[2];
 };
 static_assert(sizeof(Desc) == 64, "descriptor layout");
 static_assert(sizeof(Operand) == 16, "operand layout");
@@ -178,6 +187,8 @@ struct InlineArgs {
     uint32_t es_first;   // element bytes of source 0 (and of a copy)
     uint32_t es_rest;    // element bytes of the other sources
     uint32_t es_out;     // element bytes of the destinations
+    uint32_t fold;       // Fold of the step
+    uint32_t requant;    // 1 = round every partial to the destination type
     uint64_t src[kMaxOperands];
     uint64_t dst[kMaxOperands];
 };

@@ -90,6 +90,21 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
                 return false;
             }
             if (d.redop > RO_MIN) { err = fmt("REDUCE step %llu has an unknown operator", i); return false; }
+            if (d.fold == FOLD_PAIRWISE) {
+                const size_t n = d.srcs.size();
+                if (d.group || (n & (n - 1))) {
+                    err = fmt("REDUCE step %llu: a binary-tree fold needs a power-of-two source list", i);
+                    return false;
+                }
+                for (size_t k = 1; k < n; ++k)
+                    if (d.srcs[k].dtype != d.srcs[0].dtype) {
+                        err = fmt("REDUCE step %llu: a binary-tree fold needs one source type", i);
+                        return false;
+                    }
+            } else if (d.fold != FOLD_LIST) {
+                err = fmt("REDUCE step %llu has an unknown fold", i);
+                return false;
+            }
         } else {
             err = fmt("step %llu has an unknown op %llu", i, d.op);
             return false;

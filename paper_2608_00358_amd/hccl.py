@@ -15,7 +15,8 @@ LIB_PATH = os.path.join(_PKG, "lib", "libhccl.so")
 
 DTYPES = {"bf16": 0, "fp16": 1, "fp32": 2, "int32": 3}
 OPS = {"sum": 0, "max": 1, "min": 2}
-ALGOS = {"auto": 0, "direct": 1, "ring": 2, "two_level": 3}
+ALGOS = {"auto": 0, "direct": 1, "ring": 2, "two_level": 3, "rhd": 4}
+ORDERS = {"ascending": 0, "ring": 1, "halving": 2}
 RESULTS = {0: "hcclSuccess", 1: "hcclInvalidArgument", 2: "hcclUnsupported", 3: "hcclHipError",
            4: "hcclOutOfMemory", 5: "hcclTimeout", 6: "hcclInternalError"}
 NO_DEVICE = -1
@@ -40,7 +41,8 @@ class hcclConfig_t(ctypes.Structure):
     _fields_ = [
         ("algo", ctypes.c_int32), ("group_size", ctypes.c_int32), ("chunk_bytes", ctypes.c_uint64),
         ("fuse", ctypes.c_int32), ("max_workers", ctypes.c_int32), ("tile_bytes", ctypes.c_uint32),
-        ("timeout_ms", ctypes.c_uint32), ("validate", ctypes.c_int32), ("reserved", ctypes.c_int32 * 5),
+        ("timeout_ms", ctypes.c_uint32), ("validate", ctypes.c_int32), ("order", ctypes.c_int32),
+        ("requantize", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3),
     ]
 
 
@@ -145,6 +147,8 @@ def hccl_config_init(**kw) -> hcclConfig_t:
     for k, v in kw.items():
         if k == "algo" and isinstance(v, str):
             v = ALGOS[v]
+        if k == "order" and isinstance(v, str):
+            v = ORDERS[v]
         setattr(cfg, k, int(v))
     return cfg
 

@@ -258,3 +258,73 @@ def test_empty_group_is_a_no_op():
     with comm(2) as c:
         H.hccl_group_start(c.handle)
         H.hccl_group_end(c.handle)
+
+
+# ------------------------------------------------------------- fold orders and RHD
+@pytest.mark.parametrize("P", [1, 2, 4, 8])
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_rhd_reduce_scatter_structure(P, fuse):
+    M, chunk = 5000, 4096
+    with comm(P, algo="rhd", order="halving", fuse=fuse, chunk_bytes=chunk) as c:
+        H.hccl_reduce_scatter(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), M, "bf16")
+        info = info_of(c)
+    chunks = ceil_div(M, chunk // 2)
+    assert info["algo"] == 4
+    if fuse or P == 1:
+        # every butterfly level merged: one binary-tree step per block chunk, minimal traffic
+        assert info["num_descs"] == P * chunks and info["num_deps"] == 0
+        assert info["max_srcs"] == P and info["scratch_bytes"] == 0
+        assert info["bytes_read"] == P * P * M * 2
+    else:
+        # P ranks x (P-1) kept blocks summed over the levels, per chunk
+        assert info["num_descs"] == P * (P - 1) * chunks
+        assert (info["num_deps"] > 0) == (P > 2)     # one level has nothing to wait for
+
+
+@pytest.mark.parametrize("P", [2, 4, 8])
+@pytest.mark.parametrize("fuse", [0, 1])
+def test_rhd_allreduce_and_allgather_validate(P, fuse):
+    with comm(P, algo="rhd", order="halving", fuse=fuse, chunk_bytes=4096) as c:
+        s, r = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+        H.hccl_allreduce(c.handle, s, r, 20001, "fp32")
+        ar = info_of(c)
+        H.hccl_allreduce(c.handle, s, s, 20001, "fp32")          # in place, aliasing checked
+        H.hccl_allgather(c.handle, s, r, 3001, "bf16")
+        ag = info_of(c)
+    if fuse:
+        assert ar["num_deps"] == 0 and ar["bytes_written"] == P * 20001 * 4
+        assert ag["num_deps"] == 0 and ag["bytes_read"] == P * 3001 * 2
+
+
+@pytest.mark.parametrize("order", ["ring", "halving"])
+def test_direct_schedule_takes_any_order(order):
+    P = 8
+    with comm(P, algo="direct", order=order) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), 100000, "bf16")
+        info = info_of(c)
+    if order == "ring":
+        assert info["num_descs"] == P          # one step per shard: each has its own rotation
+    else:
+        assert info["num_descs"] == 1
+
+
+def test_requantized_partials_are_stored_in_the_buffer_type():
+    P, N = 4, 1 << 14
+    for requant, width in ((0, 4), (1, 2)):
+        with comm(P, algo="ring", fuse=0, requantize=requant) as c:
+            H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "bf16")
+            assert info_of(c)["scratch_bytes"] == N * width
+
+
+def test_incompatible_orders_and_schedules_are_rejected():
+    s, r = fake_bufs(6, 1 << 40), fake_bufs(6, 1 << 44)
+    with comm(6, order="halving") as c:
+        _expect(2, H.hccl_allreduce, c.handle, s, r, 100, "fp32")      # not a power of two
+    with comm(4, algo="ring", order="halving") as c:
+        _expect(2, H.hccl_allreduce, c.handle, s[:4], r[:4], 100, "fp32")
+    with comm(4, algo="rhd") as c:
+        _expect(2, H.hccl_allreduce, c.handle, s[:4], r[:4], 100, "fp32")
+    with comm(4, algo="two_level", group_size=2, order="ring") as c:
+        _expect(2, H.hccl_allreduce, c.handle, s[:4], r[:4], 100, "fp32")
+    with comm(4, order=7) as c:
+        _expect(1, H.hccl_allreduce, c.handle, s[:4], r[:4], 100, "fp32")
