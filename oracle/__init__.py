@@ -88,6 +88,9 @@ def _bind(lib):
     lib.orc_allgather.argtypes = [i, sz, sz, vpp, vpp]
     lib.orc_alltoallv.restype = i
     lib.orc_alltoallv.argtypes = [i, sz, vpp, szp, szp, vpp, szp, szp]
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    lib.orc_alltoallv_dynamic.restype = i
+    lib.orc_alltoallv_dynamic.argtypes = [i, sz, sz, vpp, sz, i64p, i64p, vpp, sz, i64p, i64p]
     lib.orc_allreduce_ordered.restype = i
     lib.orc_allreduce_ordered.argtypes = [i, sz, i, i, ctypes.POINTER(OrderSpec), vpp, vpp]
     lib.orc_reduce_scatter_ordered.restype = i
@@ -246,3 +249,35 @@ def alltoallv(send: list, sendcounts, sdispls, recv: list, recvcounts, rdispls) 
     if rc != 0:
         raise ValueError(f"orc_alltoallv rejected its arguments (rc={rc})")
     return recv
+
+
+def _i64(a):
+    if a is None:
+        return None
+    flat = np.ascontiguousarray(a, dtype=np.int64).reshape(-1)
+    return (ctypes.c_int64 * flat.size)(*[int(v) for v in flat])
+
+
+def alltoallv_dynamic(send: list, counts, recv: list, row_elems: int, send_cap: int, recv_cap: int,
+                      sdispls=None, rdispls=None):
+    """AllToAllvDynamic (see hccl_oracle.h): ``counts`` (P, P) rows indexed [src, dst];
+    ``sdispls`` [src, dst] and ``rdispls`` [dst, src] row offsets, None = packed. ``send[s]``
+    holds ``send_cap`` rows and ``recv[d]`` ``recv_cap`` rows of ``row_elems`` elements.
+    Returns (accepted, recvcounts): ``recv`` is updated in place only when the layout is
+    accepted; recvcounts (P, P) [dst, src] is the transposed count matrix either way."""
+    P = len(send)
+    if len(recv) != P:
+        raise ValueError("send and recv must list the same number of ranks")
+    es = send[0].dtype.itemsize
+    for a in send:
+        if a.size != send_cap * row_elems or a.dtype.itemsize != es or not a.flags["C_CONTIGUOUS"]:
+            raise ValueError("every send buffer must be contiguous and hold send_cap rows")
+    for a in recv:
+        if a.size != recv_cap * row_elems or a.dtype.itemsize != es or not a.flags["C_CONTIGUOUS"]:
+            raise ValueError("every receive buffer must be contiguous and hold recv_cap rows")
+    rc_out = (ctypes.c_int64 * (P * P))()
+    rc = _load().orc_alltoallv_dynamic(P, es, int(row_elems), _ptrs(send), int(send_cap), _i64(counts),
+                                       _i64(sdispls), _ptrs(recv), int(recv_cap), _i64(rdispls), rc_out)
+    if rc == -1:
+        raise ValueError("orc_alltoallv_dynamic rejected its arguments")
+    return rc == 0, np.array(rc_out[:], dtype=np.int64).reshape(P, P)

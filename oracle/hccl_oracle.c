@@ -12,7 +12,8 @@
  * Citations are to the paper "HCCL: Collective Communication for Meta Training and
  * Inference Accelerators": Section II-A-2 (Near Memory Compute: copy and sum, BF16/FP16/FP32
  * operands, FP32 arithmetic, re-quantisation to the buffer type) and Section III-B (Data
- * Path: the collectives AllReduce / ReduceScatter / AllGather / AllToAllv).
+ * Path: the collectives AllReduce / ReduceScatter / AllGather / AllToAllv), Section IV-B-2
+ * (device-resident collectives: AllToAllvDynamic, whose layout is read when it runs).
  */
 #include "hccl_oracle.h"
 
@@ -416,4 +417,72 @@ int orc_alltoallv(int P, size_t elem_size,
         }
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* AllToAllvDynamic (Section IV-B-2): layout from run-time metadata, then a plain AllToAllv */
+/* ------------------------------------------------------------------------------------- */
+
+/* A non-empty range [off, off + n) fits a buffer of `cap` rows. */
+static int range_fits(int64_t off, int64_t n, size_t cap) {
+    if (off < 0 || (uint64_t)off > cap) return 0;
+    return (uint64_t)n <= cap - (uint64_t)off;
+}
+
+int orc_alltoallv_dynamic(int P, size_t elem_size, size_t row_elems,
+                          const void* const* send, size_t send_cap, const int64_t* counts,
+                          const int64_t* sdispls,
+                          void* const* recv, size_t recv_cap, const int64_t* rdispls,
+                          int64_t* recvcounts_out) {
+    if (P < 1 || P > 64 || elem_size == 0 || row_elems == 0 || !counts) return -1;
+    const size_t PP = (size_t)P * P;
+    if (recvcounts_out)
+        for (int s = 0; s < P; ++s)
+            for (int d = 0; d < P; ++d) recvcounts_out[(size_t)d * P + s] = counts[(size_t)s * P + d];
+
+    /* row offsets of every pair, send side [s*P+d], receive side [d*P+s] */
+    int64_t sd[64 * 64], rd[64 * 64];
+    for (size_t i = 0; i < PP; ++i)
+        if (counts[i] < 0) return -2;
+    for (int s = 0; s < P; ++s) {
+        int64_t at = 0;  /* packed: destinations back to back, ascending */
+        for (int d = 0; d < P; ++d) {
+            const int64_t n = counts[(size_t)s * P + d];
+            sd[(size_t)s * P + d] = sdispls ? sdispls[(size_t)s * P + d] : at;
+            if (n > 0 && !range_fits(sd[(size_t)s * P + d], n, send_cap)) return -2;
+            at += n;
+        }
+    }
+    for (int d = 0; d < P; ++d) {
+        int64_t at = 0;  /* packed: sources back to back, ascending */
+        for (int s = 0; s < P; ++s) {
+            const int64_t n = counts[(size_t)s * P + d];
+            rd[(size_t)d * P + s] = rdispls ? rdispls[(size_t)d * P + s] : at;
+            if (n > 0 && !range_fits(rd[(size_t)d * P + s], n, recv_cap)) return -2;
+            at += n;
+        }
+        /* non-empty receive ranges of one destination are pairwise disjoint */
+        for (int a = 0; a < P; ++a) {
+            const int64_t na = counts[(size_t)a * P + d];
+            if (na == 0) continue;
+            for (int b = a + 1; b < P; ++b) {
+                const int64_t nb = counts[(size_t)b * P + d];
+                if (nb == 0) continue;
+                const int64_t a0 = rd[(size_t)d * P + a], b0 = rd[(size_t)d * P + b];
+                if (a0 < b0 + nb && b0 < a0 + na) return -2;
+            }
+        }
+    }
+
+    /* the layout is valid: move the data as an AllToAllv in elements */
+    size_t sc[64 * 64], so[64 * 64], rc[64 * 64], ro[64 * 64];
+    for (int s = 0; s < P; ++s)
+        for (int d = 0; d < P; ++d) {
+            const size_t n = (size_t)counts[(size_t)s * P + d] * row_elems;
+            sc[(size_t)s * P + d] = n;
+            rc[(size_t)d * P + s] = n;
+            so[(size_t)s * P + d] = (size_t)sd[(size_t)s * P + d] * row_elems;
+            ro[(size_t)d * P + s] = (size_t)rd[(size_t)d * P + s] * row_elems;
+        }
+    return orc_alltoallv(P, elem_size, send, sc, so, recv, rc, ro);
 }

@@ -104,6 +104,26 @@ int orc_alltoallv(int P, size_t elem_size,
                   const void* const* send, const size_t* sendcounts, const size_t* sdispls,
                   void* const* recv, const size_t* recvcounts, const size_t* rdispls);
 
+/*
+ * AllToAllvDynamic (Section IV-B-2, device-resident collectives): an AllToAllv whose sizes, and
+ * optionally offsets, are only known when it runs (a routing kernel writes them). Counts and
+ * offsets are in rows of `row_elems` elements.
+ *   counts[s*P + d]   rows source s sends to destination d
+ *   sdispls[s*P + d]  row offset of that range in send[s]; NULL = packed: the ranges of one
+ *                     source back to back in ascending destination order from row 0
+ *   rdispls[d*P + s]  row offset in recv[d] of the rows from s; NULL = packed: ascending sources
+ *   recvcounts_out[d*P + s] = counts[s*P + d], written whenever non-NULL (also on rejection)
+ * Send buffers hold send_cap rows, receive buffers recv_cap rows. The layout is rejected
+ * (return -2, no receive byte written) when a count is negative, a non-empty range does not lie
+ * inside its buffer, or two non-empty receive ranges of one destination overlap. Ranges with
+ * count 0 are not checked. Otherwise the rows move as orc_alltoallv moves elements.
+ */
+int orc_alltoallv_dynamic(int P, size_t elem_size, size_t row_elems,
+                          const void* const* send, size_t send_cap, const int64_t* counts,
+                          const int64_t* sdispls,
+                          void* const* recv, size_t recv_cap, const int64_t* rdispls,
+                          int64_t* recvcounts_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,16 +1,20 @@
 """The oracle's pins must reject plausible mistakes in the oracle.
 
 Each case copies the oracle's C source, plants one mistake by a textual edit, compiles the
-copy with the same flags into a temporary directory (CPU only), points the oracle module at
-it and runs a subset of the pins. A mutant that every pin accepts would mean the pins do
+copy with the same flags into a temporary directory (CPU only), and runs a subset of the pins
+against it in a child process that points the oracle module at the copy. A mutant that every pin accepts would mean the pins do
 not constrain that part of the oracle, so the test fails.
 """
+import json
 import os
 import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
 
 import pytest
 
 import oracle
+import test_oracle_dynamic_pins as dyn_pins
 import test_oracle_order_pins as order_pins
 import test_oracle_pins as pins
 
@@ -77,6 +81,30 @@ MUTANTS = {
         "return requant ? requantize(dtype, v) : v;",
         "return v;",
     ),
+    "dynamic_packed_receive_offset_inclusive": (
+        "rd[(size_t)d * P + s] = rdispls ? rdispls[(size_t)d * P + s] : at;",
+        "rd[(size_t)d * P + s] = rdispls ? rdispls[(size_t)d * P + s] : at + n;",
+    ),
+    "dynamic_rows_read_as_elements": (
+        "so[(size_t)s * P + d] = (size_t)sd[(size_t)s * P + d] * row_elems;",
+        "so[(size_t)s * P + d] = (size_t)sd[(size_t)s * P + d];",
+    ),
+    "dynamic_exact_fit_rejected": (
+        "return (uint64_t)n <= cap - (uint64_t)off;",
+        "return (uint64_t)n < cap - (uint64_t)off;",
+    ),
+    "dynamic_overlap_unchecked": (
+        "if (a0 < b0 + nb && b0 < a0 + na) return -2;",
+        "if (a0 < b0 + nb && b0 < a0 + na && 0) return -2;",
+    ),
+    "dynamic_recvcounts_not_transposed": (
+        "recvcounts_out[(size_t)d * P + s] = counts[(size_t)s * P + d];",
+        "recvcounts_out[(size_t)s * P + d] = counts[(size_t)s * P + d];",
+    ),
+    "dynamic_zero_count_ranges_checked": (
+        "if (n > 0 && !range_fits(sd[(size_t)s * P + d], n, send_cap)) return -2;",
+        "if (!range_fits(sd[(size_t)s * P + d], n, send_cap)) return -2;",
+    ),
 }
 
 # The pins run against every mutant (cheap ones, CPU only).
@@ -98,6 +126,12 @@ PIN_CALLS = [
     ("halving order", lambda: order_pins.test_halving_order_is_the_distance_halving_tree(8)),
     ("order cancellation", lambda: order_pins.test_orders_are_told_apart_by_cancellation()),
     ("requant", lambda: order_pins.test_requant_rounds_every_partial_to_bf16("ascending")),
+    ("dynamic example", lambda: dyn_pins.test_worked_example_packed_layout()),
+    ("dynamic explicit", lambda: dyn_pins.test_worked_example_explicit_offsets()),
+    ("dynamic brute", lambda: dyn_pins.test_packed_layout_is_the_brute_force_row_placement(3, 4, 2)),
+    ("dynamic capacity", lambda: dyn_pins.test_capacity_boundaries_packed()),
+    ("dynamic overlap", lambda: dyn_pins.test_receive_overlap_boundaries()),
+    ("dynamic zero ranges", lambda: dyn_pins.test_zero_count_ranges_are_never_checked()),
 ]
 
 
@@ -116,19 +150,56 @@ def _build_mutant(tmpdir, name):
     return so_path
 
 
+def run_pins_against(so_path):
+    """Entry point of the child process: every pin against one mutant library; prints the
+    labels of the pins that failed as one JSON list."""
+    caught = []
+    with oracle.use_library(so_path):
+        for label, call in PIN_CALLS:
+            try:
+                call()
+            except (AssertionError, ValueError):
+                caught.append(label)
+    print(json.dumps(caught))
+
+
+_CHILD = (
+    "import sys; sys.path[:0] = [{tests!r}, {root!r}]\n"
+    "import test_oracle_mutants as m\n"
+    "m.run_pins_against(sys.argv[1])\n"
+)
+
+
+@pytest.fixture(scope="module")
+def mutant_results(tmp_path_factory):
+    """Builds every mutant and runs the pins against each in a process of its own (a mutant
+    may write outside a buffer; that must not corrupt the test process), a few at a time."""
+    tmp = str(tmp_path_factory.mktemp("mutants"))
+    tests = os.path.dirname(os.path.abspath(__file__))
+    child = _CHILD.format(tests=tests, root=os.path.dirname(tests))
+    names = sorted(MUTANTS)
+    with ThreadPoolExecutor(max_workers=6) as pool:
+        libs = dict(zip(names, pool.map(lambda n: _build_mutant(tmp, n), names)))
+
+    def run(name):
+        try:
+            r = subprocess.run([sys.executable, "-c", child, libs[name]], capture_output=True, text=True,
+                               timeout=300)
+        except subprocess.TimeoutExpired:
+            return ["timed out"]
+        if r.returncode != 0:
+            return ["crashed"]  # the pins drove the mutant into memory it does not own
+        return json.loads(r.stdout.strip().splitlines()[-1])
+
+    with ThreadPoolExecutor(max_workers=6) as pool:
+        return dict(zip(names, pool.map(run, names)))
+
+
 def test_unmutated_source_passes_every_pin():
     for _, call in PIN_CALLS:
         call()
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
-def test_every_planted_mistake_fails_a_pin(name, tmp_path):
-    so = _build_mutant(str(tmp_path), name)
-    caught = []
-    with oracle.use_library(so):
-        for label, call in PIN_CALLS:
-            try:
-                call()
-            except (AssertionError, ValueError):
-                caught.append(label)
-    assert caught, f"mutant {name} passed every pin"
+def test_every_planted_mistake_fails_a_pin(name, mutant_results):
+    assert mutant_results[name], f"mutant {name} passed every pin"
