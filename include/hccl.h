@@ -155,13 +155,45 @@ hcclResult_t hccl_alltoallv(hcclComm_t comm,
                             hcclDataType_t dtype, void* stream);
 
 /*
+ * AllToAllvDynamic (Section IV-B-2, device-resident collectives): an AllToAllv whose row
+ * counts, and optionally row offsets, are read from device memory when the collective runs,
+ * so that a routing kernel earlier on `stream` can write them and nothing on the host waits
+ * for it. The program depends only on the capacities and is compiled once; a step of P
+ * tiles reads the layout and checks it on the device, then the rows move.
+ *
+ * All metadata arrays are device memory of P*P int64, 8-byte aligned, counted in rows of
+ * `row_elems` elements of `dtype`:
+ *   sendcounts[s*P + d]  rows source s sends to destination d (read)
+ *   sdispls[s*P + d]     row offset of that range in sendbufs[s] (read); NULL = packed: the
+ *                        ranges of one source back to back in ascending destination order
+ *   rdispls[d*P + s]     row offset in recvbufs[d] of the rows from s (read); NULL = packed:
+ *                        ascending sources back to back from row 0
+ *   recvcounts[d*P + s]  = sendcounts[s*P + d] (written; may be NULL)
+ * sendbufs[s] holds send_capacity rows and recvbufs[d] recv_capacity rows; the library reads
+ * and writes nothing outside them. Send buffers and the read metadata may alias each other;
+ * receive buffers and recvcounts alias nothing.
+ *
+ * A layout with a negative count, a non-empty range outside its buffer, or two overlapping
+ * non-empty receive ranges of one destination is rejected on the device: no receive byte is
+ * written (recvcounts is still written) and hccl_get_async_error reports hcclInvalidArgument.
+ * Until that report is read, later collectives on the communicator do nothing. Ranges of count
+ * 0 are never checked. Errors found on the host (arguments) return before anything is enqueued.
+ */
+hcclResult_t hccl_alltoallv_dynamic(hcclComm_t comm,
+                                    const void* const* sendbufs, const int64_t* sendcounts, const int64_t* sdispls,
+                                    void* const* recvbufs, int64_t* recvcounts, const int64_t* rdispls,
+                                    size_t row_elems, size_t send_capacity, size_t recv_capacity,
+                                    hcclDataType_t dtype, void* stream);
+
+/*
  * Groups (one work packet for several collectives, Section III-B: a work packet holds
  * several subgraphs). Collectives called on `comm` between hccl_group_start and the
  * matching hccl_group_end are checked when called but only recorded; hccl_group_end
  * compiles them into one program and enqueues it as one executor launch on the stream the
  * calls named (all calls of a group must name the same stream). Groups nest; only the
- * outermost end launches. The buffers of different calls in a group must not overlap, and
- * a group may name at most 128 rank buffers in total (sum of 2 * nranks over its calls).
+ * outermost end launches. Buffers of different calls in a group may overlap only where both
+ * calls just read them; a group may name at most 128 rank buffers in total (sum of 2 * nranks
+ * over its calls) and hold at most two hccl_alltoallv_dynamic calls.
  * On an error in hccl_group_end nothing of the group is enqueued.
  */
 hcclResult_t hccl_group_start(hcclComm_t comm);
@@ -175,13 +207,15 @@ const char* hccl_result_string(hcclResult_t r);
 
 /*
  * Synchronises the communicator's device and reports a device-side failure recorded since
- * the previous call (hcclTimeout when a dependency wait hit the watchdog), then clears it.
+ * the previous call (hcclTimeout when a dependency wait hit the watchdog, hcclInvalidArgument
+ * when a device-resident layout was rejected), then clears it.
  */
 hcclResult_t hccl_get_async_error(hcclComm_t comm);
 
 /* Description of the most recently compiled or reused program of a communicator. */
 typedef struct {
-    int32_t collective;          /* 0 allreduce, 1 reduce_scatter, 2 allgather, 3 alltoallv */
+    int32_t collective;          /* 0 allreduce, 1 reduce_scatter, 2 allgather, 3 alltoallv,
+                                    4 alltoallv_dynamic, -1 a group */
     int32_t algo;                /* hcclAlgo_t actually lowered */
     int32_t fused;               /* fusion pass applied */
     int32_t cache_hit;           /* 1 if the program came from the cache */

@@ -48,6 +48,7 @@ struct Call {
     CollectiveSpec spec;
     std::vector<const void*> send;
     std::vector<void*> recv;
+    std::vector<void*> meta;   // device metadata arrays of a dynamic call (MetaSlot order)
     hipStream_t stream = nullptr;
 };
 
@@ -74,6 +75,9 @@ struct hcclComm {
     ErrorRecord* d_error = nullptr;
     void* d_scratch = nullptr;
     uint64_t scratch_bytes = 0;
+    hipEvent_t scratch_done = nullptr;  // recorded after each launch that uses the scratch
+    hipStream_t scratch_stream = nullptr;
+    bool scratch_launched = false;
     std::list<std::unique_ptr<DeviceProgram>> cache;  // most recently used first
     size_t cache_limit = 64;
     bool dynamic_dispatch = false;  // tickets also for programs without dependencies
@@ -285,6 +289,9 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     }
     a.bufs[base] = (char*)c->d_scratch;  // the scratch id follows every call's buffers
     const uint32_t nuser = base;
+    uint32_t mb = base + 1;              // then the metadata arrays of the dynamic calls
+    for (const Call& k : calls)
+        for (void* m : k.meta) a.bufs[mb++] = (char*)m;
     const bool has_deps = (dp->prog.flags & PF_HAS_DEPS) != 0;
     a.dynamic = (has_deps || c->dynamic_dispatch) ? 1u : 0u;
     const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
@@ -333,10 +340,16 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         return hcclSuccess;
     }
 
-    // a program's counters serve one launch at a time: order launches across streams
+    // a program's counters serve one launch at a time, and the communicator's scratch one
+    // program at a time: order such launches across streams
     const bool stateful = a.dynamic != 0;
+    const bool scratch = dp->prog.scratch_bytes > 0;
     if (stateful && dp->launched && dp->last_stream != s) {
         hipError_t e = hipStreamWaitEvent(s, dp->done, 0);
+        if (e != hipSuccess) return hip_fail(e, "cross-stream ordering");
+    }
+    if (scratch && c->scratch_launched && c->scratch_stream != s) {
+        hipError_t e = hipStreamWaitEvent(s, c->scratch_done, 0);
         if (e != hipSuccess) return hip_fail(e, "cross-stream ordering");
     }
     hipError_t e = launch_executor(a, blocks, kind, s);
@@ -347,14 +360,22 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         dp->last_stream = s;
         dp->launched = true;
     }
+    if (scratch) {
+        e = hipEventRecord(c->scratch_done, s);
+        if (e != hipSuccess) return hip_fail(e, "completion event");
+        c->scratch_stream = s;
+        c->scratch_launched = true;
+    }
     return hcclSuccess;
 }
 
-hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* send, void* const* recv, void* stream) {
+hcclResult_t run(hcclComm* c, const CollectiveSpec& spec, const void* const* send, void* const* recv, void* stream,
+                 std::vector<void*> meta = {}) {
     Call k;
     k.spec = spec;
     k.send.assign(send, send + spec.P);
     k.recv.assign(recv, recv + spec.P);
+    k.meta = std::move(meta);
     k.stream = (hipStream_t)stream;
     if (c->group_depth > 0) {
         c->pending.push_back(std::move(k));
@@ -433,6 +454,8 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
             if (e != hipSuccess) return hip_fail(e, "executor occupancy");
             if (bpc && std::atoi(bpc) > 0) c->blocks_per_cu[k] = std::min(c->blocks_per_cu[k], std::atoi(bpc));
         }
+        e = hipEventCreateWithFlags(&c->scratch_done, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(e, "scratch event");
         e = hipMalloc(&c->d_error, sizeof(ErrorRecord));
         if (e != hipSuccess) return fail(hcclOutOfMemory, "error record allocation failed");
         e = hipMemset(c->d_error, 0, sizeof(ErrorRecord));
@@ -451,6 +474,7 @@ hcclResult_t hccl_comm_destroy(hcclComm_t comm) {
         comm->cache.clear();
         if (comm->d_scratch) (void)hipFree(comm->d_scratch);
         if (comm->d_error) (void)hipFree(comm->d_error);
+        if (comm->scratch_done) (void)hipEventDestroy(comm->scratch_done);
     }
     delete comm;
     return hcclSuccess;
@@ -584,6 +608,49 @@ hcclResult_t hccl_alltoallv(hcclComm_t comm, const void* const* sendbufs, const 
     return run(comm, s, sendbufs, recvbufs, stream);
 }
 
+hcclResult_t hccl_alltoallv_dynamic(hcclComm_t comm, const void* const* sendbufs, const int64_t* sendcounts,
+                                    const int64_t* sdispls, void* const* recvbufs, int64_t* recvcounts,
+                                    const int64_t* rdispls, size_t row_elems, size_t send_capacity,
+                                    size_t recv_capacity, hcclDataType_t dtype, void* stream) {
+    hcclResult_t r;
+    if ((r = check_comm(comm)) || (r = check_ptr_arrays(sendbufs, recvbufs)) || (r = check_dtype(dtype))) return r;
+    if (!sendcounts) return fail(hcclInvalidArgument, "null count array");
+    if (row_elems == 0) return fail(hcclInvalidArgument, "row_elems must be at least 1");
+    const int P = comm->nranks;
+    const uint64_t es = dtype_size((uint32_t)dtype);
+    const uint64_t kLimit = (1ull << 62) / 8;
+    if (row_elems > kLimit || send_capacity > kLimit / row_elems / es || recv_capacity > kLimit / row_elems / es)
+        return fail(hcclInvalidArgument, "capacity out of range");
+    const void* meta[kMetaPerDynamicCall] = {sendcounts, sdispls, rdispls, recvcounts};
+    for (const void* m : meta)
+        if ((uintptr_t)m % alignof(int64_t)) return fail(hcclInvalidArgument, "metadata arrays must be 8-byte aligned");
+    CollectiveSpec s;
+    if ((r = fill_spec(comm, s, COLL_ALLTOALLV_DYNAMIC, dtype, hcclSum))) return r;
+    s.row_elems = row_elems;
+    s.send_cap = send_capacity;
+    s.recv_cap = recv_capacity;
+    s.dyn_sdispls = sdispls != nullptr;
+    s.dyn_rdispls = rdispls != nullptr;
+    s.dyn_recvcounts = recvcounts != nullptr;
+    // ids: sends [0, P), receives [P, 2P), metadata 2P + slot. Sends and the metadata inputs
+    // are only read and may alias each other; receives and the count output alias nothing.
+    const uint64_t sb = send_capacity * row_elems * es, rb = recv_capacity * row_elems * es;
+    const uint64_t mbytes = (uint64_t)P * P * sizeof(int64_t);
+    std::vector<Range> v;
+    for (int i = 0; i < P; ++i) {
+        v.push_back({(uintptr_t)sendbufs[i], (uintptr_t)sendbufs[i] + sb, i});
+        v.push_back({(uintptr_t)recvbufs[i], (uintptr_t)recvbufs[i] + rb, P + i});
+    }
+    for (int m = 0; m < kMetaPerDynamicCall; ++m)
+        if (meta[m]) v.push_back({(uintptr_t)meta[m], (uintptr_t)meta[m] + mbytes, 2 * P + m});
+    auto read_only = [&](int id) { return id < P || (id >= 2 * P && id < 2 * P + META_RECVCOUNTS); };
+    if ((r = check_buffers(v, es, [&](const Range& a, const Range& b) { return read_only(a.id) && read_only(b.id); })))
+        return r;
+    std::vector<void*> mv;
+    for (const void* m : meta) mv.push_back(const_cast<void*>(m));
+    return run(comm, s, sendbufs, recvbufs, stream, std::move(mv));
+}
+
 hcclResult_t hccl_group_start(hcclComm_t comm) {
     if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
     comm->group_depth += 1;
@@ -599,22 +666,34 @@ hcclResult_t hccl_group_end(hcclComm_t comm) {
     if (calls.empty()) return hcclSuccess;
     for (const Call& k : calls)
         if (k.stream != calls[0].stream) return fail(hcclInvalidArgument, "calls of one group must use one stream");
-    uint32_t nbuf = 1;
-    for (const Call& k : calls) nbuf += 2 * (uint32_t)k.spec.P;
-    if (nbuf > (uint32_t)kMaxBuffers) return fail(hcclUnsupported, "a group may name at most 128 rank buffers");
-    // buffers of different calls must not overlap (each call was checked on its own)
+    uint32_t nbuf = 0, nmeta = 0;
+    for (const Call& k : calls) {
+        nbuf += 2 * (uint32_t)k.spec.P;
+        nmeta += meta_buffers(k.spec);
+    }
+    if (nbuf > 2u * (uint32_t)kMaxRanks) return fail(hcclUnsupported, "a group may name at most 128 rank buffers");
+    if (nmeta > (uint32_t)kMaxMetaBuffers) return fail(hcclUnsupported, "a group may hold at most two dynamic calls");
+    // buffers of different calls must not overlap unless both are only read (each call was
+    // checked on its own): ids are 2 * call + 1 for what a call writes, 2 * call for what it reads
     if (calls.size() > 1) {
         std::vector<Range> v;
         int id = 0;
         for (const Call& k : calls) {
             BufferSizes sz = buffer_sizes(k.spec, 0);
             for (int i = 0; i < k.spec.P; ++i) {
-                v.push_back({(uintptr_t)k.send[i], (uintptr_t)k.send[i] + sz.bytes[send_buf(i)], id});
-                v.push_back({(uintptr_t)k.recv[i], (uintptr_t)k.recv[i] + sz.bytes[recv_buf(k.spec.P, i)], id});
+                v.push_back({(uintptr_t)k.send[i], (uintptr_t)k.send[i] + sz.bytes[send_buf(i)], 2 * id});
+                v.push_back({(uintptr_t)k.recv[i], (uintptr_t)k.recv[i] + sz.bytes[recv_buf(k.spec.P, i)], 2 * id + 1});
             }
+            const uint64_t mbytes = (uint64_t)k.spec.P * k.spec.P * sizeof(int64_t);
+            for (size_t m = 0; m < k.meta.size(); ++m)
+                if (k.meta[m])
+                    v.push_back({(uintptr_t)k.meta[m], (uintptr_t)k.meta[m] + mbytes,
+                                 2 * id + (m == META_RECVCOUNTS ? 1 : 0)});
             ++id;
         }
-        hcclResult_t r = check_buffers(v, 1, [](const Range& a, const Range& b) { return a.id == b.id; });
+        hcclResult_t r = check_buffers(v, 1, [](const Range& a, const Range& b) {
+            return a.id / 2 == b.id / 2 || (a.id % 2 == 0 && b.id % 2 == 0);
+        });
         if (r != hcclSuccess) return fail(hcclInvalidArgument, "buffers of different calls in a group overlap");
     }
     return run_packet(comm, calls);
@@ -645,9 +724,17 @@ hcclResult_t hccl_get_async_error(hcclComm_t comm) {
     e = hipMemcpy(&rec, comm->d_error, sizeof rec, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "read error record");
     if (rec.code == 0) return hcclSuccess;
-    std::memset(&rec, 0, sizeof rec);
-    (void)hipMemcpy(comm->d_error, &rec, sizeof rec, hipMemcpyHostToDevice);
-    char buf[160];
+    ErrorRecord cleared;
+    std::memset(&cleared, 0, sizeof cleared);
+    (void)hipMemcpy(comm->d_error, &cleared, sizeof cleared, hipMemcpyHostToDevice);
+    char buf[200];
+    if (rec.code == 2) {
+        std::snprintf(buf, sizeof buf,
+                      "the device-resident layout read by step %u was invalid (row or column %u): "
+                      "a count or offset left its buffer, or receive ranges overlapped; nothing was moved",
+                      rec.desc, rec.tile);
+        return fail(hcclInvalidArgument, buf);
+    }
     std::snprintf(buf, sizeof buf, "a dependency wait of step %u (tile %u) exceeded the watchdog limit",
                   rec.desc, rec.tile);
     return fail(hcclTimeout, buf);

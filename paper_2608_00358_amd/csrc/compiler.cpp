@@ -32,6 +32,9 @@ constexpr uint32_t kDefaultDependentTileBytes = 128u * 1024u;
 constexpr uint64_t kSmallTargetTiles = 2048;
 constexpr uint32_t kWaveStepElems = kWaveSize * kVecElems;  // 512: one vector per lane
 constexpr uint64_t kShardAlignElems = 64;                      // 128 B of bf16, 256 B of fp32
+// Static tiles (slots) of the copy step of an AllToAllvDynamic: each moves a contiguous run
+// of about J / slots dynamic tiles, so there are enough for every wavefront of the chip.
+constexpr uint32_t kDynamicSlots = 2048;
 
 // Type of partials that leave registers: FP32 for floating sums (one rounding at the end),
 // the buffer type when every partial is re-quantised, or for MAX / MIN (exact in any type).
@@ -455,6 +458,46 @@ void lower_alltoallv(const CollectiveSpec& s, HostProgram& p) {
     p.algo = ALGO_DIRECT;
 }
 
+// ------------------------------------------------------------------ ALLTOALLV DYNAMIC
+// Device-resident AllToAllv (Section IV-B-2): the host compiles the program once for the
+// capacities, and the layout is built on the device when it runs. Step 0 (P tiles) reads the
+// count matrix, and the explicit offsets if given, from device memory, checks every range
+// and writes the plan table; step 1 waits for all of step 0 and moves the rows, its slots
+// splitting the dynamic tiles between them. Nothing on the host depends on the counts.
+void lower_alltoallv_dynamic(const CollectiveSpec& s, HostProgram& p) {
+    const int P = s.P;
+    DynA2A a;
+    std::memset(&a, 0, sizeof a);
+    a.P = (uint32_t)P;
+    a.elem_bytes = dtype_size(s.dtype);
+    a.send0 = send_buf(0);
+    a.recv0 = recv_buf(P, 0);
+    a.counts = meta_buf(P, META_COUNTS);
+    a.sdispls = s.dyn_sdispls ? meta_buf(P, META_SDISPLS) : kNoBuffer;
+    a.rdispls = s.dyn_rdispls ? meta_buf(P, META_RDISPLS) : kNoBuffer;
+    a.recvcounts = s.dyn_recvcounts ? meta_buf(P, META_RECVCOUNTS) : kNoBuffer;
+    a.table = scratch_buf(P);
+    a.table_off = 0;
+    a.row_elems = s.row_elems;
+    a.send_cap = s.send_cap;
+    a.recv_cap = s.recv_cap;
+    a.tile_elems = dynamic_tile_elems(s);
+    a.slots = dynamic_slots(s);
+    p.aux.push_back(a);
+    p.nmeta = kMetaPerDynamicCall;
+    p.scratch_bytes = plan_bytes((uint32_t)P);
+    HostDesc plan;
+    plan.op = OP_DYN_PLAN;
+    plan.aux = 0;
+    p.descs.push_back(plan);
+    HostDesc copy;
+    copy.op = OP_DYN_COPY;
+    copy.aux = 0;
+    copy.deps.push_back(Dep{0, DEP_ALL, 0, 0});
+    p.descs.push_back(copy);
+    p.algo = ALGO_DIRECT;
+}
+
 void dedupe_deps(HostDesc& d, uint32_t self) {
     std::vector<Dep> out;
     for (const Dep& e : d.deps) {
@@ -493,11 +536,29 @@ bool CollectiveSpec::operator==(const CollectiveSpec& o) const {
            sendcounts == o.sendcounts && sdispls == o.sdispls && recvcounts == o.recvcounts &&
            rdispls == o.rdispls && in_place == o.in_place && algo == o.algo && group_size == o.group_size &&
            chunk_bytes == o.chunk_bytes && fuse == o.fuse && tile_bytes == o.tile_bytes && order == o.order &&
-           requant == o.requant;
+           requant == o.requant && row_elems == o.row_elems && send_cap == o.send_cap && recv_cap == o.recv_cap &&
+           dyn_sdispls == o.dyn_sdispls && dyn_rdispls == o.dyn_rdispls && dyn_recvcounts == o.dyn_recvcounts;
+}
+
+uint64_t dynamic_tile_elems(const CollectiveSpec& s) {
+    const uint64_t tb = s.tile_bytes ? s.tile_bytes : kDefaultCopyTileBytes;
+    const uint64_t te = (tb / dtype_size(s.dtype)) / kWaveStepElems * kWaveStepElems;
+    return std::min<uint64_t>(std::max<uint64_t>(te, kWaveStepElems), 1ull << 30);
+}
+
+uint64_t dynamic_tile_bound(const CollectiveSpec& s) {
+    // a source's pairs cover at most send_cap rows, and each pair adds at most one partial tile
+    const uint64_t te = dynamic_tile_elems(s);
+    const uint64_t per_source = (s.send_cap * s.row_elems + te - 1) / te + (uint64_t)s.P;
+    return (uint64_t)s.P * per_source;
+}
+
+uint32_t dynamic_slots(const CollectiveSpec& s) {
+    return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(kDynamicSlots, dynamic_tile_bound(s)));
 }
 
 int resolve_algo(const CollectiveSpec& s) {
-    if (s.coll == COLL_ALLTOALLV) return ALGO_DIRECT;
+    if (s.coll == COLL_ALLTOALLV || s.coll == COLL_ALLTOALLV_DYNAMIC) return ALGO_DIRECT;
     if (s.algo != ALGO_AUTO) return s.algo;
     if (s.order == ORDER_HALVING) return ALGO_RHD;
     if (s.coll == COLL_ALLREDUCE && s.order == ORDER_ASCENDING && s.group_size > 1 && s.group_size < s.P &&
@@ -517,6 +578,7 @@ BufferSizes buffer_sizes(const CollectiveSpec& s, uint64_t scratch_bytes) {
             case COLL_ALLREDUCE: sb = rb = s.count * es; break;
             case COLL_REDUCE_SCATTER: sb = (uint64_t)P * s.count * es; rb = s.count * es; break;
             case COLL_ALLGATHER: sb = s.count * es; rb = (uint64_t)P * s.count * es; break;
+            case COLL_ALLTOALLV_DYNAMIC: sb = s.send_cap * s.row_elems * es; rb = s.recv_cap * s.row_elems * es; break;
             default:
                 for (int q = 0; q < P; ++q) {
                     sb = std::max(sb, (s.sdispls[(size_t)r * P + q] + s.sendcounts[(size_t)r * P + q]) * es);
@@ -535,6 +597,18 @@ bool lower(const CollectiveSpec& s, HostProgram& p, std::string& err) {
     p.P = s.P;
     if (s.coll == COLL_ALLTOALLV) {
         lower_alltoallv(s, p);
+        return true;
+    }
+    if (s.coll == COLL_ALLTOALLV_DYNAMIC) {
+        if (s.P > kMaxRanks || s.row_elems == 0) {
+            err = "alltoallv_dynamic needs 1..64 ranks and row_elems >= 1";
+            return false;
+        }
+        if (dynamic_tile_bound(s) >= (1ull << 31)) {
+            err = "alltoallv_dynamic capacities too large for one exchange";
+            return false;
+        }
+        lower_alltoallv_dynamic(s, p);
         return true;
     }
     int algo = resolve_algo(s);
@@ -769,6 +843,7 @@ void fuse(HostProgram& p) {
     bool uses_scratch = false;
     for (const auto& d : p.descs) {
         if (!d.alive) continue;
+        uses_scratch |= (d.op == OP_DYN_PLAN || d.op == OP_DYN_COPY);  // the plan table
         for (const Operand& o : d.srcs) uses_scratch |= (o.buf == scratch);
         for (const Operand& o : d.dsts) uses_scratch |= (o.buf == scratch);
     }
@@ -780,27 +855,56 @@ bool merge(std::vector<HostProgram>& parts, const std::vector<CollectiveSpec>& s
            std::string& err) {
     out = HostProgram();
     const size_t n = parts.size();
-    std::vector<uint32_t> buf_base(n), nbuf(n);
+    std::vector<uint32_t> buf_base(n), nbuf(n), meta_base(n), aux_base(n);
     std::vector<uint64_t> scratch_base(n), bytes(n);
-    uint32_t total = 0;
+    uint32_t total = 0, nmeta = 0, naux = 0;
     uint64_t scratch = 0;
     for (size_t k = 0; k < n; ++k) {
         buf_base[k] = total;
         nbuf[k] = 2u * (uint32_t)specs[k].P;
         total += nbuf[k];
+        meta_base[k] = nmeta;
+        nmeta += parts[k].nmeta;
+        aux_base[k] = naux;
+        naux += (uint32_t)parts[k].aux.size();
         scratch_base[k] = scratch;
         scratch += (parts[k].scratch_bytes + 255) & ~uint64_t(255);
         for (const auto& d : parts[k].descs)
             if (d.alive) bytes[k] += d.nelem * (d.srcs.size() + d.dsts.size());
     }
-    if (total + 1 > (uint32_t)kMaxBuffers) {
+    if (total > 2u * (uint32_t)kMaxRanks) {
         err = "a group may name at most 128 rank buffers";
+        return false;
+    }
+    if (nmeta > (uint32_t)kMaxMetaBuffers) {
+        err = "a group may hold at most two dynamic calls";
         return false;
     }
     std::vector<size_t> order(n);
     for (size_t k = 0; k < n; ++k) order[k] = k;
     std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return bytes[a] < bytes[b]; });
+    // merged ids: every call's rank buffers, then the one scratch, then every call's metadata
     const uint32_t scratch_id = total;
+    out.P = (int)(total / 2);
+    auto move_id = [&](size_t k, uint32_t id) -> uint32_t {
+        if (id == kNoBuffer) return kNoBuffer;
+        if (id < nbuf[k]) return id + buf_base[k];
+        if (id == nbuf[k]) return scratch_id;
+        return meta_buf(out.P, (int)(meta_base[k] + (id - nbuf[k] - 1)));
+    };
+    for (size_t k = 0; k < n; ++k) {
+        for (DynA2A a : parts[k].aux) {
+            a.send0 = move_id(k, a.send0);
+            a.recv0 = move_id(k, a.recv0);
+            a.counts = move_id(k, a.counts);
+            a.sdispls = move_id(k, a.sdispls);
+            a.rdispls = move_id(k, a.rdispls);
+            a.recvcounts = move_id(k, a.recvcounts);
+            a.table = move_id(k, a.table);
+            a.table_off += scratch_base[k];
+            out.aux.push_back(a);
+        }
+    }
     bool fused = true;
     for (size_t k : order) {
         HostProgram& p = parts[k];
@@ -813,14 +917,11 @@ bool merge(std::vector<HostProgram>& parts, const std::vector<CollectiveSpec>& s
             HostDesc d = p.descs[i];
             for (auto* list : {&d.srcs, &d.dsts}) {
                 for (Operand& o : *list) {
-                    if (o.buf < nbuf[k]) {
-                        o.buf += buf_base[k];
-                    } else {
-                        o.buf = scratch_id;
-                        o.offset += scratch_base[k];
-                    }
+                    if (o.buf == nbuf[k]) o.offset += scratch_base[k];
+                    o.buf = move_id(k, o.buf);
                 }
             }
+            d.aux += aux_base[k];
             out.descs.push_back(std::move(d));
         }
         for (uint32_t i = first; i < out.descs.size(); ++i) {
@@ -833,7 +934,7 @@ bool merge(std::vector<HostProgram>& parts, const std::vector<CollectiveSpec>& s
             }
         }
     }
-    out.P = (int)(total / 2);
+    out.nmeta = nmeta;
     out.algo = parts[order[0]].algo;
     out.fused = fused;
     out.scratch_bytes = scratch;
@@ -905,7 +1006,15 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
         d.fold = h.fold;
         d.requant = h.requant ? 1u : 0u;
         d.tile_elems = p.tile_elems;
+        d.aux = h.aux;
         uint64_t nt = (h.op == OP_NOOP) ? 1 : (h.nelem + te - 1) / te;
+        if (h.op == OP_DYN_PLAN || h.op == OP_DYN_COPY) {
+            if (h.aux >= p.aux.size()) {
+                err = "dynamic step without its record";
+                return false;
+            }
+            nt = (h.op == OP_DYN_PLAN) ? p.aux[h.aux].P : p.aux[h.aux].slots;
+        }
         if (nt == 0) nt = 1;
         d.ntiles = (uint32_t)nt;
         d.tile0 = (uint32_t)ntiles;
@@ -934,7 +1043,7 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     }
     p.ntiles = (uint32_t)ntiles;
     p.nstate = has_deps ? (uint32_t)(kStateDescBase + nd + ntiles) : kStateDescBase;
-    p.flags = has_deps ? PF_HAS_DEPS : 0;
+    p.flags = has_deps ? (uint32_t)PF_HAS_DEPS : 0u;
     // dependency targets: expected values, state words, signal flags
     for (uint32_t i = 0; i < nd; ++i) {
         for (uint32_t k = 0; k < out[i].ndep; ++k) {
@@ -956,6 +1065,8 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
 
     // the leanest executor kernel that covers every step
     int kind = kKindCopyOnly;
+    bool dynamic = false;
+    for (uint32_t i = 0; i < nd; ++i) dynamic |= (out[i].op == OP_DYN_PLAN || out[i].op == OP_DYN_COPY);
     for (uint32_t i = 0; i < nd; ++i) {
         if (out[i].op != OP_REDUCE) continue;
         const bool plain = out[i].sig <= SIG_INT32 && out[i].redop == RO_SUM && out[i].fold == FOLD_LIST &&
@@ -964,6 +1075,7 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
         if (kind == kKindCopyOnly) kind = out[i].sig;
         else if (kind != out[i].sig) { kind = kKindGeneric; break; }
     }
+    if (dynamic) kind = (kind == kKindCopyOnly) ? kKindDynamic : kKindGeneric;  // the two that run them
     if (kind == kKindCopyOnly) {
         bool aligned = true;
         for (const Operand& o : ops) aligned &= (o.offset % 16) == 0;
@@ -986,7 +1098,9 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     hdr.off_operand = align16(hdr.off_desc + (uint64_t)nd * sizeof(Desc));
     hdr.off_dep = align16(hdr.off_operand + ops.size() * sizeof(Operand));
     hdr.off_tile_desc = align16(hdr.off_dep + deps.size() * sizeof(Dep));
-    hdr.total_bytes = align16(hdr.off_tile_desc + tile_owner.size() * sizeof(uint32_t));
+    hdr.off_aux = align16(hdr.off_tile_desc + tile_owner.size() * sizeof(uint32_t));
+    hdr.naux = (uint32_t)p.aux.size();
+    hdr.total_bytes = align16(hdr.off_aux + p.aux.size() * sizeof(DynA2A));
     hdr.scratch_bytes = p.scratch_bytes;
     p.image.assign(hdr.total_bytes, 0);
     std::memcpy(p.image.data(), &hdr, sizeof hdr);
@@ -995,6 +1109,7 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     if (!deps.empty()) std::memcpy(p.image.data() + hdr.off_dep, deps.data(), deps.size() * sizeof(Dep));
     if (!tile_owner.empty())
         std::memcpy(p.image.data() + hdr.off_tile_desc, tile_owner.data(), tile_owner.size() * sizeof(uint32_t));
+    if (!p.aux.empty()) std::memcpy(p.image.data() + hdr.off_aux, p.aux.data(), p.aux.size() * sizeof(DynA2A));
     return true;
 }
 

@@ -17,7 +17,13 @@
 
 namespace hccl {
 
-enum Collective : int { COLL_ALLREDUCE = 0, COLL_REDUCE_SCATTER = 1, COLL_ALLGATHER = 2, COLL_ALLTOALLV = 3 };
+enum Collective : int {
+    COLL_ALLREDUCE = 0,
+    COLL_REDUCE_SCATTER = 1,
+    COLL_ALLGATHER = 2,
+    COLL_ALLTOALLV = 3,
+    COLL_ALLTOALLV_DYNAMIC = 4,  // layout read from device memory when the program runs
+};
 enum Algo : int { ALGO_AUTO = 0, ALGO_DIRECT = 1, ALGO_RING = 2, ALGO_TWO_LEVEL = 3, ALGO_RHD = 4 };
 enum Order : int { ORDER_ASCENDING = 0, ORDER_RING = 1, ORDER_HALVING = 2 };
 
@@ -36,6 +42,10 @@ struct CollectiveSpec {
     uint32_t tile_bytes = 0;
     int order = ORDER_ASCENDING;
     bool requant = false;        // round every partial to the buffer type
+    // alltoallv_dynamic: rows of row_elems elements; buffers hold send_cap / recv_cap rows;
+    // which optional metadata arrays the call passes
+    uint64_t row_elems = 0, send_cap = 0, recv_cap = 0;
+    bool dyn_sdispls = false, dyn_rdispls = false, dyn_recvcounts = false;
 
     bool operator==(const CollectiveSpec& o) const;
 };
@@ -51,6 +61,7 @@ struct HostDesc {
     std::vector<Operand> dsts;
     std::vector<Dep> deps;
     bool alive = true;
+    uint32_t aux = 0;            // OP_DYN_*: index into HostProgram::aux
 };
 
 struct HostProgram {
@@ -59,6 +70,8 @@ struct HostProgram {
     bool fused = false;
     uint64_t scratch_bytes = 0;
     std::vector<HostDesc> descs;
+    std::vector<DynA2A> aux;     // records of the dynamic steps
+    uint32_t nmeta = 0;          // metadata buffer ids in use, from meta_buf(P, 0)
 
     // filled by finalize()
     uint32_t tile_elems = 0;
@@ -78,12 +91,25 @@ struct HostProgram {
 inline uint32_t send_buf(int r) { return (uint32_t)r; }
 inline uint32_t recv_buf(int P, int r) { return (uint32_t)(P + r); }
 inline uint32_t scratch_buf(int P) { return (uint32_t)(2 * P); }
+inline uint32_t meta_buf(int P, int i) { return (uint32_t)(2 * P + 1 + i); }
+// Metadata arrays of one AllToAllvDynamic call, in buffer-id order from meta_buf(P, 0).
+enum MetaSlot : int { META_COUNTS = 0, META_SDISPLS = 1, META_RDISPLS = 2, META_RECVCOUNTS = 3 };
 
 // Byte size of every buffer id a program may touch (for bounds checks and coverage).
 struct BufferSizes {
     std::vector<uint64_t> bytes;  // indexed by buffer id, 2P + 1 entries
 };
 BufferSizes buffer_sizes(const CollectiveSpec& spec, uint64_t scratch_bytes);
+
+inline uint32_t meta_buffers(const CollectiveSpec& s) {
+    return s.coll == COLL_ALLTOALLV_DYNAMIC ? (uint32_t)kMetaPerDynamicCall : 0u;
+}
+
+// Static tiles of the copy step of an AllToAllvDynamic, and the elements per dynamic tile.
+uint32_t dynamic_slots(const CollectiveSpec& s);
+uint64_t dynamic_tile_elems(const CollectiveSpec& s);
+// Upper bound on the dynamic tiles of any layout that fits the capacities.
+uint64_t dynamic_tile_bound(const CollectiveSpec& s);
 
 // Picks the schedule for ALGO_AUTO.
 int resolve_algo(const CollectiveSpec& spec);

@@ -672,6 +672,120 @@ __device__ __forceinline__ bool wait_deps(const Dep* deps, uint32_t ndep, uint32
     return true;
 }
 
+// ---------------------------------------------------------------- AllToAllvDynamic
+// The layout of a device-resident AllToAllv (Section IV-B-2) is read from device memory when
+// the program runs. P plan tiles build a table of per-pair element counts, offsets and tile
+// prefix sums; the copy slots wait for all of them and move the rows.
+
+// Inclusive prefix sum over the lanes of a wavefront.
+__device__ __forceinline__ uint64_t wave_scan_incl(uint64_t v, uint32_t lane) {
+#pragma unroll
+    for (uint32_t d = 1; d < (uint32_t)kWaveSize; d <<= 1) {
+        const uint64_t t = __shfl_up(v, d);
+        if (lane >= d) v += t;
+    }
+    return v;
+}
+
+struct DynView {     // a DynA2A record loaded into scalar registers
+    uint32_t P, es, send0, recv0, counts, sdispls, rdispls, recvcounts, slots;
+    uint64_t row_elems, send_cap, recv_cap, tile_elems;
+    char* tab;       // the plan table
+};
+
+__device__ __forceinline__ DynView load_dyn(const DynA2A* r, const uint64_t* bufs) {
+    DynView v;
+    v.P = uni(r->P);
+    v.es = uni(r->elem_bytes);
+    v.send0 = uni(r->send0);
+    v.recv0 = uni(r->recv0);
+    v.counts = uni(r->counts);
+    v.sdispls = uni(r->sdispls);
+    v.rdispls = uni(r->rdispls);
+    v.recvcounts = uni(r->recvcounts);
+    v.slots = uni(r->slots);
+    v.row_elems = uni64(r->row_elems);
+    v.send_cap = uni64(r->send_cap);
+    v.recv_cap = uni64(r->recv_cap);
+    v.tile_elems = uni64(r->tile_elems);
+    v.tab = (char*)(uni64(bufs[uni(r->table)]) + uni64(r->table_off));
+    return v;
+}
+
+// Plan tile i: row i of the count matrix (what source i sends, one destination per lane) and
+// column i (what destination i receives, one source per lane). Every range is checked against
+// its buffer's capacity, explicit receive ranges also against each other; a failure marks the
+// table so that no row moves, and is reported in the error record.
+__device__ __forceinline__ void dyn_plan(const DynView& a, uint32_t i, const uint64_t* bufs, ErrorRecord* err,
+                                         uint32_t desc, uint32_t lane) {
+    const uint32_t P = a.P;
+    const bool on = lane < P;
+    const uint64_t R = a.row_elems, te = a.tile_elems;
+    const int64_t* counts = (const int64_t*)uni64(bufs[a.counts]);
+
+    // ---- source i
+    const int64_t c = on ? counts[(uint64_t)i * P + lane] : 0;
+    bool bad = on && (c < 0 || (uint64_t)c > a.send_cap);
+    const uint64_t cs = (on && !bad) ? (uint64_t)c : 0;  // clamped: sums of these cannot overflow
+    uint64_t so;
+    if (a.sdispls != kNoBuffer) {
+        const int64_t* sd = (const int64_t*)uni64(bufs[a.sdispls]);
+        const int64_t x = on ? sd[(uint64_t)i * P + lane] : 0;
+        if (cs && (x < 0 || (uint64_t)x > a.send_cap || cs > a.send_cap - (uint64_t)x)) bad = true;
+        so = (uint64_t)x;
+    } else {
+        const uint64_t incl = wave_scan_incl(cs, lane);
+        if (cs && incl > a.send_cap) bad = true;
+        so = incl - cs;
+    }
+    const uint64_t ne = cs * R;
+    const uint64_t pre = wave_scan_incl((ne + te - 1) / te, lane);
+    if (on) {
+        ((uint32_t*)(a.tab + kPlanPre))[i * P + lane] = (uint32_t)pre;
+        ((uint64_t*)(a.tab + plan_elems_off(P)))[i * P + lane] = ne;
+        ((uint64_t*)(a.tab + plan_soff_off(P)))[i * P + lane] = so * R;
+    }
+    if (lane == P - 1) ((uint32_t*)a.tab)[i] = (uint32_t)pre;
+
+    // ---- destination i
+    const int64_t c2 = on ? counts[(uint64_t)lane * P + i] : 0;
+    bool bad2 = on && (c2 < 0 || (uint64_t)c2 > a.recv_cap);
+    const uint64_t cr = (on && !bad2) ? (uint64_t)c2 : 0;
+    uint64_t ro;
+    if (a.rdispls != kNoBuffer) {
+        const int64_t* rd = (const int64_t*)uni64(bufs[a.rdispls]);
+        const int64_t x = on ? rd[(uint64_t)i * P + lane] : 0;
+        if (cr && (x < 0 || (uint64_t)x > a.recv_cap || cr > a.recv_cap - (uint64_t)x)) bad2 = true;
+        ro = (uint64_t)x;
+        // non-empty receive ranges of destination i must not overlap (a lane whose own range is
+        // out of bounds has already failed the layout, so the sums below are only trusted
+        // where both ranges are in bounds)
+        for (uint32_t j = 0; j < P; ++j) {
+            const uint64_t oj = from_lane(ro, j), nj = from_lane(cr, j);
+            if (j != lane && cr && nj && ro < oj + nj && oj < ro + cr) bad2 = true;
+        }
+    } else {
+        const uint64_t incl = wave_scan_incl(cr, lane);
+        if (cr && incl > a.recv_cap) bad2 = true;
+        ro = incl - cr;
+    }
+    if (on) ((uint64_t*)(a.tab + plan_roff_off(P)))[(uint64_t)lane * P + i] = ro * R;
+    if (on && a.recvcounts != kNoBuffer) ((int64_t*)uni64(bufs[a.recvcounts]))[(uint64_t)i * P + lane] = c2;
+
+    const bool any = __ballot(bad || bad2) != 0ull;
+    if (lane == 0) {
+        ((uint32_t*)(a.tab + 256))[i] = any ? 1u : 0u;
+        if (any) {
+            uint32_t zero = 0;
+            if (__hip_atomic_compare_exchange_strong(&err->code, &zero, 2u, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT)) {
+                __hip_atomic_store(&err->desc, desc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&err->tile, i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    }
+}
+
 // ----------------------------------------------------------------------- the kernel
 // Runs tile `t`. Returns false when a dependency wait failed.
 struct Shared {
@@ -709,6 +823,50 @@ __device__ __forceinline__ void exec_tile(uint32_t op, uint32_t sig, uint32_t re
     }
 }
 
+// Copy slot k: dynamic tiles [k*J/slots, (k+1)*J/slots) of the J the plan produced, numbered
+// source-major, then destination, then tile within the pair.
+template <int KIND>
+__device__ __forceinline__ void dyn_copy(const DynView& a, uint32_t k, const uint64_t* bufs, uint32_t lane) {
+    const uint32_t P = a.P;
+    const bool on = lane < P;
+    const uint32_t bad = on ? ((const uint32_t*)(a.tab + 256))[lane] : 0u;
+    if (__ballot(bad != 0u) != 0ull) return;  // the layout was rejected: move nothing
+    const uint64_t incl = wave_scan_incl(on ? ((const uint32_t*)a.tab)[lane] : 0u, lane);
+    const uint64_t J = from_lane(incl, P - 1);
+    const uint64_t j0 = (uint64_t)k * J / a.slots, j1 = (uint64_t)(k + 1) * J / a.slots;
+    const uint32_t* pre = (const uint32_t*)(a.tab + kPlanPre);
+    const uint64_t* elems = (const uint64_t*)(a.tab + plan_elems_off(P));
+    const uint64_t* soff = (const uint64_t*)(a.tab + plan_soff_off(P));
+    const uint64_t* roff = (const uint64_t*)(a.tab + plan_roff_off(P));
+    uint32_t row = 0xFFFFFFFFu;
+    uint64_t rp = 0;
+    TileOps ops;
+    ops.nsrc = 1;
+    ops.ndst = 1;
+    ops.group = 0;
+    for (uint64_t j = j0; j < j1; ++j) {
+        // the source: rows whose inclusive prefix is <= j lie before it (j < J, so s < P)
+        const uint32_t s = (uint32_t)__popcll(__ballot(on && incl <= j));
+        if (s >= P) break;  // cannot happen with a table from this launch; never index past it
+        const uint64_t jr = j - (s ? from_lane(incl, s - 1) : 0);
+        if (s != row) {
+            rp = on ? pre[s * P + lane] : ~0ull;
+            row = s;
+        }
+        // the destination within row s (jr < the row's total, so d < P)
+        const uint32_t d = (uint32_t)__popcll(__ballot(on && rp <= jr));
+        if (d >= P) break;
+        const uint64_t t = jr - (d ? from_lane(rp, d - 1) : 0);
+        const uint32_t idx = s * P + d;
+        const uint64_t ne = uni64(elems[idx]);
+        const uint64_t e0 = t * a.tile_elems;
+        const uint32_t n = (uint32_t)((ne - e0 < a.tile_elems) ? (ne - e0) : a.tile_elems);
+        ops.src = uni64(bufs[a.send0 + s]) + (uni64(soff[idx]) + e0) * a.es;
+        ops.dst = uni64(bufs[a.recv0 + d]) + (uni64(roff[idx]) + e0) * a.es;
+        exec_tile<KIND>(OP_COPY, 0, 0, a.es, ops, n, false, lane);
+    }
+}
+
 template <int KIND>
 __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, const ProgramHeader& h, uint32_t t,
                                          uint32_t lane, const uint64_t* bufs) {
@@ -728,7 +886,14 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
         if (!wait_deps(deps, ndep, k, a.state, a.error, a.timeout, d, t)) return false;
     }
 
-    if (op != OP_NOOP) {
+    if (op == OP_DYN_PLAN || op == OP_DYN_COPY) {
+        // the host runs programs with dynamic steps on these two kernels only
+        if constexpr (KIND == kKindDynamic || KIND == kKindGeneric) {
+            const DynView v = load_dyn((const DynA2A*)(prog + h.off_aux) + uni(D->aux), bufs);
+            if (op == OP_DYN_PLAN) dyn_plan(v, k, bufs, a.error, d, lane);
+            else dyn_copy<KIND>(v, k, bufs, lane);
+        }
+    } else if (op != OP_NOOP) {
         TileOps ops;
         ops.nsrc = uni(D->nsrc);
         ops.ndst = uni(D->ndst);
@@ -783,6 +948,7 @@ hccl_executor(LaunchArgs a) {
     h.off_operand = uni64(((const ProgramHeader*)prog)->off_operand);
     h.off_dep = uni64(((const ProgramHeader*)prog)->off_dep);
     h.off_tile_desc = uni64(((const ProgramHeader*)prog)->off_tile_desc);
+    h.off_aux = uni64(((const ProgramHeader*)prog)->off_aux);
     // the buffer table is indexed per lane, so it is read from the kernel-argument segment
     const uint64_t* bufs = (const uint64_t*)((const char*)__builtin_amdgcn_kernarg_segment_ptr() +
                                              offsetof(LaunchArgs, bufs));
@@ -892,6 +1058,9 @@ hipError_t launch_executor(const LaunchArgs& a, uint32_t blocks, int kind, hipSt
         case kKindCopyAligned:
             hipLaunchKernelGGL(hccl_executor<kKindCopyAligned>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
             break;
+        case kKindDynamic:
+            hipLaunchKernelGGL(hccl_executor<kKindDynamic>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
+            break;
         default:
             hipLaunchKernelGGL(hccl_executor<kKindGeneric>, dim3(blocks), dim3(kBlockThreads), 0, stream, a);
             break;
@@ -916,6 +1085,7 @@ hipError_t executor_occupancy(int kind, int* blocks_per_cu) {
         case SIG_INT32: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<SIG_INT32>, kBlockThreads, 0);
         case kKindCopyOnly: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindCopyOnly>, kBlockThreads, 0);
         case kKindCopyAligned: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindCopyAligned>, kBlockThreads, 0);
+        case kKindDynamic: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindDynamic>, kBlockThreads, 0);
         default: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_executor<kKindGeneric>, kBlockThreads, 0);
     }
 }

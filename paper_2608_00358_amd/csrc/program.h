@@ -7,7 +7,7 @@
 // the addresses arrive in the kernel arguments of each launch.
 //
 // Buffer ids: 0..P-1 = send buffers, P..2P-1 = receive buffers, 2P = the communicator's
-// FP32 scratch.
+// FP32 scratch, then the device metadata arrays of dynamic collectives (2P+1, ...).
 //
 // Each descriptor is cut into tiles of `tile_elems` elements; tiles are numbered globally
 // in descriptor order and handed out to wavefronts by ticket. A tile only waits for tiles
@@ -22,7 +22,10 @@ constexpr uint32_t kProgramMagic = 0x4C434348u;  // "HCCL"
 constexpr uint32_t kProgramVersion = 1;
 constexpr int kMaxOperands = 64;   // sources or destinations of one descriptor (one per lane)
 constexpr int kMaxRanks = 64;
-constexpr int kMaxBuffers = 2 * kMaxRanks + 1;
+constexpr int kMaxMetaBuffers = 8;      // metadata arrays of the dynamic calls of one program
+constexpr int kMetaPerDynamicCall = 4;  // counts, send offsets, receive offsets, received counts
+constexpr int kMaxBuffers = 2 * kMaxRanks + 1 + kMaxMetaBuffers;
+constexpr uint32_t kNoBuffer = 0xFFFFFFFFu;
 constexpr int kVecElems = 8;       // elements per lane per vector step
 constexpr int kWaveSize = 64;
 
@@ -30,6 +33,10 @@ enum Op : uint8_t {
     OP_COPY = 0,    // byte copy of src[0] to every destination (NMC "A = B")
     OP_REDUCE = 1,  // fold of all sources in list order, rounded once, to every destination
     OP_NOOP = 2,    // carries only dependencies (a join)
+    // AllToAllvDynamic (device-resident layout). Both steps name an auxiliary record.
+    OP_DYN_PLAN = 3,  // tile i reads row i and column i of the count matrix from device memory,
+                      // checks them, and writes the per-pair offsets and tile prefix sums
+    OP_DYN_COPY = 4,  // tile k moves its share of the rows the plan describes
 };
 
 enum DType : uint8_t { DT_BF16 = 0, DT_FP16 = 1, DT_FP32 = 2, DT_INT32 = 3 };
@@ -84,11 +91,12 @@ enum Signature : uint8_t {
 };
 
 // Executor kernel specialisations ("kinds"): a plain signature id for programs whose
-// reductions all have that signature and SUM, or one of these two.
+// reductions all have that signature and SUM, or one of these.
 constexpr int kKindCopyOnly = SIG_COUNT;         // no reductions at all
 constexpr int kKindGeneric = SIG_COUNT + 1;      // anything else
 constexpr int kKindCopyAligned = SIG_COUNT + 2;  // copies only, every operand 16-byte aligned
-constexpr int kNumKinds = SIG_COUNT + 3;
+constexpr int kKindDynamic = SIG_COUNT + 3;      // copies and AllToAllvDynamic steps
+constexpr int kNumKinds = SIG_COUNT + 4;
 
 inline uint8_t reduce_signature(uint32_t t0, uint32_t tr, uint32_t to) {
     if (t0 == tr && tr == to) return (uint8_t)t0;  // DT_* and SIG_* plain ids coincide
@@ -121,9 +129,43 @@ struct Desc {           // 64 bytes
     uint64_t nelem;
     uint32_t fold;      // FOLD_LIST (grouped / flat, per `group`) or FOLD_PAIRWISE
     uint32_t requant;   // 1 = round every partial to the destination type
-    uint32_t pad1[2];
+    uint32_t aux;       // OP_DYN_*: index of the DynA2A record
+    uint32_t pad1;
 };
 static_assert(sizeof(Desc) == 64, "descriptor layout");
+
+// Auxiliary record of an AllToAllvDynamic (Section IV-B-2): what the plan reads and where the
+// plan table lives. Counts and offsets are int64 rows of `row_elems` elements.
+struct DynA2A {            // 80 bytes
+    uint32_t P;
+    uint32_t elem_bytes;
+    uint32_t send0;        // buffer id of send buffer 0 (send buffer s is send0 + s)
+    uint32_t recv0;        // buffer id of receive buffer 0
+    uint32_t counts;       // buffer id of the count matrix, [s*P + d]
+    uint32_t sdispls;      // buffer id of explicit send offsets [s*P + d], or kNoBuffer (packed)
+    uint32_t rdispls;      // buffer id of explicit receive offsets [d*P + s], or kNoBuffer (packed)
+    uint32_t recvcounts;   // buffer id of the received-count output [d*P + s], or kNoBuffer
+    uint32_t table;        // buffer id holding the plan table (the scratch)
+    uint32_t slots;        // tiles of the copy step; slot k moves dynamic tiles [k*J/slots, (k+1)*J/slots)
+    uint64_t table_off;    // byte offset of the plan table in that buffer
+    uint64_t row_elems;
+    uint64_t send_cap;     // rows per send buffer
+    uint64_t recv_cap;     // rows per receive buffer
+    uint64_t tile_elems;   // elements per dynamic tile
+};
+static_assert(sizeof(DynA2A) == 80, "auxiliary record layout");
+
+// Plan table of one AllToAllvDynamic (byte offsets from its start; pair index s*P + d):
+//   [0, 256)     u32 row_tiles[64]  dynamic tiles of source row s
+//   [256, 512)   u32 bad[64]        plan tile i found an invalid range (rewritten every launch)
+//   kPlanPre     u32 pre[P*P]       inclusive prefix of the pair tile counts within row s
+//   then         u64 elems[P*P], soff[P*P], roff[P*P]: pair element count, element offset
+//                in send buffer s, element offset in receive buffer d
+constexpr uint64_t kPlanPre = 512;
+constexpr uint64_t plan_elems_off(uint32_t P) { return kPlanPre + (((uint64_t)P * P * 4 + 7) & ~7ull); }
+constexpr uint64_t plan_soff_off(uint32_t P) { return plan_elems_off(P) + (uint64_t)P * P * 8; }
+constexpr uint64_t plan_roff_off(uint32_t P) { return plan_soff_off(P) + (uint64_t)P * P * 8; }
+constexpr uint64_t plan_bytes(uint32_t P) { return plan_roff_off(P) + (uint64_t)P * P * 8; }
 static_assert(sizeof(Operand) == 16, "operand layout");
 static_assert(sizeof(Dep) == 16, "dependency layout");
 
@@ -143,6 +185,9 @@ struct ProgramHeader {
     uint64_t off_tile_desc;  // u32 per tile: the descriptor that owns it
     uint64_t total_bytes;
     uint64_t scratch_bytes;
+    uint64_t off_aux;      // DynA2A records
+    uint32_t naux;
+    uint32_t pad;
 };
 
 // Device state words: [0] ticket counter, [1] finished-wavefront counter, then one tile
@@ -153,7 +198,7 @@ constexpr uint32_t kStateDescBase = 2;
 
 // Device-side error record (per communicator).
 struct ErrorRecord {
-    uint32_t code;   // 0 = none, 1 = dependency wait timed out
+    uint32_t code;   // 0 = none, 1 = dependency wait timed out, 2 = a dynamic layout was invalid
     uint32_t desc;
     uint32_t tile;
     uint32_t pad;

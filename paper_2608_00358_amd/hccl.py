@@ -27,7 +27,7 @@ EXPORTS = [
     "hccl_config_init", "hccl_comm_create", "hccl_comm_destroy", "hccl_comm_set_config",
     "hccl_allreduce", "hccl_reduce_scatter", "hccl_allgather", "hccl_alltoallv",
     "hccl_get_last_error", "hccl_result_string", "hccl_get_async_error", "hccl_comm_last_program",
-    "hccl_group_start", "hccl_group_end",
+    "hccl_group_start", "hccl_group_end", "hccl_alltoallv_dynamic",
 ]
 
 
@@ -81,6 +81,7 @@ def load(path: str = LIB_PATH):
     lib.hccl_reduce_scatter.argtypes = [vp, vpp, vpp, sz, i32, i32, vp]
     lib.hccl_allgather.argtypes = [vp, vpp, vpp, sz, i32, vp]
     lib.hccl_alltoallv.argtypes = [vp, vpp, szp, szp, vpp, szp, szp, i32, vp]
+    lib.hccl_alltoallv_dynamic.argtypes = [vp, vpp, vp, vp, vpp, vp, vp, sz, sz, sz, i32, vp]
     lib.hccl_get_last_error.argtypes = []
     lib.hccl_get_last_error.restype = ctypes.c_char_p
     lib.hccl_result_string.argtypes = [i32]
@@ -105,6 +106,10 @@ def _addr(x) -> int:
     if isinstance(x, int):
         return x
     return int(x.data_ptr())
+
+
+def _addr_or_null(x) -> Optional[int]:
+    return None if x is None else _addr(x)
 
 
 def _ptr_array(bufs: Sequence) -> ctypes.Array:
@@ -189,6 +194,16 @@ def hccl_alltoallv(comm, sendbufs, sendcounts, sdispls, recvbufs, recvcounts, rd
                                  _dtype_code(dtype), _stream_handle(stream)))
 
 
+def hccl_alltoallv_dynamic(comm, sendbufs, sendcounts, sdispls, recvbufs, recvcounts, rdispls, row_elems: int,
+                           send_capacity: int, recv_capacity: int, dtype, stream=None) -> None:
+    """Counts and offsets are device int64 arrays (tensors or addresses); sdispls, rdispls and
+    recvcounts may be None."""
+    _check(load().hccl_alltoallv_dynamic(comm, _ptr_array(sendbufs), _addr_or_null(sendcounts), _addr_or_null(sdispls),
+                                         _ptr_array(recvbufs), _addr_or_null(recvcounts), _addr_or_null(rdispls),
+                                         row_elems, send_capacity, recv_capacity, _dtype_code(dtype),
+                                         _stream_handle(stream)))
+
+
 def hccl_group_start(comm) -> None:
     _check(load().hccl_group_start(comm))
 
@@ -266,6 +281,21 @@ class Comm:
     def alltoallv(self, send, sendcounts, sdispls, recv, recvcounts, rdispls, stream=None):
         hccl_alltoallv(self.handle, send, sendcounts, sdispls, recv, recvcounts, rdispls, send[0].dtype, stream)
 
+    @staticmethod
+    def _capacity(bufs, row_elems):
+        n = bufs[0].numel()
+        if any(b.numel() != n for b in bufs) or n % row_elems:
+            raise ValueError("buffers must share one size, a whole number of rows")
+        return n // row_elems
+
+    def alltoallv_dynamic(self, send, counts, recv, row_elems, sdispls=None, rdispls=None, recvcounts=None,
+                          stream=None):
+        """AllToAllvDynamic: ``counts`` (and the optional offsets / received-count output) are
+        int64 device tensors of P*P rows; capacities are the buffers' sizes in rows."""
+        hccl_alltoallv_dynamic(self.handle, send, counts, sdispls, recv, recvcounts, rdispls, row_elems,
+                               self._capacity(send, row_elems), self._capacity(recv, row_elems), send[0].dtype,
+                               stream)
+
     # The bind_* methods marshal the arguments once and return a no-argument callable that
     # enqueues the collective: for loops that reuse the same buffers, where per-call ctypes
     # marshalling would otherwise cost more than a small collective itself.
@@ -284,6 +314,13 @@ class Comm:
     def bind_alltoallv(self, send, sendcounts, sdispls, recv, recvcounts, rdispls, stream=None):
         return _bound(load().hccl_alltoallv, self.handle, _ptr_array(send), _size_array(sendcounts),
                       _size_array(sdispls), _ptr_array(recv), _size_array(recvcounts), _size_array(rdispls),
+                      _dtype_code(send[0].dtype), _stream_handle(stream))
+
+    def bind_alltoallv_dynamic(self, send, counts, recv, row_elems, sdispls=None, rdispls=None, recvcounts=None,
+                               stream=None):
+        return _bound(load().hccl_alltoallv_dynamic, self.handle, _ptr_array(send), _addr(counts),
+                      _addr_or_null(sdispls), _ptr_array(recv), _addr_or_null(recvcounts), _addr_or_null(rdispls),
+                      row_elems, self._capacity(send, row_elems), self._capacity(recv, row_elems),
                       _dtype_code(send[0].dtype), _stream_handle(stream))
 
     def group(self):

@@ -328,3 +328,91 @@ def test_incompatible_orders_and_schedules_are_rejected():
         _expect(2, H.hccl_allreduce, c.handle, s[:4], r[:4], 100, "fp32")
     with comm(4, order=7) as c:
         _expect(1, H.hccl_allreduce, c.handle, s[:4], r[:4], 100, "fp32")
+
+
+# ------------------------------------------------------------------ AllToAllvDynamic
+def plan_bytes(P):
+    # the plan table: row totals, error marks, per-pair tile prefix, three u64 arrays per pair
+    return 512 + ((P * P * 4 + 7) & ~7) + 3 * P * P * 8
+
+
+def dyn_slots(P, send_cap, R, es, tile_bytes=8192):
+    te = max(512, (tile_bytes // es) // 512 * 512)
+    bound = P * (ceil_div(send_cap * R, te) + P)
+    return max(1, min(2048, bound))
+
+
+META = 1 << 47   # fake device metadata arrays, far from the data buffers
+
+
+@pytest.mark.parametrize("P", [1, 2, 8, 64])
+@pytest.mark.parametrize("dt", ["bf16", "int32"])
+def test_dynamic_alltoallv_is_a_plan_and_a_copy(P, dt):
+    R, send_cap, recv_cap = 128, 5000, 7000
+    with comm(P) as c:
+        H.hccl_alltoallv_dynamic(c.handle, fake_bufs(P, 1 << 40), META, None, fake_bufs(P, 1 << 44), None, None,
+                                 R, send_cap, recv_cap, dt)
+        info = info_of(c)
+        assert info["collective"] == 4 and info["num_descs"] == 2 and info["num_deps"] == 1
+        assert info["num_tiles"] == P + dyn_slots(P, send_cap, R, ES[dt])
+        assert info["scratch_bytes"] == plan_bytes(P) and info["num_operands"] == 0
+        # the program does not depend on the counts: other metadata arrays reuse it
+        H.hccl_alltoallv_dynamic(c.handle, fake_bufs(P, 1 << 40), META + (1 << 20), META + (2 << 20),
+                                 fake_bufs(P, 1 << 44), META + (3 << 20), None, R, send_cap, recv_cap, dt)
+        assert info_of(c)["cache_hit"] == 0    # explicit send offsets and a count output: another program
+        H.hccl_alltoallv_dynamic(c.handle, fake_bufs(P, 1 << 41), META + (5 << 20), META + (6 << 20),
+                                 fake_bufs(P, 1 << 45), META + (7 << 20), None, R, send_cap, recv_cap, dt)
+        assert info_of(c)["cache_hit"] == 1
+
+
+def test_dynamic_alltoallv_small_capacities_get_few_slots():
+    with comm(2) as c:
+        H.hccl_alltoallv_dynamic(c.handle, fake_bufs(2, 1 << 40), META, None, fake_bufs(2, 1 << 44), None, None,
+                                 1, 3, 6, "fp32")
+        assert info_of(c)["num_tiles"] == 2 + 2 * (1 + 2)
+        H.hccl_alltoallv_dynamic(c.handle, fake_bufs(2, 1 << 40), META, None, fake_bufs(2, 1 << 44), None, None,
+                                 1, 0, 0, "fp32")
+        assert info_of(c)["num_tiles"] == 2 + 2 * 2
+
+
+def test_dynamic_alltoallv_argument_errors():
+    P = 4
+    s, r = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+    with comm(P) as c:
+        f = H.hccl_alltoallv_dynamic
+        _expect(1, f, c.handle, s, None, None, r, None, None, 8, 10, 10, "bf16")          # no counts
+        _expect(1, f, c.handle, s, META, None, r, None, None, 0, 10, 10, "bf16")          # row_elems 0
+        _expect(1, f, c.handle, s, META + 4, None, r, None, None, 8, 10, 10, "bf16")      # misaligned
+        _expect(1, f, c.handle, s, META, None, r, None, None, 8, 1 << 60, 10, "bf16")     # capacity
+        _expect(1, f, c.handle, s, META, None, r, r[1], None, 8, 10, 10, "bf16")          # output on a receive
+        _expect(1, f, c.handle, s, META, None, r, META + 64, None, 8, 10, 10, "bf16")     # output on the counts
+        _expect(1, f, c.handle, s, META, None, r, None, r[2] + 8, 8, 10, 10, "bf16")      # offsets on a receive
+        f(c.handle, s, s[0], s[1], r, None, None, 8, 10, 10, "bf16")                        # read-only aliases
+        _expect(2, f, c.handle, s, META, None, r, None, None, 1 << 20, 1 << 21, 10, "bf16")  # too many tiles
+
+
+def test_dynamic_alltoallv_groups():
+    P = 8
+    with comm(P) as c:
+        # embedding rows and their ids exchanged with one count matrix: two dynamic calls
+        with c.group():
+            H.hccl_alltoallv_dynamic(c.handle, fake_bufs(P, 1 << 40), META, None, fake_bufs(P, 1 << 44), None,
+                                     None, 128, 4096, 4096, "bf16")
+            H.hccl_alltoallv_dynamic(c.handle, fake_bufs(P, 1 << 41), META, None, fake_bufs(P, 1 << 45),
+                                     META + (1 << 20), None, 1, 4096, 4096, "int32")
+            H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 42), fake_bufs(P, 1 << 43), 1000, "fp32")
+        g = info_of(c)
+        assert g["collective"] == -1 and g["num_deps"] == 2
+        assert g["scratch_bytes"] >= 2 * plan_bytes(P)
+        H.hccl_group_start(c.handle)
+        for k in range(3):
+            H.hccl_alltoallv_dynamic(c.handle, fake_bufs(P, (1 << 40) + k * (1 << 37)), META, None,
+                                     fake_bufs(P, (1 << 44) + k * (1 << 37)), None, None, 1, 64, 64, "fp32")
+        _expect(2, H.hccl_group_end, c.handle)
+        # two calls writing the same count output conflict
+        H.hccl_group_start(c.handle)
+        for k in range(2):
+            H.hccl_alltoallv_dynamic(c.handle, fake_bufs(P, (1 << 40) + k * (1 << 37)), META, None,
+                                     fake_bufs(P, (1 << 44) + k * (1 << 37)), META + (1 << 20), None, 1, 64, 64,
+                                     "fp32")
+        _expect(1, H.hccl_group_end, c.handle)

@@ -1,0 +1,259 @@
+"""GPU parity for AllToAllvDynamic (device-resident layout, paper Section IV-B-2).
+
+The count matrix (and optionally the offsets) live in device memory; the library compiles a
+program for the capacities only, and the plan is built on the device when it runs. Every
+case compares whole receive buffers (written ranges and untouched ones) and the received
+count output with the oracle, and checks the guard zones around every buffer.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_00358_amd as H
+from gpu_helpers import GUARD, NP_BITS, Guarded, to_device, to_host
+from test_gpu_parity import inputs
+from workloads import device_normal_bf16, row_ids_int32, zipf_counts
+
+pytestmark = pytest.mark.gpu
+
+
+def dev_i64(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int64).reshape(-1).copy()).to("cuda:0")
+
+
+def run_dynamic(P, R, dt, counts, send_cap, recv_cap, sd=None, rd=None, seed=0, want_counts=True, **cfg):
+    """One dynamic exchange through the C-ABI; returns (accepted by the oracle, info)."""
+    print(f"alltoallv_dynamic P={P} R={R} dt={dt} caps={send_cap}/{recv_cap} explicit={sd is not None}/"
+          f"{rd is not None} seed={seed}", flush=True)
+    x = inputs(P, send_cap * R, dt, seed) if send_cap else np.zeros((P, 0), NP_BITS[dt])
+    send = [Guarded(send_cap * R, dt, fill=x[s]) for s in range(P)]
+    recv = [Guarded(recv_cap * R, dt) for _ in range(P)]
+    d_counts = dev_i64(counts)
+    d_sd = dev_i64(sd) if sd is not None else None
+    d_rd = dev_i64(rd) if rd is not None else None
+    d_rc = torch.full((P * P,), -7, dtype=torch.int64, device="cuda:0") if want_counts else None
+    with H.Comm(P, device=0, **cfg) as c:
+        H.hccl_alltoallv_dynamic(c.handle, [b.view for b in send], d_counts, d_sd, [b.view for b in recv], d_rc,
+                                 d_rd, R, send_cap, recv_cap, dt)
+        torch.cuda.synchronize()
+        err = c.async_error()
+        info = c.last_program()
+    want = [r.host_init[GUARD:GUARD + recv_cap * R].copy() for r in recv]
+    ok, want_rc = oracle.alltoallv_dynamic([np.ascontiguousarray(x[s]) for s in range(P)], np.asarray(counts),
+                                           want, R, send_cap, recv_cap, sdispls=sd, rdispls=rd)
+    assert err == (0 if ok else 1), f"async error {err}, oracle accepted={ok}"
+    for d in range(P):
+        got = recv[d].result()
+        assert np.array_equal(got.view(np.uint8), want[d].view(np.uint8)), f"destination {d}"
+        assert recv[d].guards_intact() and send[d].guards_intact()
+        assert np.array_equal(send[d].result().view(np.uint8), x[d].view(np.uint8)), "a send buffer changed"
+    if want_counts:
+        assert np.array_equal(d_rc.cpu().numpy().reshape(P, P), want_rc)
+    return ok, info
+
+
+def random_counts(P, rows, seed, zero_frac=0.2):
+    rng = np.random.default_rng(seed)
+    c = rng.integers(0, rows + 1, size=(P, P))
+    c[rng.random((P, P)) < zero_frac] = 0
+    return c
+
+
+@pytest.mark.parametrize("dt", ["bf16", "fp32", "int32", "fp16"])
+@pytest.mark.parametrize("P", [1, 2, 3, 8])
+@pytest.mark.parametrize("R", [1, 3, 128])
+def test_packed_layout(dt, P, R):
+    counts = random_counts(P, 40, seed=P * 100 + R)
+    send_cap = int(counts.sum(axis=1).max()) + 5
+    recv_cap = int(counts.sum(axis=0).max()) + 3
+    ok, info = run_dynamic(P, R, dt, counts, send_cap, recv_cap, seed=P + R)
+    assert ok and info["collective"] == 4 and info["num_descs"] == 2
+
+
+@pytest.mark.parametrize("dt", ["bf16", "int32"])
+@pytest.mark.parametrize("P", [2, 5, 8])
+def test_explicit_offsets_with_gaps(dt, P):
+    rng = np.random.default_rng(P)
+    R = 7
+    counts = random_counts(P, 30, seed=P + 1)
+    send_cap = 64
+    sd = np.array([[rng.integers(0, send_cap - counts[s, d] + 1) for d in range(P)] for s in range(P)])
+    rd = np.zeros((P, P), np.int64)
+    recv_cap = 0
+    for d in range(P):
+        at = int(rng.integers(0, 3))
+        for s in rng.permutation(P):
+            rd[d, s] = at
+            at += counts[s, d] + int(rng.integers(0, 3))
+        recv_cap = max(recv_cap, at)
+    ok, _ = run_dynamic(P, R, dt, counts, send_cap, recv_cap, sd=sd, rd=rd, seed=P)
+    assert ok
+    # only one side explicit
+    ok, _ = run_dynamic(P, R, dt, counts, send_cap, int(counts.sum(axis=0).max()), sd=sd, seed=P + 1)
+    assert ok
+    ok, _ = run_dynamic(P, R, dt, counts, int(counts.sum(axis=1).max()), recv_cap, rd=rd, seed=P + 2)
+    assert ok
+
+
+def test_many_ranks_and_tiny_tiles():
+    P = 64
+    counts = random_counts(P, 9, seed=64, zero_frac=0.5)
+    ok, info = run_dynamic(P, 5, "bf16", counts, int(counts.sum(axis=1).max()), int(counts.sum(axis=0).max()),
+                           seed=3, tile_bytes=1024)
+    assert ok
+
+
+@pytest.mark.parametrize("case", ["send_over", "recv_over", "negative", "overlap", "offset_out"])
+def test_rejected_layouts_move_nothing(case):
+    P, R = 4, 16
+    counts = random_counts(P, 10, seed=7, zero_frac=0.0) + 1
+    send_cap = int(counts.sum(axis=1).max())
+    recv_cap = int(counts.sum(axis=0).max())
+    sd = rd = None
+    if case == "send_over":
+        send_cap -= 1
+    elif case == "recv_over":
+        recv_cap -= 1
+    elif case == "negative":
+        counts[2, 1] = -1
+    elif case == "overlap":
+        rd = np.zeros((P, P), np.int64)
+        for d in range(P):
+            rd[d] = np.concatenate([[0], np.cumsum(counts[:, d])[:-1]])
+        rd[3, 2] -= 1                       # source 2's rows at rank 3 start one row early
+    elif case == "offset_out":
+        sd = np.zeros((P, P), np.int64)
+        for s in range(P):
+            sd[s] = np.concatenate([[0], np.cumsum(counts[s])[:-1]])
+        sd[1, 3] = send_cap - counts[1, 3] + 1
+    ok, _ = run_dynamic(P, R, "fp32", counts, send_cap, recv_cap, sd=sd, rd=rd, seed=9)
+    assert not ok
+
+
+def test_empty_and_zero_capacity_exchanges():
+    for P in (1, 3):
+        run_dynamic(P, 4, "bf16", np.zeros((P, P), np.int64), 5, 5)
+        run_dynamic(P, 4, "bf16", np.zeros((P, P), np.int64), 0, 0)
+
+
+def test_counts_change_between_launches_without_recompiling():
+    """The same program (one compile) serves every layout that fits the capacities, and the
+    counts array may be rewritten on the device between launches."""
+    P, R, S = 8, 32, 100
+    cap = P * S
+    x = inputs(P, S * R, "bf16", 11)
+    send = [to_device(x[s], "bf16") for s in range(P)]
+    recv = [torch.empty(cap * R, dtype=torch.bfloat16, device="cuda:0") for _ in range(P)]
+    d_counts = torch.zeros(P * P, dtype=torch.int64, device="cuda:0")
+    d_rc = torch.zeros(P * P, dtype=torch.int64, device="cuda:0")
+    with H.Comm(P, device=0) as c:
+        run = c.bind_alltoallv_dynamic(send, d_counts, recv, R, recvcounts=d_rc)
+        for it in range(6):
+            counts = zipf_counts(P, S - 3 * it, 1.1, seed=it)
+            for t in recv:
+                t.fill_(0)
+            d_counts.copy_(dev_i64(counts))
+            run()
+            torch.cuda.synchronize()
+            assert c.async_error() == 0
+            assert c.last_program()["cache_hit"] == (1 if it else 0)
+            want = [np.zeros(cap * R, np.uint16) for _ in range(P)]
+            ok, rc = oracle.alltoallv_dynamic([x[s] for s in range(P)], counts, want, R, S, cap)
+            assert ok
+            for d in range(P):
+                assert np.array_equal(to_host(recv[d], "bf16"), want[d]), f"iteration {it} destination {d}"
+            assert np.array_equal(d_rc.cpu().numpy().reshape(P, P), rc)
+
+
+def test_routing_kernel_then_dynamic_exchange_on_one_stream():
+    """MoE dispatch: a routing step on the GPU picks a destination for every token, counts the
+    tokens per destination and sorts them; the dynamic exchange follows on the same stream with
+    no host step between (rows and their ids in one group, sharing the count matrix)."""
+    P, T, D = 8, 4096, 64
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(5)
+    tokens = device_normal_bf16(P, T * D, seed=5)
+    ids = [to_device(row_ids_int32(P, T, seed=6)[s], "int32") for s in range(P)]
+    # routing: skewed destinations (squared uniform), counts by bincount, rows sorted by destination
+    dest = [(torch.rand(T, generator=g, device="cuda:0") ** 2 * P).long().clamp_(max=P - 1) for _ in range(P)]
+    d_counts = torch.stack([torch.bincount(dest[s], minlength=P) for s in range(P)]).reshape(-1).contiguous()
+    order = [torch.argsort(dest[s], stable=True) for s in range(P)]
+    send_rows = [tokens[s].view(T, D)[order[s]].reshape(-1).contiguous() for s in range(P)]
+    send_ids = [ids[s][order[s]].contiguous() for s in range(P)]
+    cap = P * T
+    recv_rows = [torch.zeros(cap * D, dtype=torch.bfloat16, device="cuda:0") for _ in range(P)]
+    recv_ids = [torch.full((cap,), -1, dtype=torch.int32, device="cuda:0") for _ in range(P)]
+    d_rc = torch.zeros(P * P, dtype=torch.int64, device="cuda:0")
+    with H.Comm(P, device=0) as c:
+        with c.group():
+            H.hccl_alltoallv_dynamic(c.handle, send_rows, d_counts, None, recv_rows, d_rc, None, D, T, cap, "bf16")
+            H.hccl_alltoallv_dynamic(c.handle, send_ids, d_counts, None, recv_ids, None, None, 1, T, cap, "int32")
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+        assert c.last_program()["collective"] == -1
+    counts = d_counts.cpu().numpy().reshape(P, P)
+    host_rows = [to_host(t, "bf16") for t in send_rows]
+    host_ids = [to_host(t, "int32") for t in send_ids]
+    want_rows = [np.zeros(cap * D, np.uint16) for _ in range(P)]
+    want_ids = [np.full(cap, -1, np.int32) for _ in range(P)]
+    assert oracle.alltoallv_dynamic(host_rows, counts, want_rows, D, T, cap)[0]
+    ok, rc = oracle.alltoallv_dynamic(host_ids, counts, want_ids, 1, T, cap)
+    assert ok
+    for d in range(P):
+        assert np.array_equal(to_host(recv_rows[d], "bf16"), want_rows[d]), f"rows at {d}"
+        assert np.array_equal(to_host(recv_ids[d], "int32"), want_ids[d]), f"ids at {d}"
+    assert np.array_equal(d_rc.cpu().numpy().reshape(P, P), rc)
+
+
+def test_full_size_zipf_embedding_rows_and_ids():
+    """The benchmark workload in its dynamic form: P=8, 2^18 rows of 128 bf16 per rank with a
+    Zipf(1.1) destination split, rows and int32 ids in one group, counts in device memory."""
+    P, R, D = 8, 1 << 18, 128
+    print("full config: alltoallv_dynamic P=8 2^18 rows x 128 bf16 Zipf(1.1) + int32 ids", flush=True)
+    counts = zipf_counts(P, R, 1.1, seed=0)
+    cap = int(counts.sum(axis=0).max())
+    send_rows = device_normal_bf16(P, R * D, seed=0)
+    id_vals = row_ids_int32(P, R, seed=1)
+    send_ids = [to_device(id_vals[s], "int32") for s in range(P)]
+    recv_rows = [torch.empty(cap * D, dtype=torch.bfloat16, device="cuda:0") for _ in range(P)]
+    recv_ids = [torch.empty(cap, dtype=torch.int32, device="cuda:0") for _ in range(P)]
+    for t in recv_rows + recv_ids:
+        t.fill_(0)
+    d_counts = dev_i64(counts)
+    with H.Comm(P, device=0) as c:
+        with c.group():
+            c.alltoallv_dynamic(send_rows, d_counts, recv_rows, D)
+            c.alltoallv_dynamic(send_ids, d_counts, recv_ids, 1)
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+    host_rows = [to_host(t, "bf16") for t in send_rows]
+    want_rows = [np.zeros(cap * D, np.uint16) for _ in range(P)]
+    assert oracle.alltoallv_dynamic(host_rows, counts, want_rows, D, R, cap)[0]
+    want_ids = [np.zeros(cap, np.int32) for _ in range(P)]
+    assert oracle.alltoallv_dynamic([id_vals[s] for s in range(P)], counts, want_ids, 1, R, cap)[0]
+    for d in range(P):
+        assert np.array_equal(to_host(recv_rows[d], "bf16"), want_rows[d]), f"rows at destination {d}"
+        assert np.array_equal(to_host(recv_ids[d], "int32"), want_ids[d]), f"ids at destination {d}"
+
+
+def test_error_is_reported_once_then_the_communicator_works_again():
+    P, R = 2, 8
+    x = inputs(P, 10 * R, "fp32", 1)
+    send = [to_device(x[s], "fp32") for s in range(P)]
+    recv = [torch.zeros(10 * R, dtype=torch.float32, device="cuda:0") for _ in range(P)]
+    with H.Comm(P, device=0) as c:
+        c.alltoallv_dynamic(send, dev_i64([[11, 0], [0, 0]]), recv, R)     # 11 rows > 10 of capacity
+        torch.cuda.synchronize()
+        assert c.async_error() == 1
+        assert "layout" in H.hccl_get_last_error()
+        assert c.async_error() == 0
+        assert all(float(t.abs().sum()) == 0.0 for t in recv)
+        counts = np.array([[3, 4], [2, 5]])
+        c.alltoallv_dynamic(send, dev_i64(counts), recv, R)
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+    want = [np.zeros(10 * R, np.float32) for _ in range(P)]
+    assert oracle.alltoallv_dynamic([x[s] for s in range(P)], counts, want, R, 10, 10)[0]
+    for d in range(P):
+        assert np.array_equal(to_host(recv[d], "fp32"), want[d])
