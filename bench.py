@@ -371,6 +371,113 @@ def bench_overlap_c5a(device, rs_send, rs_recv, n_rs=100, rs_cus=16):
             "n_rs": n_rs, "n_gemm": n_gemm, "overlap": results}
 
 
+# ------------------------------------------------------------------ AllToAllvDynamic
+def bench_dynamic_alltoallv(device, w, iters=20):
+    """The headline exchange with its count matrix in device memory (hccl_alltoallv_dynamic,
+    rows and ids grouped, one launch): time per launch against the host-layout AllToAllv, and
+    the fixed cost of the on-device plan (an exchange whose counts are all zero)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_00358_amd as H
+
+    P, R, D = w["P"], w["R"], w["D"]
+    counts = w["counts"]
+    cap = int(counts.sum(axis=0).max())
+    send_rows = w["send_rows"]
+    send_ids = [torch.from_numpy(w["id_vals"][s].copy()).to(device) for s in range(P)]
+    recv_rows = [torch.empty(cap * D, dtype=torch.bfloat16, device=device) for _ in range(P)]
+    recv_ids = [torch.empty(cap, dtype=torch.int32, device=device) for _ in range(P)]
+    d_counts = torch.from_numpy(counts.reshape(-1).astype(np.int64)).to(device)
+    d_zero = torch.zeros_like(d_counts)
+    algo = 2 * int(counts.sum()) * (D * 2 + 4)
+    out = {"workload": "alltoallv_dynamic P=8, 2^18 rows/rank of 128 bf16 + int32 ids, Zipf(1.1), counts in "
+                       "device memory, rows and ids grouped (one launch)", "algo_bytes": algo}
+    with H.Comm(P, device=0) as c:
+        def step(dc):
+            H.hccl_group_start(c.handle)
+            calls[dc][0]()
+            calls[dc][1]()
+            H.hccl_group_end(c.handle)
+
+        calls = {}
+        for key, dc in (("full", d_counts), ("zero", d_zero)):
+            calls[key] = (c.bind_alltoallv_dynamic(send_rows, dc, recv_rows, D),
+                          c.bind_alltoallv_dynamic(send_ids, dc, recv_ids, 1))
+        for _ in range(3):
+            step("full")
+        ms = _time_events(lambda: step("full"), iters)
+        info = c.last_program()
+        ms_zero = _time_events(lambda: step("zero"), iters)
+        if c.async_error() != 0:
+            raise RuntimeError(H.hccl_get_last_error())
+    out.update({"us": ms * 1e3, "gbs": algo / (ms * 1e-3) / 1e9, "frac": algo / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "plan_only_us": ms_zero * 1e3, "tiles": info["num_tiles"], "workers": info["workers"]})
+    return out
+
+
+def bench_moe_dispatch(device, iters=60, warmup=10):
+    """Routing on the GPU followed by the dispatch exchange, every iteration a new routing:
+    (a) device-resident: routing, then hccl_alltoallv_dynamic on the same stream, no host step;
+    (b) eager: routing, copy the counts to the host, build the layout, hccl_alltoallv (a new
+    program whenever the counts change). Wall time per iteration, synchronised at its end."""
+    import numpy as np
+    import torch
+
+    import paper_2608_00358_amd as H
+
+    P, T, D = 8, 256, 4096      # 256 tokens of 4096 bf16 per rank: 2 MiB per rank
+    g = torch.Generator(device=device)
+    g.manual_seed(7)
+    tokens = torch.randn(P, T, D, generator=g, device=device).to(torch.bfloat16)
+    send_all = torch.empty(P, T * D, dtype=torch.bfloat16, device=device)
+    send = [send_all[s] for s in range(P)]
+    cap = P * T
+    recv = [torch.empty(cap * D, dtype=torch.bfloat16, device=device) for _ in range(P)]
+    d_counts = torch.empty(P * P, dtype=torch.int64, device=device)
+    rank_base = (torch.arange(P, device=device) * P).view(P, 1)
+
+    def route():
+        # skewed destinations, per-(source, destination) counts, tokens sorted by destination
+        dest = (torch.rand(P, T, generator=g, device=device) ** 2 * P).long().clamp_(max=P - 1)
+        d_counts.copy_(torch.bincount((dest + rank_base).view(-1), minlength=P * P))
+        order = torch.argsort(dest, dim=1, stable=True)
+        torch.take_along_dim(tokens, order.unsqueeze(-1), dim=1, out=send_all.view(P, T, D))
+
+    def timed(fn):
+        samples = []
+        for i in range(warmup + iters):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            if i >= warmup:
+                samples.append((time.perf_counter() - t0) * 1e6)
+        return statistics.median(samples)
+
+    with H.Comm(P, device=0) as c:
+        dyn = c.bind_alltoallv_dynamic(send, d_counts, recv, D)
+
+        def eager():
+            route()
+            counts = d_counts.cpu().numpy().reshape(P, P)
+            sd = np.zeros((P, P), np.int64)
+            rd = np.zeros((P, P), np.int64)
+            sd[:, 1:] = np.cumsum(counts, axis=1)[:, :-1] * D
+            rd[:, 1:] = np.cumsum(counts.T, axis=1)[:, :-1] * D
+            H.hccl_alltoallv(c.handle, send, counts * D, sd, recv, counts.T * D, rd, "bf16")
+
+        t_route = timed(route)
+        t_dyn = timed(lambda: (route(), dyn()))
+        t_eager = timed(eager)
+        if c.async_error() != 0:
+            raise RuntimeError(H.hccl_get_last_error())
+    return {"workload": "MoE dispatch P=8, 256 tokens x 4096 bf16 per rank, skewed routing on the GPU each "
+                        "iteration", "route_only_us": t_route, "device_resident_us": t_dyn, "eager_host_layout_us": t_eager,
+            "exchange_exposed_device_resident_us": t_dyn - t_route,
+            "exchange_exposed_eager_us": t_eager - t_route}
+
+
 # ---------------------------------------------------------------------- CPU baseline
 def cpu_baseline(w, budget_s=12.0):
     """The oracle's AllToAllv on the host cores (single-threaded C), same inputs."""
@@ -433,6 +540,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overlap", action="store_true")
     ap.add_argument("--latency-only", action="store_true", help="only the 64 KiB all-reduce latency test")
+    ap.add_argument("--dynamic-only", action="store_true",
+                    help="only the AllToAllvDynamic measurements (headline exchange, MoE dispatch)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run torch's device copy of 1 GiB (the known-size kernel that scales "
                          "the FETCH_SIZE / WRITE_SIZE counters)")
@@ -463,6 +572,12 @@ def main():
 
     if args.latency_only:
         print(json.dumps(bench_latency_c5b(device)), flush=True)
+        return
+
+    if args.dynamic_only:
+        w = alltoallv_workload(device)
+        print(json.dumps({"alltoallv_dynamic_rows_ids_p8": bench_dynamic_alltoallv(device, w),
+                          "moe_dispatch_p8": bench_moe_dispatch(device)}), flush=True)
         return
 
     head, w = run_headline(args, device)
@@ -515,6 +630,10 @@ def main():
         extras["allreduce_two_level_p64_bf16"] = bench_two_level_c4(device)
         _log("c5b latency")
         extras["latency_allreduce_p8_64KiB_fp32"] = bench_latency_c5b(device)
+        _log("alltoallv_dynamic")
+        extras["alltoallv_dynamic_rows_ids_p8"] = bench_dynamic_alltoallv(device, w)
+        _log("moe dispatch: device-resident vs eager")
+        extras["moe_dispatch_p8"] = bench_moe_dispatch(device)
         line["collectives"] = extras
     if not args.no_cpu_baseline:
         _log("cpu baseline")

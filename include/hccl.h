@@ -158,8 +158,8 @@ hcclResult_t hccl_alltoallv(hcclComm_t comm,
  * AllToAllvDynamic (Section IV-B-2, device-resident collectives): an AllToAllv whose row
  * counts, and optionally row offsets, are read from device memory when the collective runs,
  * so that a routing kernel earlier on `stream` can write them and nothing on the host waits
- * for it. The program depends only on the capacities and is compiled once; a step of P
- * tiles reads the layout and checks it on the device, then the rows move.
+ * for it. The program depends only on the capacities and is compiled once; on the device,
+ * every slot of it reads the layout, checks it, and moves its share of the rows.
  *
  * All metadata arrays are device memory of P*P int64, 8-byte aligned, counted in rows of
  * `row_elems` elements of `dtype`:

@@ -293,7 +293,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     for (const Call& k : calls)
         for (void* m : k.meta) a.bufs[mb++] = (char*)m;
     const bool has_deps = (dp->prog.flags & PF_HAS_DEPS) != 0;
-    a.dynamic = (has_deps || c->dynamic_dispatch) ? 1u : 0u;
+    a.dynamic = c->dynamic_dispatch ? 1u : 0u;  // tickets only on request (HCCL_DISPATCH=dynamic)
     const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
     a.timeout_ticks = ms * c->wall_clock_khz;
 
@@ -312,7 +312,9 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     a.nworkers = blocks * wpb;
     info.workers = a.nworkers;
 
-    if (c->inline_single_step && dp->prog.descs.size() == 1 && !has_deps && !c->dynamic_dispatch) {
+    const bool plain_step = dp->prog.descs.size() == 1 &&
+                            (dp->prog.descs[0].op == OP_COPY || dp->prog.descs[0].op == OP_REDUCE);
+    if (c->inline_single_step && plain_step && !has_deps && !c->dynamic_dispatch) {
         const HostDesc& d = dp->prog.descs[0];
         InlineArgs ia;
         std::memset(&ia, 0, sizeof ia);
@@ -342,7 +344,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
 
     // a program's counters serve one launch at a time, and the communicator's scratch one
     // program at a time: order such launches across streams
-    const bool stateful = a.dynamic != 0;
+    const bool stateful = has_deps || a.dynamic != 0;
     const bool scratch = dp->prog.scratch_bytes > 0;
     if (stateful && dp->launched && dp->last_stream != s) {
         hipError_t e = hipStreamWaitEvent(s, dp->done, 0);

@@ -34,7 +34,7 @@ constexpr uint32_t kWaveStepElems = kWaveSize * kVecElems;  // 512: one vector p
 constexpr uint64_t kShardAlignElems = 64;                      // 128 B of bf16, 256 B of fp32
 // Static tiles (slots) of the copy step of an AllToAllvDynamic: each moves a contiguous run
 // of about J / slots dynamic tiles, so there are enough for every wavefront of the chip.
-constexpr uint32_t kDynamicSlots = 2048;
+constexpr uint32_t kDynamicSlots = 8192;
 
 // Type of partials that leave registers: FP32 for floating sums (one rounding at the end),
 // the buffer type when every partial is re-quantised, or for MAX / MIN (exact in any type).
@@ -460,10 +460,10 @@ void lower_alltoallv(const CollectiveSpec& s, HostProgram& p) {
 
 // ------------------------------------------------------------------ ALLTOALLV DYNAMIC
 // Device-resident AllToAllv (Section IV-B-2): the host compiles the program once for the
-// capacities, and the layout is built on the device when it runs. Step 0 (P tiles) reads the
-// count matrix, and the explicit offsets if given, from device memory, checks every range
-// and writes the plan table; step 1 waits for all of step 0 and moves the rows, its slots
-// splitting the dynamic tiles between them. Nothing on the host depends on the counts.
+// capacities, and the layout is worked out on the device when it runs. The program is one
+// step of `slots` tiles; each slot reads the count matrix (and the explicit offsets, if given)
+// from device memory, checks the whole layout, and moves its share of the rows. Nothing on the
+// host depends on the counts, and no slot waits for another.
 void lower_alltoallv_dynamic(const CollectiveSpec& s, HostProgram& p) {
     const int P = s.P;
     DynA2A a;
@@ -476,8 +476,6 @@ void lower_alltoallv_dynamic(const CollectiveSpec& s, HostProgram& p) {
     a.sdispls = s.dyn_sdispls ? meta_buf(P, META_SDISPLS) : kNoBuffer;
     a.rdispls = s.dyn_rdispls ? meta_buf(P, META_RDISPLS) : kNoBuffer;
     a.recvcounts = s.dyn_recvcounts ? meta_buf(P, META_RECVCOUNTS) : kNoBuffer;
-    a.table = scratch_buf(P);
-    a.table_off = 0;
     a.row_elems = s.row_elems;
     a.send_cap = s.send_cap;
     a.recv_cap = s.recv_cap;
@@ -485,15 +483,9 @@ void lower_alltoallv_dynamic(const CollectiveSpec& s, HostProgram& p) {
     a.slots = dynamic_slots(s);
     p.aux.push_back(a);
     p.nmeta = kMetaPerDynamicCall;
-    p.scratch_bytes = plan_bytes((uint32_t)P);
-    HostDesc plan;
-    plan.op = OP_DYN_PLAN;
-    plan.aux = 0;
-    p.descs.push_back(plan);
     HostDesc copy;
     copy.op = OP_DYN_COPY;
     copy.aux = 0;
-    copy.deps.push_back(Dep{0, DEP_ALL, 0, 0});
     p.descs.push_back(copy);
     p.algo = ALGO_DIRECT;
 }
@@ -843,7 +835,6 @@ void fuse(HostProgram& p) {
     bool uses_scratch = false;
     for (const auto& d : p.descs) {
         if (!d.alive) continue;
-        uses_scratch |= (d.op == OP_DYN_PLAN || d.op == OP_DYN_COPY);  // the plan table
         for (const Operand& o : d.srcs) uses_scratch |= (o.buf == scratch);
         for (const Operand& o : d.dsts) uses_scratch |= (o.buf == scratch);
     }
@@ -900,8 +891,6 @@ bool merge(std::vector<HostProgram>& parts, const std::vector<CollectiveSpec>& s
             a.sdispls = move_id(k, a.sdispls);
             a.rdispls = move_id(k, a.rdispls);
             a.recvcounts = move_id(k, a.recvcounts);
-            a.table = move_id(k, a.table);
-            a.table_off += scratch_base[k];
             out.aux.push_back(a);
         }
     }
@@ -1008,12 +997,12 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
         d.tile_elems = p.tile_elems;
         d.aux = h.aux;
         uint64_t nt = (h.op == OP_NOOP) ? 1 : (h.nelem + te - 1) / te;
-        if (h.op == OP_DYN_PLAN || h.op == OP_DYN_COPY) {
+        if (h.op == OP_DYN_COPY) {
             if (h.aux >= p.aux.size()) {
                 err = "dynamic step without its record";
                 return false;
             }
-            nt = (h.op == OP_DYN_PLAN) ? p.aux[h.aux].P : p.aux[h.aux].slots;
+            nt = p.aux[h.aux].slots;
         }
         if (nt == 0) nt = 1;
         d.ntiles = (uint32_t)nt;
@@ -1066,7 +1055,7 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     // the leanest executor kernel that covers every step
     int kind = kKindCopyOnly;
     bool dynamic = false;
-    for (uint32_t i = 0; i < nd; ++i) dynamic |= (out[i].op == OP_DYN_PLAN || out[i].op == OP_DYN_COPY);
+    for (uint32_t i = 0; i < nd; ++i) dynamic |= out[i].op == OP_DYN_COPY;
     for (uint32_t i = 0; i < nd; ++i) {
         if (out[i].op != OP_REDUCE) continue;
         const bool plain = out[i].sig <= SIG_INT32 && out[i].redop == RO_SUM && out[i].fold == FOLD_LIST &&

@@ -672,120 +672,6 @@ __device__ __forceinline__ bool wait_deps(const Dep* deps, uint32_t ndep, uint32
     return true;
 }
 
-// ---------------------------------------------------------------- AllToAllvDynamic
-// The layout of a device-resident AllToAllv (Section IV-B-2) is read from device memory when
-// the program runs. P plan tiles build a table of per-pair element counts, offsets and tile
-// prefix sums; the copy slots wait for all of them and move the rows.
-
-// Inclusive prefix sum over the lanes of a wavefront.
-__device__ __forceinline__ uint64_t wave_scan_incl(uint64_t v, uint32_t lane) {
-#pragma unroll
-    for (uint32_t d = 1; d < (uint32_t)kWaveSize; d <<= 1) {
-        const uint64_t t = __shfl_up(v, d);
-        if (lane >= d) v += t;
-    }
-    return v;
-}
-
-struct DynView {     // a DynA2A record loaded into scalar registers
-    uint32_t P, es, send0, recv0, counts, sdispls, rdispls, recvcounts, slots;
-    uint64_t row_elems, send_cap, recv_cap, tile_elems;
-    char* tab;       // the plan table
-};
-
-__device__ __forceinline__ DynView load_dyn(const DynA2A* r, const uint64_t* bufs) {
-    DynView v;
-    v.P = uni(r->P);
-    v.es = uni(r->elem_bytes);
-    v.send0 = uni(r->send0);
-    v.recv0 = uni(r->recv0);
-    v.counts = uni(r->counts);
-    v.sdispls = uni(r->sdispls);
-    v.rdispls = uni(r->rdispls);
-    v.recvcounts = uni(r->recvcounts);
-    v.slots = uni(r->slots);
-    v.row_elems = uni64(r->row_elems);
-    v.send_cap = uni64(r->send_cap);
-    v.recv_cap = uni64(r->recv_cap);
-    v.tile_elems = uni64(r->tile_elems);
-    v.tab = (char*)(uni64(bufs[uni(r->table)]) + uni64(r->table_off));
-    return v;
-}
-
-// Plan tile i: row i of the count matrix (what source i sends, one destination per lane) and
-// column i (what destination i receives, one source per lane). Every range is checked against
-// its buffer's capacity, explicit receive ranges also against each other; a failure marks the
-// table so that no row moves, and is reported in the error record.
-__device__ __forceinline__ void dyn_plan(const DynView& a, uint32_t i, const uint64_t* bufs, ErrorRecord* err,
-                                         uint32_t desc, uint32_t lane) {
-    const uint32_t P = a.P;
-    const bool on = lane < P;
-    const uint64_t R = a.row_elems, te = a.tile_elems;
-    const int64_t* counts = (const int64_t*)uni64(bufs[a.counts]);
-
-    // ---- source i
-    const int64_t c = on ? counts[(uint64_t)i * P + lane] : 0;
-    bool bad = on && (c < 0 || (uint64_t)c > a.send_cap);
-    const uint64_t cs = (on && !bad) ? (uint64_t)c : 0;  // clamped: sums of these cannot overflow
-    uint64_t so;
-    if (a.sdispls != kNoBuffer) {
-        const int64_t* sd = (const int64_t*)uni64(bufs[a.sdispls]);
-        const int64_t x = on ? sd[(uint64_t)i * P + lane] : 0;
-        if (cs && (x < 0 || (uint64_t)x > a.send_cap || cs > a.send_cap - (uint64_t)x)) bad = true;
-        so = (uint64_t)x;
-    } else {
-        const uint64_t incl = wave_scan_incl(cs, lane);
-        if (cs && incl > a.send_cap) bad = true;
-        so = incl - cs;
-    }
-    const uint64_t ne = cs * R;
-    const uint64_t pre = wave_scan_incl((ne + te - 1) / te, lane);
-    if (on) {
-        ((uint32_t*)(a.tab + kPlanPre))[i * P + lane] = (uint32_t)pre;
-        ((uint64_t*)(a.tab + plan_elems_off(P)))[i * P + lane] = ne;
-        ((uint64_t*)(a.tab + plan_soff_off(P)))[i * P + lane] = so * R;
-    }
-    if (lane == P - 1) ((uint32_t*)a.tab)[i] = (uint32_t)pre;
-
-    // ---- destination i
-    const int64_t c2 = on ? counts[(uint64_t)lane * P + i] : 0;
-    bool bad2 = on && (c2 < 0 || (uint64_t)c2 > a.recv_cap);
-    const uint64_t cr = (on && !bad2) ? (uint64_t)c2 : 0;
-    uint64_t ro;
-    if (a.rdispls != kNoBuffer) {
-        const int64_t* rd = (const int64_t*)uni64(bufs[a.rdispls]);
-        const int64_t x = on ? rd[(uint64_t)i * P + lane] : 0;
-        if (cr && (x < 0 || (uint64_t)x > a.recv_cap || cr > a.recv_cap - (uint64_t)x)) bad2 = true;
-        ro = (uint64_t)x;
-        // non-empty receive ranges of destination i must not overlap (a lane whose own range is
-        // out of bounds has already failed the layout, so the sums below are only trusted
-        // where both ranges are in bounds)
-        for (uint32_t j = 0; j < P; ++j) {
-            const uint64_t oj = from_lane(ro, j), nj = from_lane(cr, j);
-            if (j != lane && cr && nj && ro < oj + nj && oj < ro + cr) bad2 = true;
-        }
-    } else {
-        const uint64_t incl = wave_scan_incl(cr, lane);
-        if (cr && incl > a.recv_cap) bad2 = true;
-        ro = incl - cr;
-    }
-    if (on) ((uint64_t*)(a.tab + plan_roff_off(P)))[(uint64_t)lane * P + i] = ro * R;
-    if (on && a.recvcounts != kNoBuffer) ((int64_t*)uni64(bufs[a.recvcounts]))[(uint64_t)i * P + lane] = c2;
-
-    const bool any = __ballot(bad || bad2) != 0ull;
-    if (lane == 0) {
-        ((uint32_t*)(a.tab + 256))[i] = any ? 1u : 0u;
-        if (any) {
-            uint32_t zero = 0;
-            if (__hip_atomic_compare_exchange_strong(&err->code, &zero, 2u, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT)) {
-                __hip_atomic_store(&err->desc, desc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(&err->tile, i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
-    }
-}
-
 // ----------------------------------------------------------------------- the kernel
 // Runs tile `t`. Returns false when a dependency wait failed.
 struct Shared {
@@ -823,47 +709,192 @@ __device__ __forceinline__ void exec_tile(uint32_t op, uint32_t sig, uint32_t re
     }
 }
 
-// Copy slot k: dynamic tiles [k*J/slots, (k+1)*J/slots) of the J the plan produced, numbered
-// source-major, then destination, then tile within the pair.
-template <int KIND>
-__device__ __forceinline__ void dyn_copy(const DynView& a, uint32_t k, const uint64_t* bufs, uint32_t lane) {
+// ---------------------------------------------------------------- AllToAllvDynamic
+// The layout of a device-resident AllToAllv (Section IV-B-2) is read from device memory when
+// the program runs. Every copy slot plans the whole exchange from the count matrix by itself,
+// row by row with lane d standing for destination d, so no slot waits for another and nothing
+// is shared between wavefronts: pass 1 checks every range and counts the dynamic tiles J,
+// pass 2 walks the rows again and moves the slot's tiles [k*J/S, (k+1)*J/S). Dynamic tiles are
+// numbered source-major, then destination, then tile within the pair.
+
+// Inclusive prefix sum over the lanes of a wavefront.
+__device__ __forceinline__ uint64_t wave_scan_incl(uint64_t v, uint32_t lane) {
+#pragma unroll
+    for (uint32_t d = 1; d < (uint32_t)kWaveSize; d <<= 1) {
+        const uint64_t t = __shfl_up(v, d);
+        if (lane >= d) v += t;
+    }
+    return v;
+}
+
+struct DynView {     // a DynA2A record loaded into scalar registers
+    uint32_t P, es, send0, recv0, counts, sdispls, rdispls, recvcounts, slots;
+    uint64_t row_elems, send_cap, recv_cap, tile_elems;
+};
+
+__device__ __forceinline__ DynView load_dyn(const DynA2A* r) {
+    DynView v;
+    v.P = uni(r->P);
+    v.es = uni(r->elem_bytes);
+    v.send0 = uni(r->send0);
+    v.recv0 = uni(r->recv0);
+    v.counts = uni(r->counts);
+    v.sdispls = uni(r->sdispls);
+    v.rdispls = uni(r->rdispls);
+    v.recvcounts = uni(r->recvcounts);
+    v.slots = uni(r->slots);
+    v.row_elems = uni64(r->row_elems);
+    v.send_cap = uni64(r->send_cap);
+    v.recv_cap = uni64(r->recv_cap);
+    v.tile_elems = uni64(r->tile_elems);
+    return v;
+}
+
+// Slot k of an AllToAllvDynamic.
+//  Pass 1, lane i standing for rank i: walks row i of the count matrix (what source i sends) and
+//  column i (what destination i receives) with per-lane sums only, checks every range as the
+//  oracle does (a packed side fits iff its total fits, since counts are non-negative), and
+//  counts the dynamic tiles of row i. One scan over the lanes then gives each row's first tile.
+//  Pass 2, lane d standing for destination d: from the row holding the slot's first tile, works
+//  out the pairs' offsets and moves the slot's tiles.
+// ES / ER: the exchange has explicit send / receive offsets.
+template <int KIND, bool ES, bool ER>
+__device__ __forceinline__ void dyn_slot(const DynView& a, uint32_t k, const uint64_t* bufs, ErrorRecord* err,
+                                         uint32_t desc, uint32_t lane) {
+    constexpr uint32_t B = 2;  // rows whose loads are in flight together
     const uint32_t P = a.P;
     const bool on = lane < P;
-    const uint32_t bad = on ? ((const uint32_t*)(a.tab + 256))[lane] : 0u;
-    if (__ballot(bad != 0u) != 0ull) return;  // the layout was rejected: move nothing
-    const uint64_t incl = wave_scan_incl(on ? ((const uint32_t*)a.tab)[lane] : 0u, lane);
-    const uint64_t J = from_lane(incl, P - 1);
+    const uint64_t R = a.row_elems, te = a.tile_elems;
+    const int64_t* counts = (const int64_t*)uni64(bufs[a.counts]);
+    const int64_t* sdis = ES ? (const int64_t*)uni64(bufs[a.sdispls]) : nullptr;
+    const int64_t* rdis = ER ? (const int64_t*)uni64(bufs[a.rdispls]) : nullptr;
+    const uint64_t cmax = a.send_cap < a.recv_cap ? a.send_cap : a.recv_cap;
+
+    // ---- pass 1
+    bool bad = false;
+    uint64_t srow = 0, scol = 0, trow = 0;  // rows sent, rows received, tiles of row `lane`
+    for (uint32_t t0 = 0; t0 < P; t0 += B) {
+        int64_t cr[B], cc[B];
+#pragma unroll
+        for (uint32_t u = 0; u < B; ++u) {
+            const bool in = on && t0 + u < P;
+            cr[u] = in ? counts[(uint64_t)lane * P + t0 + u] : 0;  // source lane -> destination t
+            cc[u] = in ? counts[(uint64_t)(t0 + u) * P + lane] : 0;  // source t -> destination lane
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < B; ++u) {
+            const uint32_t t = t0 + u;
+            if (t < P) {
+                bad |= on && (cr[u] < 0 || (uint64_t)cr[u] > cmax);
+                const uint64_t c = (cr[u] > 0 && (uint64_t)cr[u] <= cmax) ? (uint64_t)cr[u] : 0;
+                const uint64_t c2 = (cc[u] > 0 && (uint64_t)cc[u] <= cmax) ? (uint64_t)cc[u] : 0;
+                srow = (srow > ~0ull - c) ? ~0ull : srow + c;  // saturating: 64 counts near the
+                scol = (scol > ~0ull - c2) ? ~0ull : scol + c2;  // capacity limit could wrap
+                trow += (c * R + te - 1) / te;
+                if constexpr (ES) {
+                    const int64_t x = on ? sdis[(uint64_t)lane * P + t] : 0;
+                    if (c && (x < 0 || (uint64_t)x > a.send_cap || c > a.send_cap - (uint64_t)x)) bad = true;
+                }
+                if constexpr (ER) {
+                    const int64_t x = on ? rdis[(uint64_t)lane * P + t] : 0;
+                    if (c2 && (x < 0 || (uint64_t)x > a.recv_cap || c2 > a.recv_cap - (uint64_t)x)) bad = true;
+                }
+            }
+        }
+    }
+    if (!ES && srow > a.send_cap) bad = true;
+    if (!ER && scol > a.recv_cap) bad = true;
+    if constexpr (ER) {
+        // non-empty receive ranges of one destination must not overlap (lane = source here; a
+        // range that is out of bounds has already failed, so only in-bounds sums are trusted)
+        for (uint32_t d = 0; d < P; ++d) {
+            const int64_t cx = on ? counts[(uint64_t)lane * P + d] : 0;
+            const int64_t rx = on ? rdis[(uint64_t)d * P + lane] : 0;
+            const uint64_t c = (cx > 0) ? (uint64_t)cx : 0, r = (uint64_t)rx;
+            for (uint32_t j = 0; j < P; ++j) {
+                const uint64_t cj = from_lane(c, j), rj = from_lane(r, j);
+                if (j != lane && c && cj && r < rj + cj && rj < r + c) bad = true;
+            }
+        }
+    }
+    const bool rejected = __ballot(bad) != 0ull;
+    if (k == 0) {
+        // slot 0 reports: the received counts, always, and a rejected layout
+        if (a.recvcounts != kNoBuffer) {
+            int64_t* rc = (int64_t*)uni64(bufs[a.recvcounts]);
+            for (uint32_t t = 0; t < P; ++t)
+                if (on) rc[(uint64_t)lane * P + t] = counts[(uint64_t)t * P + lane];
+        }
+        if (rejected && lane == 0) {
+            uint32_t zero = 0;
+            if (__hip_atomic_compare_exchange_strong(&err->code, &zero, 2u, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT)) {
+                __hip_atomic_store(&err->desc, desc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&err->tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    }
+    if (rejected) return;  // move nothing
+
+    // ---- pass 2
+    const uint64_t gincl = wave_scan_incl(trow, lane);  // lane s: tiles of rows 0..s
+    const uint64_t J = from_lane(gincl, P - 1);
     const uint64_t j0 = (uint64_t)k * J / a.slots, j1 = (uint64_t)(k + 1) * J / a.slots;
-    const uint32_t* pre = (const uint32_t*)(a.tab + kPlanPre);
-    const uint64_t* elems = (const uint64_t*)(a.tab + plan_elems_off(P));
-    const uint64_t* soff = (const uint64_t*)(a.tab + plan_soff_off(P));
-    const uint64_t* roff = (const uint64_t*)(a.tab + plan_roff_off(P));
-    uint32_t row = 0xFFFFFFFFu;
-    uint64_t rp = 0;
+    if (j0 == j1) return;
+    // the row holding tile j0 (rows with no tiles before it are skipped by the ballot)
+    uint32_t s = (uint32_t)__popcll(__ballot(on && gincl <= j0));
+    uint64_t G = s ? from_lane(gincl, s - 1) : 0;  // tiles of the rows before s
+    // lane d: rows destination d receives from the sources before s (the packed receive offset)
+    uint64_t col = 0;
+    if constexpr (!ER) {
+        for (uint32_t q0 = 0; q0 < s; q0 += B) {
+            int64_t cq[B];
+#pragma unroll
+            for (uint32_t u = 0; u < B; ++u) cq[u] = (on && q0 + u < s) ? counts[(uint64_t)(q0 + u) * P + lane] : 0;
+#pragma unroll
+            for (uint32_t u = 0; u < B; ++u) col += (uint64_t)cq[u];
+        }
+    }
     TileOps ops;
     ops.nsrc = 1;
     ops.ndst = 1;
     ops.group = 0;
-    for (uint64_t j = j0; j < j1; ++j) {
-        // the source: rows whose inclusive prefix is <= j lie before it (j < J, so s < P)
-        const uint32_t s = (uint32_t)__popcll(__ballot(on && incl <= j));
-        if (s >= P) break;  // cannot happen with a table from this launch; never index past it
-        const uint64_t jr = j - (s ? from_lane(incl, s - 1) : 0);
-        if (s != row) {
-            rp = on ? pre[s * P + lane] : ~0ull;
-            row = s;
+    const uint64_t send_elems = a.send_cap * R, recv_elems = a.recv_cap * R;
+    for (; s < P && G < j1; ++s) {
+        // checked in pass 1; clamped again so that a count rewritten while this runs (a race in
+        // the caller) still cannot move a byte outside the buffers (see the guard below)
+        const int64_t cx = on ? counts[(uint64_t)s * P + lane] : 0;
+        const uint64_t c = (cx > 0 && (uint64_t)cx <= cmax) ? (uint64_t)cx : 0;
+        uint64_t so, ro;
+        if constexpr (ES) so = on ? (uint64_t)sdis[(uint64_t)s * P + lane] : 0;
+        else so = wave_scan_incl(c, lane) - c;
+        if constexpr (ER) {
+            ro = on ? (uint64_t)rdis[(uint64_t)lane * P + s] : 0;
+        } else {
+            ro = col;
+            col += c;
         }
-        // the destination within row s (jr < the row's total, so d < P)
-        const uint32_t d = (uint32_t)__popcll(__ballot(on && rp <= jr));
-        if (d >= P) break;
-        const uint64_t t = jr - (d ? from_lane(rp, d - 1) : 0);
-        const uint32_t idx = s * P + d;
-        const uint64_t ne = uni64(elems[idx]);
-        const uint64_t e0 = t * a.tile_elems;
-        const uint32_t n = (uint32_t)((ne - e0 < a.tile_elems) ? (ne - e0) : a.tile_elems);
-        ops.src = uni64(bufs[a.send0 + s]) + (uni64(soff[idx]) + e0) * a.es;
-        ops.dst = uni64(bufs[a.recv0 + d]) + (uni64(roff[idx]) + e0) * a.es;
-        exec_tile<KIND>(OP_COPY, 0, 0, a.es, ops, n, false, lane);
+        const uint64_t ne = c * R;
+        const uint64_t pre = wave_scan_incl((ne + te - 1) / te, lane);
+        const uint64_t T = from_lane(pre, P - 1);
+        const uint64_t lo = j0 > G ? j0 : G, hi = j1 < G + T ? j1 : G + T;
+        const uint64_t src_base = uni64(bufs[a.send0 + s]);
+        for (uint64_t j = lo; j < hi; ++j) {
+            const uint64_t jr = j - G;  // < T, so the destination below is < P
+            const uint32_t d = (uint32_t)__popcll(__ballot(on && pre <= jr));
+            if (d >= P) break;
+            const uint64_t t = jr - (d ? from_lane(pre, d - 1) : 0);
+            const uint64_t e0 = t * te, n_pair = from_lane(ne, d);
+            const uint32_t n = (uint32_t)((n_pair - e0 < te) ? (n_pair - e0) : te);
+            const uint64_t sod = from_lane(so, d), rod = from_lane(ro, d);
+            if (sod > a.send_cap || rod > a.recv_cap || sod * R + e0 + n > send_elems ||
+                rod * R + e0 + n > recv_elems)
+                continue;  // only a caller race on the metadata gets here
+            ops.src = src_base + (sod * R + e0) * a.es;
+            ops.dst = uni64(bufs[a.recv0 + d]) + (rod * R + e0) * a.es;
+            exec_tile<KIND>(OP_COPY, 0, 0, a.es, ops, n, false, lane);
+        }
+        G += T;
     }
 }
 
@@ -886,12 +917,15 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
         if (!wait_deps(deps, ndep, k, a.state, a.error, a.timeout, d, t)) return false;
     }
 
-    if (op == OP_DYN_PLAN || op == OP_DYN_COPY) {
+    if (op == OP_DYN_COPY) {
         // the host runs programs with dynamic steps on these two kernels only
         if constexpr (KIND == kKindDynamic || KIND == kKindGeneric) {
-            const DynView v = load_dyn((const DynA2A*)(prog + h.off_aux) + uni(D->aux), bufs);
-            if (op == OP_DYN_PLAN) dyn_plan(v, k, bufs, a.error, d, lane);
-            else dyn_copy<KIND>(v, k, bufs, lane);
+            const DynView v = load_dyn((const DynA2A*)(prog + h.off_aux) + uni(D->aux));
+            const bool es = v.sdispls != kNoBuffer, er = v.rdispls != kNoBuffer;
+            if (!es && !er) dyn_slot<KIND, false, false>(v, k, bufs, a.error, d, lane);
+            else if (es && !er) dyn_slot<KIND, true, false>(v, k, bufs, a.error, d, lane);
+            else if (!es) dyn_slot<KIND, false, true>(v, k, bufs, a.error, d, lane);
+            else dyn_slot<KIND, true, true>(v, k, bufs, a.error, d, lane);
         }
     } else if (op != OP_NOOP) {
         TileOps ops;
@@ -959,31 +993,48 @@ hccl_executor(LaunchArgs a) {
     sh.timeout = a.timeout_ticks;
     const uint32_t nworkers = a.nworkers;
 
+    const bool has_deps = (uni(((const ProgramHeader*)prog)->flags) & PF_HAS_DEPS) != 0u;
     if (!a.dynamic) {
-        for (uint32_t t = wave; t < h.ntiles; t += nworkers) run_tile<KIND>(sh, prog, h, t, lane, bufs);
-        return;
+        // Wavefront w runs tiles w, w + W, w + 2W, ... in order. A tile waits only for tiles with
+        // lower numbers, and everything a wavefront ran before its current tile is lower too, so
+        // with the whole grid resident the lowest unfinished tile is always running.
+        for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
+            if (has_deps && load_relaxed(&a.error->code) != 0u) break;
+            if (!run_tile<KIND>(sh, prog, h, t, lane, bufs)) break;
+        }
+        if (!has_deps) return;  // no counter was touched (the same for every thread of the grid)
+    } else {
+        uint32_t* ticket = a.state + kStateTicket;
+        uint32_t mine = 0;
+        if (lane == 0) mine = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint32_t t = uni(__shfl(mine, 0));
+        while (t < h.ntiles) {
+            if (load_relaxed(&a.error->code) != 0u) break;
+            // claim the next ticket now; its latency hides behind this tile's work
+            uint32_t next = 0;
+            if (lane == 0) next = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (!run_tile<KIND>(sh, prog, h, t, lane, bufs)) break;
+            t = uni(__shfl(next, 0));
+        }
     }
 
-    uint32_t* ticket = a.state + kStateTicket;
-    uint32_t mine = 0;
-    if (lane == 0) mine = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint32_t t = uni(__shfl(mine, 0));
-    while (t < h.ntiles) {
-        if (load_relaxed(&a.error->code) != 0u) break;
-        // claim the next ticket now; its latency hides behind this tile's work
-        uint32_t next = 0;
-        if (lane == 0) next = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (!run_tile<KIND>(sh, prog, h, t, lane, bufs)) break;
-        t = uni(__shfl(next, 0));
+    // The last workgroup to finish clears the counters for the next launch (one atomic per
+    // workgroup: same-address atomics from thousands of wavefronts would serialise). Every
+    // counter update is an agent-scope atomic, so it is enough that each wavefront's updates
+    // have completed (vmcnt(0) counts stores and atomics on this GPU) before its workgroup
+    // counts itself done; an agent-scope release here would write back the whole L2 once per
+    // workgroup.
+    __shared__ uint32_t last_block;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t prev =
+            __hip_atomic_fetch_add(a.state + kStateDone, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last_block = (prev == gridDim.x - 1) ? 1u : 0u;
     }
-
-    // The last wavefront to finish clears the counters for the next launch.
-    uint32_t prev = 0;
-    if (lane == 0)
-        prev = __hip_atomic_fetch_add(a.state + kStateDone, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    prev = uni(__shfl(prev, 0));
-    if (prev == nworkers - 1) {
-        for (uint32_t i = lane; i < h.nstate; i += kWaveSize)
+    __syncthreads();
+    if (last_block) {
+        for (uint32_t i = threadIdx.x; i < h.nstate; i += kBlockThreads)
             __hip_atomic_store(a.state + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }

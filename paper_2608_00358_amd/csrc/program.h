@@ -10,8 +10,9 @@
 // FP32 scratch, then the device metadata arrays of dynamic collectives (2P+1, ...).
 //
 // Each descriptor is cut into tiles of `tile_elems` elements; tiles are numbered globally
-// in descriptor order and handed out to wavefronts by ticket. A tile only waits for tiles
-// with lower numbers, so the wavefront holding the lowest unfinished ticket can always run.
+// in descriptor order. Wavefront w of a grid of W runs tiles w, w + W, ... in order (or, on
+// request, takes tiles by atomic ticket). A tile only waits for tiles with lower numbers, so
+// the lowest unfinished tile can always run.
 #pragma once
 
 #include <stdint.h>
@@ -33,10 +34,9 @@ enum Op : uint8_t {
     OP_COPY = 0,    // byte copy of src[0] to every destination (NMC "A = B")
     OP_REDUCE = 1,  // fold of all sources in list order, rounded once, to every destination
     OP_NOOP = 2,    // carries only dependencies (a join)
-    // AllToAllvDynamic (device-resident layout). Both steps name an auxiliary record.
-    OP_DYN_PLAN = 3,  // tile i reads row i and column i of the count matrix from device memory,
-                      // checks them, and writes the per-pair offsets and tile prefix sums
-    OP_DYN_COPY = 4,  // tile k moves its share of the rows the plan describes
+    // AllToAllvDynamic (device-resident layout): tile k ("slot" k) reads the count matrix from
+    // device memory, checks the layout and moves its share of the rows. Names a DynA2A record.
+    OP_DYN_COPY = 4,
 };
 
 enum DType : uint8_t { DT_BF16 = 0, DT_FP16 = 1, DT_FP32 = 2, DT_INT32 = 3 };
@@ -129,14 +129,14 @@ struct Desc {           // 64 bytes
     uint64_t nelem;
     uint32_t fold;      // FOLD_LIST (grouped / flat, per `group`) or FOLD_PAIRWISE
     uint32_t requant;   // 1 = round every partial to the destination type
-    uint32_t aux;       // OP_DYN_*: index of the DynA2A record
+    uint32_t aux;       // OP_DYN_COPY: index of the DynA2A record
     uint32_t pad1;
 };
 static_assert(sizeof(Desc) == 64, "descriptor layout");
 
-// Auxiliary record of an AllToAllvDynamic (Section IV-B-2): what the plan reads and where the
-// plan table lives. Counts and offsets are int64 rows of `row_elems` elements.
-struct DynA2A {            // 80 bytes
+// Auxiliary record of an AllToAllvDynamic (Section IV-B-2): where its layout is read from.
+// Counts and offsets are int64 rows of `row_elems` elements.
+struct DynA2A {            // 72 bytes
     uint32_t P;
     uint32_t elem_bytes;
     uint32_t send0;        // buffer id of send buffer 0 (send buffer s is send0 + s)
@@ -145,29 +145,14 @@ struct DynA2A {            // 80 bytes
     uint32_t sdispls;      // buffer id of explicit send offsets [s*P + d], or kNoBuffer (packed)
     uint32_t rdispls;      // buffer id of explicit receive offsets [d*P + s], or kNoBuffer (packed)
     uint32_t recvcounts;   // buffer id of the received-count output [d*P + s], or kNoBuffer
-    uint32_t table;        // buffer id holding the plan table (the scratch)
-    uint32_t slots;        // tiles of the copy step; slot k moves dynamic tiles [k*J/slots, (k+1)*J/slots)
-    uint64_t table_off;    // byte offset of the plan table in that buffer
+    uint32_t slots;        // tiles of the step; slot k moves dynamic tiles [k*J/slots, (k+1)*J/slots)
+    uint32_t pad;
     uint64_t row_elems;
     uint64_t send_cap;     // rows per send buffer
     uint64_t recv_cap;     // rows per receive buffer
     uint64_t tile_elems;   // elements per dynamic tile
 };
-static_assert(sizeof(DynA2A) == 80, "auxiliary record layout");
-
-// Plan table of one AllToAllvDynamic (byte offsets from its start; pair index s*P + d):
-//   [0, 256)     u32 row_tiles[64]  dynamic tiles of source row s
-//   [256, 512)   u32 bad[64]        plan tile i found an invalid range (rewritten every launch)
-//   kPlanPre     u32 pre[P*P]       inclusive prefix of the pair tile counts within row s
-//   then         u64 elems[P*P], soff[P*P], roff[P*P]: pair element count, element offset
-//                in send buffer s, element offset in receive buffer d
-constexpr uint64_t kPlanPre = 512;
-constexpr uint64_t plan_elems_off(uint32_t P) { return kPlanPre + (((uint64_t)P * P * 4 + 7) & ~7ull); }
-constexpr uint64_t plan_soff_off(uint32_t P) { return plan_elems_off(P) + (uint64_t)P * P * 8; }
-constexpr uint64_t plan_roff_off(uint32_t P) { return plan_soff_off(P) + (uint64_t)P * P * 8; }
-constexpr uint64_t plan_bytes(uint32_t P) { return plan_roff_off(P) + (uint64_t)P * P * 8; }
-static_assert(sizeof(Operand) == 16, "operand layout");
-static_assert(sizeof(Dep) == 16, "dependency layout");
+static_assert(sizeof(DynA2A) == 72, "auxiliary record layout");
 
 // Device image: header, then the arrays at the offsets the header records (16-byte aligned).
 struct ProgramHeader {
@@ -210,8 +195,8 @@ struct LaunchArgs {
     uint32_t* state;         // nstate words
     ErrorRecord* error;
     uint32_t nworkers;       // wavefronts in the grid
-    uint32_t dynamic;        // 1 = tiles by atomic ticket (always when PF_HAS_DEPS);
-                             // 0 = wavefront w runs tiles w, w + nworkers, ... (no state used)
+    uint32_t dynamic;        // 1 = tiles by atomic ticket; 0 = wavefront w runs tiles w,
+                             // w + nworkers, ... (counters used only by dependencies)
     uint64_t timeout_ticks;  // watchdog for one dependency wait, in wall-clock counter ticks
     char* bufs[kMaxBuffers];
 };

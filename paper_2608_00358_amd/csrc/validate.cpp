@@ -11,8 +11,7 @@
 //     dependency closure (per tile only when both walk the bytes with the same tiling);
 //   * every scratch byte a step reads was written by a step ordered before it;
 //   * the steps write exactly the bytes the collective defines as its output (for a dynamic
-//     exchange, whose bytes depend on the counts: one plan, and one copy that waits for all of
-//     it and stays inside the buffers' capacities).
+//     exchange, whose bytes depend on the counts: one dynamic step inside the capacities).
 #include <algorithm>
 #include <cstdio>
 #include <map>
@@ -72,36 +71,23 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
         }
         if (d.op == OP_NOOP) {
             if (!d.srcs.empty() || !d.dsts.empty()) { err = fmt("NOOP step %llu has operands", i); return false; }
-        } else if (d.op == OP_DYN_PLAN || d.op == OP_DYN_COPY) {
+        } else if (d.op == OP_DYN_COPY) {
             if (!d.srcs.empty() || !d.dsts.empty()) { err = fmt("dynamic step %llu has operands", i); return false; }
             if (d.aux >= p.aux.size()) { err = fmt("dynamic step %llu names record %llu", i, d.aux); return false; }
             const DynA2A& a = p.aux[d.aux];
             const uint32_t nid = (uint32_t)(2 * P + 1) + p.nmeta;
             auto bad_id = [&](uint32_t id, bool optional) { return id == kNoBuffer ? !optional : id >= nid; };
             if (a.P != (uint32_t)P || a.send0 != send_buf(0) || a.recv0 != recv_buf(P, 0) ||
-                a.table != scratch_buf(P) || bad_id(a.counts, false) || a.counts <= scratch_buf(P) ||
-                bad_id(a.sdispls, true) || bad_id(a.rdispls, true) || bad_id(a.recvcounts, true)) {
+                bad_id(a.counts, false) || a.counts <= scratch_buf(P) || bad_id(a.sdispls, true) ||
+                bad_id(a.rdispls, true) || bad_id(a.recvcounts, true)) {
                 err = fmt("dynamic step %llu: its record names the wrong buffers", i);
-                return false;
-            }
-            if (a.table_off % 8 || a.table_off + plan_bytes(a.P) > sizes.bytes[scratch_buf(P)]) {
-                err = fmt("dynamic step %llu: the plan table does not fit the scratch", i);
                 return false;
             }
             if (a.slots == 0 || a.tile_elems == 0 || a.tile_elems % (kWaveSize * kVecElems)) {
                 err = fmt("dynamic step %llu: bad slots or tile size", i);
                 return false;
             }
-            if (d.op == OP_DYN_COPY) {
-                bool planned = false;
-                for (const Dep& e : d.deps)
-                    planned |= e.kind == DEP_ALL && e.desc < i && p.descs[e.desc].op == OP_DYN_PLAN &&
-                               p.descs[e.desc].aux == d.aux;
-                if (!planned) {
-                    err = fmt("dynamic copy %llu does not wait for all of its plan", i);
-                    return false;
-                }
-            }
+            if (!d.deps.empty()) { err = fmt("dynamic step %llu waits for another step", i); return false; }
         } else if (d.op == OP_COPY) {
             if (d.srcs.size() != 1 || d.dsts.empty()) { err = fmt("COPY step %llu needs 1 source and >= 1 destination", i); return false; }
             for (const Operand& o : d.dsts)
@@ -205,19 +191,15 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
     std::vector<std::vector<Access>> acc(nbuf);
     for (uint32_t i = 0; i < D; ++i) {
         const HostDesc& d = p.descs[i];
-        if (d.op == OP_DYN_PLAN || d.op == OP_DYN_COPY) {
-            // the plan writes its table; the copy reads it, may read any send byte and write
-            // any receive byte inside the capacities (es = 0: no per-tile identity)
+        if (d.op == OP_DYN_COPY) {
+            // it may read any send byte and write any receive byte inside the capacities
+            // (es = 0: no per-tile identity with another step)
             const DynA2A& a = p.aux[d.aux];
-            const uint64_t t0 = a.table_off;
-            acc[scratch_buf(P)].push_back(Access{t0, t0 + plan_bytes(a.P), i, 0, d.op == OP_DYN_PLAN});
-            if (d.op == OP_DYN_COPY) {
-                for (int r = 0; r < P; ++r) {
-                    const uint64_t sb = a.send_cap * a.row_elems * a.elem_bytes;
-                    const uint64_t rb = a.recv_cap * a.row_elems * a.elem_bytes;
-                    if (sb) acc[memory_object(send_buf(r))].push_back(Access{0, sb, i, 0, false});
-                    if (rb) acc[memory_object(recv_buf(P, r))].push_back(Access{0, rb, i, 0, true});
-                }
+            const uint64_t sb = a.send_cap * a.row_elems * a.elem_bytes;
+            const uint64_t rb = a.recv_cap * a.row_elems * a.elem_bytes;
+            for (int r = 0; r < P; ++r) {
+                if (sb) acc[memory_object(send_buf(r))].push_back(Access{0, sb, i, 0, false});
+                if (rb) acc[memory_object(recv_buf(P, r))].push_back(Access{0, rb, i, 0, true});
             }
             continue;
         }
@@ -278,18 +260,9 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
 
     // ----------------------------------------------------------------- coverage
     if (spec.coll == COLL_ALLTOALLV_DYNAMIC) {
-        // the bytes written depend on the counts: require exactly one plan and one copy
-        uint32_t plans = 0, copies = 0;
-        for (const HostDesc& d : p.descs) {
-            plans += d.op == OP_DYN_PLAN;
-            copies += d.op == OP_DYN_COPY;
-            if (d.op != OP_DYN_PLAN && d.op != OP_DYN_COPY) {
-                err = "a dynamic exchange has a static step";
-                return false;
-            }
-        }
-        if (plans != 1 || copies != 1) {
-            err = "a dynamic exchange needs one plan and one copy step";
+        // the bytes written depend on the counts: require the one dynamic step
+        if (D != 1 || p.descs[0].op != OP_DYN_COPY) {
+            err = "a dynamic exchange is one dynamic step";
             return false;
         }
         return true;

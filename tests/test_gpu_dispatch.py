@@ -1,0 +1,76 @@
+"""GPU parity of dependent programs under both ways of handing tiles to wavefronts.
+
+By default wavefront w runs tiles w, w + W, ...; HCCL_DISPATCH=dynamic makes every wavefront
+take tiles by atomic ticket instead, and HCCL_INLINE=0 sends one-step programs through the
+device image too. Each mode must give the oracle's bits, launch after launch (the counters are
+cleared at the end of every launch).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_00358_amd as H
+from gpu_helpers import Guarded, first_mismatch, same_bits, to_device, to_host
+from test_gpu_parity import inputs
+
+pytestmark = pytest.mark.gpu
+
+SMALL = dict(chunk_bytes=4096, tile_bytes=4096)
+
+
+@pytest.fixture(params=["static", "tickets", "no_inline"])
+def mode(request, monkeypatch):
+    if request.param == "tickets":
+        monkeypatch.setenv("HCCL_DISPATCH", "dynamic")
+    if request.param == "no_inline":
+        monkeypatch.setenv("HCCL_INLINE", "0")
+    return request.param
+
+
+@pytest.mark.parametrize("algo,cfg", [("ring", dict(fuse=0)), ("two_level", dict(group_size=4, fuse=0)),
+                                      ("rhd", dict(order="halving", fuse=0)), ("direct", {})])
+def test_allreduce_repeated_launches(mode, algo, cfg):
+    P, N = 8, 12345
+    x = inputs(P, N, "bf16", 21)
+    print(f"dispatch={mode} allreduce algo={algo} cfg={cfg}", flush=True)
+    want = oracle.allreduce_ordered(x, "bf16", order=cfg.get("order", "two_level" if algo == "two_level" else
+                                                           "ascending"), group=cfg.get("group_size", 0))
+    with H.Comm(P, device=0, algo=algo, **cfg, **SMALL) as c:
+        send = [to_device(x[r], "bf16") for r in range(P)]
+        outs = [Guarded(N, "bf16") for _ in range(P)]
+        for it in range(4):
+            for o in outs:
+                o.view.fill_(0)
+            H.hccl_allreduce(c.handle, send, [o.view for o in outs], N, "bf16")
+            torch.cuda.synchronize()
+            assert c.async_error() == 0
+            for r in range(P):
+                got = outs[r].result()
+                assert same_bits(got, want[r], "bf16"), f"launch {it} rank {r}: {first_mismatch(got, want[r])}"
+                assert outs[r].guards_intact()
+
+
+def test_dynamic_alltoallv_repeated_launches(mode):
+    P, R, S = 8, 16, 64
+    cap = P * S
+    x = inputs(P, S * R, "int32", 22)
+    send = [to_device(x[s], "int32") for s in range(P)]
+    recv = [torch.empty(cap * R, dtype=torch.int32, device="cuda:0") for _ in range(P)]
+    d_counts = torch.zeros(P * P, dtype=torch.int64, device="cuda:0")
+    rng = np.random.default_rng(3)
+    print(f"dispatch={mode} alltoallv_dynamic", flush=True)
+    with H.Comm(P, device=0) as c:
+        run = c.bind_alltoallv_dynamic(send, d_counts, recv, R)
+        for it in range(4):
+            counts = np.stack([rng.multinomial(S - it, np.full(P, 1.0 / P)) for _ in range(P)])
+            d_counts.copy_(torch.from_numpy(counts.reshape(-1)).to("cuda:0"))
+            for t in recv:
+                t.fill_(-1)
+            run()
+            torch.cuda.synchronize()
+            assert c.async_error() == 0
+            want = [np.full(cap * R, -1, np.int32) for _ in range(P)]
+            assert oracle.alltoallv_dynamic([x[s] for s in range(P)], counts, want, R, S, cap)[0]
+            for d in range(P):
+                assert np.array_equal(to_host(recv[d], "int32"), want[d]), f"launch {it} destination {d}"
