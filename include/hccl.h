@@ -93,7 +93,7 @@ typedef struct {
                               0 = run every lowered step as its own dependent descriptor */
     int32_t max_workers;   /* upper bound on executor wavefronts (0 = size from the device) */
     uint32_t tile_bytes;   /* work claimed per ticket, bytes read per tile (0 = default) */
-    uint32_t timeout_ms;   /* watchdog for one dependency wait on the device (0 = 2000) */
+    uint32_t timeout_ms;   /* watchdog for one dependency or trigger wait on the device (0 = 2000) */
     int32_t validate;      /* 1 = run the program validator on every compile */
     int32_t order;         /* hcclOrder_t */
     int32_t requantize;    /* 1 = round every partial to the buffer type */
@@ -199,6 +199,37 @@ hcclResult_t hccl_alltoallv_dynamic(hcclComm_t comm,
 hcclResult_t hccl_group_start(hcclComm_t comm);
 hcclResult_t hccl_group_end(hcclComm_t comm);
 
+/*
+ * Device-triggered collectives (Section IV-B-3). The trigger set here applies to the next work
+ * packet the communicator enqueues (one collective called outside a group, or the next
+ * outermost hccl_group_end), or rejects, and is then cleared; trigger == NULL clears it.
+ *
+ * wait_addr (device memory, 8-byte aligned, or NULL): the executor is launched at once and
+ *   occupies its CUs, but no step starts until (*wait_addr CMP wait_value) holds, compared as
+ *   unsigned 64-bit values. The word is read with system-scope loads, so a kernel on another
+ *   stream, a device copy or the host may write it; whatever the writer stored before the word
+ *   (inputs, counts) is visible to the collective. Because the waiting executor holds its CUs,
+ *   the signalling kernel must find room elsewhere: issue triggered collectives on a CU-masked
+ *   stream (hipExtStreamCreateWithCUMask) or cap max_workers. A wait longer than the
+ *   communicator's timeout ends the launch with hcclTimeout from hccl_get_async_error; outputs
+ *   are then unspecified and the completion word is not written.
+ * done_addr (device memory, 8-byte aligned, or NULL): done_value is stored there with a
+ *   system-scope release once every step has finished and its results are visible device-wide.
+ * The two words must not overlap any buffer of the collective.
+ */
+typedef enum { hcclCmpEq = 0, hcclCmpNe = 1, hcclCmpGe = 2, hcclCmpGt = 3, hcclCmpLe = 4, hcclCmpLt = 5 } hcclCmp_t;
+
+typedef struct {
+    const uint64_t* wait_addr;
+    uint64_t wait_value;
+    int32_t wait_cmp;          /* hcclCmp_t */
+    int32_t reserved;
+    uint64_t* done_addr;
+    uint64_t done_value;
+} hcclTrigger_t;
+
+hcclResult_t hccl_set_trigger(hcclComm_t comm, const hcclTrigger_t* trigger);
+
 /* Thread-local text of the last error returned on this thread ("" if none). */
 const char* hccl_get_last_error(void);
 
@@ -207,8 +238,8 @@ const char* hccl_result_string(hcclResult_t r);
 
 /*
  * Synchronises the communicator's device and reports a device-side failure recorded since
- * the previous call (hcclTimeout when a dependency wait hit the watchdog, hcclInvalidArgument
- * when a device-resident layout was rejected), then clears it.
+ * the previous call (hcclTimeout when a dependency wait or a trigger wait hit the watchdog,
+ * hcclInvalidArgument when a device-resident layout was rejected), then clears it.
  */
 hcclResult_t hccl_get_async_error(hcclComm_t comm);
 

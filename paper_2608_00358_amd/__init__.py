@@ -8,5 +8,6 @@ from .hccl import (  # noqa: F401
     ALGOS, DTYPES, EXPORTS, LIB_PATH, MAX_RANKS, NO_DEVICE, OPS, Comm, HcclError,
     hccl_allgather, hccl_allreduce, hccl_alltoallv, hccl_alltoallv_dynamic, hccl_comm_create, hccl_comm_destroy,
     hccl_comm_last_program, hccl_comm_set_config, hccl_config_init, hccl_get_async_error,
-    hccl_get_last_error, hccl_group_end, hccl_group_start, hccl_reduce_scatter, hccl_result_string, load,
+    hccl_get_last_error, hccl_group_end, hccl_group_start, hccl_reduce_scatter, hccl_result_string,
+    hccl_set_trigger, load,
 )

@@ -84,6 +84,8 @@ struct hcclComm {
     bool inline_single_step = true;  // one-step programs travel in the launch packet
     int group_depth = 0;             // > 0 between hccl_group_start and hccl_group_end
     std::vector<Call> pending;       // calls recorded inside a group
+    bool has_trigger = false;        // hccl_set_trigger for the next work packet
+    hcclTrigger_t trigger{};
     hcclProgramInfo_t last{};
 };
 
@@ -247,6 +249,10 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     DeviceGuard guard(c->device);
     std::vector<CollectiveSpec> specs;
     for (const Call& k : calls) specs.push_back(k.spec);
+    // the trigger belongs to this packet, whether it is enqueued or rejected
+    const bool triggered = c->has_trigger;
+    const hcclTrigger_t trig = c->trigger;
+    c->has_trigger = false;
     hcclResult_t r = compile_program(c, specs, dp, hit);
     if (r != hcclSuccess) return r;
 
@@ -267,6 +273,21 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     info.program_bytes = dp->prog.image.size();
     info.compile_us = dp->compile_us;
 
+    if (triggered) {
+        if (dp->prog.ntiles == 0) return fail(hcclInvalidArgument, "a triggered work packet has no work to run");
+        // the trigger words must not overlap a buffer of the packet
+        for (const Call& k : calls) {
+            BufferSizes sz = buffer_sizes(k.spec, 0);
+            for (int i = 0; i < k.spec.P; ++i) {
+                const std::pair<uintptr_t, uint64_t> spans[2] = {{(uintptr_t)k.send[i], sz.bytes[send_buf(i)]},
+                                                                 {(uintptr_t)k.recv[i], sz.bytes[recv_buf(k.spec.P, i)]}};
+                for (const auto& sp : spans)
+                    for (const void* w : {(const void*)trig.wait_addr, (const void*)trig.done_addr})
+                        if (w && (uintptr_t)w + 8 > sp.first && (uintptr_t)w < sp.first + sp.second)
+                            return fail(hcclInvalidArgument, "a trigger word overlaps a buffer of the collective");
+            }
+        }
+    }
     if (c->device == HCCL_NO_DEVICE || dp->prog.ntiles == 0) return hcclSuccess;
 
     r = ensure_scratch(c, dp->prog.scratch_bytes);
@@ -296,6 +317,14 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     a.dynamic = c->dynamic_dispatch ? 1u : 0u;  // tickets only on request (HCCL_DISPATCH=dynamic)
     const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
     a.timeout_ticks = ms * c->wall_clock_khz;
+    if (triggered) {
+        a.wait_addr = trig.wait_addr;
+        a.wait_value = trig.wait_value;
+        a.wait_cmp = (uint32_t)trig.wait_cmp;
+        a.done_addr = trig.done_addr;
+        a.done_value = trig.done_value;
+    }
+    const bool signals = a.done_addr != nullptr;
 
     const uint32_t wpb = (uint32_t)executor_waves_per_block();
     uint32_t cus = stream_cu_count(c, s);
@@ -314,7 +343,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
 
     const bool plain_step = dp->prog.descs.size() == 1 &&
                             (dp->prog.descs[0].op == OP_COPY || dp->prog.descs[0].op == OP_REDUCE);
-    if (c->inline_single_step && plain_step && !has_deps && !c->dynamic_dispatch) {
+    if (c->inline_single_step && plain_step && !has_deps && !c->dynamic_dispatch && !triggered) {
         const HostDesc& d = dp->prog.descs[0];
         InlineArgs ia;
         std::memset(&ia, 0, sizeof ia);
@@ -344,7 +373,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
 
     // a program's counters serve one launch at a time, and the communicator's scratch one
     // program at a time: order such launches across streams
-    const bool stateful = has_deps || a.dynamic != 0;
+    const bool stateful = has_deps || a.dynamic != 0 || signals;
     const bool scratch = dp->prog.scratch_bytes > 0;
     if (stateful && dp->launched && dp->last_stream != s) {
         hipError_t e = hipStreamWaitEvent(s, dp->done, 0);
@@ -653,6 +682,22 @@ hcclResult_t hccl_alltoallv_dynamic(hcclComm_t comm, const void* const* sendbufs
     return run(comm, s, sendbufs, recvbufs, stream, std::move(mv));
 }
 
+hcclResult_t hccl_set_trigger(hcclComm_t comm, const hcclTrigger_t* t) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (!t) {
+        comm->has_trigger = false;
+        return hcclSuccess;
+    }
+    if (t->wait_cmp < hcclCmpEq || t->wait_cmp > hcclCmpLt) return fail(hcclInvalidArgument, "unknown comparator");
+    if ((uintptr_t)t->wait_addr % 8 || (uintptr_t)t->done_addr % 8)
+        return fail(hcclInvalidArgument, "trigger words must be 8-byte aligned");
+    if (t->wait_addr && (const void*)t->wait_addr == (const void*)t->done_addr)
+        return fail(hcclInvalidArgument, "the wait and completion words must differ");
+    comm->trigger = *t;
+    comm->has_trigger = true;
+    return hcclSuccess;
+}
+
 hcclResult_t hccl_group_start(hcclComm_t comm) {
     if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
     comm->group_depth += 1;
@@ -736,6 +781,13 @@ hcclResult_t hccl_get_async_error(hcclComm_t comm) {
                       "a count or offset left its buffer, or receive ranges overlapped; nothing was moved",
                       rec.desc, rec.tile);
         return fail(hcclInvalidArgument, buf);
+    }
+    if (rec.code == 3) {
+        std::snprintf(buf, sizeof buf,
+                      "the trigger word did not satisfy its comparison within the watchdog limit "
+                      "(workgroup %u gave up); the collective's outputs are unspecified",
+                      rec.tile);
+        return fail(hcclTimeout, buf);
     }
     std::snprintf(buf, sizeof buf, "a dependency wait of step %u (tile %u) exceeded the watchdog limit",
                   rec.desc, rec.tile);

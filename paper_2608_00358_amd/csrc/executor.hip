@@ -966,6 +966,53 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
     return true;
 }
 
+// ------------------------------------------------------------------ device trigger
+// A pre-launched collective holds until a device word satisfies a comparison (Section IV-B-3:
+// the caller attaches an address and a comparator; the collective is enqueued at once and
+// blocks on the device until the compute side signals). One thread per workgroup polls the
+// word with system-scope loads (the writer may be another kernel, a copy or the host), backing
+// off between polls; the rest of the workgroup waits at the barrier, issuing no memory
+// traffic. Returns false when the watchdog fired or another workgroup recorded an error.
+__device__ __forceinline__ bool trigger_cmp(uint64_t x, uint64_t v, uint32_t cmp) {
+    switch (cmp) {
+        case CMP_EQ: return x == v;
+        case CMP_NE: return x != v;
+        case CMP_GE: return x >= v;
+        case CMP_GT: return x > v;
+        case CMP_LE: return x <= v;
+        default: return x < v;
+    }
+}
+
+__device__ __forceinline__ bool trigger_wait(const LaunchArgs& a) {
+    __shared__ uint32_t go;
+    if (threadIdx.x == 0) {
+        uint32_t ok = 1;
+        const uint64_t t0 = wall_clock64();
+        while (!trigger_cmp(__hip_atomic_load(a.wait_addr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM),
+                            a.wait_value, a.wait_cmp)) {
+            if (load_relaxed(&a.error->code) != 0u) {
+                ok = 0;
+                break;
+            }
+            if (wall_clock64() - t0 > a.timeout_ticks) {
+                uint32_t zero = 0;
+                if (__hip_atomic_compare_exchange_strong(&a.error->code, &zero, 3u, __ATOMIC_RELAXED,
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+                    __hip_atomic_store(&a.error->tile, blockIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ok = 0;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(8);
+        }
+        // whatever the signalling side wrote before the word is visible from here on
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        go = ok;
+    }
+    __syncthreads();
+    return go != 0u;
+}
+
 // Four waves per SIMD for the specialised kernels; the generic kernel (every fold, mixed types)
 // may use more registers rather than spill.
 template <int KIND>
@@ -994,16 +1041,19 @@ hccl_executor(LaunchArgs a) {
     const uint32_t nworkers = a.nworkers;
 
     const bool has_deps = (uni(((const ProgramHeader*)prog)->flags) & PF_HAS_DEPS) != 0u;
-    if (!a.dynamic) {
+    const bool triggered = a.wait_addr != nullptr;
+    const bool signals = a.done_addr != nullptr;
+    // a workgroup whose trigger wait failed runs no tile but still counts itself done below
+    const bool started = !triggered || trigger_wait(a);
+    if (started && !a.dynamic) {
         // Wavefront w runs tiles w, w + W, w + 2W, ... in order. A tile waits only for tiles with
         // lower numbers, and everything a wavefront ran before its current tile is lower too, so
         // with the whole grid resident the lowest unfinished tile is always running.
         for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
-            if (has_deps && load_relaxed(&a.error->code) != 0u) break;
+            if ((has_deps || triggered) && load_relaxed(&a.error->code) != 0u) break;
             if (!run_tile<KIND>(sh, prog, h, t, lane, bufs)) break;
         }
-        if (!has_deps) return;  // no counter was touched (the same for every thread of the grid)
-    } else {
+    } else if (started) {
         uint32_t* ticket = a.state + kStateTicket;
         uint32_t mine = 0;
         if (lane == 0) mine = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1018,16 +1068,21 @@ hccl_executor(LaunchArgs a) {
         }
     }
 
+    // no counter was touched and nothing is signalled (the same for every thread of the grid)
+    if (!has_deps && !a.dynamic && !signals) return;
+
     // The last workgroup to finish clears the counters for the next launch (one atomic per
     // workgroup: same-address atomics from thousands of wavefronts would serialise). Every
     // counter update is an agent-scope atomic, so it is enough that each wavefront's updates
     // have completed (vmcnt(0) counts stores and atomics on this GPU) before its workgroup
-    // counts itself done; an agent-scope release here would write back the whole L2 once per
-    // workgroup.
+    // counts itself done. Only when a completion word is requested does every workgroup also
+    // release its data stores at agent scope (an L2 write-back), so that whoever sees the word
+    // sees the collective's results.
     __shared__ uint32_t last_block;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) {
+        if (signals) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         const uint32_t prev =
             __hip_atomic_fetch_add(a.state + kStateDone, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         last_block = (prev == gridDim.x - 1) ? 1u : 0u;
@@ -1036,6 +1091,14 @@ hccl_executor(LaunchArgs a) {
     if (last_block) {
         for (uint32_t i = threadIdx.x; i < h.nstate; i += kBlockThreads)
             __hip_atomic_store(a.state + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (signals) {
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            // the completion word, written once every workgroup has finished, and only if no
+            // error was recorded (a failed trigger wait or dependency wait ran nothing or part)
+            if (threadIdx.x == 0 && load_relaxed(&a.error->code) == 0u)
+                __hip_atomic_store(a.done_addr, a.done_value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
     }
 }
 

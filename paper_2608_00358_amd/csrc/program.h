@@ -183,7 +183,8 @@ constexpr uint32_t kStateDescBase = 2;
 
 // Device-side error record (per communicator).
 struct ErrorRecord {
-    uint32_t code;   // 0 = none, 1 = dependency wait timed out, 2 = a dynamic layout was invalid
+    uint32_t code;   // 0 = none, 1 = dependency wait timed out, 2 = a dynamic layout was invalid,
+                     // 3 = the trigger word never satisfied its comparison
     uint32_t desc;
     uint32_t tile;
     uint32_t pad;
@@ -198,8 +199,19 @@ struct LaunchArgs {
     uint32_t dynamic;        // 1 = tiles by atomic ticket; 0 = wavefront w runs tiles w,
                              // w + nworkers, ... (counters used only by dependencies)
     uint64_t timeout_ticks;  // watchdog for one dependency wait, in wall-clock counter ticks
+    // Device trigger (Section IV-B-3): no tile starts before (*wait_addr CMP wait_value) holds
+    // (wait_addr NULL: start at once); done_value is written to done_addr (if not NULL) once
+    // every tile has finished and its stores are visible.
+    const uint64_t* wait_addr;
+    uint64_t wait_value;
+    uint64_t* done_addr;
+    uint64_t done_value;
+    uint32_t wait_cmp;       // TriggerCmp
+    uint32_t pad;
     char* bufs[kMaxBuffers];
 };
+
+enum TriggerCmp : uint32_t { CMP_EQ = 0, CMP_NE = 1, CMP_GE = 2, CMP_GT = 3, CMP_LE = 4, CMP_LT = 5 };
 
 // Kernel arguments of a one-step program launched inline: the step and its operands,
 // already resolved to addresses of element 0, travel in the launch packet.

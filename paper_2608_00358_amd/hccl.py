@@ -27,8 +27,9 @@ EXPORTS = [
     "hccl_config_init", "hccl_comm_create", "hccl_comm_destroy", "hccl_comm_set_config",
     "hccl_allreduce", "hccl_reduce_scatter", "hccl_allgather", "hccl_alltoallv",
     "hccl_get_last_error", "hccl_result_string", "hccl_get_async_error", "hccl_comm_last_program",
-    "hccl_group_start", "hccl_group_end", "hccl_alltoallv_dynamic",
+    "hccl_group_start", "hccl_group_end", "hccl_alltoallv_dynamic", "hccl_set_trigger",
 ]
+CMPS = {"eq": 0, "ne": 1, "ge": 2, "gt": 3, "le": 4, "lt": 5}
 
 
 class HcclError(RuntimeError):
@@ -43,6 +44,13 @@ class hcclConfig_t(ctypes.Structure):
         ("fuse", ctypes.c_int32), ("max_workers", ctypes.c_int32), ("tile_bytes", ctypes.c_uint32),
         ("timeout_ms", ctypes.c_uint32), ("validate", ctypes.c_int32), ("order", ctypes.c_int32),
         ("requantize", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3),
+    ]
+
+
+class hcclTrigger_t(ctypes.Structure):
+    _fields_ = [
+        ("wait_addr", ctypes.c_void_p), ("wait_value", ctypes.c_uint64), ("wait_cmp", ctypes.c_int32),
+        ("reserved", ctypes.c_int32), ("done_addr", ctypes.c_void_p), ("done_value", ctypes.c_uint64),
     ]
 
 
@@ -82,6 +90,7 @@ def load(path: str = LIB_PATH):
     lib.hccl_allgather.argtypes = [vp, vpp, vpp, sz, i32, vp]
     lib.hccl_alltoallv.argtypes = [vp, vpp, szp, szp, vpp, szp, szp, i32, vp]
     lib.hccl_alltoallv_dynamic.argtypes = [vp, vpp, vp, vp, vpp, vp, vp, sz, sz, sz, i32, vp]
+    lib.hccl_set_trigger.argtypes = [vp, ctypes.POINTER(hcclTrigger_t)]
     lib.hccl_get_last_error.argtypes = []
     lib.hccl_get_last_error.restype = ctypes.c_char_p
     lib.hccl_result_string.argtypes = [i32]
@@ -204,6 +213,22 @@ def hccl_alltoallv_dynamic(comm, sendbufs, sendcounts, sdispls, recvbufs, recvco
                                          _stream_handle(stream)))
 
 
+def hccl_set_trigger(comm, wait=None, done=None) -> None:
+    """Trigger for the next work packet: ``wait`` = (word, cmp, value) with cmp in CMPS,
+    ``done`` = (word, value); words are device int64 tensors or addresses. Both None clears."""
+    if wait is None and done is None:
+        _check(load().hccl_set_trigger(comm, None))
+        return
+    t = hcclTrigger_t()
+    if wait is not None:
+        word, cmp, value = wait
+        t.wait_addr, t.wait_cmp, t.wait_value = _addr(word), CMPS[cmp] if isinstance(cmp, str) else int(cmp), value
+    if done is not None:
+        word, value = done
+        t.done_addr, t.done_value = _addr(word), value
+    _check(load().hccl_set_trigger(comm, ctypes.byref(t)))
+
+
 def hccl_group_start(comm) -> None:
     _check(load().hccl_group_start(comm))
 
@@ -322,6 +347,22 @@ class Comm:
                       _addr_or_null(sdispls), _ptr_array(recv), _addr_or_null(recvcounts), _addr_or_null(rdispls),
                       row_elems, self._capacity(send, row_elems), self._capacity(recv, row_elems),
                       _dtype_code(send[0].dtype), _stream_handle(stream))
+
+    def triggered(self, wait=None, done=None):
+        """Context manager: the next work packet called inside waits for ``wait`` =
+        (word, cmp, value) and writes ``done`` = (word, value) (see hccl_set_trigger)."""
+        comm = self
+
+        class _Triggered:
+            def __enter__(self):
+                hccl_set_trigger(comm.handle, wait, done)
+                return comm
+
+            def __exit__(self, *exc):
+                hccl_set_trigger(comm.handle)   # a trigger no call consumed does not linger
+                return False
+
+        return _Triggered()
 
     def group(self):
         """Context manager: the collectives called inside run as one launch at its end."""

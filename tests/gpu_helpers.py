@@ -86,3 +86,62 @@ def first_mismatch(a: np.ndarray, b: np.ndarray) -> str:
         return "no mismatch"
     i = int(idx[0])
     return f"{idx.size} mismatches, first at {i}: got {a[i]!r} want {b[i]!r}"
+
+
+class MaskedStream:
+    """A HIP stream confined to the first `per_xcd` CUs of every XCD (mask bit i selects a CU of
+    XCD i mod 8), at the default priority; destroyed on exit."""
+
+    def __init__(self, per_xcd=2):
+        import ctypes
+
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
+                                                           ctypes.POINTER(ctypes.c_uint32)]
+        self._hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+        ncu = torch.cuda.get_device_properties(0).multi_processor_count
+        words = (ncu + 31) // 32
+        bits = [0] * words
+        for i in range(8 * per_xcd):
+            bits[i // 32] |= 1 << (i % 32)
+        arr = (ctypes.c_uint32 * words)(*bits)
+        handle = ctypes.c_void_p()
+        rc = self._hip.hipExtStreamCreateWithCUMask(ctypes.byref(handle), words, arr)
+        if rc != 0:
+            raise RuntimeError(f"hipExtStreamCreateWithCUMask failed ({rc})")
+        self.handle = handle.value
+        self.stream = torch.cuda.ExternalStream(self.handle)
+
+    def __enter__(self):
+        return self.stream
+
+    def __exit__(self, *exc):
+        self.stream.synchronize()
+        self._hip.hipStreamDestroy(self.handle)
+        return False
+
+
+class SideStream:
+    """A non-blocking HIP stream at the default priority (work on it never waits for the null
+    stream, and the null stream never waits for it); destroyed on exit."""
+
+    def __init__(self):
+        import ctypes
+
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipStreamCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32]
+        self._hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+        handle = ctypes.c_void_p()
+        rc = self._hip.hipStreamCreateWithFlags(ctypes.byref(handle), 1)  # hipStreamNonBlocking
+        if rc != 0:
+            raise RuntimeError(f"hipStreamCreateWithFlags failed ({rc})")
+        self.handle = handle.value
+        self.stream = torch.cuda.ExternalStream(self.handle)
+
+    def __enter__(self):
+        return self.stream
+
+    def __exit__(self, *exc):
+        self.stream.synchronize()
+        self._hip.hipStreamDestroy(self.handle)
+        return False

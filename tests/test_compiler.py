@@ -411,3 +411,25 @@ def test_dynamic_alltoallv_groups():
                                      fake_bufs(P, (1 << 44) + k * (1 << 37)), META + (1 << 20), None, 1, 64, 64,
                                      "fp32")
         _expect(1, H.hccl_group_end, c.handle)
+
+
+# ------------------------------------------------------------------------- triggers
+def test_trigger_arguments_and_consumption():
+    P = 4
+    s, r = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+    word = META
+    with comm(P) as c:
+        _expect(1, H.hccl_set_trigger, c.handle, (word + 4, "eq", 1), None)            # misaligned
+        _expect(1, H.hccl_set_trigger, c.handle, (word, "eq", 1), (word, 2))           # same word
+        _expect(1, H.hccl_set_trigger, c.handle, (word, 9, 1), None)                   # comparator
+        # a word inside a receive buffer is rejected when the packet is enqueued ...
+        H.hccl_set_trigger(c.handle, (r[1] + 64, "ge", 1), None)
+        _expect(1, H.hccl_allreduce, c.handle, s, r, 100, "fp32")
+        # ... and the trigger went with that packet: the next call is untriggered
+        H.hccl_allreduce(c.handle, s, r, 100, "fp32")
+        # an empty packet cannot carry a trigger
+        H.hccl_set_trigger(c.handle, None, (word, 1))
+        _expect(1, H.hccl_allreduce, c.handle, s, r, 0, "fp32")
+        H.hccl_set_trigger(c.handle, (word, "lt", 3), (word + 8, 1))
+        H.hccl_set_trigger(c.handle)                                                    # cleared
+        H.hccl_allreduce(c.handle, s, r, 0, "fp32")
