@@ -478,6 +478,136 @@ def bench_moe_dispatch(device, iters=60, warmup=10):
             "exchange_exposed_eager_us": t_eager - t_route}
 
 
+def bench_triggered_dispatch(device, iters=60, warmup=10, per_xcd=16, done_word=True):
+    """Routing followed by the dispatch exchange, the compute side on its own stream:
+    (a) eager: counts to the host, layout, hccl_alltoallv on the compute stream;
+    (b) device-resident: hccl_alltoallv_dynamic on the compute stream right after routing;
+    (c) device-resident and device-triggered: the dynamic exchange is enqueued first on a stream
+        masked to `per_xcd` CUs per XCD and waits on a device word; routing ends by writing it.
+    Wall time per iteration (synchronised at its end), and the exposed exchange time from the
+    end of routing to the end of the exchange (HIP events)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_00358_amd as H
+
+    P, T, D = 8, 256, 4096
+    g = torch.Generator(device=device)
+    g.manual_seed(11)
+    tokens = torch.randn(P, T, D, generator=g, device=device).to(torch.bfloat16)
+    send_all = torch.empty(P, T * D, dtype=torch.bfloat16, device=device)
+    send = [send_all[s] for s in range(P)]
+    cap = P * T
+    recv = [torch.empty(cap * D, dtype=torch.bfloat16, device=device) for _ in range(P)]
+    d_counts = torch.empty(P * P, dtype=torch.int64, device=device)
+    flag = torch.zeros(1, dtype=torch.int64, device=device)
+    done = torch.zeros(1, dtype=torch.int64, device=device)
+    rank_base = (torch.arange(P, device=device) * P).view(P, 1)
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipStreamCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32]
+    h = ctypes.c_void_p()
+    if hip.hipStreamCreateWithFlags(ctypes.byref(h), 1) != 0:   # non-blocking, default priority
+        raise RuntimeError("hipStreamCreateWithFlags failed")
+    cs = torch.cuda.ExternalStream(h.value)
+    props = torch.cuda.get_device_properties(0)
+    words = (props.multi_processor_count + 31) // 32
+    bits = [0] * words
+    for i in range(8 * per_xcd):
+        bits[i // 32] |= 1 << (i % 32)
+    ms, _ = _cu_masked_stream(bits)
+
+    def route():
+        dest = (torch.rand(P, T, generator=g, device=device) ** 2 * P).long().clamp_(max=P - 1)
+        d_counts.copy_(torch.bincount((dest + rank_base).view(-1), minlength=P * P))
+        order = torch.argsort(dest, dim=1, stable=True)
+        torch.take_along_dim(tokens, order.unsqueeze(-1), dim=1, out=send_all.view(P, T, D))
+
+    out = {"workload": "MoE dispatch P=8, 256 tokens x 4096 bf16 per rank, GPU routing on a compute stream, "
+                       f"triggered exchange on {8 * per_xcd} CUs"}
+    with H.Comm(P, device=0) as c:
+        dyn_c = c.bind_alltoallv_dynamic(send, d_counts, recv, D, stream=cs)
+
+        def eager():
+            route()
+            counts = d_counts.cpu().numpy().reshape(P, P)   # waits for the compute stream
+            sd = np.zeros((P, P), np.int64)
+            rd = np.zeros((P, P), np.int64)
+            sd[:, 1:] = np.cumsum(counts, axis=1)[:, :-1] * D
+            rd[:, 1:] = np.cumsum(counts.T, axis=1)[:, :-1] * D
+            H.hccl_alltoallv(c.handle, send, counts * D, sd, recv, counts.T * D, rd, "bf16", stream=cs)
+
+        def timed(body, exposed, pre=None):
+            wall, exp = [], []
+            for i in range(warmup + iters):
+                if pre:
+                    pre(i)   # enqueued ahead of the compute work, outside the timed region
+                time.sleep(0.0002)
+                t0 = time.perf_counter()
+                e = body(i)
+                torch.cuda.synchronize()
+                if i >= warmup:
+                    wall.append((time.perf_counter() - t0) * 1e6)
+                    if exposed:
+                        exp.append(e[0].elapsed_time(e[1]) * 1e3)
+            return statistics.median(wall), (statistics.median(exp) if exp else None)
+
+        def run_eager(i):
+            with torch.cuda.stream(cs):
+                eager()
+
+        def run_resident(i):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            with torch.cuda.stream(cs):
+                route()
+                a.record(cs)
+                dyn_c()
+                b.record(cs)
+            return a, b
+
+        seq = [0]
+        dyn_m = c.bind_alltoallv_dynamic(send, d_counts, recv, D, stream=ms)
+
+        def prelaunch(i):
+            torch.cuda.synchronize()
+            seq[0] += 1
+            v = seq[0]
+            H.hccl_set_trigger(c.handle, (flag, "ge", v), (done, v) if done_word else None)
+            dyn_m()   # the exchange is resident and waiting before routing starts
+
+        def run_triggered(i):
+            v = seq[0]
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            with torch.cuda.stream(cs):
+                route()
+                flag.fill_(v)
+                a.record(cs)
+            b.record(ms)
+            return a, b
+
+        out["eager_wall_us"], _ = timed(run_eager, False)
+        out["resident_wall_us"], out["resident_exposed_us"] = timed(run_resident, True)
+        out["triggered_wall_us"], out["triggered_exposed_us"] = timed(run_triggered, True, prelaunch)
+        if c.async_error() != 0:
+            raise RuntimeError(H.hccl_get_last_error())
+        if done_word and int(done.item()) != seq[0]:
+            raise RuntimeError("completion word not written")
+    route_only = []
+    for i in range(warmup + iters):
+        torch.cuda.synchronize()
+        time.sleep(0.0002)
+        t0 = time.perf_counter()
+        with torch.cuda.stream(cs):
+            route()
+        torch.cuda.synchronize()
+        if i >= warmup:
+            route_only.append((time.perf_counter() - t0) * 1e6)
+    out["route_only_wall_us"] = statistics.median(route_only)
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    torch.cuda.synchronize()
+    hip.hipStreamDestroy(h.value)
+    return out
+
+
 # ---------------------------------------------------------------------- CPU baseline
 def cpu_baseline(w, budget_s=12.0):
     """The oracle's AllToAllv on the host cores (single-threaded C), same inputs."""
@@ -577,7 +707,8 @@ def main():
     if args.dynamic_only:
         w = alltoallv_workload(device)
         print(json.dumps({"alltoallv_dynamic_rows_ids_p8": bench_dynamic_alltoallv(device, w),
-                          "moe_dispatch_p8": bench_moe_dispatch(device)}), flush=True)
+                          "moe_dispatch_p8": bench_moe_dispatch(device),
+                          "moe_dispatch_triggered_p8": bench_triggered_dispatch(device)}), flush=True)
         return
 
     head, w = run_headline(args, device)
@@ -634,6 +765,8 @@ def main():
         extras["alltoallv_dynamic_rows_ids_p8"] = bench_dynamic_alltoallv(device, w)
         _log("moe dispatch: device-resident vs eager")
         extras["moe_dispatch_p8"] = bench_moe_dispatch(device)
+        _log("moe dispatch: device-triggered")
+        extras["moe_dispatch_triggered_p8"] = bench_triggered_dispatch(device)
         line["collectives"] = extras
     if not args.no_cpu_baseline:
         _log("cpu baseline")

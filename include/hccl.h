@@ -214,7 +214,9 @@ hcclResult_t hccl_group_end(hcclComm_t comm);
  *   communicator's timeout ends the launch with hcclTimeout from hccl_get_async_error; outputs
  *   are then unspecified and the completion word is not written.
  * done_addr (device memory, 8-byte aligned, or NULL): done_value is stored there with a
- *   system-scope release once every step has finished and its results are visible device-wide.
+ *   system-scope release once every step has finished and its results are visible device-wide
+ *   (by a one-thread kernel enqueued right behind the executor on the same stream); it is not
+ *   written when the launch recorded an error.
  * The two words must not overlap any buffer of the collective.
  */
 typedef enum { hcclCmpEq = 0, hcclCmpNe = 1, hcclCmpGe = 2, hcclCmpGt = 3, hcclCmpLe = 4, hcclCmpLt = 5 } hcclCmp_t;

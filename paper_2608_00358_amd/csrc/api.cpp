@@ -25,6 +25,7 @@ namespace hccl {
 hipError_t launch_executor(const LaunchArgs& a, uint32_t blocks, int kind, hipStream_t stream);
 hipError_t launch_executor_inline(const InlineArgs& a, uint32_t blocks, int kind, hipStream_t stream);
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t stream);
+hipError_t launch_signal(uint64_t* word, uint64_t value, const ErrorRecord* err, hipStream_t stream);
 hipError_t executor_occupancy(int kind, int* blocks_per_cu);
 int executor_waves_per_block();
 }  // namespace hccl
@@ -321,10 +322,8 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         a.wait_addr = trig.wait_addr;
         a.wait_value = trig.wait_value;
         a.wait_cmp = (uint32_t)trig.wait_cmp;
-        a.done_addr = trig.done_addr;
-        a.done_value = trig.done_value;
     }
-    const bool signals = a.done_addr != nullptr;
+    const bool signals = triggered && trig.done_addr != nullptr;
 
     const uint32_t wpb = (uint32_t)executor_waves_per_block();
     uint32_t cus = stream_cu_count(c, s);
@@ -373,7 +372,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
 
     // a program's counters serve one launch at a time, and the communicator's scratch one
     // program at a time: order such launches across streams
-    const bool stateful = has_deps || a.dynamic != 0 || signals;
+    const bool stateful = has_deps || a.dynamic != 0;
     const bool scratch = dp->prog.scratch_bytes > 0;
     if (stateful && dp->launched && dp->last_stream != s) {
         hipError_t e = hipStreamWaitEvent(s, dp->done, 0);
@@ -385,6 +384,10 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     }
     hipError_t e = launch_executor(a, blocks, kind, s);
     if (e != hipSuccess) return hip_fail(e, "executor launch");
+    if (signals) {
+        e = launch_signal(trig.done_addr, trig.done_value, c->d_error, s);
+        if (e != hipSuccess) return hip_fail(e, "completion word");
+    }
     if (stateful) {
         e = hipEventRecord(dp->done, s);
         if (e != hipSuccess) return hip_fail(e, "completion event");

@@ -200,12 +200,9 @@ struct LaunchArgs {
                              // w + nworkers, ... (counters used only by dependencies)
     uint64_t timeout_ticks;  // watchdog for one dependency wait, in wall-clock counter ticks
     // Device trigger (Section IV-B-3): no tile starts before (*wait_addr CMP wait_value) holds
-    // (wait_addr NULL: start at once); done_value is written to done_addr (if not NULL) once
-    // every tile has finished and its stores are visible.
+    // (wait_addr NULL: start at once). The completion word is set by a kernel of its own.
     const uint64_t* wait_addr;
     uint64_t wait_value;
-    uint64_t* done_addr;
-    uint64_t done_value;
     uint32_t wait_cmp;       // TriggerCmp
     uint32_t pad;
     char* bufs[kMaxBuffers];
