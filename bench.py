@@ -672,6 +672,8 @@ def main():
     ap.add_argument("--latency-only", action="store_true", help="only the 64 KiB all-reduce latency test")
     ap.add_argument("--dynamic-only", action="store_true",
                     help="only the AllToAllvDynamic measurements (headline exchange, MoE dispatch)")
+    ap.add_argument("--dynamic-exchange-only", action="store_true",
+                    help="only the AllToAllvDynamic form of the headline exchange")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run torch's device copy of 1 GiB (the known-size kernel that scales "
                          "the FETCH_SIZE / WRITE_SIZE counters)")
@@ -702,6 +704,11 @@ def main():
 
     if args.latency_only:
         print(json.dumps(bench_latency_c5b(device)), flush=True)
+        return
+
+    if args.dynamic_exchange_only:
+        w = alltoallv_workload(device)
+        print(json.dumps({"alltoallv_dynamic_rows_ids_p8": bench_dynamic_alltoallv(device, w)}), flush=True)
         return
 
     if args.dynamic_only:
