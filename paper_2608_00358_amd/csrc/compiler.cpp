@@ -952,7 +952,9 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     }
     p.descs = std::move(live);
 
-    // one tile size for the whole program, so per-tile dependencies line up
+    // One tile size for a program with dependencies, so per-tile dependencies line up; without
+    // them every step gets the tile size for its own element width (the bf16 rows of a group
+    // with int32 ids keep 8 KiB tiles instead of taking the ids' element count).
     uint64_t max_bpe = 1, total_elems = 0;
     bool any_reduce = false, any_deps = false;
     for (const auto& d : p.descs) {
@@ -972,6 +974,16 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     te = std::max<uint64_t>(te, kWaveStepElems);
     te = std::min<uint64_t>(te, 1ull << 30);
     p.tile_elems = (uint32_t)te;
+    auto step_tile = [&](const HostDesc& h) -> uint64_t {
+        if (any_deps || tile_bytes) return te;
+        uint64_t bpe = 0;
+        for (const Operand& o : h.srcs) bpe += dtype_size(o.dtype);
+        if (bpe == 0) return te;
+        uint64_t t = (tb / bpe) / kWaveStepElems * kWaveStepElems;
+        if (any_reduce) t = std::max<uint64_t>(t, kMinReduceTileElems);
+        t = std::min<uint64_t>(t, total_elems / kSmallTargetTiles / kWaveStepElems * kWaveStepElems);
+        return std::min<uint64_t>(std::max<uint64_t>(t, kWaveStepElems), 1ull << 30);
+    };
 
     const uint32_t nd = (uint32_t)p.descs.size();
     std::vector<Desc> out(nd);
@@ -994,9 +1006,10 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
         d.nelem = h.nelem;
         d.fold = h.fold;
         d.requant = h.requant ? 1u : 0u;
-        d.tile_elems = p.tile_elems;
+        const uint64_t dte = step_tile(h);
+        d.tile_elems = (uint32_t)dte;
         d.aux = h.aux;
-        uint64_t nt = (h.op == OP_NOOP) ? 1 : (h.nelem + te - 1) / te;
+        uint64_t nt = (h.op == OP_NOOP) ? 1 : (h.nelem + dte - 1) / dte;
         if (h.op == OP_DYN_COPY) {
             if (h.aux >= p.aux.size()) {
                 err = "dynamic step without its record";

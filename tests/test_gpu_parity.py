@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import paper_2608_00358_amd as H
-from gpu_helpers import Guarded, same_bits, first_mismatch, to_device, to_host
+from gpu_helpers import GUARD, Guarded, same_bits, first_mismatch, to_device, to_host
 from workloads import alltoallv_layout, normal_bf16, normal_f32, row_ids_int32, uniform_f32, zipf_counts
 
 pytestmark = pytest.mark.gpu
@@ -353,3 +353,30 @@ def test_group_of_dependent_programs_with_scratch(fuse):
         assert same_bits(oa[r].result(), wa[r], "bf16") and oa[r].guards_intact()
         assert same_bits(ob[r].result(), wb[r], "bf16") and ob[r].guards_intact()
         assert np.array_equal(oc[r].result().view(np.uint8), wc[r].view(np.uint8)) and oc[r].guards_intact()
+
+
+@pytest.mark.parametrize("es_dt", ["bf16", "int32"])
+def test_copy_every_source_and_destination_alignment(es_dt):
+    """Every (source, destination) byte offset modulo 16 and lengths around the 16-byte and
+    wavefront boundaries, as one-rank AllToAllv copies (the offsets set the alignments)."""
+    es = 2 if es_dt == "bf16" else 4
+    per = 16 // es
+    lengths = [1, 2, per - 1, per, per + 1, 3 * per + 1, 64 * per - 1, 64 * per, 64 * per + 3, 131 * per + 5,
+               1000]
+    print(f"copy alignments dt={es_dt}", flush=True)
+    rng = np.random.default_rng(es)
+    with H.Comm(1, device=0, tile_bytes=2048) as c:
+        for n in lengths:
+            for so in range(per):
+                for ro in range(per):
+                    src = rng.integers(0, 1 << 15, size=so + n + per).astype(np.uint16 if es == 2 else np.int32)
+                    send = to_device(src, es_dt)
+                    out = Guarded(ro + n + per, es_dt)
+                    H.hccl_alltoallv(c.handle, [send], [n], [so], [out.view], [n], [ro], es_dt)
+                    torch.cuda.synchronize()
+                    got = out.result()
+                    want = out.host_init[GUARD:GUARD + ro + n + per].copy()
+                    want[ro:ro + n] = src[so:so + n]
+                    assert np.array_equal(got.view(np.uint8), want.view(np.uint8)), (n, so, ro)
+                    assert out.guards_intact(), (n, so, ro)
+        assert c.async_error() == 0
