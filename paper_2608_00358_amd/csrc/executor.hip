@@ -2,16 +2,18 @@
 //
 // One launch runs one program (the single-GPU form of a work packet; paper, Section III-B).
 // Every wavefront is an independent worker, the analogue of a message engine's control core
-// (Section II-A-2: fetch the graph, evaluate dependencies, issue the work): it takes a tile
-// ticket, waits for the tile's dependencies, performs the copy or reduction of the tile with
-// 128-bit coalesced loads and stores (the near-memory-compute analogue: FP32 arithmetic,
-// one rounding to the buffer type), and signals completion with monotonically growing
-// counters (the signal pairs of Section III-B).
+// (Section II-A-2: fetch the graph, evaluate dependencies, issue the work): it runs tiles w,
+// w + W, ... of the program (or takes them by ticket on request), waits for each tile's
+// dependencies, performs the copy or reduction of the tile with 128-bit coalesced loads and
+// stores (the near-memory-compute analogue: FP32 arithmetic, one rounding to the buffer type),
+// and signals completion with monotonically growing counters (the signal pairs of Section
+// III-B). A launch may first wait on a trigger word (Section IV-B-3), and an AllToAllvDynamic
+// step plans its layout on the device (Section IV-B-2).
 //
 // Memory model: dependency counters are written with agent-scope release and read with
 // agent-scope acquire, so a consumer on another XCD (each XCD has its own L2) sees the
-// producer's data. Programs without dependencies use no counters at all: wavefront w runs
-// tiles w, w + W, ... and nothing is shared between wavefronts.
+// producer's data. Programs without dependencies use no counters at all and nothing is shared
+// between wavefronts.
 #include <hip/hip_runtime.h>
 
 #include <stddef.h>
@@ -673,7 +675,7 @@ __device__ __forceinline__ bool wait_deps(const Dep* deps, uint32_t ndep, uint32
 }
 
 // ----------------------------------------------------------------------- the kernel
-// Runs tile `t`. Returns false when a dependency wait failed.
+// What every tile of a launch shares.
 struct Shared {
     uint32_t* state;
     ErrorRecord* error;

@@ -74,3 +74,36 @@ def test_dynamic_alltoallv_repeated_launches(mode):
             assert oracle.alltoallv_dynamic([x[s] for s in range(P)], counts, want, R, S, cap)[0]
             for d in range(P):
                 assert np.array_equal(to_host(recv[d], "int32"), want[d]), f"launch {it} destination {d}"
+
+
+def test_triggered_dependent_program(mode):
+    """A pre-launched unfused ring all-reduce (dependent steps) released by a device word, in
+    every dispatch mode."""
+    import time
+
+    from gpu_helpers import MaskedStream, SideStream
+
+    P, N = 4, 20000
+    x = inputs(P, N, "fp32", 23)
+    src = [to_device(x[r], "fp32") for r in range(P)]
+    send = [torch.zeros(N, dtype=torch.float32, device="cuda:0") for _ in range(P)]
+    recv = [torch.empty(N, dtype=torch.float32, device="cuda:0") for _ in range(P)]
+    flag = torch.zeros(1, dtype=torch.int64, device="cuda:0")
+    done = torch.zeros(1, dtype=torch.int64, device="cuda:0")
+    torch.cuda.synchronize()
+    print(f"dispatch={mode} triggered unfused ring", flush=True)
+    with MaskedStream(2) as s, SideStream() as cs, H.Comm(P, device=0, algo="ring", fuse=0, **SMALL) as c:
+        with c.triggered(wait=(flag, "eq", 3), done=(done, 4)):
+            H.hccl_allreduce(c.handle, send, recv, N, "fp32", stream=s)
+        time.sleep(0.01)
+        with torch.cuda.stream(cs):
+            for r in range(P):
+                send[r].copy_(src[r])
+            flag.fill_(3)
+        cs.synchronize()
+        s.synchronize()
+        assert c.async_error() == 0
+    assert int(done.item()) == 4
+    want = oracle.allreduce(x, "fp32")
+    for r in range(P):
+        assert same_bits(to_host(recv[r], "fp32"), want[r], "fp32")

@@ -274,3 +274,30 @@ def test_error_is_reported_once_then_the_communicator_works_again():
     assert oracle.alltoallv_dynamic([x[s] for s in range(P)], counts, want, R, 10, 10)[0]
     for d in range(P):
         assert np.array_equal(to_host(recv[d], "fp32"), want[d])
+
+
+def test_dynamic_exchange_grouped_with_a_reduction_runs_on_the_generic_kernel():
+    """A group holding a reduction and a dynamic exchange compiles to the generic executor,
+    which carries the dynamic slots too."""
+    P, R, S = 4, 8, 50
+    cap = P * S
+    x = inputs(P, S * R, "fp16", 41)
+    send = [to_device(x[s], "fp16") for s in range(P)]
+    recv = [torch.zeros(cap * R, dtype=torch.float16, device="cuda:0") for _ in range(P)]
+    counts = random_counts(P, 12, seed=41)
+    y = inputs(P, 3001, "bf16", 42)
+    ar_send = [to_device(y[r], "bf16") for r in range(P)]
+    ar_recv = [torch.empty(3001, dtype=torch.bfloat16, device="cuda:0") for _ in range(P)]
+    with H.Comm(P, device=0) as c:
+        with c.group():
+            c.allreduce(ar_send, ar_recv, op="max")
+            c.alltoallv_dynamic(send, dev_i64(counts), recv, R)
+        torch.cuda.synchronize()
+        assert c.async_error() == 0
+    want = [np.zeros(cap * R, np.uint16) for _ in range(P)]
+    assert oracle.alltoallv_dynamic([x[s] for s in range(P)], counts, want, R, S, cap)[0]
+    for d in range(P):
+        assert np.array_equal(to_host(recv[d], "fp16"), want[d]), f"destination {d}"
+    want_ar = oracle.allreduce(y, "bf16", op="max")
+    for r in range(P):
+        assert np.array_equal(to_host(ar_recv[r], "bf16"), want_ar[r])
