@@ -900,6 +900,91 @@ __device__ __forceinline__ void dyn_slot(const DynView& a, uint32_t k, const uin
     }
 }
 
+// Slot k of an AllToAllvDynamic with P*P <= 64 (P <= 8): lane l stands for the pair
+// (s, d) = (l / P, l % P), so one load brings the whole count matrix into registers; row and
+// column sums, the packed offsets and the overlap checks are P shuffles each, and the tiles
+// are found with one scan, with no further loads. Same rules and results as dyn_slot.
+template <int KIND, bool ES, bool ER>
+__device__ __forceinline__ void dyn_slot_small(const DynView& a, uint32_t k, const uint64_t* bufs, ErrorRecord* err,
+                                               uint32_t desc, uint32_t lane) {
+    const uint32_t P = a.P, PP = a.P * a.P;
+    const bool on = lane < PP;
+    const uint32_t s = on ? lane / P : 0u, d = on ? lane % P : 0u;
+    const uint64_t R = a.row_elems, te = a.tile_elems;
+    const uint64_t cmax = a.send_cap < a.recv_cap ? a.send_cap : a.recv_cap;
+    const int64_t* counts = (const int64_t*)uni64(bufs[a.counts]);
+    const int64_t cx = on ? counts[lane] : 0;
+    bool bad = on && (cx < 0 || (uint64_t)cx > cmax);
+    const uint64_t c = (on && !bad) ? (uint64_t)cx : 0;  // at most 2^59: sums of 8 cannot wrap
+    uint64_t row = 0, col = 0, row_before = 0, col_before = 0;
+    for (uint32_t j = 0; j < P; ++j) {
+        const uint64_t cr = __shfl(c, (int)(s * P + j));  // pair (s, j)
+        const uint64_t cc = __shfl(c, (int)(j * P + d));  // pair (j, d)
+        row += cr;
+        col += cc;
+        if (j < d) row_before += cr;
+        if (j < s) col_before += cc;
+    }
+    uint64_t so, ro;
+    if constexpr (ES) {
+        const int64_t x = on ? ((const int64_t*)uni64(bufs[a.sdispls]))[lane] : 0;
+        if (c && (x < 0 || (uint64_t)x > a.send_cap || c > a.send_cap - (uint64_t)x)) bad = true;
+        so = (uint64_t)x;
+    } else {
+        if (on && row > a.send_cap) bad = true;  // a packed source fits iff its total fits
+        so = row_before;
+    }
+    if constexpr (ER) {
+        const int64_t x = on ? ((const int64_t*)uni64(bufs[a.rdispls]))[(uint64_t)d * P + s] : 0;
+        if (c && (x < 0 || (uint64_t)x > a.recv_cap || c > a.recv_cap - (uint64_t)x)) bad = true;
+        ro = (uint64_t)x;
+        // the other sources of destination d (an out-of-bounds range has already failed)
+        for (uint32_t j = 0; j < P; ++j) {
+            const uint64_t cj = __shfl(c, (int)(j * P + d)), rj = __shfl(ro, (int)(j * P + d));
+            if (j != s && c && cj && ro < rj + cj && rj < ro + c) bad = true;
+        }
+    } else {
+        if (on && col > a.recv_cap) bad = true;
+        ro = col_before;
+    }
+    const bool rejected = __ballot(bad) != 0ull;
+    if (k == 0) {
+        if (a.recvcounts != kNoBuffer && on) ((int64_t*)uni64(bufs[a.recvcounts]))[(uint64_t)d * P + s] = cx;
+        if (rejected && lane == 0) {
+            uint32_t zero = 0;
+            if (__hip_atomic_compare_exchange_strong(&err->code, &zero, 2u, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT)) {
+                __hip_atomic_store(&err->desc, desc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&err->tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    }
+    if (rejected) return;  // move nothing
+
+    const uint64_t ne = c * R;
+    const uint64_t incl = wave_scan_incl((ne + te - 1) / te, lane);  // tiles of pairs 0..l
+    const uint64_t J = from_lane(incl, kWaveSize - 1);
+    const uint64_t j0 = (uint64_t)k * J / a.slots, j1 = (uint64_t)(k + 1) * J / a.slots;
+    const uint64_t send_elems = a.send_cap * R, recv_elems = a.recv_cap * R;
+    TileOps ops;
+    ops.nsrc = 1;
+    ops.ndst = 1;
+    ops.group = 0;
+    for (uint64_t j = j0; j < j1; ++j) {
+        const uint32_t pr = (uint32_t)__popcll(__ballot(incl <= j));  // j < J, so pr < P*P
+        if (pr >= PP) break;
+        const uint64_t t = j - (pr ? from_lane(incl, pr - 1) : 0);
+        const uint64_t e0 = t * te, n_pair = from_lane(ne, pr);
+        const uint32_t n = (uint32_t)((n_pair - e0 < te) ? (n_pair - e0) : te);
+        const uint64_t sod = from_lane(so, pr), rod = from_lane(ro, pr);
+        if (sod > a.send_cap || rod > a.recv_cap || sod * R + e0 + n > send_elems || rod * R + e0 + n > recv_elems)
+            continue;  // only a caller race on the metadata gets here
+        ops.src = uni64(bufs[a.send0 + pr / P]) + (sod * R + e0) * a.es;
+        ops.dst = uni64(bufs[a.recv0 + pr % P]) + (rod * R + e0) * a.es;
+        exec_tile<KIND>(OP_COPY, 0, 0, a.es, ops, n, false, lane);
+    }
+}
+
 template <int KIND>
 __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, const ProgramHeader& h, uint32_t t,
                                          uint32_t lane, const uint64_t* bufs) {
@@ -924,10 +1009,24 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
         if constexpr (KIND == kKindDynamic || KIND == kKindGeneric) {
             const DynView v = load_dyn((const DynA2A*)(prog + h.off_aux) + uni(D->aux));
             const bool es = v.sdispls != kNoBuffer, er = v.rdispls != kNoBuffer;
-            if (!es && !er) dyn_slot<KIND, false, false>(v, k, bufs, a.error, d, lane);
-            else if (es && !er) dyn_slot<KIND, true, false>(v, k, bufs, a.error, d, lane);
-            else if (!es) dyn_slot<KIND, false, true>(v, k, bufs, a.error, d, lane);
-            else dyn_slot<KIND, true, true>(v, k, bufs, a.error, d, lane);
+            // the register-resident planner only in the dynamic kernel: the generic one carries
+            // every other path already, and the general planner covers every P
+            bool small = false;
+            if constexpr (KIND == kKindDynamic) {
+                small = v.P * v.P <= (uint32_t)kWaveSize;
+                if (small) {
+                    if (!es && !er) dyn_slot_small<KIND, false, false>(v, k, bufs, a.error, d, lane);
+                    else if (es && !er) dyn_slot_small<KIND, true, false>(v, k, bufs, a.error, d, lane);
+                    else if (!es) dyn_slot_small<KIND, false, true>(v, k, bufs, a.error, d, lane);
+                    else dyn_slot_small<KIND, true, true>(v, k, bufs, a.error, d, lane);
+                }
+            }
+            if (!small) {
+                if (!es && !er) dyn_slot<KIND, false, false>(v, k, bufs, a.error, d, lane);
+                else if (es && !er) dyn_slot<KIND, true, false>(v, k, bufs, a.error, d, lane);
+                else if (!es) dyn_slot<KIND, false, true>(v, k, bufs, a.error, d, lane);
+                else dyn_slot<KIND, true, true>(v, k, bufs, a.error, d, lane);
+            }
         }
     } else if (op != OP_NOOP) {
         TileOps ops;
