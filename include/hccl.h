@@ -25,6 +25,15 @@
  *
  * Calls on one communicator must not run concurrently from several host threads. Calls
  * may be issued on different streams: the library orders a program's launches by itself.
+ *
+ * Graph capture: a call (or group) whose program is already compiled enqueues kernel launches
+ * only, so it may be made on a stream that is capturing a HIP graph. The first call of a given
+ * shape compiles and uploads its program and may grow the communicator's scratch; made under
+ * capture it fails with hcclUnsupported and enqueues nothing, so make it once outside the
+ * capture first. A graph records the device addresses of the program and the scratch it used;
+ * the communicator keeps both allocated until hccl_comm_destroy, after which the graph must
+ * not be launched. Launches inside a graph are not ordered by the library against launches of
+ * the same program on other streams: the caller orders graph launches against such work.
  */
 #ifndef HCCL_H
 #define HCCL_H

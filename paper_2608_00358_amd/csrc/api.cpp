@@ -61,6 +61,7 @@ struct DeviceProgram {
     hipEvent_t done = nullptr;       // recorded after each launch
     hipStream_t last_stream = nullptr;
     bool launched = false;
+    bool captured = false;           // a graph holds its image and state: never freed before the communicator
     double compile_us = 0;
 };
 
@@ -79,7 +80,10 @@ struct hcclComm {
     hipEvent_t scratch_done = nullptr;  // recorded after each launch that uses the scratch
     hipStream_t scratch_stream = nullptr;
     bool scratch_launched = false;
+    bool scratch_captured = false;      // a graph holds d_scratch: growth keeps the old allocation
+    std::vector<void*> retired_scratch;
     std::list<std::unique_ptr<DeviceProgram>> cache;  // most recently used first
+    std::vector<std::unique_ptr<DeviceProgram>> retired;  // evicted programs that a graph holds
     size_t cache_limit = 64;
     bool dynamic_dispatch = false;  // tickets also for programs without dependencies
     bool inline_single_step = true;  // one-step programs travel in the launch packet
@@ -156,7 +160,10 @@ hcclResult_t check_buffers(const std::vector<Range>& v, size_t es, Allow allow) 
 
 // Compiles (or finds in the cache) the program of one work packet: one collective, or the
 // collectives of a group, merged into one program whose steps use disjoint buffer ids.
-hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& specs, DeviceProgram*& out, bool& hit) {
+// `may_compile` is false while the stream is being captured into a graph: compiling uploads
+// the image with a synchronous copy, which a capture does not allow.
+hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& specs, DeviceProgram*& out, bool& hit,
+                             bool may_compile) {
     for (auto it = c->cache.begin(); it != c->cache.end(); ++it) {
         if ((*it)->specs == specs) {
             if (it != c->cache.begin()) c->cache.splice(c->cache.begin(), c->cache, it);
@@ -166,6 +173,9 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
         }
     }
     hit = false;
+    if (!may_compile)
+        return fail(hcclUnsupported, "the stream is capturing a graph and this program is not compiled yet: "
+                                     "make the same call once outside the capture first");
     auto t0 = std::chrono::steady_clock::now();
     auto dp = std::make_unique<DeviceProgram>();
     dp->specs = specs;
@@ -213,7 +223,10 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
     }
     c->cache.push_front(std::move(dp));
     while (c->cache.size() > c->cache_limit) {
-        free_program(c->cache.back().get());
+        if (c->cache.back()->captured)
+            c->retired.push_back(std::move(c->cache.back()));
+        else
+            free_program(c->cache.back().get());
         c->cache.pop_back();
     }
     out = c->cache.front().get();
@@ -224,8 +237,12 @@ hcclResult_t ensure_scratch(hcclComm* c, uint64_t bytes) {
     if (bytes <= c->scratch_bytes) return hcclSuccess;
     hipError_t e = hipDeviceSynchronize();  // the old scratch may still be in use
     if (e != hipSuccess) return hip_fail(e, "synchronize before scratch growth");
-    if (c->d_scratch) (void)hipFree(c->d_scratch);
+    if (c->d_scratch && c->scratch_captured)
+        c->retired_scratch.push_back(c->d_scratch);
+    else if (c->d_scratch)
+        (void)hipFree(c->d_scratch);
     c->d_scratch = nullptr;
+    c->scratch_captured = false;
     c->scratch_bytes = 0;
     e = hipMalloc(&c->d_scratch, bytes);
     if (e != hipSuccess) return fail(hcclOutOfMemory, "scratch allocation failed");
@@ -254,7 +271,18 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     const bool triggered = c->has_trigger;
     const hcclTrigger_t trig = c->trigger;
     c->has_trigger = false;
-    hcclResult_t r = compile_program(c, specs, dp, hit);
+    // Under graph capture the packet may only enqueue: kernel launches on the capturing stream.
+    // (The null stream is never captured, and querying it during another stream's capture is
+    // itself an error, so it is not asked.)
+    hipStream_t s = calls[0].stream;
+    bool capturing = false;
+    if (c->device != HCCL_NO_DEVICE && s) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(s, &cs);
+        if (e != hipSuccess) return hip_fail(e, "stream capture query");
+        capturing = cs != hipStreamCaptureStatusNone;
+    }
+    hcclResult_t r = compile_program(c, specs, dp, hit, !capturing);
     if (r != hcclSuccess) return r;
 
     hcclProgramInfo_t& info = c->last;
@@ -291,10 +319,16 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     }
     if (c->device == HCCL_NO_DEVICE || dp->prog.ntiles == 0) return hcclSuccess;
 
+    if (capturing && dp->prog.scratch_bytes > c->scratch_bytes)
+        return fail(hcclUnsupported, "the stream is capturing a graph and the communicator's scratch must grow: "
+                                     "make the same call once outside the capture first");
     r = ensure_scratch(c, dp->prog.scratch_bytes);
     if (r != hcclSuccess) return r;
+    if (capturing) {  // the graph keeps this image, state and scratch address
+        dp->captured = true;
+        if (dp->prog.scratch_bytes > 0) c->scratch_captured = true;
+    }
 
-    hipStream_t s = calls[0].stream;
     LaunchArgs a;
     std::memset(&a, 0, sizeof a);
     a.prog = dp->d_image;
@@ -371,9 +405,13 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     }
 
     // a program's counters serve one launch at a time, and the communicator's scratch one
-    // program at a time: order such launches across streams
-    const bool stateful = has_deps || a.dynamic != 0;
-    const bool scratch = dp->prog.scratch_bytes > 0;
+    // program at a time: order such launches across streams. A captured launch is left out of
+    // this bookkeeping: an event recorded outside a capture cannot be waited on inside it, and
+    // one recorded inside stands for a graph node, not for a launch. Replays run in the order
+    // of the stream they are launched on; the caller orders them against eager launches of the
+    // same program, or of programs that use scratch, on other streams.
+    const bool stateful = (has_deps || a.dynamic != 0) && !capturing;
+    const bool scratch = dp->prog.scratch_bytes > 0 && !capturing;
     if (stateful && dp->launched && dp->last_stream != s) {
         hipError_t e = hipStreamWaitEvent(s, dp->done, 0);
         if (e != hipSuccess) return hip_fail(e, "cross-stream ordering");
@@ -505,8 +543,11 @@ hcclResult_t hccl_comm_destroy(hcclComm_t comm) {
         DeviceGuard guard(comm->device);
         if (comm->device != HCCL_NO_DEVICE) (void)hipDeviceSynchronize();
         for (auto& p : comm->cache) free_program(p.get());
+        for (auto& p : comm->retired) free_program(p.get());
         comm->cache.clear();
+        comm->retired.clear();
         if (comm->d_scratch) (void)hipFree(comm->d_scratch);
+        for (void* p : comm->retired_scratch) (void)hipFree(p);
         if (comm->d_error) (void)hipFree(comm->d_error);
         if (comm->scratch_done) (void)hipEventDestroy(comm->scratch_done);
     }
