@@ -284,6 +284,59 @@ def bench_latency_c5b(device, warmup=100, iters=1000, isolated=200):
             "tiles": info["num_tiles"]}
 
 
+def bench_resident_c5b(device, blocks=0, warmup=200, iters=1000):
+    """The same 64 KiB all-reduce handed to the resident executor through the host doorbell:
+    host round trip (submit, then poll pinned memory until the packet is reported complete) and
+    back-to-back rate (submit `iters` packets, then wait for the last), beside the launched
+    kernel's round trip (launch, then synchronise the stream)."""
+    import torch
+
+    import paper_2608_00358_amd as H
+    from workloads import uniform_f32
+
+    P, N = 8, 1 << 14
+    x = uniform_f32(P, N, seed=5)
+    send = [torch.from_numpy(x[r].copy()).to(device) for r in range(P)]
+    recv = [torch.empty(N, dtype=torch.float32, device=device) for _ in range(P)]
+    s = torch.cuda.current_stream()
+    with H.Comm(P, device=0, algo="direct") as c:
+        call = c.bind_allreduce(send, recv)
+        for _ in range(warmup):
+            call()
+        torch.cuda.synchronize()
+        launched = []
+        for _ in range(iters):
+            t0 = time.perf_counter()
+            call()
+            s.synchronize()
+            launched.append((time.perf_counter() - t0) * 1e6)
+        with c.resident(blocks=blocks, idle_ms=20000):
+            for _ in range(warmup):
+                call()
+            c.resident_wait(timeout_ms=10000)
+            rt = []
+            for _ in range(iters):
+                t0 = time.perf_counter()
+                call()
+                c.resident_wait()
+                rt.append((time.perf_counter() - t0) * 1e6)
+            t0 = time.perf_counter()
+            for _ in range(iters):
+                call()
+            c.resident_wait(timeout_ms=10000)
+            b2b = (time.perf_counter() - t0) * 1e6 / iters
+            t0 = time.perf_counter()
+            for _ in range(iters):
+                H.hccl_resident_last_seq(c.handle)     # the cost of one ctypes call, for scale
+            ctypes_us = (time.perf_counter() - t0) * 1e6 / iters
+    return {"workload": "allreduce direct P=8 64KiB/rank fp32, resident executor",
+            "blocks": blocks or 32, "resident_roundtrip_median_us": statistics.median(rt),
+            "resident_roundtrip_p99_us": sorted(rt)[int(0.99 * len(rt))],
+            "resident_back_to_back_us": b2b,
+            "launched_roundtrip_median_us": statistics.median(launched),
+            "ctypes_call_us": ctypes_us}
+
+
 def _cu_masked_stream(mask_words):
     """hipExtStreamCreateWithCUMask on the current device (default priority)."""
     import torch
@@ -704,6 +757,8 @@ def main():
 
     if args.latency_only:
         print(json.dumps(bench_latency_c5b(device)), flush=True)
+        for blocks in (1, 2, 4, 8, 32):
+            print(json.dumps(bench_resident_c5b(device, blocks=blocks)), flush=True)
         return
 
     if args.dynamic_exchange_only:
@@ -768,6 +823,8 @@ def main():
         extras["allreduce_two_level_p64_bf16"] = bench_two_level_c4(device)
         _log("c5b latency")
         extras["latency_allreduce_p8_64KiB_fp32"] = bench_latency_c5b(device)
+        _log("c5b latency through the resident executor")
+        extras["resident_allreduce_p8_64KiB_fp32"] = bench_resident_c5b(device)
         _log("alltoallv_dynamic")
         extras["alltoallv_dynamic_rows_ids_p8"] = bench_dynamic_alltoallv(device, w)
         _log("moe dispatch: device-resident vs eager")

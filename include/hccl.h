@@ -254,6 +254,52 @@ const char* hccl_result_string(hcclResult_t r);
  */
 hcclResult_t hccl_get_async_error(hcclComm_t comm);
 
+/*
+ * Resident executor (Section II-A-2: the message engine's control core waits for work packets
+ * and runs each as it arrives; Section V-B: once a packet is compiled and cached, handing it
+ * over again is the whole per-call cost, which the paper keeps under 10 us).
+ *
+ * hccl_resident_start launches one executor that stays on the device, on a stream of its own,
+ * and takes work packets through a doorbell: a ring of slots in coherent pinned host memory.
+ * From then until hccl_resident_stop, every call (or group) on the communicator is handed to it
+ * instead of being launched: the call writes the packet's arguments into the next slot and
+ * then the slot's sequence number (1, 2, ...), and returns. No kernel is launched per call.
+ *
+ *   blocks   workgroups of 4 wavefronts (0 = 32); they must all fit on the device at once,
+ *            else hcclInvalidArgument.
+ *   idle_ms  the executor ends by itself after this long without a packet (0 = 10 s, at most
+ *            10 minutes), so an abandoned executor cannot hold the device.
+ *
+ * In this mode the `stream` argument of a call is ignored: a packet runs when the executor
+ * reaches it, in submission order, one packet at a time. The caller makes the inputs ready
+ * (e.g. synchronises the stream that wrote them) before the call, and reads the outputs after
+ * hccl_resident_wait has reported the packet complete; outputs are then visible to the host,
+ * to copies and to kernels launched afterwards. Submitting more than 64 packets ahead of the
+ * executor blocks the call until a slot is free (or fails with hcclTimeout after the
+ * communicator's timeout). A packet whose program is not cached is compiled on the host as
+ * usual; one that would grow the communicator's scratch, a triggered packet and a call on a
+ * capturing stream fail with hcclUnsupported. Programs handed to the executor stay allocated
+ * until hccl_comm_destroy. hccl_get_async_error is not available while the executor runs.
+ * hipDeviceSynchronize (and anything that waits for every stream of the device) waits for the
+ * executor too, which ends only at hccl_resident_stop or its idle limit: synchronise streams.
+ */
+hcclResult_t hccl_resident_start(hcclComm_t comm, uint32_t blocks, uint32_t idle_ms);
+
+/* Ends the resident executor after the packets already submitted and frees its doorbell;
+ * returns once it has left the device. A no-op if it is not running. hccl_comm_destroy stops
+ * it too. Afterwards calls are launched on their streams again. */
+hcclResult_t hccl_resident_stop(hcclComm_t comm);
+
+/* Waits (on the host, polling pinned memory) until packet `seq` has completed (0 = the last
+ * one submitted). Returns hcclTimeout after `timeout_ms` (0 = 2 s) or if the executor ended
+ * before the packet ran (idle limit passed), and otherwise the first device error recorded
+ * by any completed packet since the last report (hcclInvalidArgument for a rejected
+ * device-resident layout, hcclTimeout for a dependency watchdog), which it then clears. */
+hcclResult_t hccl_resident_wait(hcclComm_t comm, uint64_t seq, uint32_t timeout_ms);
+
+/* The sequence number of the last packet handed to the resident executor (0 = none). */
+hcclResult_t hccl_resident_last_seq(hcclComm_t comm, uint64_t* seq);
+
 /* Description of the most recently compiled or reused program of a communicator. */
 typedef struct {
     int32_t collective;          /* 0 allreduce, 1 reduce_scatter, 2 allgather, 3 alltoallv,

@@ -9,5 +9,5 @@ from .hccl import (  # noqa: F401
     hccl_allgather, hccl_allreduce, hccl_alltoallv, hccl_alltoallv_dynamic, hccl_comm_create, hccl_comm_destroy,
     hccl_comm_last_program, hccl_comm_set_config, hccl_config_init, hccl_get_async_error,
     hccl_get_last_error, hccl_group_end, hccl_group_start, hccl_reduce_scatter, hccl_result_string,
-    hccl_set_trigger, load,
+    hccl_resident_last_seq, hccl_resident_start, hccl_resident_stop, hccl_resident_wait, hccl_set_trigger, load,
 )

@@ -8,7 +8,9 @@
 #include <hip/hip_ext.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
+#include <thread>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -27,6 +29,8 @@ hipError_t launch_executor_inline(const InlineArgs& a, uint32_t blocks, int kind
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t stream);
 hipError_t launch_signal(uint64_t* word, uint64_t value, const ErrorRecord* err, hipStream_t stream);
 hipError_t executor_occupancy(int kind, int* blocks_per_cu);
+hipError_t launch_resident(const ResidentArgs& r, uint32_t blocks, hipStream_t stream);
+hipError_t resident_occupancy(int* blocks_per_cu);
 int executor_waves_per_block();
 }  // namespace hccl
 
@@ -35,6 +39,10 @@ using namespace hccl;
 namespace {
 
 thread_local std::string g_last_error;
+
+constexpr uint32_t kResidentDefaultBlocks = 32;       // 128 wavefronts, 4 workgroups per XCD
+constexpr uint32_t kResidentDefaultIdleMs = 10000;
+constexpr uint32_t kResidentMaxIdleMs = 600000;
 
 hcclResult_t fail(hcclResult_t code, const std::string& msg) {
     g_last_error = msg;
@@ -92,6 +100,12 @@ struct hcclComm {
     bool has_trigger = false;        // hccl_set_trigger for the next work packet
     hcclTrigger_t trigger{};
     hcclProgramInfo_t last{};
+    // resident executor (hccl_resident_start .. hccl_resident_stop)
+    bool resident = false;
+    ResidentQueue* rq = nullptr;      // coherent pinned host memory, shared with the executor
+    uint32_t* d_ctl = nullptr;
+    hipStream_t resident_stream = nullptr;
+    uint64_t resident_seq = 0;        // last packet published
 };
 
 namespace {
@@ -214,7 +228,8 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
             return fail(hcclOutOfMemory, "program state allocation failed");
         }
         e = launch_fill_u32(dp->d_state, dp->prog.nstate, 0u, nullptr);
-        if (e == hipSuccess) e = hipDeviceSynchronize();
+        // only the fill is waited for: a resident executor on its own stream does not end by itself
+        if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&dp->done, hipEventDisableTiming);
         if (e != hipSuccess) {
             free_program(dp.get());
@@ -223,7 +238,8 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
     }
     c->cache.push_front(std::move(dp));
     while (c->cache.size() > c->cache_limit) {
-        if (c->cache.back()->captured)
+        // (a free would also wait for a running resident executor, which ends only when stopped)
+        if (c->cache.back()->captured || c->resident)
             c->retired.push_back(std::move(c->cache.back()));
         else
             free_program(c->cache.back().get());
@@ -258,6 +274,47 @@ uint32_t stream_cu_count(hcclComm* c, hipStream_t s) {
     for (uint32_t w : mask) n += (uint32_t)__builtin_popcount(w);
     if (n == 0 || n > (uint32_t)c->cus) return (uint32_t)c->cus;
     return n;
+}
+
+// ---- resident executor: host side of the doorbell
+uint64_t resident_done(const hcclComm* c) { return __atomic_load_n(&c->rq->done_seq, __ATOMIC_ACQUIRE); }
+bool resident_exited(const hcclComm* c) { return __atomic_load_n(&c->rq->exited, __ATOMIC_ACQUIRE) != 0u; }
+
+// Waits until packet `seq` has completed; fails if the executor stopped or `ms` passed first.
+hcclResult_t resident_wait_for(hcclComm* c, uint64_t seq, uint64_t ms) {
+    if (resident_done(c) >= seq) return hcclSuccess;
+    const auto t0 = std::chrono::steady_clock::now();
+    for (uint32_t spin = 0;; ++spin) {
+        if (resident_done(c) >= seq) return hcclSuccess;
+        if (resident_exited(c) && resident_done(c) < seq)
+            return fail(hcclTimeout, "the resident executor stopped before the packet completed (idle limit "
+                                     "reached, or a workgroup gave up waiting for the others)");
+        if ((spin & 1023u) == 1023u) {
+            const double el = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+            if (el > (double)ms) return fail(hcclTimeout, "the resident executor did not complete the packet in time");
+            std::this_thread::yield();
+        }
+    }
+}
+
+// Publishes one packet: its arguments into the next ring slot, then the slot's sequence number.
+hcclResult_t resident_submit(hcclComm* c, const LaunchArgs& a, DeviceProgram* dp) {
+    const uint64_t k = c->resident_seq + 1;
+    const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
+    if (resident_exited(c)) return fail(hcclTimeout, "the resident executor has stopped: restart it");
+    // the slot last held packet k - kResidentSlots, whose arguments every workgroup has read
+    // once it has completed
+    if (k > kResidentSlots) {
+        hcclResult_t r = resident_wait_for(c, k - kResidentSlots, ms);
+        if (r != hcclSuccess) return r;
+    }
+    ResidentSlot& slot = c->rq->slots[(k - 1) % kResidentSlots];
+    std::memcpy((void*)&slot.args, &a, sizeof a);
+    std::atomic_thread_fence(std::memory_order_release);
+    __atomic_store_n(&slot.seq, k, __ATOMIC_RELEASE);
+    c->resident_seq = k;
+    dp->captured = true;  // the executor may read the image after the call returns: never freed early
+    return hcclSuccess;
 }
 
 // Compiles and enqueues one work packet (a list of collective calls on one stream).
@@ -317,6 +374,14 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
             }
         }
     }
+    if (c->resident) {
+        if (triggered) return fail(hcclUnsupported, "a triggered work packet cannot go to the resident executor");
+        if (capturing)
+            return fail(hcclUnsupported, "the resident executor takes packets from the host, not from a captured stream");
+        if (dp->prog.scratch_bytes > c->scratch_bytes)
+            return fail(hcclUnsupported, "the communicator's scratch must grow, which cannot happen while the resident "
+                                         "executor runs: make the same call once before hccl_resident_start");
+    }
     if (c->device == HCCL_NO_DEVICE || dp->prog.ntiles == 0) return hcclSuccess;
 
     if (capturing && dp->prog.scratch_bytes > c->scratch_bytes)
@@ -358,6 +423,8 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         a.wait_cmp = (uint32_t)trig.wait_cmp;
     }
     const bool signals = triggered && trig.done_addr != nullptr;
+
+    if (c->resident) return resident_submit(c, a, dp);
 
     const uint32_t wpb = (uint32_t)executor_waves_per_block();
     uint32_t cus = stream_cu_count(c, s);
@@ -541,6 +608,7 @@ hcclResult_t hccl_comm_destroy(hcclComm_t comm) {
     if (!comm) return hcclSuccess;
     {
         DeviceGuard guard(comm->device);
+        (void)hccl_resident_stop(comm);
         if (comm->device != HCCL_NO_DEVICE) (void)hipDeviceSynchronize();
         for (auto& p : comm->cache) free_program(p.get());
         for (auto& p : comm->retired) free_program(p.get());
@@ -805,9 +873,36 @@ const char* hccl_result_string(hcclResult_t r) {
     return "unknown hcclResult_t";
 }
 
+namespace {
+
+// The result code and message of a device error record.
+hcclResult_t device_error(uint32_t code, uint32_t desc, uint32_t tile) {
+    char buf[200];
+    if (code == 2) {
+        std::snprintf(buf, sizeof buf,
+                      "the device-resident layout read by step %u was invalid (row or column %u): "
+                      "a count or offset left its buffer, or receive ranges overlapped; nothing was moved",
+                      desc, tile);
+        return fail(hcclInvalidArgument, buf);
+    }
+    if (code == 3) {
+        std::snprintf(buf, sizeof buf,
+                      "the trigger word did not satisfy its comparison within the watchdog limit "
+                      "(workgroup %u gave up); the collective's outputs are unspecified",
+                      tile);
+        return fail(hcclTimeout, buf);
+    }
+    std::snprintf(buf, sizeof buf, "a dependency wait of step %u (tile %u) exceeded the watchdog limit", desc, tile);
+    return fail(hcclTimeout, buf);
+}
+
+}  // namespace
+
 hcclResult_t hccl_get_async_error(hcclComm_t comm) {
     if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
     if (comm->device == HCCL_NO_DEVICE) return hcclSuccess;
+    if (comm->resident)
+        return fail(hcclInvalidArgument, "the resident executor is running: hccl_resident_wait reports its errors");
     DeviceGuard guard(comm->device);
     hipError_t e = hipDeviceSynchronize();
     if (e != hipSuccess) return hip_fail(e, "synchronize");
@@ -818,24 +913,107 @@ hcclResult_t hccl_get_async_error(hcclComm_t comm) {
     ErrorRecord cleared;
     std::memset(&cleared, 0, sizeof cleared);
     (void)hipMemcpy(comm->d_error, &cleared, sizeof cleared, hipMemcpyHostToDevice);
-    char buf[200];
-    if (rec.code == 2) {
-        std::snprintf(buf, sizeof buf,
-                      "the device-resident layout read by step %u was invalid (row or column %u): "
-                      "a count or offset left its buffer, or receive ranges overlapped; nothing was moved",
-                      rec.desc, rec.tile);
-        return fail(hcclInvalidArgument, buf);
+    return device_error(rec.code, rec.desc, rec.tile);
+}
+
+hcclResult_t hccl_resident_start(hcclComm_t comm, uint32_t blocks, uint32_t idle_ms) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (comm->device == HCCL_NO_DEVICE) return fail(hcclInvalidArgument, "the resident executor needs a device");
+    if (comm->resident) return fail(hcclInvalidArgument, "the resident executor is already running");
+    if (comm->group_depth > 0) return fail(hcclInvalidArgument, "hccl_resident_start inside a group");
+    DeviceGuard guard(comm->device);
+    int per_cu = 0;
+    hipError_t e = resident_occupancy(&per_cu);
+    if (e != hipSuccess) return hip_fail(e, "resident executor occupancy");
+    const uint32_t most = (uint32_t)comm->cus * (uint32_t)std::max(per_cu, 0);
+    if (blocks == 0) blocks = std::min<uint32_t>(kResidentDefaultBlocks, most);
+    if (blocks == 0 || blocks > most)
+        return fail(hcclInvalidArgument, "blocks must fit on the device at once (at most " + std::to_string(most) + ")");
+    if (idle_ms == 0) idle_ms = kResidentDefaultIdleMs;
+    if (idle_ms > kResidentMaxIdleMs) return fail(hcclInvalidArgument, "idle_ms is above the limit of 10 minutes");
+
+    void* q = nullptr;
+    e = hipHostMalloc(&q, sizeof(ResidentQueue), hipHostMallocCoherent | hipHostMallocMapped);
+    if (e != hipSuccess) return fail(hcclOutOfMemory, "pinned doorbell allocation failed");
+    std::memset(q, 0, sizeof(ResidentQueue));
+    void* qdev = nullptr;
+    uint32_t* ctl = nullptr;
+    hipStream_t st = nullptr;
+    e = hipHostGetDevicePointer(&qdev, q, 0);
+    // control words, then the device mirror of the published packet's arguments
+    const size_t ctl_bytes = 64 + sizeof(LaunchArgs);
+    if (e == hipSuccess) e = hipMalloc(&ctl, ctl_bytes);
+    if (e == hipSuccess) e = hipMemset(ctl, 0, ctl_bytes);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
+    ResidentArgs r;
+    std::memset(&r, 0, sizeof r);
+    r.q = (ResidentQueue*)qdev;
+    r.ctl = ctl;
+    r.mirror = (uint64_t*)((char*)ctl + 64);
+    r.error = comm->d_error;
+    r.timeout_ticks = (comm->cfg.timeout_ms ? comm->cfg.timeout_ms : 2000u) * comm->wall_clock_khz;
+    r.idle_ticks = (uint64_t)idle_ms * comm->wall_clock_khz;
+    if (e == hipSuccess) e = launch_resident(r, blocks, st);
+    if (e != hipSuccess) {
+        if (st) (void)hipStreamDestroy(st);
+        if (ctl) (void)hipFree(ctl);
+        (void)hipHostFree(q);
+        return hip_fail(e, "resident executor start");
     }
-    if (rec.code == 3) {
-        std::snprintf(buf, sizeof buf,
-                      "the trigger word did not satisfy its comparison within the watchdog limit "
-                      "(workgroup %u gave up); the collective's outputs are unspecified",
-                      rec.tile);
-        return fail(hcclTimeout, buf);
+    comm->rq = (ResidentQueue*)q;
+    comm->d_ctl = ctl;
+    comm->resident_stream = st;
+    comm->resident_seq = 0;
+    comm->resident = true;
+    return hcclSuccess;
+}
+
+hcclResult_t hccl_resident_stop(hcclComm_t comm) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (!comm->resident) return hcclSuccess;
+    DeviceGuard guard(comm->device);
+    hcclResult_t r = hcclSuccess;
+    if (!resident_exited(comm)) {
+        const uint64_t k = comm->resident_seq + 1;
+        const uint64_t ms = comm->cfg.timeout_ms ? comm->cfg.timeout_ms : 2000u;
+        if (k > kResidentSlots) r = resident_wait_for(comm, k - kResidentSlots, ms);
+        if (r == hcclSuccess) {
+            ResidentSlot& slot = comm->rq->slots[(k - 1) % kResidentSlots];
+            __atomic_store_n(&slot.seq, k | kResidentStop, __ATOMIC_RELEASE);
+        }
     }
-    std::snprintf(buf, sizeof buf, "a dependency wait of step %u (tile %u) exceeded the watchdog limit",
-                  rec.desc, rec.tile);
-    return fail(hcclTimeout, buf);
+    // every wait of the executor is bounded, so this returns
+    hipError_t e = hipStreamSynchronize(comm->resident_stream);
+    (void)hipStreamDestroy(comm->resident_stream);
+    (void)hipFree(comm->d_ctl);
+    (void)hipHostFree(comm->rq);
+    comm->resident_stream = nullptr;
+    comm->d_ctl = nullptr;
+    comm->rq = nullptr;
+    comm->resident = false;
+    if (e != hipSuccess) return hip_fail(e, "resident executor stop");
+    return r;
+}
+
+hcclResult_t hccl_resident_wait(hcclComm_t comm, uint64_t seq, uint32_t timeout_ms) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (!comm->resident) return fail(hcclInvalidArgument, "the resident executor is not running");
+    if (seq == 0) seq = comm->resident_seq;
+    if (seq > comm->resident_seq) return fail(hcclInvalidArgument, "no packet with that number was submitted");
+    hcclResult_t r = resident_wait_for(comm, seq, timeout_ms ? timeout_ms : 2000u);
+    if (r != hcclSuccess) return r;
+    const uint32_t code = __atomic_load_n(&comm->rq->error, __ATOMIC_ACQUIRE);
+    if (code == 0) return hcclSuccess;
+    const uint32_t desc = comm->rq->err_desc, tile = comm->rq->err_tile;
+    __atomic_store_n(&comm->rq->error, 0u, __ATOMIC_RELEASE);
+    return device_error(code, desc, tile);
+}
+
+hcclResult_t hccl_resident_last_seq(hcclComm_t comm, uint64_t* seq) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (!seq) return fail(hcclInvalidArgument, "null output");
+    *seq = comm->resident_seq;
+    return hcclSuccess;
 }
 
 hcclResult_t hccl_comm_last_program(hcclComm_t comm, hcclProgramInfo_t* info) {

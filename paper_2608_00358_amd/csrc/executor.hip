@@ -1210,6 +1210,189 @@ __global__ void hccl_signal(uint64_t* word, uint64_t value, const ErrorRecord* e
         __hip_atomic_store(word, value, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// ------------------------------------------------------------------ resident executor
+// An executor that stays running and takes work packets through a doorbell in host memory
+// (Section II-A-2: the message engine's control core waits for work and unrolls each packet as
+// it arrives; Section V-B: re-enqueueing a cached packet is the whole per-call cost). The host
+// writes a packet's arguments into a ring slot, then its sequence number. Workgroup 0 is the
+// relay: its thread 0 polls that number with system-scope loads, the workgroup copies the
+// arguments into a device mirror and publishes the number in device memory, so that only one
+// workgroup pays the PCIe round trips. Every workgroup then copies the arguments into LDS and
+// runs its share of the tiles exactly as a launched executor does (wavefront w takes tiles
+// w, w + W, ...). The last workgroup to finish clears the program's counters, writes the
+// results back for readers outside the GPU and stores the sequence number in host memory; the
+// relay waits for that before it takes the next packet. Every wait is bounded: the relay ends
+// the executor after `idle_ticks` without a packet, and a workgroup that waits longer than its
+// limit for the others ends too.
+__device__ __forceinline__ void backoff(uint32_t& nap, uint32_t cap) {
+    if (nap == 1) __builtin_amdgcn_s_sleep(1);
+    else if (nap == 2) __builtin_amdgcn_s_sleep(2);
+    else if (nap == 4) __builtin_amdgcn_s_sleep(4);
+    else if (nap == 8) __builtin_amdgcn_s_sleep(8);
+    else if (nap == 16) __builtin_amdgcn_s_sleep(16);
+    else __builtin_amdgcn_s_sleep(32);
+    if (nap < cap) nap *= 2;
+}
+
+// Polls a device word until it equals `want`; false after `limit` wall-clock ticks.
+__device__ __forceinline__ bool wait_word(const uint32_t* w, uint32_t want, uint64_t limit) {
+    uint32_t nap = 1;
+    const uint64_t t0 = wall_clock64();
+    while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != want) {
+        if (wall_clock64() - t0 > limit) return false;
+        backoff(nap, 4);
+    }
+    return true;
+}
+
+__global__ void __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(3)))
+hccl_resident(ResidentArgs r) {
+    static_assert(sizeof(LaunchArgs) % 8 == 0, "the packet is copied in 8-byte words");
+    constexpr uint32_t kWords = sizeof(LaunchArgs) / 8;
+    __shared__ uint64_t pk[kWords];
+    __shared__ uint32_t stop;
+    __shared__ uint32_t last_block;
+    const uint32_t lane = __lane_id();
+    const uint32_t wave = uni(blockIdx.x * kWavesPerBlock + (threadIdx.x / kWaveSize));
+    const uint32_t nworkers = gridDim.x * kWavesPerBlock;
+    const bool relay = blockIdx.x == 0;
+    uint32_t* const arrived = r.ctl;
+    uint32_t* const finished = r.ctl + 1;
+    uint32_t* const published = r.ctl + 2;
+    uint32_t* const stop_flag = r.ctl + 3;
+
+    for (uint64_t k = 1;; ++k) {
+        if (relay) {
+            ResidentSlot* slot = &r.q->slots[(k - 1) % kResidentSlots];
+            if (threadIdx.x == 0) {
+                uint32_t end = 0, nap = 1;
+                const uint64_t t0 = wall_clock64();
+                for (;;) {
+                    const uint64_t v = __hip_atomic_load(&slot->seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                    if ((v & ~kResidentStop) == k) {
+                        end = (v & kResidentStop) ? 1u : 0u;
+                        break;
+                    }
+                    if (wall_clock64() - t0 > r.idle_ticks) {
+                        end = 1;
+                        break;
+                    }
+                    backoff(nap, 4);
+                }
+                // the slot's arguments, and whatever was written to the packet's buffers before
+                // the doorbell, are visible from here on (stale cache lines are dropped)
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+                stop = end;
+            }
+            __syncthreads();
+            if (!stop) {
+                const uint64_t* from = (const uint64_t*)&slot->args;
+                for (uint32_t i = threadIdx.x; i < kWords; i += kBlockThreads) {
+                    const uint64_t w = __hip_atomic_load(from + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                    pk[i] = w;
+                    __hip_atomic_store(r.mirror + i, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                __hip_atomic_store(stop_flag, stop, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(published, (uint32_t)k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        } else {
+            if (threadIdx.x == 0) {
+                // the relay may idle for up to idle_ticks, then finish the previous packet's wait
+                uint32_t end = wait_word(published, (uint32_t)k, r.idle_ticks + 2 * r.timeout_ticks) ? 0u : 1u;
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+                if (!end && __hip_atomic_load(stop_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) end = 1;
+                stop = end;
+            }
+            __syncthreads();
+            if (!stop)
+                for (uint32_t i = threadIdx.x; i < kWords; i += kBlockThreads)
+                    pk[i] = __hip_atomic_load(r.mirror + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __syncthreads();
+        }
+        if (stop) break;
+
+        const LaunchArgs& a = *(const LaunchArgs*)pk;
+        const uint8_t* prog = a.prog;
+        ProgramHeader h;
+        h.ndesc = uni(((const ProgramHeader*)prog)->ndesc);
+        h.ntiles = uni(((const ProgramHeader*)prog)->ntiles);
+        h.nstate = uni(((const ProgramHeader*)prog)->nstate);
+        h.off_desc = uni64(((const ProgramHeader*)prog)->off_desc);
+        h.off_operand = uni64(((const ProgramHeader*)prog)->off_operand);
+        h.off_dep = uni64(((const ProgramHeader*)prog)->off_dep);
+        h.off_tile_desc = uni64(((const ProgramHeader*)prog)->off_tile_desc);
+        h.off_aux = uni64(((const ProgramHeader*)prog)->off_aux);
+        const bool has_deps = (uni(((const ProgramHeader*)prog)->flags) & PF_HAS_DEPS) != 0u;
+        const uint64_t* bufs = pk + offsetof(LaunchArgs, bufs) / 8;
+        Shared sh;
+        sh.state = a.state;
+        sh.error = r.error;
+        sh.timeout = r.timeout_ticks;
+        for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
+            if (has_deps && load_relaxed(&r.error->code) != 0u) break;
+            if (!run_tile<kKindGeneric>(sh, prog, h, t, lane, bufs)) break;
+        }
+
+        // this workgroup's stores and counter updates are complete and visible device-wide
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const uint32_t prev = __hip_atomic_fetch_add(arrived, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+            last_block = (prev == gridDim.x - 1) ? 1u : 0u;
+        }
+        __syncthreads();
+        if (last_block) {
+            if (has_deps)
+                for (uint32_t i = threadIdx.x; i < h.nstate; i += kBlockThreads)
+                    __hip_atomic_store(a.state + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                const uint32_t code = load_relaxed(&r.error->code);
+                if (code != 0u) {
+                    // only this thread writes the record (packets complete one at a time), so plain
+                    // stores suffice: no atomic read-modify-write goes to host memory
+                    if (__hip_atomic_load(&r.q->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) == 0u) {
+                        __hip_atomic_store(&r.q->error, code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                        __hip_atomic_store(&r.q->err_desc, load_relaxed(&r.error->desc), __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_SYSTEM);
+                        __hip_atomic_store(&r.q->err_tile, load_relaxed(&r.error->tile), __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_SYSTEM);
+                    }
+                    __hip_atomic_store(&r.error->code, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+                __hip_atomic_store(arrived, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                // results and counters reach memory before the host or the relay sees the number
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
+                __hip_atomic_store(&r.q->done_seq, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                __hip_atomic_store(finished, (uint32_t)k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        if (relay) {
+            // the next packet may reuse these counters and the mirror: wait for every workgroup
+            if (threadIdx.x == 0) {
+                if (!last_block && !wait_word(finished, (uint32_t)k, r.timeout_ticks)) stop = 1;
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            }
+            __syncthreads();
+            if (stop) {
+                // release the others from their wait for packet k + 1
+                if (threadIdx.x == 0) {
+                    __hip_atomic_store(stop_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(published, (uint32_t)(k + 1), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+                }
+                break;
+            }
+        }
+    }
+    if (threadIdx.x == 0 && relay) __hip_atomic_store(&r.q->exited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // A program of one step needs no device image: its step travels inside the launch packet
 // with every operand already resolved to an address (the analogue of the express doorbell,
 // where the work request itself is the doorbell write and nothing is fetched first).
@@ -1293,6 +1476,15 @@ hipError_t launch_executor(const LaunchArgs& a, uint32_t blocks, int kind, hipSt
 hipError_t launch_signal(uint64_t* word, uint64_t value, const ErrorRecord* err, hipStream_t stream) {
     hipLaunchKernelGGL(hccl_signal, dim3(1), dim3(64), 0, stream, word, value, err);
     return hipGetLastError();
+}
+
+hipError_t launch_resident(const ResidentArgs& r, uint32_t blocks, hipStream_t stream) {
+    hipLaunchKernelGGL(hccl_resident, dim3(blocks), dim3(kBlockThreads), 0, stream, r);
+    return hipGetLastError();
+}
+
+hipError_t resident_occupancy(int* blocks_per_cu) {
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, hccl_resident, kBlockThreads, 0);
 }
 
 hipError_t launch_fill_u32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t stream) {

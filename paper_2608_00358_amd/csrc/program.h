@@ -208,6 +208,44 @@ struct LaunchArgs {
     char* bufs[kMaxBuffers];
 };
 
+// Resident executor: work packets handed to an executor that is already running, through a
+// ring of slots in coherent pinned host memory (the doorbell). The host fills a slot's
+// arguments, then publishes its sequence number; every workgroup polls that number, runs the
+// packet, and the last workgroup to finish reports the sequence number back.
+constexpr uint32_t kResidentSlots = 64;
+
+constexpr uint64_t kResidentStop = 1ull << 63;  // set in a slot's seq: no packet, the executor ends
+
+struct ResidentSlot {
+    uint64_t seq;      // written last by the host: the packet's sequence number (1, 2, ...),
+                       // with kResidentStop set for the stop request (one read gives both)
+    uint64_t pad;
+    LaunchArgs args;   // nworkers, dynamic and the trigger fields are ignored
+};
+
+struct ResidentQueue {
+    uint64_t done_seq;   // written by the device: every packet up to this number has completed
+    uint32_t error;      // first error code of any completed packet (ErrorRecord codes), sticky
+    uint32_t exited;     // written by the device when the executor has stopped taking packets
+    uint32_t err_desc;
+    uint32_t err_tile;
+    uint64_t pad[5];
+    ResidentSlot slots[kResidentSlots];
+};
+
+// Kernel arguments of the resident executor. `ctl` is device memory, zero at launch: word 0
+// counts the workgroups that finished the current packet, word 1 is the last packet they all
+// finished, word 2 the last packet workgroup 0 published to the others and word 3 its stop
+// flag. `mirror` is the device copy of the published packet's arguments.
+struct ResidentArgs {
+    ResidentQueue* q;
+    uint32_t* ctl;
+    uint64_t* mirror;
+    ErrorRecord* error;
+    uint64_t timeout_ticks;  // watchdog for one dependency wait or completion wait
+    uint64_t idle_ticks;     // the executor ends after this long without a packet
+};
+
 enum TriggerCmp : uint32_t { CMP_EQ = 0, CMP_NE = 1, CMP_GE = 2, CMP_GT = 3, CMP_LE = 4, CMP_LT = 5 };
 
 // Kernel arguments of a one-step program launched inline: the step and its operands,

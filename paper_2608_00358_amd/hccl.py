@@ -28,6 +28,7 @@ EXPORTS = [
     "hccl_allreduce", "hccl_reduce_scatter", "hccl_allgather", "hccl_alltoallv",
     "hccl_get_last_error", "hccl_result_string", "hccl_get_async_error", "hccl_comm_last_program",
     "hccl_group_start", "hccl_group_end", "hccl_alltoallv_dynamic", "hccl_set_trigger",
+    "hccl_resident_start", "hccl_resident_stop", "hccl_resident_wait", "hccl_resident_last_seq",
 ]
 CMPS = {"eq": 0, "ne": 1, "ge": 2, "gt": 3, "le": 4, "lt": 5}
 
@@ -99,6 +100,10 @@ def load(path: str = LIB_PATH):
     lib.hccl_comm_last_program.argtypes = [vp, ctypes.POINTER(hcclProgramInfo_t)]
     lib.hccl_group_start.argtypes = [vp]
     lib.hccl_group_end.argtypes = [vp]
+    lib.hccl_resident_start.argtypes = [vp, ctypes.c_uint32, ctypes.c_uint32]
+    lib.hccl_resident_stop.argtypes = [vp]
+    lib.hccl_resident_wait.argtypes = [vp, ctypes.c_uint64, ctypes.c_uint32]
+    lib.hccl_resident_last_seq.argtypes = [vp, ctypes.POINTER(ctypes.c_uint64)]
     for name in EXPORTS:
         if name not in ("hccl_get_last_error", "hccl_result_string"):
             getattr(lib, name).restype = res
@@ -250,6 +255,24 @@ def hccl_get_async_error(comm) -> int:
     return int(load().hccl_get_async_error(comm))
 
 
+def hccl_resident_start(comm, blocks: int = 0, idle_ms: int = 0) -> None:
+    _check(load().hccl_resident_start(comm, blocks, idle_ms))
+
+
+def hccl_resident_stop(comm) -> None:
+    _check(load().hccl_resident_stop(comm))
+
+
+def hccl_resident_wait(comm, seq: int = 0, timeout_ms: int = 0) -> None:
+    _check(load().hccl_resident_wait(comm, seq, timeout_ms))
+
+
+def hccl_resident_last_seq(comm) -> int:
+    out = ctypes.c_uint64(0)
+    _check(load().hccl_resident_last_seq(comm, ctypes.byref(out)))
+    return int(out.value)
+
+
 def hccl_comm_last_program(comm) -> dict:
     info = hcclProgramInfo_t()
     _check(load().hccl_comm_last_program(comm, ctypes.byref(info)))
@@ -384,3 +407,25 @@ class Comm:
 
     def async_error(self) -> int:
         return hccl_get_async_error(self.handle)
+
+    def resident(self, blocks: int = 0, idle_ms: int = 0):
+        """Context manager: calls inside go to a resident executor through the host doorbell
+        (see hccl_resident_start); it is stopped on exit."""
+        comm = self
+
+        class _Resident:
+            def __enter__(self):
+                hccl_resident_start(comm.handle, blocks, idle_ms)
+                return comm
+
+            def __exit__(self, *exc):
+                hccl_resident_stop(comm.handle)
+                return False
+
+        return _Resident()
+
+    def resident_wait(self, seq: int = 0, timeout_ms: int = 0) -> None:
+        hccl_resident_wait(self.handle, seq, timeout_ms)
+
+    def resident_seq(self) -> int:
+        return hccl_resident_last_seq(self.handle)

@@ -39,3 +39,17 @@ def test_comm_create_rejects_bad_rank_counts(n):
     with pytest.raises(H.HcclError) as e:
         H.hccl_comm_create(n, H.NO_DEVICE)
     assert e.value.code == 1
+
+
+def test_resident_executor_host_only_rules():
+    """A host-only communicator has no device to keep an executor on; stopping one that is not
+    running is a no-op, and waiting on one is an error."""
+    with H.Comm(4, device=H.NO_DEVICE) as c:
+        with pytest.raises(H.HcclError) as e:
+            H.hccl_resident_start(c.handle)
+        assert e.value.code == 1 and "device" in str(e.value)
+        H.hccl_resident_stop(c.handle)
+        with pytest.raises(H.HcclError) as e:
+            H.hccl_resident_wait(c.handle)
+        assert e.value.code == 1
+        assert H.hccl_resident_last_seq(c.handle) == 0
