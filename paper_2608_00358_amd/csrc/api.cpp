@@ -940,8 +940,8 @@ hcclResult_t hccl_resident_start(hcclComm_t comm, uint32_t blocks, uint32_t idle
     uint32_t* ctl = nullptr;
     hipStream_t st = nullptr;
     e = hipHostGetDevicePointer(&qdev, q, 0);
-    // control words, then the device mirror of the published packet's arguments
-    const size_t ctl_bytes = 64 + sizeof(LaunchArgs);
+    // control words, then two device mirrors of packet arguments (one is filled ahead)
+    const size_t ctl_bytes = 64 + 2 * sizeof(LaunchArgs);
     if (e == hipSuccess) e = hipMalloc(&ctl, ctl_bytes);
     if (e == hipSuccess) e = hipMemset(ctl, 0, ctl_bytes);
     if (e == hipSuccess) e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);

@@ -1214,16 +1214,16 @@ __global__ void hccl_signal(uint64_t* word, uint64_t value, const ErrorRecord* e
 // An executor that stays running and takes work packets through a doorbell in host memory
 // (Section II-A-2: the message engine's control core waits for work and unrolls each packet as
 // it arrives; Section V-B: re-enqueueing a cached packet is the whole per-call cost). The host
-// writes a packet's arguments into a ring slot, then its sequence number. Workgroup 0 is the
-// relay: its thread 0 polls that number with system-scope loads, the workgroup copies the
-// arguments into a device mirror and publishes the number in device memory, so that only one
-// workgroup pays the PCIe round trips. Every workgroup then copies the arguments into LDS and
-// runs its share of the tiles exactly as a launched executor does (wavefront w takes tiles
+// writes a packet's arguments into a ring slot, then its sequence number. The last workgroup
+// is the relay: its thread 0 polls that number with system-scope loads, the workgroup copies
+// the arguments into a device mirror and publishes the number in device memory, so that only
+// one workgroup pays the PCIe round trips. Every workgroup then copies the arguments into LDS
+// and runs its share of the tiles exactly as a launched executor does (wavefront w takes tiles
 // w, w + W, ...). The last workgroup to finish clears the program's counters, writes the
 // results back for readers outside the GPU and stores the sequence number in host memory; the
-// relay waits for that before it takes the next packet. Every wait is bounded: the relay ends
-// the executor after `idle_ticks` without a packet, and a workgroup that waits longer than its
-// limit for the others ends too.
+// relay waits for that before it publishes the next packet, and fetches that packet meanwhile
+// if it has arrived. Every wait is bounded: the relay ends the executor after `idle_ticks`
+// without a packet, and a workgroup that waits longer than its limit for the others ends too.
 __device__ __forceinline__ void backoff(uint32_t& nap, uint32_t cap) {
     if (nap == 1) __builtin_amdgcn_s_sleep(1);
     else if (nap == 2) __builtin_amdgcn_s_sleep(2);
@@ -1252,50 +1252,67 @@ hccl_resident(ResidentArgs r) {
     __shared__ uint64_t pk[kWords];
     __shared__ uint32_t stop;
     __shared__ uint32_t last_block;
+    __shared__ uint32_t ahead;       // relay: the next packet is already in pk and its mirror
+    __shared__ uint32_t ahead_stop;  // relay: ... and it is the stop request
+    __shared__ uint32_t sig, fetch;  // relay: decisions of thread 0 while it waits
     const uint32_t lane = __lane_id();
     const uint32_t wave = uni(blockIdx.x * kWavesPerBlock + (threadIdx.x / kWaveSize));
     const uint32_t nworkers = gridDim.x * kWavesPerBlock;
-    const bool relay = blockIdx.x == 0;
+    // the relay is the last workgroup: its wavefronts come last in the tile order, so on small
+    // packets it has no tiles and is free to fetch the next packet while the others work
+    const bool relay = blockIdx.x == gridDim.x - 1;
     uint32_t* const arrived = r.ctl;
     uint32_t* const finished = r.ctl + 1;
     uint32_t* const published = r.ctl + 2;
     uint32_t* const stop_flag = r.ctl + 3;
+    if (threadIdx.x == 0) {
+        ahead = 0;
+        ahead_stop = 0;
+    }
+    __syncthreads();
 
     for (uint64_t k = 1;; ++k) {
+        uint64_t* const mirror = r.mirror + (k & 1) * kWords;  // two copies: one is filled ahead
         if (relay) {
             ResidentSlot* slot = &r.q->slots[(k - 1) % kResidentSlots];
             if (threadIdx.x == 0) {
-                uint32_t end = 0, nap = 1;
-                const uint64_t t0 = wall_clock64();
-                for (;;) {
-                    const uint64_t v = __hip_atomic_load(&slot->seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-                    if ((v & ~kResidentStop) == k) {
-                        end = (v & kResidentStop) ? 1u : 0u;
-                        break;
+                uint32_t end = 0;
+                if (ahead) {
+                    end = ahead_stop;
+                } else {
+                    uint32_t nap = 1;
+                    const uint64_t t0 = wall_clock64();
+                    for (;;) {
+                        const uint64_t v = __hip_atomic_load(&slot->seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                        if ((v & ~kResidentStop) == k) {
+                            end = (v & kResidentStop) ? 1u : 0u;
+                            break;
+                        }
+                        if (wall_clock64() - t0 > r.idle_ticks) {
+                            end = 1;
+                            break;
+                        }
+                        backoff(nap, 4);
                     }
-                    if (wall_clock64() - t0 > r.idle_ticks) {
-                        end = 1;
-                        break;
-                    }
-                    backoff(nap, 4);
+                    // the slot's arguments, and whatever was written to the packet's buffers
+                    // before the doorbell, are visible from here on (stale lines are dropped)
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
                 }
-                // the slot's arguments, and whatever was written to the packet's buffers before
-                // the doorbell, are visible from here on (stale cache lines are dropped)
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
                 stop = end;
             }
             __syncthreads();
-            if (!stop) {
+            if (!stop && !ahead) {
                 const uint64_t* from = (const uint64_t*)&slot->args;
                 for (uint32_t i = threadIdx.x; i < kWords; i += kBlockThreads) {
                     const uint64_t w = __hip_atomic_load(from + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
                     pk[i] = w;
-                    __hip_atomic_store(r.mirror + i, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(mirror + i, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (threadIdx.x == 0) {
+                ahead = 0;
                 __hip_atomic_store(stop_flag, stop, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 __hip_atomic_store(published, (uint32_t)k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
             }
@@ -1310,7 +1327,7 @@ hccl_resident(ResidentArgs r) {
             __syncthreads();
             if (!stop)
                 for (uint32_t i = threadIdx.x; i < kWords; i += kBlockThreads)
-                    pk[i] = __hip_atomic_load(r.mirror + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    pk[i] = __hip_atomic_load(mirror + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __syncthreads();
         }
         if (stop) break;
@@ -1327,9 +1344,10 @@ hccl_resident(ResidentArgs r) {
         h.off_tile_desc = uni64(((const ProgramHeader*)prog)->off_tile_desc);
         h.off_aux = uni64(((const ProgramHeader*)prog)->off_aux);
         const bool has_deps = (uni(((const ProgramHeader*)prog)->flags) & PF_HAS_DEPS) != 0u;
+        uint32_t* const state = a.state;
         const uint64_t* bufs = pk + offsetof(LaunchArgs, bufs) / 8;
         Shared sh;
-        sh.state = a.state;
+        sh.state = state;
         sh.error = r.error;
         sh.timeout = r.timeout_ticks;
         for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
@@ -1349,7 +1367,7 @@ hccl_resident(ResidentArgs r) {
         if (last_block) {
             if (has_deps)
                 for (uint32_t i = threadIdx.x; i < h.nstate; i += kBlockThreads)
-                    __hip_atomic_store(a.state + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(state + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (threadIdx.x == 0) {
@@ -1374,11 +1392,55 @@ hccl_resident(ResidentArgs r) {
             }
         }
         if (relay) {
-            // the next packet may reuse these counters and the mirror: wait for every workgroup
-            if (threadIdx.x == 0) {
-                if (!last_block && !wait_word(finished, (uint32_t)k, r.timeout_ticks)) stop = 1;
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            // Wait until every workgroup has finished packet k (the next packet may reuse its
+            // counters). Meanwhile, if packet k + 1 is already at the doorbell, bring its
+            // arguments into LDS and the other mirror, so that its PCIe round trips overlap the
+            // others' work on packet k. (pk is free: this workgroup has finished packet k.)
+            ResidentSlot* next = &r.q->slots[k % kResidentSlots];
+            uint64_t* const next_mirror = r.mirror + ((k + 1) & 1) * kWords;
+            uint32_t nap = 1;
+            const uint64_t t0 = wall_clock64();
+            for (;;) {
+                if (threadIdx.x == 0) {
+                    uint32_t g = 0;  // 1 = packet k finished, 2 = gave up waiting
+                    if (last_block || __hip_atomic_load(finished, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)k)
+                        g = 1;
+                    else if (wall_clock64() - t0 > r.timeout_ticks)
+                        g = 2;
+                    uint32_t f = 0;  // 1 = fetch packet k + 1 now, 2 = it is the stop request
+                    if (!ahead) {
+                        const uint64_t v = __hip_atomic_load(&next->seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                        if ((v & ~kResidentStop) == k + 1) {
+                            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+                            f = (v & kResidentStop) ? 2u : 1u;
+                        }
+                    }
+                    sig = g;
+                    fetch = f;
+                }
+                __syncthreads();
+                const uint32_t g = sig, f = fetch;
+                if (f == 1u) {
+                    const uint64_t* from = (const uint64_t*)&next->args;
+                    for (uint32_t i = threadIdx.x; i < kWords; i += kBlockThreads) {
+                        const uint64_t w = __hip_atomic_load(from + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                        pk[i] = w;
+                        __hip_atomic_store(next_mirror + i, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    __builtin_amdgcn_s_waitcnt(0);
+                }
+                __syncthreads();
+                if (threadIdx.x == 0) {
+                    if (f != 0u) {
+                        ahead = 1;
+                        ahead_stop = f == 2u ? 1u : 0u;
+                    }
+                    if (g == 2u) stop = 1;
+                    if (g == 0u) backoff(nap, 4);
+                }
+                if (g != 0u) break;
             }
+            if (threadIdx.x == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             __syncthreads();
             if (stop) {
                 // release the others from their wait for packet k + 1

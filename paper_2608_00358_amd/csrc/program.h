@@ -236,7 +236,7 @@ struct ResidentQueue {
 // Kernel arguments of the resident executor. `ctl` is device memory, zero at launch: word 0
 // counts the workgroups that finished the current packet, word 1 is the last packet they all
 // finished, word 2 the last packet workgroup 0 published to the others and word 3 its stop
-// flag. `mirror` is the device copy of the published packet's arguments.
+// flag. `mirror` holds two device copies of packet arguments: packet k uses copy k mod 2.
 struct ResidentArgs {
     ResidentQueue* q;
     uint32_t* ctl;
