@@ -215,3 +215,36 @@ def test_resident_executor_ends_when_idle_and_restarts():
         with pytest.raises(H.HcclError) as e:
             H.hccl_resident_start(c.handle, 100000, 0)   # cannot all be resident at once
         assert e.value.code == 1
+
+
+@pytest.mark.parametrize("blocks", [3, 32])
+def test_resident_large_packets_where_the_relay_runs_tiles(blocks):
+    """Packets with far more tiles than wavefronts, so the relay workgroup runs tiles of its own
+    before it fetches the next packet; a direct and a dependent (unfused ring) program alternate,
+    queued without waiting, and the last of each is checked. Two communicators run an executor
+    each at the same time."""
+    P, N = 8, 1 << 20
+    x = inputs(P, N, "bf16", 150)
+    send = [to_device(x[r], "bf16") for r in range(P)]
+    out_a = [torch.zeros(N, dtype=torch.bfloat16, device="cuda:0") for _ in range(P)]
+    out_b = [torch.zeros(N, dtype=torch.bfloat16, device="cuda:0") for _ in range(P)]
+    print(f"resident large packets blocks={blocks}", flush=True)
+    with H.Comm(P, device=0, algo="direct") as ca, H.Comm(P, device=0, algo="ring", fuse=0,
+                                                          chunk_bytes=65536) as cb:
+        ca.allreduce(send, out_a)
+        cb.allreduce(send, out_b)
+        torch.cuda.synchronize()
+        assert ca.last_program()["num_tiles"] > 32 * 4 and cb.last_program()["num_deps"] > 0
+        for t in out_a + out_b:
+            t.zero_()
+        torch.cuda.synchronize()
+        with ca.resident(blocks=blocks, idle_ms=IDLE_MS), cb.resident(blocks=blocks, idle_ms=IDLE_MS):
+            for _ in range(6):
+                ca.allreduce(send, out_a)
+                cb.allreduce(send, out_b)
+            ca.resident_wait(timeout_ms=20000)
+            cb.resident_wait(timeout_ms=20000)
+    want = oracle.allreduce(x, "bf16")
+    for r in range(P):
+        assert same_bits(to_host(out_a[r], "bf16"), want[r], "bf16"), f"direct rank {r}"
+        assert same_bits(to_host(out_b[r], "bf16"), want[r], "bf16"), f"ring rank {r}"
