@@ -51,7 +51,7 @@ extern "C" {
 typedef enum {
     hcclSuccess = 0,
     hcclInvalidArgument = 1, /* a pointer, size, count, displacement or enum is invalid */
-    hcclUnsupported = 2,     /* valid request this build does not implement */
+    hcclUnsupported = 2,     /* valid request the library does not implement */
     hcclHipError = 3,        /* a HIP runtime call failed */
     hcclOutOfMemory = 4,     /* device allocation for a program or scratch failed */
     hcclTimeout = 5,         /* a device dependency wait exceeded the watchdog limit */
