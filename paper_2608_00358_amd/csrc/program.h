@@ -15,6 +15,7 @@
 // the lowest unfinished tile can always run.
 #pragma once
 
+#include <stddef.h>
 #include <stdint.h>
 
 namespace hccl {
@@ -232,6 +233,12 @@ struct ResidentQueue {
     uint64_t pad[5];
     ResidentSlot slots[kResidentSlots];
 };
+
+// The host writes and the device reads these in place: their layout must not depend on the compiler.
+static_assert(sizeof(LaunchArgs) % 8 == 0, "packet arguments are copied in 8-byte words");
+static_assert(offsetof(ResidentSlot, args) == 16, "slot header is two words");
+static_assert(offsetof(ResidentQueue, slots) == 64, "queue header is one cache line");
+static_assert(sizeof(ResidentSlot) % 8 == 0, "slots stay 8-byte aligned");
 
 // Kernel arguments of the resident executor. `ctl` is device memory, zero at launch: word 0
 // counts the workgroups that finished the current packet, word 1 is the last packet they all
