@@ -248,3 +248,35 @@ def test_resident_large_packets_where_the_relay_runs_tiles(blocks):
     for r in range(P):
         assert same_bits(to_host(out_a[r], "bf16"), want[r], "bf16"), f"direct rank {r}"
         assert same_bits(to_host(out_b[r], "bf16"), want[r], "bf16"), f"ring rank {r}"
+
+
+def test_resident_wait_by_sequence_number():
+    P, N = 4, 4096
+    x = inputs(P, N, "fp32", 160)
+    send = [to_device(x[r], "fp32") for r in range(P)]
+    outs = [[torch.zeros(N, dtype=torch.float32, device="cuda:0") for _ in range(P)] for _ in range(5)]
+    print("resident wait by sequence number", flush=True)
+    with H.Comm(P, device=0) as c:
+        for o in outs:
+            c.allreduce(send, o)
+        torch.cuda.synchronize()
+        for o in outs:
+            for t in o:
+                t.zero_()
+        torch.cuda.synchronize()
+        with c.resident(blocks=4, idle_ms=IDLE_MS):
+            for o in outs:
+                c.allreduce(send, o)
+            assert c.resident_seq() == 5
+            c.resident_wait(seq=2)                   # the first two have completed, in order
+            want = oracle.allreduce(x, "fp32")
+            for o in outs[:2]:
+                for r in range(P):
+                    assert same_bits(to_host(o[r], "fp32"), want[r], "fp32")
+            with pytest.raises(H.HcclError) as e:
+                c.resident_wait(seq=6)               # never submitted
+            assert e.value.code == 1
+            c.resident_wait()
+            for o in outs[2:]:
+                for r in range(P):
+                    assert same_bits(to_host(o[r], "fp32"), want[r], "fp32")
