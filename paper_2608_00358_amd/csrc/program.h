@@ -242,8 +242,9 @@ static_assert(sizeof(ResidentSlot) % 8 == 0, "slots stay 8-byte aligned");
 
 // Kernel arguments of the resident executor. `ctl` is device memory, zero at launch: word 0
 // counts the workgroups that finished the current packet, word 1 is the last packet they all
-// finished, word 2 the last packet workgroup 0 published to the others and word 3 its stop
-// flag. `mirror` holds two device copies of packet arguments: packet k uses copy k mod 2.
+// finished, word 2 the last packet the relay (the last workgroup) published to the others,
+// word 3 its stop flag. `mirror` holds two device copies of packet arguments: packet k uses
+// copy k mod 2.
 struct ResidentArgs {
     ResidentQueue* q;
     uint32_t* ctl;
