@@ -144,6 +144,16 @@ def run_headline(args, device):
     return result, w
 
 
+def _extra(name, fn):
+    """Runs one secondary measurement; an error in it is recorded in its place instead of
+    costing the headline line (a GPU fault still ends the process)."""
+    try:
+        return fn()
+    except Exception as e:  # noqa: BLE001
+        _log(f"{name} failed: {type(e).__name__}: {e}")
+        return {"error": f"{type(e).__name__}: {e}"}
+
+
 # --------------------------------------------------------------------- other configs
 def bench_allreduce_ring_c1(device, iters=200, cold_sets=40):
     """All-reduce P=4 x 2^20 fp32 U[-1,1), ring reduce-scatter + all-gather, 64 KiB chunks."""
@@ -809,28 +819,28 @@ def main():
     if not args.headline_only:
         extras = {}
         _log("c1 ring all-reduce")
-        extras["allreduce_ring_p4_fp32"] = bench_allreduce_ring_c1(device)
+        extras["allreduce_ring_p4_fp32"] = _extra("c1", lambda: bench_allreduce_ring_c1(device))
         _log("c3 ring reduce-scatter")
         c3, rs_send, rs_recv = bench_reduce_scatter_c3(device)
         extras["reduce_scatter_ring_p8_bf16"] = c3
         _log(f"c3 {c3['gbs']:.1f} GB/s")
         if not args.no_overlap:
             _log("c5a overlap")
-            extras["overlap_rs16cu_gemm"] = bench_overlap_c5a(device, rs_send, rs_recv)
+            extras["overlap_rs16cu_gemm"] = _extra("c5a overlap", lambda: bench_overlap_c5a(device, rs_send, rs_recv))
         del rs_send, rs_recv
         torch.cuda.empty_cache()
         _log("c4 two-level all-reduce")
-        extras["allreduce_two_level_p64_bf16"] = bench_two_level_c4(device)
+        extras["allreduce_two_level_p64_bf16"] = _extra("c4", lambda: bench_two_level_c4(device))
         _log("c5b latency")
-        extras["latency_allreduce_p8_64KiB_fp32"] = bench_latency_c5b(device)
+        extras["latency_allreduce_p8_64KiB_fp32"] = _extra("c5b latency", lambda: bench_latency_c5b(device))
         _log("c5b latency through the resident executor")
-        extras["resident_allreduce_p8_64KiB_fp32"] = bench_resident_c5b(device)
+        extras["resident_allreduce_p8_64KiB_fp32"] = _extra("resident", lambda: bench_resident_c5b(device))
         _log("alltoallv_dynamic")
-        extras["alltoallv_dynamic_rows_ids_p8"] = bench_dynamic_alltoallv(device, w)
+        extras["alltoallv_dynamic_rows_ids_p8"] = _extra("dynamic", lambda: bench_dynamic_alltoallv(device, w))
         _log("moe dispatch: device-resident vs eager")
-        extras["moe_dispatch_p8"] = bench_moe_dispatch(device)
+        extras["moe_dispatch_p8"] = _extra("moe", lambda: bench_moe_dispatch(device))
         _log("moe dispatch: device-triggered")
-        extras["moe_dispatch_triggered_p8"] = bench_triggered_dispatch(device)
+        extras["moe_dispatch_triggered_p8"] = _extra("moe triggered", lambda: bench_triggered_dispatch(device))
         line["collectives"] = extras
     if not args.no_cpu_baseline:
         _log("cpu baseline")
