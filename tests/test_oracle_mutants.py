@@ -77,6 +77,14 @@ MUTANTS = {
         "int first = (c + 1) % P;\n        float acc",
         "int first = c % P;\n        float acc",
     ),
+    "two_level_cross_group_fold_not_requantised": (
+        "total = (g == 0) ? part : comb_q(op, dtype, q, total, part);",
+        "total = (g == 0) ? part : combine_f32(op, total, part);",
+    ),
+    "two_level_in_group_fold_not_requantised": (
+        "part = comb_q(op, dtype, q, part, load_as_f32(src[r], dtype, i));",
+        "part = combine_f32(op, part, load_as_f32(src[r], dtype, i));",
+    ),
     "requant_ignored": (
         "return requant ? requantize(dtype, v) : v;",
         "return v;",
@@ -126,6 +134,7 @@ PIN_CALLS = [
     ("halving order", lambda: order_pins.test_halving_order_is_the_distance_halving_tree(8)),
     ("order cancellation", lambda: order_pins.test_orders_are_told_apart_by_cancellation()),
     ("requant", lambda: order_pins.test_requant_rounds_every_partial_to_bf16("ascending")),
+    ("requant two-level", lambda: order_pins.test_two_level_requant_rounds_inside_and_across_groups(2)),
     ("dynamic example", lambda: dyn_pins.test_worked_example_packed_layout()),
     ("dynamic explicit", lambda: dyn_pins.test_worked_example_explicit_offsets()),
     ("dynamic brute", lambda: dyn_pins.test_packed_layout_is_the_brute_force_row_placement(3, 4, 2)),

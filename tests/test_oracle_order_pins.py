@@ -107,6 +107,47 @@ def test_requant_rounds_every_partial_to_bf16(order):
     assert not np.array_equal(out[0], once[0])
 
 
+def _group_partials(wide, group, rnd):
+    """Each run of `group` consecutive ranks folded ascending, `rnd` applied after every add."""
+    parts = []
+    for g0 in range(0, wide.shape[0], group):
+        acc = wide[g0].copy()
+        for r in range(g0 + 1, g0 + group):
+            acc = rnd((acc + wide[r]).astype(np.float32))
+        parts.append(acc)
+    return parts
+
+
+@pytest.mark.parametrize("group", [2, 4])
+def test_two_level_requant_rounds_inside_and_across_groups(group):
+    """Two-level order with re-quantisation (every NMC result rounded to the buffer type): the
+    group partials are rounded after every in-group add, and so is every add of the
+    cross-group fold. Each of the two roundings is shown to matter on its own."""
+    P = 8
+    xb = normal_bf16(P, 8192, std=3.0, seed=81 + group)
+    wide = np.stack([_widen(xb[r]) for r in range(P)])
+    out = oracle.allreduce_ordered(xb, "bf16", order="two_level", group=group, requant=True)
+    parts = _group_partials(wide, group, _bf16_round)
+    tot = parts[0]
+    for p in parts[1:]:
+        tot = _bf16_round((tot + p).astype(np.float32))
+    assert np.array_equal(out[0], _to_bits(tot))
+    # in-group rounding only: the cross-group fold in FP32, rounded once at the end
+    cross_f32 = parts[0]
+    for p in parts[1:]:
+        cross_f32 = (cross_f32 + p).astype(np.float32)
+    if len(parts) > 2:   # with two groups the one cross-group add is rounded either way
+        assert not np.array_equal(out[0], _to_bits(cross_f32))
+    # cross-group rounding only: FP32 group partials
+    raw = _group_partials(wide, group, lambda v: v)
+    tot_raw = raw[0]
+    for p in raw[1:]:
+        tot_raw = _bf16_round((tot_raw + p).astype(np.float32))
+    assert not np.array_equal(out[0], _to_bits(tot_raw))
+    # and the two-level order without re-quantisation differs too
+    assert not np.array_equal(out[0], oracle.allreduce_ordered(xb, "bf16", order="two_level", group=group)[0])
+
+
 def test_requant_is_a_no_op_for_fp32_and_int32():
     x = normal_f32(8, 999, seed=90)
     a = oracle.allreduce_ordered(x, "fp32", order="ring", shard=100, requant=True)
