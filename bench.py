@@ -74,7 +74,8 @@ def run_headline(args, device):
     One pair of HIP events on the launch stream brackets the K back-to-back launches: their
     span / K is the average launch duration (the gaps between launches included), and nothing
     is recorded between steps, so the host-timed steps carry no instrumentation. Also times
-    the two calls issued separately."""
+    the two calls issued separately (before the grouped steps, so that the receive buffers
+    hold the timed steps' results for the CPU baseline's check)."""
     import torch
 
     import paper_2608_00358_amd as H
@@ -100,10 +101,29 @@ def run_headline(args, device):
         ids_call()
         H.hccl_group_end(comm.handle)
 
+    algo_step = 2 * (row_bytes + id_bytes)
+    # the same two collectives as two launches (timed first: the receive buffers must hold
+    # what the timed grouped steps wrote)
+    separate = {}
+    if not args.headline_only:
+        for _ in range(3):
+            rows_call()
+            ids_call()
+        ms_rows = _time_events(rows_call, args.steps)
+        ms_sep = _time_events(lambda: (rows_call(), ids_call()), args.steps)
+        separate = {"rows_launch_us": ms_rows * 1e3, "rows_launch_gbs": 2 * row_bytes / (ms_rows * 1e-3) / 1e9,
+                    "two_launch_step_us": ms_sep * 1e3,
+                    "two_launch_step_gbs": algo_step / (ms_sep * 1e-3) / 1e9}
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     info_step = comm.last_program()
+    # poison the receive buffers: after the timed steps they hold only what those steps wrote
+    for t in recv_rows:
+        t.fill_(float("nan"))
+    for t in recv_ids:
+        t.fill_(-1)
 
     s = torch.cuda.current_stream()
     first = torch.cuda.Event(enable_timing=True)
@@ -120,20 +140,9 @@ def run_headline(args, device):
         raise RuntimeError(H.hccl_get_last_error())
     ms_step = elapsed * 1e3 / args.steps
     launch_ms = first.elapsed_time(last) / args.steps
-    algo_step = 2 * (row_bytes + id_bytes)
 
-    # the same two collectives as two launches
-    separate = {}
-    if not args.headline_only:
-        for _ in range(3):
-            rows_call()
-            ids_call()
-        ms_rows = _time_events(rows_call, args.steps)
-        ms_sep = _time_events(lambda: (rows_call(), ids_call()), args.steps)
-        separate = {"rows_launch_us": ms_rows * 1e3, "rows_launch_gbs": 2 * row_bytes / (ms_rows * 1e-3) / 1e9,
-                    "two_launch_step_us": ms_sep * 1e3,
-                    "two_launch_step_gbs": algo_step / (ms_sep * 1e-3) / 1e9}
     recv_counts = w["counts"].sum(axis=0)
+    w.update({"send_ids": send_ids, "recv_rows": recv_rows, "recv_ids": recv_ids})
     result = {
         "ms_per_step": ms_step,
         "value": algo_step / (ms_step * 1e-3) / 1e9,
@@ -350,19 +359,51 @@ def bench_resident_c5b(device, blocks=0, warmup=200, iters=1000):
             "ctypes_call_us": ctypes_us}
 
 
-def _cu_masked_stream(mask_words):
-    """hipExtStreamCreateWithCUMask on the current device (default priority)."""
+class _HipStream:
+    """A HIP stream created through ctypes (CU-masked, or non-blocking), at the default
+    priority. Used as a context manager: on exit it is synchronised and destroyed, so that no
+    stream of ours is left for the runtime to tear down at process exit."""
+
+    def __init__(self, mask_words=None):
+        import torch
+
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+        s = ctypes.c_void_p()
+        if mask_words is not None:
+            self._hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
+                                                               ctypes.POINTER(ctypes.c_uint32)]
+            arr = (ctypes.c_uint32 * len(mask_words))(*mask_words)
+            rc = self._hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), len(mask_words), arr)
+            what = "hipExtStreamCreateWithCUMask"
+        else:
+            self._hip.hipStreamCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32]
+            rc = self._hip.hipStreamCreateWithFlags(ctypes.byref(s), 1)   # hipStreamNonBlocking
+            what = "hipStreamCreateWithFlags"
+        if rc != 0:
+            raise RuntimeError(f"{what} failed ({rc})")
+        self.handle = s.value
+        self.stream = torch.cuda.ExternalStream(self.handle)
+
+    def __enter__(self):
+        return self.stream
+
+    def __exit__(self, *exc):
+        self.stream.synchronize()
+        self._hip.hipStreamDestroy(self.handle)
+        self.handle = None
+        return False
+
+
+def _first_cus_mask(n_per_xcd_total):
+    """Mask words selecting the first n bits (bit i is a CU of XCD i mod 8)."""
     import torch
 
-    hip = ctypes.CDLL("libamdhip64.so")
-    hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32,
-                                                 ctypes.POINTER(ctypes.c_uint32)]
-    s = ctypes.c_void_p()
-    arr = (ctypes.c_uint32 * len(mask_words))(*mask_words)
-    rc = hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), len(mask_words), arr)
-    if rc != 0:
-        raise RuntimeError(f"hipExtStreamCreateWithCUMask failed ({rc})")
-    return torch.cuda.ExternalStream(s.value), s.value
+    words = (torch.cuda.get_device_properties(0).multi_processor_count + 31) // 32
+    bits = [0] * words
+    for i in range(n_per_xcd_total):
+        bits[i // 32] |= 1 << (i % 32)
+    return bits
 
 
 def bench_overlap_c5a(device, rs_send, rs_recv, n_rs=100, rs_cus=16):
@@ -375,14 +416,19 @@ def bench_overlap_c5a(device, rs_send, rs_recv, n_rs=100, rs_cus=16):
     props = torch.cuda.get_device_properties(0)
     ncu = props.multi_processor_count
     words = (ncu + 31) // 32
-    rs_bits = [0] * words
-    for i in range(rs_cus):
-        rs_bits[i // 32] |= 1 << (i % 32)
+    rs_bits = _first_cus_mask(rs_cus)
     rest_bits = [((~rs_bits[w]) & 0xFFFFFFFF) for w in range(words)]
     if ncu % 32:
         rest_bits[-1] &= (1 << (ncu % 32)) - 1
-    rs_stream, _ = _cu_masked_stream(rs_bits)
-    rest_stream, _ = _cu_masked_stream(rest_bits)
+    with _HipStream(rs_bits) as rs_stream, _HipStream(rest_bits) as rest_stream:
+        return _overlap_c5a(device, rs_send, rs_recv, n_rs, rs_stream, rest_stream)
+
+
+def _overlap_c5a(device, rs_send, rs_recv, n_rs, rs_stream, rest_stream):
+    import torch
+
+    import paper_2608_00358_amd as H
+
     gemm_stream = torch.cuda.Stream()
     n = 8192
     g = torch.Generator(device=device).manual_seed(0)
@@ -569,18 +615,17 @@ def bench_triggered_dispatch(device, iters=60, warmup=10, per_xcd=16, done_word=
     flag = torch.zeros(1, dtype=torch.int64, device=device)
     done = torch.zeros(1, dtype=torch.int64, device=device)
     rank_base = (torch.arange(P, device=device) * P).view(P, 1)
-    hip = ctypes.CDLL("libamdhip64.so")
-    hip.hipStreamCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint32]
-    h = ctypes.c_void_p()
-    if hip.hipStreamCreateWithFlags(ctypes.byref(h), 1) != 0:   # non-blocking, default priority
-        raise RuntimeError("hipStreamCreateWithFlags failed")
-    cs = torch.cuda.ExternalStream(h.value)
-    props = torch.cuda.get_device_properties(0)
-    words = (props.multi_processor_count + 31) // 32
-    bits = [0] * words
-    for i in range(8 * per_xcd):
-        bits[i // 32] |= 1 << (i % 32)
-    ms, _ = _cu_masked_stream(bits)
+    with _HipStream() as cs, _HipStream(_first_cus_mask(8 * per_xcd)) as ms:
+        return _triggered_dispatch(device, iters, warmup, per_xcd, done_word, P, T, D, g, tokens, send_all, send,
+                                   recv, d_counts, flag, done, rank_base, cs, ms)
+
+
+def _triggered_dispatch(device, iters, warmup, per_xcd, done_word, P, T, D, g, tokens, send_all, send, recv,
+                        d_counts, flag, done, rank_base, cs, ms):
+    import numpy as np
+    import torch
+
+    import paper_2608_00358_amd as H
 
     def route():
         dest = (torch.rand(P, T, generator=g, device=device) ** 2 * P).long().clamp_(max=P - 1)
@@ -668,44 +713,130 @@ def bench_triggered_dispatch(device, iters=60, warmup=10, per_xcd=16, done_word=
         if i >= warmup:
             route_only.append((time.perf_counter() - t0) * 1e6)
     out["route_only_wall_us"] = statistics.median(route_only)
-    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
     torch.cuda.synchronize()
-    hip.hipStreamDestroy(h.value)
     return out
 
 
 # ---------------------------------------------------------------------- CPU baseline
-def cpu_baseline(w, budget_s=12.0):
-    """The oracle's AllToAllv on the host cores (single-threaded C), same inputs."""
+def _cpu_description():
+    """CPU model and topology of the host, from lscpu (falls back to /proc/cpuinfo)."""
+    import subprocess
+
+    keys = ("Model name", "Vendor ID", "CPU family", "Model", "Thread(s) per core", "Core(s) per socket",
+            "Socket(s)", "CPU(s)", "On-line CPU(s) list", "CPU max MHz", "L3 cache")
+    out = {}
+    try:
+        text = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in text.splitlines():
+            k, _, v = line.partition(":")
+            if k.strip() in keys:
+                out[k.strip()] = v.strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    if "Model name" not in out:
+        try:
+            for line in open("/proc/cpuinfo"):
+                if line.startswith("model name"):
+                    out["Model name"] = line.split(":", 1)[1].strip()
+                    break
+        except OSError:
+            pass
+    try:
+        out["affinity_cpus"] = len(os.sched_getaffinity(0))
+    except OSError:
+        pass
+    return out
+
+
+def _pair_groups(sendcounts, n):
+    """(source, destination) pairs split into n groups of about equal element counts."""
+    P = sendcounts.shape[0]
+    pairs = sorted(((int(sendcounts[s, d]), s, d) for s in range(P) for d in range(P)), reverse=True)
+    groups, load = [[] for _ in range(n)], [0] * n
+    for c, s, d in pairs:
+        k = load.index(min(load))
+        groups[k].append((s, d))
+        load[k] += c
+    return [g for g in groups if g]
+
+
+def _masked(lay, pairs):
+    """The layout with every count outside `pairs` set to zero (send [s, d], receive [d, s])."""
+    import numpy as np
+
+    sc = np.zeros_like(lay["sendcounts"])
+    for s, d in pairs:
+        sc[s, d] = lay["sendcounts"][s, d]
+    return sc, sc.T.copy()
+
+
+def cpu_baseline(w, budget_s=10.0, par_budget_s=5.0):
+    """The oracle's AllToAllv of the timed step (embedding rows and int32 ids, the same inputs)
+    on the host cores: single-threaded, then chunk-parallel (host threads each run the
+    unchanged oracle on their own (source, destination) pairs; the oracle releases the GIL).
+    The oracle's result is compared element by element with what the GPU left in the receive
+    buffers after its last timed step."""
     import numpy as np
     import torch
+    from concurrent.futures import ThreadPoolExecutor
 
     import oracle
 
     P = w["P"]
-    rows = w["rows"]
-    send = [t.view(torch.int16).cpu().numpy().view(np.uint16) for t in w["send_rows"]]
-    recv = [np.empty(int(rows["recv_len"][d]), np.uint16) for d in range(P)]
+    rows, ids = w["rows"], w["ids"]
+    send_r = [t.view(torch.int16).cpu().numpy().view(np.uint16) for t in w["send_rows"]]
+    send_i = [np.ascontiguousarray(w["id_vals"][s]) for s in range(P)]
+    got_r = [t.view(torch.int16).cpu().numpy().view(np.uint16) for t in w["recv_rows"]]
+    got_i = [t.cpu().numpy() for t in w["recv_ids"]]
     oracle.build(force=False)
+    out_r = [np.zeros(int(rows["recv_len"][d]), np.uint16) for d in range(P)]
+    out_i = [np.zeros(int(ids["recv_len"][d]), np.int32) for d in range(P)]
+
+    def step():
+        oracle.alltoallv(send_r, rows["sendcounts"], rows["sdispls"], out_r, rows["recvcounts"], rows["rdispls"])
+        oracle.alltoallv(send_i, ids["sendcounts"], ids["sdispls"], out_i, ids["recvcounts"], ids["rdispls"])
+
     reps, t = 0, 0.0
-    while t < budget_s and reps < 50:
+    while t < budget_s and reps < 100:
         t0 = time.perf_counter()
-        oracle.alltoallv(send, rows["sendcounts"], rows["sdispls"], recv, rows["recvcounts"], rows["rdispls"])
+        step()
         t += time.perf_counter() - t0
         reps += 1
-    algo = 2 * int(rows["sendcounts"].sum()) * 2
-    model = ""
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                model = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
+    verified = all(np.array_equal(got_r[d], out_r[d]) and np.array_equal(got_i[d], out_i[d]) for d in range(P))
+    mism = [d for d in range(P) if not (np.array_equal(got_r[d], out_r[d]) and np.array_equal(got_i[d], out_i[d]))]
+
+    nthreads = max(1, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1))
+    groups = _pair_groups(rows["sendcounts"], nthreads)
+    masks = [(_masked(rows, g), _masked(ids, g)) for g in groups]
+    par_r = [np.zeros_like(o) for o in out_r]
+    par_i = [np.zeros_like(o) for o in out_i]
+
+    def part(k):
+        (rs, rr), (is_, ir) = masks[k]
+        oracle.alltoallv(send_r, rs, rows["sdispls"], par_r, rr, rows["rdispls"])
+        oracle.alltoallv(send_i, is_, ids["sdispls"], par_i, ir, ids["rdispls"])
+
+    preps, pt = 0, 0.0
+    with ThreadPoolExecutor(max_workers=len(groups)) as pool:
+        while pt < par_budget_s and preps < 200:
+            t0 = time.perf_counter()
+            list(pool.map(part, range(len(groups))))
+            pt += time.perf_counter() - t0
+            preps += 1
+    par_same = all(np.array_equal(par_r[d], out_r[d]) and np.array_equal(par_i[d], out_i[d]) for d in range(P))
+
+    algo = 2 * (int(rows["sendcounts"].sum()) * 2 + int(ids["sendcounts"].sum()) * 4)
     return {"value": algo * reps / t / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"embedding-row AllToAllv of the same workload (8 ranks x 64 MiB bf16), "
-                      f"{reps} full repetitions in {t:.1f}s, single-threaded C oracle",
-            "cpu_model": model, "host_threads_available": os.cpu_count()}
+            "sample": f"the timed step's AllToAllv (8 ranks x 64 MiB bf16 rows + 1 MiB int32 ids, the same "
+                      f"inputs), {reps} full repetitions in {t:.1f}s, single-threaded C oracle",
+            "verified": bool(verified), "verified_what": "every element of the GPU's receive buffers after the "
+                                                           "last timed step equals the oracle's result",
+            "mismatched_destinations": mism,
+            "parallel": {"value": algo * preps / pt / 1e9, "unit": "GB/s", "cores": len(groups),
+                         "sample": f"{preps} repetitions in {pt:.1f}s, {len(groups)} host threads, each running "
+                                   f"the oracle on its share of the 64 (source, destination) pairs",
+                         "same_result": bool(par_same)},
+            "cpu": _cpu_description(), "host_threads_available": os.cpu_count()}
 
 
 # ------------------------------------------------------------------------ roofline
@@ -849,6 +980,9 @@ def main():
         _log("cpu baseline")
         line["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(line), flush=True)
+    if not args.no_cpu_baseline and not line["cpu_baseline"]["verified"]:
+        _log("the GPU's receive buffers differ from the oracle's result: the measured step is wrong")
+        sys.exit(3)
 
 
 if __name__ == "__main__":

@@ -4,7 +4,7 @@
  * The library follows the compiled communication model of the paper "HCCL: Collective
  * Communication for Meta Training and Inference Accelerators": for every collective the
  * host lowers the call into a complete program of chunked copy / reduce steps with
- * dependency ids (Section III-B "Data Path": work packets, subgraphs, WQEs and their
+ * dependency ids (Section III-B-2 "Data Path": work packets, subgraphs, WQEs and their
  * dependency kinds), and one device-resident executor runs that program (Section II-A-2:
  * the message engine's control core unrolls the graph and evaluates dependencies; the
  * near-memory compute unit performs copies and sums with FP32 arithmetic).
@@ -67,7 +67,7 @@ typedef enum { hcclBf16 = 0, hcclFp16 = 1, hcclFp32 = 2, hcclInt32 = 3 } hcclDat
  * INT32 SUM wraps modulo 2^32. */
 typedef enum { hcclSum = 0, hcclMax = 1, hcclMin = 2 } hcclRedOp_t;
 
-/* Schedules (Section III-B ring AllReduce; Section V-D topology-aware algorithms).
+/* Schedules (Section III-B-2 ring AllReduce; Section V-D topology-aware algorithms).
  * All of them fold the contributors of an element in ascending rank order, except
  * TWO_LEVEL, which folds ascending inside each group of `group_size` consecutive ranks
  * into FP32 partials and then folds the partials in ascending group order. */
@@ -84,7 +84,7 @@ typedef enum {
 /* Order in which the contributors of an element are folded (the result depends on it).
  * ASCENDING: ranks 0, 1, ..., P-1 (TWO_LEVEL: ascending inside each group, then over groups).
  * RING: an element of shard c is folded starting at rank c+1: c+1, c+2, ..., P-1, 0, ..., c,
- *   the order a ring reduce-scatter accumulates it (Section III-B ring AllReduce). For
+ *   the order a ring reduce-scatter accumulates it (Section III-B-2 ring AllReduce). For
  *   reduce-scatter, shard c is block c; for all-reduce, element i is in shard i / q with
  *   q = ceil(count / P) rounded up to a multiple of 64.
  * HALVING: the recursive-halving tree: values whose rank differs in bit P/2 are combined first,
@@ -94,6 +94,18 @@ typedef enum {
  * stay FP32 and the result is rounded once. */
 typedef enum { hcclOrderAscending = 0, hcclOrderRing = 1, hcclOrderHalving = 2 } hcclOrder_t;
 
+/*
+ * Configuration of a communicator (Section V-D: topology-aware algorithm selection, here the
+ * schedule, the fold order and the group size of the two-level schedule; Section III-B-2: the
+ * work packet's chunking into WQEs, here the chunk and tile sizes). Fields left at zero take the
+ * defaults.
+ *
+ * Two knobs of the paper have no field here. The message engines' cache-partition request
+ * bits (Section II-A-3) keep collective buffers from evicting application data; the executor's
+ * loads, and its copies' stores, always carry the non-temporal hint instead (the cache policy is
+ * an instruction field fixed when the executor is compiled). Per-packet counters (Section V-C)
+ * are the `trace` field.
+ */
 typedef struct {
     int32_t algo;          /* hcclAlgo_t */
     int32_t group_size;    /* ranks per group for TWO_LEVEL; 0 = none */
@@ -106,15 +118,21 @@ typedef struct {
     int32_t validate;      /* 1 = run the program validator on every compile */
     int32_t order;         /* hcclOrder_t */
     int32_t requantize;    /* 1 = round every partial to the buffer type */
-    int32_t reserved[3];
+    int32_t trace;         /* 1 = record a timestamp pair per tile of every launch (hccl_comm_trace) */
+    int32_t reserved[2];
 } hcclConfig_t;
 
 typedef struct hcclComm* hcclComm_t;
 
-/* Fills *cfg with the defaults. */
+/* Fills *cfg with the defaults (automatic schedule, fusion on, every other field zero).
+ * hcclInvalidArgument if cfg is NULL. */
 hcclResult_t hccl_config_init(hcclConfig_t* cfg);
 
 /*
+ * Communicator lifecycle (Section III-B-1 "Control Path": the host creates the resources a
+ * collective needs on demand and reuses them; Section V-B: compiled work packets stay in device
+ * memory so that a later call only re-enqueues them).
+ *
  * Creates a communicator of `nranks` virtual ranks on HIP device `device`. With
  * device == HCCL_NO_DEVICE the communicator is host-only: collective calls validate their
  * arguments and compile (and validate) the program, then return hcclSuccess without
@@ -124,13 +142,23 @@ hcclResult_t hccl_config_init(hcclConfig_t* cfg);
  */
 hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, hcclComm_t* comm);
 
-/* Waits for the communicator's outstanding work, then frees everything it owns. */
+/* Waits for the communicator's outstanding work, then frees everything it owns. NULL is a no-op.
+ * Buffers passed to collectives are the caller's and are not touched. */
 hcclResult_t hccl_comm_destroy(hcclComm_t comm);
 
-/* Replaces the configuration used by later calls (cached programs stay valid). */
+/* Replaces the configuration used by later calls (cached programs stay valid: the cache is keyed
+ * by the whole collective, configuration included). hcclInvalidArgument for a NULL argument. */
 hcclResult_t hccl_comm_set_config(hcclComm_t comm, const hcclConfig_t* cfg);
 
 /*
+ * The three reduction collectives (Section III-B-2 "Data Path": the ring AllReduce built from
+ * receive, NMC sum and send steps; Section II-A-2: the NMC sums BF16 / FP16 / FP32 buffers with
+ * FP32 arithmetic and re-quantises the result). sendbufs and recvbufs are arrays of P device
+ * pointers (rank r's buffer at index r), aligned to the element size; counts are elements.
+ * hcclInvalidArgument for NULL arrays or buffers, misalignment, bad enums or overlapping buffers;
+ * hcclUnsupported for a schedule / order combination that does not exist (for example HALVING
+ * with a rank count that is not a power of two). Nothing is enqueued on any error.
+ *
  * AllReduce: recvbufs[r][i] = R(sendbufs[0][i], ..., sendbufs[P-1][i]) for every rank r
  * and i < count. In place (sendbufs[r] == recvbufs[r] for every r) is allowed; any other
  * overlap between buffers is not.
@@ -139,14 +167,17 @@ hcclResult_t hccl_allreduce(hcclComm_t comm, const void* const* sendbufs, void* 
                             size_t count, hcclDataType_t dtype, hcclRedOp_t op, void* stream);
 
 /*
- * ReduceScatter: sendbufs[r] holds P * recvcount elements; recvbufs[c][j] =
+ * ReduceScatter (Section III-B-2; the first half of the ring AllReduce): sendbufs[r] holds
+ * P * recvcount elements; recvbufs[c][j] =
  * R(sendbufs[0][c*recvcount + j], ..., sendbufs[P-1][c*recvcount + j]). Receive buffers
  * must not overlap any send buffer.
  */
 hcclResult_t hccl_reduce_scatter(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,
                                  size_t recvcount, hcclDataType_t dtype, hcclRedOp_t op, void* stream);
 
-/* AllGather: recvbufs[r][q*sendcount + j] = sendbufs[q][j]. A byte copy for every dtype. */
+/* AllGather (Section III-B-2, the second half of the ring AllReduce; Section II-A-2: the NMC
+ * copy "A = B" doubles as a copy engine): recvbufs[r][q*sendcount + j] = sendbufs[q][j]. A byte
+ * copy for every dtype; buffers must not overlap. Errors as for the reductions above. */
 hcclResult_t hccl_allgather(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,
                             size_t sendcount, hcclDataType_t dtype, void* stream);
 
@@ -195,7 +226,7 @@ hcclResult_t hccl_alltoallv_dynamic(hcclComm_t comm,
                                     hcclDataType_t dtype, void* stream);
 
 /*
- * Groups (one work packet for several collectives, Section III-B: a work packet holds
+ * Groups (one work packet for several collectives, Section III-B-2: a work packet holds
  * several subgraphs). Collectives called on `comm` between hccl_group_start and the
  * matching hccl_group_end are checked when called but only recorded; hccl_group_end
  * compiles them into one program and enqueues it as one executor launch on the stream the
@@ -241,16 +272,21 @@ typedef struct {
 
 hcclResult_t hccl_set_trigger(hcclComm_t comm, const hcclTrigger_t* trigger);
 
-/* Thread-local text of the last error returned on this thread ("" if none). */
+/* Thread-local text of the last error returned on this thread ("" if none). The string belongs
+ * to the library and stays valid until the thread's next failing call. */
 const char* hccl_get_last_error(void);
 
-/* Name of a result code. */
+/* Name of a result code (a static string). */
 const char* hccl_result_string(hcclResult_t r);
 
 /*
- * Synchronises the communicator's device and reports a device-side failure recorded since
- * the previous call (hcclTimeout when a dependency wait or a trigger wait hit the watchdog,
- * hcclInvalidArgument when a device-resident layout was rejected), then clears it.
+ * Completion errors (Section III-B-2: the message engine reports every work request through a
+ * completion queue; Section V-C: completion and event handling on the device side). Work is
+ * enqueue-only, so a failure found on the device is kept in the communicator's error record.
+ * This call synchronises the communicator's device and reports a device-side failure recorded
+ * since the previous call (hcclTimeout when a dependency wait or a trigger wait hit the watchdog,
+ * hcclInvalidArgument when a device-resident layout was rejected), then clears it. While a
+ * triggered packet waits on the device, this waits for it too.
  */
 hcclResult_t hccl_get_async_error(hcclComm_t comm);
 
@@ -320,6 +356,8 @@ typedef struct {
     uint64_t scratch_bytes;      /* FP32 scratch the program needs */
     uint64_t program_bytes;      /* size of the device copy of the program */
     double compile_us;           /* host time to lower, fuse, validate and pack */
+    uint32_t step_tile_min;      /* smallest and largest tile (elements) of the program's copy and */
+    uint32_t step_tile_max;      /* reduce steps: steps of different element widths may differ */
 } hcclProgramInfo_t;
 
 hcclResult_t hccl_comm_last_program(hcclComm_t comm, hcclProgramInfo_t* info);

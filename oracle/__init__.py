@@ -6,7 +6,7 @@ library: the two share no code. The arithmetic lives in ``hccl_oracle.c`` (plain
 element and one contributor at a time); this module only builds it with gcc and marshals
 numpy arrays through ctypes.
 
-Semantics (paper, Section II-A-2 "Near Memory Compute" and Section III-B "Data Path"):
+Semantics (paper, Section II-A-2 "Near Memory Compute" and Section III-B-2 "Data Path"):
 BF16 / FP16 / FP32 buffers are reduced with FP32 arithmetic and re-quantised once to the
 buffer type with round-to-nearest-even; INT32 sums wrap modulo 2^32. The contributors of an
 element are folded in ascending rank order (``group=0``) or in the two-level order

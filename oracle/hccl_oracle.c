@@ -11,7 +11,7 @@
  *
  * Citations are to the paper "HCCL: Collective Communication for Meta Training and
  * Inference Accelerators": Section II-A-2 (Near Memory Compute: copy and sum, BF16/FP16/FP32
- * operands, FP32 arithmetic, re-quantisation to the buffer type) and Section III-B (Data
+ * operands, FP32 arithmetic, re-quantisation to the buffer type) and Section III-B-2 (Data
  * Path: the collectives AllReduce / ReduceScatter / AllGather / AllToAllv), Section IV-B-2
  * (device-resident collectives: AllToAllvDynamic, whose layout is read when it runs).
  */

@@ -6,7 +6,7 @@
  * They share no code, header, table or helper with the GPU library: every conversion and
  * every fold below is written out again here on purpose.
  *
- * What is computed (paper: Section III-B "Data Path" names the collectives, Section II-A-2
+ * What is computed (paper: Section III-B-2 "Data Path" names the collectives, Section II-A-2
  * "Near Memory Compute" fixes the arithmetic):
  *   - element types BF16, FP16 and FP32 are reduced with FP32 arithmetic and re-quantised
  *     once to the buffer type (round to nearest, ties to even); INT32 is added with two's
@@ -37,7 +37,7 @@ enum { ORC_BF16 = 0, ORC_FP16 = 1, ORC_FP32 = 2, ORC_INT32 = 3 };
 enum { ORC_SUM = 0, ORC_MAX = 1, ORC_MIN = 2 };
 
 /*
- * Fold orders beyond the default (paper: Section III-B ring AllReduce; Section II-A-2: the
+ * Fold orders beyond the default (paper: Section III-B-2 ring AllReduce; Section II-A-2: the
  * near-memory compute unit re-quantises every result to the buffer type).
  *   ORC_ORDER_ASCENDING : contributors 0, 1, ..., P-1.
  *   ORC_ORDER_TWO_LEVEL : `group` consecutive ranks folded ascending into a partial, then the

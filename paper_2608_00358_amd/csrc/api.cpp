@@ -1,6 +1,6 @@
 // api.cpp -- the C ABI: argument checks, program cache, upload and launch.
 //
-// Mirrors the host side of the paper's compiled model (Section III-B "Data Path"; Section V-B
+// Mirrors the host side of the paper's compiled model (Section III-B-2 "Data Path"; Section V-B
 // "Host-side Performance"): a collective call is validated, lowered into a complete program
 // (or found in the cache of compiled work packets, which then costs only a re-enqueue),
 // copied to device memory once, and enqueued as one executor launch on the caller's stream.
@@ -358,6 +358,8 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     info.scratch_bytes = dp->prog.scratch_bytes;
     info.program_bytes = dp->prog.image.size();
     info.compile_us = dp->compile_us;
+    info.step_tile_min = dp->prog.step_tile_min;
+    info.step_tile_max = dp->prog.step_tile_max;
 
     if (triggered) {
         if (dp->prog.ntiles == 0) return fail(hcclInvalidArgument, "a triggered work packet has no work to run");

@@ -1,6 +1,6 @@
 // compiler.cpp -- lowering, fusion and packing of descriptor programs (host only).
 //
-// Lowerings write out the schedules the paper describes (Section III-B: the ring AllReduce
+// Lowerings write out the schedules the paper describes (Section III-B-2: the ring AllReduce
 // built from per-hop receive/compute/send steps with dependencies; Section V-D: topology-
 // aware two-level schedules that keep most traffic inside a group of consecutive ranks).
 // On one GPU a "send" from rank a to rank b is a read of a's buffer by the step that writes
@@ -107,7 +107,7 @@ void for_chunks(uint64_t begin, uint64_t end, uint64_t C, F&& f) {
 
 // ---------------------------------------------------------------------------- DIRECT
 // One step per chunk: read every contributor, write every destination (the one-shot,
-// all-to-all style schedule used for small messages, Section V-E).
+// all-to-all style schedule of the PE collective kernels for small messages, Section V-F-3).
 void lower_direct(const CollectiveSpec& s, HostProgram& p) {
     Builder b{p};
     const int P = s.P;
@@ -993,6 +993,7 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     uint64_t ntiles = 0;
     p.bytes_read = p.bytes_written = 0;
     p.max_srcs = 0;
+    p.step_tile_min = p.step_tile_max = 0;
     bool has_deps = false;
     for (uint32_t i = 0; i < nd; ++i) {
         const HostDesc& h = p.descs[i];
@@ -1008,6 +1009,10 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
         d.requant = h.requant ? 1u : 0u;
         const uint64_t dte = step_tile(h);
         d.tile_elems = (uint32_t)dte;
+        if (h.op == OP_COPY || h.op == OP_REDUCE) {
+            p.step_tile_min = p.step_tile_min ? std::min<uint32_t>(p.step_tile_min, (uint32_t)dte) : (uint32_t)dte;
+            p.step_tile_max = std::max<uint32_t>(p.step_tile_max, (uint32_t)dte);
+        }
         d.aux = h.aux;
         uint64_t nt = (h.op == OP_NOOP) ? 1 : (h.nelem + dte - 1) / dte;
         if (h.op == OP_DYN_COPY) {

@@ -1,7 +1,7 @@
 // compiler.h -- host-side lowering of collectives into descriptor programs.
 //
 // The host builds the complete description of a collective, dependencies included, before
-// anything runs on the device (paper, Section III-B "Data Path"; host-side generation,
+// anything runs on the device (paper, Section III-B-2 "Data Path"; host-side generation,
 // Section V-B). Lowerings emit the schedule step by step (ring reduce chains and forwarding
 // hops, two-level group phases); the fusion pass then merges chained steps whose
 // intermediate only feeds the next step, which keeps the arithmetic (same operations in
@@ -75,6 +75,8 @@ struct HostProgram {
 
     // filled by finalize()
     uint32_t tile_elems = 0;
+    uint32_t step_tile_min = 0;  // smallest and largest per-step tile (elements) of the packed
+    uint32_t step_tile_max = 0;  // program; they differ where steps of other widths share it
     uint32_t ntiles = 0;
     uint32_t ndeps = 0;
     uint32_t noperands = 0;

@@ -1,6 +1,6 @@
 // program.h -- the descriptor program shared by the host compiler and the device executor.
 //
-// A program is the single-GPU form of a work packet (paper, Section III-B "Data Path"):
+// A program is the single-GPU form of a work packet (paper, Section III-B-2 "Data Path"):
 // a topologically ordered list of steps (descriptors, the analogue of WQEs) with explicit
 // dependency ids. Descriptors refer to buffers by id, never by address, so a compiled
 // program is reused for any buffers of the same shape (work packet caching, Section V-B);

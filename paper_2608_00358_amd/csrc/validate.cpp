@@ -1,7 +1,7 @@
 // validate.cpp -- structural checks of a finalized descriptor program (host only).
 //
 // The paper's compiled model puts the whole dependency structure of a collective in the
-// host-generated graph (Section III-B: Fence, Sync, WQE Sync, Receive Sync, Send Sync and
+// host-generated graph (Section III-B-2: Fence, Sync, WQE Sync, Receive Sync, Send Sync and
 // NOOP joins). Here every ordering is an explicit dependency id, so the host can prove, before
 // anything runs, that the program is well formed:
 //   * every dependency names an earlier step (the program is topologically ordered), and a

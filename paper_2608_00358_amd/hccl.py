@@ -44,7 +44,7 @@ class hcclConfig_t(ctypes.Structure):
         ("algo", ctypes.c_int32), ("group_size", ctypes.c_int32), ("chunk_bytes", ctypes.c_uint64),
         ("fuse", ctypes.c_int32), ("max_workers", ctypes.c_int32), ("tile_bytes", ctypes.c_uint32),
         ("timeout_ms", ctypes.c_uint32), ("validate", ctypes.c_int32), ("order", ctypes.c_int32),
-        ("requantize", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3),
+        ("requantize", ctypes.c_int32), ("trace", ctypes.c_int32), ("reserved", ctypes.c_int32 * 2),
     ]
 
 
@@ -63,6 +63,7 @@ class hcclProgramInfo_t(ctypes.Structure):
         ("max_srcs", ctypes.c_uint32), ("inline_launch", ctypes.c_uint32), ("pad", ctypes.c_uint32),
         ("bytes_read", ctypes.c_uint64), ("bytes_written", ctypes.c_uint64),
         ("scratch_bytes", ctypes.c_uint64), ("program_bytes", ctypes.c_uint64), ("compile_us", ctypes.c_double),
+        ("step_tile_min", ctypes.c_uint32), ("step_tile_max", ctypes.c_uint32),
     ]
 
 

@@ -232,6 +232,29 @@ def test_group_merges_calls_into_one_program():
     assert g["collective"] == -1
 
 
+@pytest.mark.parametrize("rows_per_rank, tiles", [(5000, (2048, 2048)), (12000, (2048, 4096)),
+                                                  (1 << 18, (2048, 4096))])
+def test_grouped_rows_and_ids_tile_each_step_by_its_width(rows_per_rank, tiles):
+    """The embedding exchange recorded as one group (rows of 128 bf16 plus int32 ids): without
+    dependencies every step is cut by its own element width (8 KiB tiles: 4096 bf16 or 2048
+    int32 elements), capped so that small programs still spread over 2048 tiles."""
+    P, D = 8, 128
+    counts = zipf_counts(P, rows_per_rank, 1.1, seed=0)
+    rows, ids = alltoallv_layout(counts, D), alltoallv_layout(counts, 1)
+    with comm(P) as c:
+        H.hccl_group_start(c.handle)
+        H.hccl_alltoallv(c.handle, fake_bufs(P, 1 << 40), rows["sendcounts"], rows["sdispls"], fake_bufs(P, 1 << 44),
+                         rows["recvcounts"], rows["rdispls"], "bf16")
+        H.hccl_alltoallv(c.handle, fake_bufs(P, 1 << 42), ids["sendcounts"], ids["sdispls"], fake_bufs(P, 1 << 46),
+                         ids["recvcounts"], ids["rdispls"], "int32")
+        H.hccl_group_end(c.handle)
+        info = info_of(c)
+    assert (info["step_tile_min"], info["step_tile_max"]) == tiles
+    payload = int(rows["sendcounts"].sum()) * 2 + int(ids["sendcounts"].sum()) * 4
+    assert info["bytes_read"] == info["bytes_written"] == payload
+    assert info["num_deps"] == 0 and info["scratch_bytes"] == 0
+
+
 def test_group_rejects_overlap_between_calls_and_unbalanced_end():
     P = 2
     with comm(P) as c:

@@ -1,9 +1,11 @@
-"""Parity at the full benchmark sizes, in the launch configuration bench.py times.
+"""Parity at the full benchmark sizes.
 
 Every output element is compared with the oracle (the oracle finishes each of these in
 seconds on the host). Inputs come from the same seeded generators as bench.py: host
 generators for the small configurations, the seeded device generator for the large ones
-(copied back to the host for the oracle).
+(copied back to the host for the oracle). The AllToAllv configuration is run both in the
+form bench.py times (rows and ids recorded in one group: one program, one launch, whose copy
+steps have 4096-element bf16 tiles beside 2048-element int32 tiles) and as two launches.
 """
 import numpy as np
 import pytest
@@ -39,9 +41,54 @@ def test_allreduce_ring_p4_fp32_full():
         assert same_bits(got, want[r], "fp32", nan_equal=False), f"rank {r}: {first_mismatch(got, want[r])}"
 
 
-def test_alltoallv_zipf_p8_embedding_rows_and_ids_full():
+def _alltoallv_rows_ids_oracle(send_rows, id_vals, rows, ids, P):
+    host_rows = [to_host(t, "bf16") for t in send_rows]
+    want_rows = [np.zeros(int(rows["recv_len"][d]), np.uint16) for d in range(P)]
+    oracle.alltoallv(host_rows, rows["sendcounts"], rows["sdispls"], want_rows, rows["recvcounts"], rows["rdispls"])
+    want_ids = [np.zeros(int(ids["recv_len"][d]), np.int32) for d in range(P)]
+    oracle.alltoallv([id_vals[s] for s in range(P)], ids["sendcounts"], ids["sdispls"], want_ids,
+                     ids["recvcounts"], ids["rdispls"])
+    return want_rows, want_ids
+
+
+def test_alltoallv_zipf_p8_rows_and_ids_grouped_one_launch_as_benchmarked():
+    """The timed headline step: rows and ids as one group, compiled into one program whose row
+    steps keep 8 KiB (4096-element) tiles beside the ids' 2048-element tiles, one launch."""
     P, R, D = 8, 1 << 18, 128
-    print("full config: alltoallv P=8 2^18 rows x 128 bf16 Zipf(1.1) + int32 ids", flush=True)
+    print("full config: alltoallv P=8 2^18 rows x 128 bf16 Zipf(1.1) + int32 ids, one grouped launch", flush=True)
+    counts = zipf_counts(P, R, 1.1, seed=0)
+    rows, ids = alltoallv_layout(counts, D), alltoallv_layout(counts, 1)
+    send_rows = device_normal_bf16(P, R * D, seed=0)
+    id_vals = row_ids_int32(P, R, seed=1)
+    send_ids = [to_device(id_vals[s], "int32") for s in range(P)]
+    # receive buffers start from a poison pattern: a range the launch skipped would show
+    recv_rows = [torch.full((int(rows["recv_len"][d]),), -7.0, dtype=torch.bfloat16, device="cuda:0")
+                 for d in range(P)]
+    recv_ids = [torch.full((int(ids["recv_len"][d]),), -5, dtype=torch.int32, device="cuda:0") for d in range(P)]
+    with H.Comm(P, device=0) as c:
+        for _ in range(2):   # the second launch reuses the cached program, as the timed steps do
+            with c.group():
+                c.alltoallv(send_rows, rows["sendcounts"], rows["sdispls"], recv_rows, rows["recvcounts"],
+                            rows["rdispls"])
+                c.alltoallv(send_ids, ids["sendcounts"], ids["sdispls"], recv_ids, ids["recvcounts"], ids["rdispls"])
+        torch.cuda.synchronize()
+        info = c.last_program()
+        assert c.async_error() == 0
+    assert info["collective"] == -1 and info["cache_hit"] == 1 and info["inline_launch"] == 0
+    assert (info["step_tile_min"], info["step_tile_max"]) == (2048, 4096), info
+    assert info["bytes_read"] == info["bytes_written"] == int(rows["sendcounts"].sum()) * 2 + int(
+        ids["sendcounts"].sum()) * 4
+    want_rows, want_ids = _alltoallv_rows_ids_oracle(send_rows, id_vals, rows, ids, P)
+    for d in range(P):
+        assert np.array_equal(to_host(recv_rows[d], "bf16"), want_rows[d]), f"rows at destination {d}"
+        assert np.array_equal(to_host(recv_ids[d], "int32"), want_ids[d]), f"ids at destination {d}"
+    print(f"grouped launch: {info['num_descs']} steps, {info['num_tiles']} tiles, {info['workers']} wavefronts",
+          flush=True)
+
+
+def test_alltoallv_zipf_p8_embedding_rows_and_ids_full_as_two_launches():
+    P, R, D = 8, 1 << 18, 128
+    print("full config: alltoallv P=8 2^18 rows x 128 bf16 Zipf(1.1) + int32 ids, two launches", flush=True)
     counts = zipf_counts(P, R, 1.1, seed=0)
     rows, ids = alltoallv_layout(counts, D), alltoallv_layout(counts, 1)
     send_rows = device_normal_bf16(P, R * D, seed=0)
@@ -54,12 +101,7 @@ def test_alltoallv_zipf_p8_embedding_rows_and_ids_full():
         c.alltoallv(send_ids, ids["sendcounts"], ids["sdispls"], recv_ids, ids["recvcounts"], ids["rdispls"])
         torch.cuda.synchronize()
         assert c.async_error() == 0
-    host_rows = [to_host(t, "bf16") for t in send_rows]
-    want_rows = [np.zeros(int(rows["recv_len"][d]), np.uint16) for d in range(P)]
-    oracle.alltoallv(host_rows, rows["sendcounts"], rows["sdispls"], want_rows, rows["recvcounts"], rows["rdispls"])
-    want_ids = [np.zeros(int(ids["recv_len"][d]), np.int32) for d in range(P)]
-    oracle.alltoallv([id_vals[s] for s in range(P)], ids["sendcounts"], ids["sdispls"], want_ids,
-                     ids["recvcounts"], ids["rdispls"])
+    want_rows, want_ids = _alltoallv_rows_ids_oracle(send_rows, id_vals, rows, ids, P)
     for d in range(P):
         assert np.array_equal(to_host(recv_rows[d], "bf16"), want_rows[d]), f"rows at destination {d}"
         assert np.array_equal(to_host(recv_ids[d], "int32"), want_ids[d]), f"ids at destination {d}"

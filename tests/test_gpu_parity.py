@@ -297,14 +297,17 @@ def test_single_step_allgather_copy_inline():
         assert np.array_equal(out.result(), x[0]) and out.guards_intact()
 
 
-def test_group_of_embedding_rows_and_ids_is_one_launch():
+@pytest.mark.parametrize("rows_per_rank", [5000, 12000])
+def test_group_of_embedding_rows_and_ids_is_one_launch(rows_per_rank):
+    """5000 rows per rank cut every step into one 2048-element tile size; from about 8200 rows
+    the bf16 row steps keep 4096-element tiles beside the int32 ids' 2048."""
     P = 8
-    counts = zipf_counts(P, 5000, 1.1, seed=40)
+    counts = zipf_counts(P, rows_per_rank, 1.1, seed=40)
     rows, ids = alltoallv_layout(counts, 128), alltoallv_layout(counts, 1)
     rng = np.random.default_rng(41)
     rows_h = [rng.integers(0, 2 ** 16, int(rows["send_len"][s]), dtype=np.int64).astype(np.uint16) for s in range(P)]
     ids_h = [rng.integers(-2 ** 31, 2 ** 31, int(ids["send_len"][s]), dtype=np.int64).astype(np.int32) for s in range(P)]
-    print("group: alltoallv rows + ids", flush=True)
+    print(f"group: alltoallv rows + ids, {rows_per_rank} rows per rank", flush=True)
     with H.Comm(P, device=0) as c:
         sr = [to_device(rows_h[s], "bf16") for s in range(P)]
         si = [to_device(ids_h[s], "int32") for s in range(P)]
@@ -317,6 +320,8 @@ def test_group_of_embedding_rows_and_ids_is_one_launch():
         info = c.last_program()
         assert c.async_error() == 0
     assert info["collective"] == -1
+    tiles = (2048, 2048) if rows_per_rank == 5000 else (2048, 4096)
+    assert (info["step_tile_min"], info["step_tile_max"]) == tiles, info
     want_r = [np.zeros(o.n, np.uint16) for o in rr]
     want_i = [np.zeros(o.n, np.int32) for o in ri]
     oracle.alltoallv(rows_h, rows["sendcounts"], rows["sdispls"], want_r, rows["recvcounts"], rows["rdispls"])

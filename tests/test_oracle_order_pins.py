@@ -1,5 +1,5 @@
 """Pins for the oracle's other fold orders: ring (rotated per shard), recursive-halving tree,
-and per-combine re-quantisation to the buffer type (paper, Section III-B ring AllReduce;
+and per-combine re-quantisation to the buffer type (paper, Section III-B-2 ring AllReduce;
 Section II-A-2 NMC re-quantisation). Each order is checked against an independent numpy /
 torch formulation, closed forms and hand-built cancellation cases that tell the orders apart.
 """

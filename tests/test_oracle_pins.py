@@ -3,7 +3,7 @@
 Each test ties the oracle to a library routine that implements the same definition
 independently (numpy / torch IEEE conversions and float32 adds), to a closed form, to a
 brute-force pure-Python loop on tiny inputs, or to an invariant of the collective
-definitions (paper, Section III-B "Data Path"; arithmetic of Section II-A-2 "Near Memory
+definitions (paper, Section III-B-2 "Data Path"; arithmetic of Section II-A-2 "Near Memory
 Compute"). The set is chosen so that a plausible slip in the oracle -- a dropped or extra
 term, a wrong block or rank index, the wrong fold order, a +0.0 seed, a bad rounding rule,
 a transposed count table -- fails at least one of them.
