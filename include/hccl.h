@@ -167,6 +167,26 @@ hcclResult_t hccl_allreduce(hcclComm_t comm, const void* const* sendbufs, void* 
                             size_t count, hcclDataType_t dtype, hcclRedOp_t op, void* stream);
 
 /*
+ * Allocation-free AllReduce, for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc. Same result, arguments
+ * and argument checks as hccl_allreduce under the communicator's configuration. The call's
+ * program image, dependency counters and FP32 partials live in a static workspace of 64 MiB
+ * that the library holds on every device it runs on until the process ends; the call makes no
+ * hipMalloc, hipFree or other device allocation (its program is compiled, and cached, in host
+ * memory). On `stream` it copies the program into the workspace, clears the counters with a
+ * fill kernel and launches the executor (a one-step program goes in the launch packet and does
+ * not touch the workspace). The communicator must have a device (its error record, allocated
+ * by hccl_comm_create, is used); the inputs and outputs are the caller's as usual.
+ * Every call on one device shares that workspace and finds it as the last call left it: calls
+ * whose work can overlap in time on one GPU (other streams, other communicators) race, and the
+ * caller must order them. A call that needs more than the workspace holds (image + counters +
+ * partials) fails with hcclInvalidArgument before anything is enqueued. Inside a group, with a
+ * pending trigger or while the resident executor runs: hcclUnsupported.
+ */
+hcclResult_t hccl_allreduce_noalloc(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,
+                                    size_t count, hcclDataType_t dtype, hcclRedOp_t op, void* stream);
+
+/*
  * ReduceScatter (Section III-B-2; the first half of the ring AllReduce): sendbufs[r] holds
  * P * recvcount elements; recvbufs[c][j] =
  * R(sendbufs[0][c*recvcount + j], ..., sendbufs[P-1][c*recvcount + j]). Receive buffers

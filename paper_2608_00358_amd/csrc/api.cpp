@@ -32,6 +32,8 @@ hipError_t executor_occupancy(int kind, int* blocks_per_cu);
 hipError_t launch_resident(const ResidentArgs& r, uint32_t blocks, hipStream_t stream);
 hipError_t resident_occupancy(int* blocks_per_cu);
 int executor_waves_per_block();
+size_t workspace_bytes();
+hipError_t workspace_address(void** ptr);
 }  // namespace hccl
 
 using namespace hccl;
@@ -106,6 +108,10 @@ struct hcclComm {
     uint32_t* d_ctl = nullptr;
     hipStream_t resident_stream = nullptr;
     uint64_t resident_seq = 0;        // last packet published
+    // allocation-free calls: this device's static workspace and host-only compiled programs
+    void* workspace = nullptr;
+    std::string workspace_error;
+    std::list<std::pair<CollectiveSpec, std::unique_ptr<HostProgram>>> host_cache;
 };
 
 namespace {
@@ -317,6 +323,81 @@ hcclResult_t resident_submit(hcclComm* c, const LaunchArgs& a, DeviceProgram* dp
     return hcclSuccess;
 }
 
+// Executor kernel and grid of a launch: the leanest kernel that covers the program (the aligned
+// copy kernel only if every user buffer is 16-byte aligned), sized to the resident capacity of
+// the CUs the stream may use, capped by the configuration and by the program's tiles.
+// Sets a.nworkers and `blocks`; returns the kernel kind.
+int launch_shape(hcclComm* c, const HostProgram& prog, LaunchArgs& a, uint32_t nuser, hipStream_t s,
+                 uint32_t& blocks) {
+    const uint32_t wpb = (uint32_t)executor_waves_per_block();
+    uint32_t cus = stream_cu_count(c, s);
+    int kind = prog.kind;
+    if (kind == kKindCopyAligned) {
+        for (uint32_t i = 0; i < nuser; ++i)
+            if ((uintptr_t)a.bufs[i] % 16) kind = kKindCopyOnly;
+    }
+    uint32_t slots = cus * (uint32_t)std::max(1, c->blocks_per_cu[kind]) * wpb;
+    if (c->cfg.max_workers > 0) slots = std::min<uint32_t>(slots, (uint32_t)c->cfg.max_workers);
+    uint32_t workers = std::min<uint32_t>(slots, prog.ntiles);
+    blocks = (workers + wpb - 1) / wpb;
+    if (blocks == 0) blocks = 1;
+    a.nworkers = blocks * wpb;
+    return kind;
+}
+
+// A program of one plain step without dependencies travels in the launch packet itself.
+bool inline_eligible(const hcclComm* c, const HostProgram& prog, bool triggered) {
+    const bool plain_step = prog.descs.size() == 1 && (prog.descs[0].op == OP_COPY || prog.descs[0].op == OP_REDUCE);
+    return c->inline_single_step && plain_step && (prog.flags & PF_HAS_DEPS) == 0 && !c->dynamic_dispatch &&
+           !triggered;
+}
+
+hipError_t launch_inline_step(const HostProgram& prog, const LaunchArgs& a, uint32_t blocks, int kind, hipStream_t s) {
+    const HostDesc& d = prog.descs[0];
+    InlineArgs ia;
+    std::memset(&ia, 0, sizeof ia);
+    ia.nelem = d.nelem;
+    ia.tile_elems = prog.tile_elems;
+    ia.ntiles = prog.ntiles;
+    ia.nworkers = a.nworkers;
+    ia.op = d.op;
+    ia.redop = d.redop;
+    ia.nsrc = (uint32_t)d.srcs.size();
+    ia.ndst = (uint32_t)d.dsts.size();
+    ia.group = d.group;
+    ia.fold = d.fold;
+    ia.requant = d.requant ? 1u : 0u;
+    ia.es_first = dtype_size(d.srcs[0].dtype);
+    ia.es_rest = dtype_size(d.srcs.size() > 1 ? d.srcs[1].dtype : d.srcs[0].dtype);
+    ia.es_out = dtype_size(d.dsts[0].dtype);
+    ia.sig = reduce_signature(d.srcs[0].dtype, d.srcs.size() > 1 ? d.srcs[1].dtype : d.srcs[0].dtype, d.dsts[0].dtype);
+    for (size_t j = 0; j < d.srcs.size(); ++j) ia.src[j] = (uint64_t)(uintptr_t)a.bufs[d.srcs[j].buf] + d.srcs[j].offset;
+    for (size_t j = 0; j < d.dsts.size(); ++j) ia.dst[j] = (uint64_t)(uintptr_t)a.bufs[d.dsts[j].buf] + d.dsts[j].offset;
+    return launch_executor_inline(ia, blocks, kind, s);
+}
+
+// Program description for hccl_comm_last_program.
+void describe(hcclProgramInfo_t& info, const std::vector<CollectiveSpec>& specs, const HostProgram& prog, bool hit,
+              double compile_us) {
+    std::memset(&info, 0, sizeof info);
+    info.collective = specs.size() == 1 ? specs[0].coll : -1;
+    info.algo = prog.algo;
+    info.fused = prog.fused ? 1 : 0;
+    info.cache_hit = hit ? 1 : 0;
+    info.num_descs = (uint32_t)prog.descs.size();
+    info.num_tiles = prog.ntiles;
+    info.num_deps = prog.ndeps;
+    info.num_operands = prog.noperands;
+    info.max_srcs = prog.max_srcs;
+    info.bytes_read = prog.bytes_read;
+    info.bytes_written = prog.bytes_written;
+    info.scratch_bytes = prog.scratch_bytes;
+    info.program_bytes = prog.image.size();
+    info.compile_us = compile_us;
+    info.step_tile_min = prog.step_tile_min;
+    info.step_tile_max = prog.step_tile_max;
+}
+
 // Compiles and enqueues one work packet (a list of collective calls on one stream).
 hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     DeviceProgram* dp = nullptr;
@@ -343,23 +424,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     if (r != hcclSuccess) return r;
 
     hcclProgramInfo_t& info = c->last;
-    std::memset(&info, 0, sizeof info);
-    info.collective = specs.size() == 1 ? specs[0].coll : -1;
-    info.algo = dp->prog.algo;
-    info.fused = dp->prog.fused ? 1 : 0;
-    info.cache_hit = hit ? 1 : 0;
-    info.num_descs = (uint32_t)dp->prog.descs.size();
-    info.num_tiles = dp->prog.ntiles;
-    info.num_deps = dp->prog.ndeps;
-    info.num_operands = dp->prog.noperands;
-    info.max_srcs = dp->prog.max_srcs;
-    info.bytes_read = dp->prog.bytes_read;
-    info.bytes_written = dp->prog.bytes_written;
-    info.scratch_bytes = dp->prog.scratch_bytes;
-    info.program_bytes = dp->prog.image.size();
-    info.compile_us = dp->compile_us;
-    info.step_tile_min = dp->prog.step_tile_min;
-    info.step_tile_max = dp->prog.step_tile_max;
+    describe(info, specs, dp->prog, hit, dp->compile_us);
 
     if (triggered) {
         if (dp->prog.ntiles == 0) return fail(hcclInvalidArgument, "a triggered work packet has no work to run");
@@ -428,47 +493,13 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
 
     if (c->resident) return resident_submit(c, a, dp);
 
-    const uint32_t wpb = (uint32_t)executor_waves_per_block();
-    uint32_t cus = stream_cu_count(c, s);
-    int kind = dp->prog.kind;
-    if (kind == kKindCopyAligned) {
-        for (uint32_t i = 0; i < nuser; ++i)
-            if ((uintptr_t)a.bufs[i] % 16) kind = kKindCopyOnly;
-    }
-    uint32_t slots = cus * (uint32_t)std::max(1, c->blocks_per_cu[kind]) * wpb;
-    if (c->cfg.max_workers > 0) slots = std::min<uint32_t>(slots, (uint32_t)c->cfg.max_workers);
-    uint32_t workers = std::min<uint32_t>(slots, dp->prog.ntiles);
-    uint32_t blocks = (workers + wpb - 1) / wpb;
-    if (blocks == 0) blocks = 1;
-    a.nworkers = blocks * wpb;
+    uint32_t blocks = 0;
+    const int kind = launch_shape(c, dp->prog, a, nuser, s, blocks);
     info.workers = a.nworkers;
 
-    const bool plain_step = dp->prog.descs.size() == 1 &&
-                            (dp->prog.descs[0].op == OP_COPY || dp->prog.descs[0].op == OP_REDUCE);
-    if (c->inline_single_step && plain_step && !has_deps && !c->dynamic_dispatch && !triggered) {
-        const HostDesc& d = dp->prog.descs[0];
-        InlineArgs ia;
-        std::memset(&ia, 0, sizeof ia);
-        ia.nelem = d.nelem;
-        ia.tile_elems = dp->prog.tile_elems;
-        ia.ntiles = dp->prog.ntiles;
-        ia.nworkers = a.nworkers;
-        ia.op = d.op;
-        ia.redop = d.redop;
-        ia.nsrc = (uint32_t)d.srcs.size();
-        ia.ndst = (uint32_t)d.dsts.size();
-        ia.group = d.group;
-        ia.fold = d.fold;
-        ia.requant = d.requant ? 1u : 0u;
-        ia.es_first = dtype_size(d.srcs[0].dtype);
-        ia.es_rest = dtype_size(d.srcs.size() > 1 ? d.srcs[1].dtype : d.srcs[0].dtype);
-        ia.es_out = dtype_size(d.dsts[0].dtype);
-        ia.sig = reduce_signature(d.srcs[0].dtype, d.srcs.size() > 1 ? d.srcs[1].dtype : d.srcs[0].dtype,
-                                  d.dsts[0].dtype);
-        for (size_t j = 0; j < d.srcs.size(); ++j) ia.src[j] = (uint64_t)(uintptr_t)a.bufs[d.srcs[j].buf] + d.srcs[j].offset;
-        for (size_t j = 0; j < d.dsts.size(); ++j) ia.dst[j] = (uint64_t)(uintptr_t)a.bufs[d.dsts[j].buf] + d.dsts[j].offset;
+    if (inline_eligible(c, dp->prog, triggered)) {
         info.inline_launch = 1;
-        hipError_t e = launch_executor_inline(ia, blocks, kind, s);
+        hipError_t e = launch_inline_step(dp->prog, a, blocks, kind, s);
         if (e != hipSuccess) return hip_fail(e, "inline executor launch");
         return hcclSuccess;
     }
@@ -601,6 +632,11 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
         if (e != hipSuccess) return fail(hcclOutOfMemory, "error record allocation failed");
         e = hipMemset(c->d_error, 0, sizeof(ErrorRecord));
         if (e != hipSuccess) return hip_fail(e, "error record init");
+        // the device address of the static workspace, looked up once per device (allocation-free calls)
+        void* ws = nullptr;
+        e = workspace_address(&ws);
+        if (e == hipSuccess) c->workspace = ws;
+        else c->workspace_error = hipGetErrorString(e);
     }
     *out = c.release();
     return hcclSuccess;
@@ -632,8 +668,13 @@ hcclResult_t hccl_comm_set_config(hcclComm_t comm, const hcclConfig_t* cfg) {
     return hcclSuccess;
 }
 
-hcclResult_t hccl_allreduce(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs, size_t count,
-                            hcclDataType_t dtype, hcclRedOp_t op, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of an all-reduce and its collective spec.
+hcclResult_t allreduce_spec(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs, size_t count,
+                            hcclDataType_t dtype, hcclRedOp_t op, CollectiveSpec& s) {
     hcclResult_t r;
     if ((r = check_comm(comm)) || (r = check_ptr_arrays(sendbufs, recvbufs)) || (r = check_dtype(dtype)) ||
         (r = check_op(op)))
@@ -657,11 +698,120 @@ hcclResult_t hccl_allreduce(hcclComm_t comm, const void* const* sendbufs, void* 
         });
         if (r) return r;
     }
-    CollectiveSpec s;
     if ((r = fill_spec(comm, s, COLL_ALLREDUCE, dtype, op))) return r;
     s.count = count;
     s.in_place = in_place && count > 0;
+    return hcclSuccess;
+}
+
+// Host-only program of an allocation-free call: lowered, fused, packed (and validated on
+// request), kept in a small cache on the communicator. Only host memory is used.
+hcclResult_t host_program(hcclComm* c, const CollectiveSpec& s, const HostProgram*& out, bool& hit,
+                          double& compile_us) {
+    for (auto it = c->host_cache.begin(); it != c->host_cache.end(); ++it) {
+        if (it->first == s) {
+            if (it != c->host_cache.begin()) c->host_cache.splice(c->host_cache.begin(), c->host_cache, it);
+            out = c->host_cache.front().second.get();
+            hit = true;
+            compile_us = 0;
+            return hcclSuccess;
+        }
+    }
+    hit = false;
+    const auto t0 = std::chrono::steady_clock::now();
+    auto hp = std::make_unique<HostProgram>();
+    std::string err;
+    if (!lower(s, *hp, err)) return fail(hcclUnsupported, err);
+    if (s.fuse) fuse(*hp);
+    if (!finalize(*hp, s.tile_bytes, err)) return fail(hcclInternalError, err);
+    if ((c->cfg.validate || env_flag("HCCL_VALIDATE")) && !validate(*hp, s, err))
+        return fail(hcclInternalError, "program validation failed: " + err);
+    compile_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+    c->host_cache.emplace_front(s, std::move(hp));
+    while (c->host_cache.size() > 16) c->host_cache.pop_back();
+    out = c->host_cache.front().second.get();
+    return hcclSuccess;
+}
+
+uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+
+}  // namespace
+
+extern "C" {
+
+hcclResult_t hccl_allreduce(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs, size_t count,
+                            hcclDataType_t dtype, hcclRedOp_t op, void* stream) {
+    CollectiveSpec s;
+    hcclResult_t r = allreduce_spec(comm, sendbufs, recvbufs, count, dtype, op, s);
+    if (r != hcclSuccess) return r;
     return run(comm, s, sendbufs, recvbufs, stream);
+}
+
+hcclResult_t hccl_allreduce_noalloc(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,
+                                    size_t count, hcclDataType_t dtype, hcclRedOp_t op, void* stream) {
+    CollectiveSpec s;
+    hcclResult_t r = allreduce_spec(comm, sendbufs, recvbufs, count, dtype, op, s);
+    if (r != hcclSuccess) return r;
+    if (comm->device == HCCL_NO_DEVICE)
+        return fail(hcclInvalidArgument, "hccl_allreduce_noalloc needs a communicator with a device");
+    if (comm->group_depth > 0) return fail(hcclUnsupported, "hccl_allreduce_noalloc cannot be recorded in a group");
+    if (comm->resident)
+        return fail(hcclUnsupported, "hccl_allreduce_noalloc is launched on its stream, not handed to the resident executor");
+    if (comm->has_trigger)
+        return fail(hcclUnsupported, "a trigger is set for the next work packet; hccl_allreduce_noalloc takes none");
+    if (!comm->workspace)
+        return fail(hcclHipError, "the static workspace is not available on this device: " + comm->workspace_error);
+    DeviceGuard guard(comm->device);
+    const HostProgram* hp = nullptr;
+    bool hit = false;
+    double compile_us = 0;
+    if ((r = host_program(comm, s, hp, hit, compile_us)) != hcclSuccess) return r;
+    describe(comm->last, {s}, *hp, hit, compile_us);
+    if (hp->ntiles == 0) return hcclSuccess;
+
+    // workspace layout of this call: program image, counters, FP32 partials
+    const uint64_t off_state = align256(hp->image.size());
+    const uint64_t off_scratch = align256(off_state + (uint64_t)hp->nstate * sizeof(uint32_t));
+    const uint64_t need = off_scratch + hp->scratch_bytes;
+    if (need > workspace_bytes())
+        return fail(hcclInvalidArgument, "hccl_allreduce_noalloc: this all-reduce needs " + std::to_string(need) +
+                                             " bytes of workspace (program, counters and partials); the static "
+                                             "workspace holds " + std::to_string(workspace_bytes()));
+    char* ws = (char*)comm->workspace;
+    hipStream_t st = (hipStream_t)stream;
+    LaunchArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.prog = (const uint8_t*)ws;
+    a.state = (uint32_t*)(ws + off_state);
+    a.error = comm->d_error;
+    const int P = s.P;
+    for (int i = 0; i < P; ++i) {
+        a.bufs[send_buf(i)] = (char*)sendbufs[i];
+        a.bufs[recv_buf(P, i)] = (char*)recvbufs[i];
+    }
+    a.bufs[scratch_buf(P)] = ws + off_scratch;
+    a.dynamic = comm->dynamic_dispatch ? 1u : 0u;
+    const uint64_t ms = comm->cfg.timeout_ms ? comm->cfg.timeout_ms : 2000u;
+    a.timeout_ticks = ms * comm->wall_clock_khz;
+    uint32_t blocks = 0;
+    const int kind = launch_shape(comm, *hp, a, 2u * (uint32_t)P, st, blocks);
+    comm->last.workers = a.nworkers;
+    hipError_t e;
+    if (inline_eligible(comm, *hp, false)) {
+        comm->last.inline_launch = 1;
+        e = launch_inline_step(*hp, a, blocks, kind, st);
+        if (e != hipSuccess) return hip_fail(e, "inline executor launch");
+        return hcclSuccess;
+    }
+    // the image goes in with a copy on the stream, the counters start from zero (a fill kernel),
+    // the partials need no clearing: every one is written before it is read
+    e = hipMemcpyAsync(ws, hp->image.data(), hp->image.size(), hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return hip_fail(e, "program copy into the static workspace");
+    e = launch_fill_u32(a.state, hp->nstate, 0u, st);
+    if (e != hipSuccess) return hip_fail(e, "counter clear in the static workspace");
+    e = launch_executor(a, blocks, kind, st);
+    if (e != hipSuccess) return hip_fail(e, "executor launch");
+    return hcclSuccess;
 }
 
 hcclResult_t hccl_reduce_scatter(hcclComm_t comm, const void* const* sendbufs, void* const* recvbufs,

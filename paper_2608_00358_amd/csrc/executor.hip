@@ -18,11 +18,20 @@
 
 #include <stddef.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "program.h"
 
 namespace hccl {
+
+// Workspace of the allocation-free entry point: the program image, the dependency counters and
+// the FP32 partials of one call live here instead of in memory the library allocates. Every
+// device the library runs on holds its own copy, from the loading of this code object until
+// the process ends. In host code `scratch` only names the symbol: its device address comes
+// from workspace_address(), and only that address is ever handed to a kernel or a copy.
+constexpr size_t kWorkspaceBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kWorkspaceBytes];
 
 namespace {
 
@@ -1509,6 +1518,29 @@ hipError_t launch_executor_inline(const InlineArgs& a, uint32_t blocks, int kind
 }
 
 int executor_block_threads() { return kBlockThreads; }
+
+size_t workspace_bytes() { return kWorkspaceBytes; }
+
+// Device address of the static workspace on the current device, looked up once per device
+// and kept for the rest of the process.
+hipError_t workspace_address(void** ptr) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 int executor_waves_per_block() { return kWavesPerBlock; }
 
 // kind: a plain signature (SIG_BF16 .. SIG_INT32) for SUM-only programs of that signature,

@@ -29,6 +29,7 @@ EXPORTS = [
     "hccl_get_last_error", "hccl_result_string", "hccl_get_async_error", "hccl_comm_last_program",
     "hccl_group_start", "hccl_group_end", "hccl_alltoallv_dynamic", "hccl_set_trigger",
     "hccl_resident_start", "hccl_resident_stop", "hccl_resident_wait", "hccl_resident_last_seq",
+    "hccl_allreduce_noalloc",
 ]
 CMPS = {"eq": 0, "ne": 1, "ge": 2, "gt": 3, "le": 4, "lt": 5}
 
@@ -88,6 +89,7 @@ def load(path: str = LIB_PATH):
     lib.hccl_comm_destroy.argtypes = [vp]
     lib.hccl_comm_set_config.argtypes = [vp, ctypes.POINTER(hcclConfig_t)]
     lib.hccl_allreduce.argtypes = [vp, vpp, vpp, sz, i32, i32, vp]
+    lib.hccl_allreduce_noalloc.argtypes = [vp, vpp, vpp, sz, i32, i32, vp]
     lib.hccl_reduce_scatter.argtypes = [vp, vpp, vpp, sz, i32, i32, vp]
     lib.hccl_allgather.argtypes = [vp, vpp, vpp, sz, i32, vp]
     lib.hccl_alltoallv.argtypes = [vp, vpp, szp, szp, vpp, szp, szp, i32, vp]
@@ -191,6 +193,11 @@ def hccl_comm_set_config(comm, cfg: hcclConfig_t) -> None:
 def hccl_allreduce(comm, sendbufs, recvbufs, count: int, dtype, op: str = "sum", stream=None) -> None:
     _check(load().hccl_allreduce(comm, _ptr_array(sendbufs), _ptr_array(recvbufs), count, _dtype_code(dtype),
                                  OPS[op], _stream_handle(stream)))
+
+
+def hccl_allreduce_noalloc(comm, sendbufs, recvbufs, count: int, dtype, op: str = "sum", stream=None) -> None:
+    _check(load().hccl_allreduce_noalloc(comm, _ptr_array(sendbufs), _ptr_array(recvbufs), count, _dtype_code(dtype),
+                                         OPS[op], _stream_handle(stream)))
 
 
 def hccl_reduce_scatter(comm, sendbufs, recvbufs, recvcount: int, dtype, op: str = "sum", stream=None) -> None:
@@ -320,6 +327,9 @@ class Comm:
 
     def allreduce(self, send, recv, op="sum", stream=None):
         hccl_allreduce(self.handle, send, recv, send[0].numel(), send[0].dtype, op, stream)
+
+    def allreduce_noalloc(self, send, recv, op="sum", stream=None):
+        hccl_allreduce_noalloc(self.handle, send, recv, send[0].numel(), send[0].dtype, op, stream)
 
     def reduce_scatter(self, send, recv, op="sum", stream=None):
         hccl_reduce_scatter(self.handle, send, recv, recv[0].numel(), send[0].dtype, op, stream)
