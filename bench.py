@@ -230,7 +230,31 @@ def bench_reduce_scatter_c3(device, iters=20):
     return res, send, recv
 
 
-def bench_two_level_c4(device, iters=10):
+def bench_executor_copy(device, iters=20, nbytes=1 << 30):
+    """The executor's own copy path on one contiguous 1 GiB buffer (a one-rank AllToAllv: the
+    aligned-copy kernel, 8 KiB tiles): a streaming-copy reference measured with the library's
+    code, and the known-size kernel that scales the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+
+    import paper_2608_00358_amd as H
+
+    n = nbytes // 2
+    src = torch.empty(n, dtype=torch.bfloat16, device=device).fill_(1.5)
+    dst = torch.empty_like(src)
+    with H.Comm(1, device=0) as c:
+        call = c.bind_alltoallv([src], [n], [0], [dst], [n], [0])
+        for _ in range(3):
+            call()
+        ms = _time_events(call, iters)
+        info = c.last_program()
+    torch.cuda.synchronize()
+    assert bool(torch.equal(src, dst))
+    return {"workload": "executor copy of one contiguous 1 GiB buffer (one-rank AllToAllv)", "bytes_read": nbytes,
+            "bytes_written": nbytes, "us": ms * 1e3, "gbs": 2 * nbytes / (ms * 1e-3) / 1e9,
+            "tiles": info["num_tiles"], "workers": info["workers"]}
+
+
+def bench_two_level_c4(device, iters=10, unfused=True):
     """Two-level all-reduce P=64 (8 groups x 8) x 32 MiB bf16 N(0,1)."""
     import torch
 
@@ -247,7 +271,11 @@ def bench_two_level_c4(device, iters=10):
         c.allreduce(send, recv)
         ms = _time_events(lambda: c.allreduce(send, recv), iters)
         info = c.last_program()
-        out.update({"us": ms * 1e3, "gbs": algo / (ms * 1e-3) / 1e9, "descs": info["num_descs"]})
+        out.update({"us": ms * 1e3, "gbs": algo / (ms * 1e-3) / 1e9, "descs": info["num_descs"],
+                    "tiles": info["num_tiles"], "workers": info["workers"]})
+        if not unfused:
+            out["frac"] = out["gbs"] / HBM_PEAK_GBS
+            return out
         c.set_config(algo="two_level", group_size=L, fuse=0)
         c.allreduce(send, recv)
         ms = _time_events(lambda: c.allreduce(send, recv), iters)
@@ -858,6 +886,23 @@ def traffic_record(kernel: str):
     return entry.get("bytes_per_launch")
 
 
+def _only_c3(device):
+    res, send, recv = bench_reduce_scatter_c3(device)
+    del send, recv
+    return res
+
+
+# single measurements for profiling runs (bench.py --only NAME)
+ONLY = {
+    "copy": bench_executor_copy,
+    "c1": bench_allreduce_ring_c1,
+    "c3": _only_c3,
+    "c4": lambda d: bench_two_level_c4(d, unfused=False),
+    "c4_both": bench_two_level_c4,
+    "c5b": bench_latency_c5b,
+}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -872,8 +917,8 @@ def main():
     ap.add_argument("--dynamic-exchange-only", action="store_true",
                     help="only the AllToAllvDynamic form of the headline exchange")
     ap.add_argument("--calibrate-copy", action="store_true",
-                    help="only run torch's device copy of 1 GiB (the known-size kernel that scales "
-                         "the FETCH_SIZE / WRITE_SIZE counters)")
+                    help="only run torch's device copy of 1 GiB")
+    ap.add_argument("--only", choices=sorted(ONLY), help="run one secondary measurement and print it")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the P ranks are buffers in one MI355X's HBM; "
@@ -897,6 +942,10 @@ def main():
         ms = _time_events(lambda: b.copy_(a), 5)
         print(json.dumps({"calibration": "torch copy_ 1 GiB", "bytes_read": 1 << 30, "bytes_written": 1 << 30,
                           "us": ms * 1e3}), flush=True)
+        return
+
+    if args.only:
+        print(json.dumps({args.only: ONLY[args.only](device)}), flush=True)
         return
 
     if args.latency_only:
