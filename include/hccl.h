@@ -118,7 +118,7 @@ typedef struct {
     int32_t validate;      /* 1 = run the program validator on every compile */
     int32_t order;         /* hcclOrder_t */
     int32_t requantize;    /* 1 = round every partial to the buffer type */
-    int32_t trace;         /* 1 = record a timestamp pair per tile of every launch (hccl_comm_trace) */
+    int32_t trace;         /* 1 = record times and place of every tile of every launch (hccl_comm_trace) */
     int32_t reserved[2];
 } hcclConfig_t;
 
@@ -381,6 +381,30 @@ typedef struct {
 } hcclProgramInfo_t;
 
 hcclResult_t hccl_comm_last_program(hcclComm_t comm, hcclProgramInfo_t* info);
+
+/*
+ * Per-tile trace (Section V-C: counters on every work packet and subgraph show when each
+ * component handled it; the control-core overhead is read off them). With hcclConfig_t.trace
+ * set, every launch records, for each tile of its program, the wall-clock time at which an
+ * executor wavefront took it, how long its dependency waits lasted, when its data had moved
+ * and its signals were set, and where it ran. One-step programs then also run from a device
+ * image instead of the launch packet. Launches under graph capture and resident packets are
+ * not traced.
+ */
+typedef struct {
+    uint64_t start;     /* wall-clock ticks when a wavefront took the tile */
+    uint32_t ready;     /* ticks from start until its dependencies were satisfied */
+    uint32_t done;      /* ticks from start until its data had moved and its signals were set */
+    uint32_t wave;      /* executor wavefront that ran it */
+    uint32_t where;     /* XCC id << 24 | shader engine << 16 | CU << 8 | SIMD */
+    uint64_t reserved;
+} hcclTileTrace_t;
+
+/* Waits for the device, then copies the records of the last traced launch of `comm` (index =
+ * tile number) into out[0 .. min(capacity, *count)). *count = records of that launch (0 if
+ * none); *clock_khz (may be NULL) = rate of the wall clock the times use. */
+hcclResult_t hccl_comm_trace(hcclComm_t comm, hcclTileTrace_t* out, size_t capacity, size_t* count,
+                             uint64_t* clock_khz);
 
 #ifdef __cplusplus
 }

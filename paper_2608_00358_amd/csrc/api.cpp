@@ -108,6 +108,10 @@ struct hcclComm {
     uint32_t* d_ctl = nullptr;
     hipStream_t resident_stream = nullptr;
     uint64_t resident_seq = 0;        // last packet published
+    // per-tile trace of the last traced launch (cfg.trace)
+    TileStamp* d_trace = nullptr;
+    uint64_t trace_cap = 0;           // records the buffer holds
+    uint32_t trace_tiles = 0;         // records the last traced launch wrote
     // allocation-free calls: this device's static workspace and host-only compiled programs
     void* workspace = nullptr;
     std::string workspace_error;
@@ -332,6 +336,7 @@ int launch_shape(hcclComm* c, const HostProgram& prog, LaunchArgs& a, uint32_t n
     const uint32_t wpb = (uint32_t)executor_waves_per_block();
     uint32_t cus = stream_cu_count(c, s);
     int kind = prog.kind;
+    if (a.trace) kind = kKindGeneric;  // the kernel that records the trace
     if (kind == kKindCopyAligned) {
         for (uint32_t i = 0; i < nuser; ++i)
             if ((uintptr_t)a.bufs[i] % 16) kind = kKindCopyOnly;
@@ -349,7 +354,22 @@ int launch_shape(hcclComm* c, const HostProgram& prog, LaunchArgs& a, uint32_t n
 bool inline_eligible(const hcclComm* c, const HostProgram& prog, bool triggered) {
     const bool plain_step = prog.descs.size() == 1 && (prog.descs[0].op == OP_COPY || prog.descs[0].op == OP_REDUCE);
     return c->inline_single_step && plain_step && (prog.flags & PF_HAS_DEPS) == 0 && !c->dynamic_dispatch &&
-           !triggered;
+           !triggered && !c->cfg.trace;
+}
+
+// Trace buffer for `tiles` records (grown on demand; traced launches are a diagnostic mode).
+hcclResult_t ensure_trace(hcclComm* c, uint64_t tiles) {
+    if (tiles <= c->trace_cap) return hcclSuccess;
+    hipError_t e = hipDeviceSynchronize();  // the old buffer may still be written
+    if (e != hipSuccess) return hip_fail(e, "synchronize before trace growth");
+    if (c->d_trace) (void)hipFree(c->d_trace);
+    c->d_trace = nullptr;
+    c->trace_cap = 0;
+    c->trace_tiles = 0;
+    e = hipMalloc(&c->d_trace, tiles * sizeof(TileStamp));
+    if (e != hipSuccess) return fail(hcclOutOfMemory, "trace buffer allocation failed");
+    c->trace_cap = tiles;
+    return hcclSuccess;
 }
 
 hipError_t launch_inline_step(const HostProgram& prog, const LaunchArgs& a, uint32_t blocks, int kind, hipStream_t s) {
@@ -456,6 +476,8 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
                                      "make the same call once outside the capture first");
     r = ensure_scratch(c, dp->prog.scratch_bytes);
     if (r != hcclSuccess) return r;
+    const bool traced = c->cfg.trace != 0 && !capturing && !c->resident;
+    if (traced && (r = ensure_trace(c, dp->prog.ntiles)) != hcclSuccess) return r;
     if (capturing) {  // the graph keeps this image, state and scratch address
         dp->captured = true;
         if (dp->prog.scratch_bytes > 0) c->scratch_captured = true;
@@ -490,6 +512,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         a.wait_cmp = (uint32_t)trig.wait_cmp;
     }
     const bool signals = triggered && trig.done_addr != nullptr;
+    if (traced) a.trace = c->d_trace;
 
     if (c->resident) return resident_submit(c, a, dp);
 
@@ -510,6 +533,11 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     // one recorded inside stands for a graph node, not for a launch. Replays run in the order
     // of the stream they are launched on; the caller orders them against eager launches of the
     // same program, or of programs that use scratch, on other streams.
+    if (traced) {  // every record of this launch starts cleared, then each tile writes its own
+        c->trace_tiles = dp->prog.ntiles;
+        hipError_t e = launch_fill_u32((uint32_t*)c->d_trace, (uint64_t)dp->prog.ntiles * sizeof(TileStamp) / 4, 0u, s);
+        if (e != hipSuccess) return hip_fail(e, "trace clear");
+    }
     const bool stateful = (has_deps || a.dynamic != 0) && !capturing;
     const bool scratch = dp->prog.scratch_bytes > 0 && !capturing;
     if (stateful && dp->launched && dp->last_stream != s) {
@@ -655,6 +683,7 @@ hcclResult_t hccl_comm_destroy(hcclComm_t comm) {
         if (comm->d_scratch) (void)hipFree(comm->d_scratch);
         for (void* p : comm->retired_scratch) (void)hipFree(p);
         if (comm->d_error) (void)hipFree(comm->d_error);
+        if (comm->d_trace) (void)hipFree(comm->d_trace);
         if (comm->scratch_done) (void)hipEventDestroy(comm->scratch_done);
     }
     delete comm;
@@ -1165,6 +1194,29 @@ hcclResult_t hccl_resident_last_seq(hcclComm_t comm, uint64_t* seq) {
     if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
     if (!seq) return fail(hcclInvalidArgument, "null output");
     *seq = comm->resident_seq;
+    return hcclSuccess;
+}
+
+hcclResult_t hccl_comm_trace(hcclComm_t comm, hcclTileTrace_t* out, size_t capacity, size_t* count,
+                             uint64_t* clock_khz) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (!count) return fail(hcclInvalidArgument, "null count");
+    if (capacity && !out) return fail(hcclInvalidArgument, "null trace output");
+    static_assert(sizeof(hcclTileTrace_t) == sizeof(TileStamp), "trace record layout");
+    *count = 0;
+    if (clock_khz) *clock_khz = comm->wall_clock_khz;
+    if (comm->device == HCCL_NO_DEVICE || comm->trace_tiles == 0) return hcclSuccess;
+    if (comm->resident)
+        return fail(hcclInvalidArgument, "the resident executor is running: stop it before reading the trace");
+    DeviceGuard guard(comm->device);
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "synchronize");
+    const size_t n = std::min<size_t>(capacity, comm->trace_tiles);
+    if (n) {
+        e = hipMemcpy(out, comm->d_trace, n * sizeof(TileStamp), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e, "read trace");
+    }
+    *count = comm->trace_tiles;
     return hcclSuccess;
 }
 

@@ -39,12 +39,17 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlockThreads = kWavesPerBlock * kWaveSize;
-constexpr int kSrcBatch = 8;  // sources whose loads are issued together
+#ifndef HCCL_SRC_BATCH
+#define HCCL_SRC_BATCH 4
+#endif
+constexpr int kSrcBatch = HCCL_SRC_BATCH;  // sources whose loads are issued together
 
 // 128-bit global accesses. Every byte of a collective is read once and written once, so the
 // nontemporal hint streams it past the caches instead of evicting the program, the counters
 // and other waves' lines. Copies store nontemporally too; reductions keep ordinary stores
-// (measured faster for their small write share).
+// (measured faster for their small write share) unless they write many destinations (the
+// two-level all-reduce's 64: half its traffic is stores, and streaming them measured 2 %
+// faster).
 #ifndef HCCL_NT_LOAD
 #define HCCL_NT_LOAD 1
 #endif
@@ -65,11 +70,13 @@ __device__ __forceinline__ u32x4 vld(const char* p) {
     if constexpr (HCCL_NT_LOAD) return __builtin_nontemporal_load((const u32x4*)p);
     else return *(const u32x4*)p;
 }
-// store of reduction results
+// store of reduction results (NT: a step with many destinations)
+template <bool NT = false>
 __device__ __forceinline__ void vst(char* p, u32x4 v) {
-    if constexpr (HCCL_NT_STORE_REDUCE) __builtin_nontemporal_store(v, (u32x4*)p);
+    if constexpr (HCCL_NT_STORE_REDUCE || NT) __builtin_nontemporal_store(v, (u32x4*)p);
     else *(u32x4*)p = v;
 }
+constexpr uint32_t kWideStoreDsts = 8;  // destinations from which reduction results stream
 // store of copied data
 __device__ __forceinline__ void vst_copy(char* p, u32x4 v) {
     if constexpr (HCCL_NT_STORE_COPY) __builtin_nontemporal_store(v, (u32x4*)p);
@@ -175,7 +182,7 @@ __device__ __forceinline__ void widen8(const Raw8<DT>& r, A (&x)[8]) {
     }
 }
 
-template <int DT, typename A>
+template <int DT, typename A, bool NT = false>
 __device__ __forceinline__ void store8(char* p, const A (&x)[8]) {
     if constexpr (DT == DT_BF16 || DT == DT_FP16) {
         u32x4 w;
@@ -184,7 +191,7 @@ __device__ __forceinline__ void store8(char* p, const A (&x)[8]) {
             if constexpr (DT == DT_BF16) w[i] = bf16_bits(x[2 * i]) | (bf16_bits(x[2 * i + 1]) << 16);
             else w[i] = f16_bits(x[2 * i]) | (f16_bits(x[2 * i + 1]) << 16);
         }
-        vst(p, w);
+        vst<NT>(p, w);
     } else {
         u32x4 a, b;
 #pragma unroll
@@ -197,8 +204,8 @@ __device__ __forceinline__ void store8(char* p, const A (&x)[8]) {
                 b[i] = (uint32_t)x[4 + i];
             }
         }
-        vst(p, a);
-        vst(p + 16, b);
+        vst<NT>(p, a);
+        vst<NT>(p + 16, b);
     }
 }
 
@@ -337,12 +344,23 @@ __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, ui
             for (int i = 0; i < 8; ++i)
                 tot[u][i] = (g0 == 0) ? part[u][i] : combq<OPR, TO, REQ>(tot[u][i], part[u][i]);
     }
-    for (uint32_t j = 0; j < t.ndst; ++j) {
-        char* b = (char*)from_lane(t.dst, j);
+    if (t.ndst >= kWideStoreDsts) {
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* b = (char*)from_lane(t.dst, j);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
-            store8<TO, A>(b + (uint64_t)e * DtInfo<TO>::size, tot[u]);
+            for (int u = 0; u < U; ++u) {
+                uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
+                store8<TO, A, true>(b + (uint64_t)e * DtInfo<TO>::size, tot[u]);
+            }
+        }
+    } else {
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* b = (char*)from_lane(t.dst, j);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
+                store8<TO, A>(b + (uint64_t)e * DtInfo<TO>::size, tot[u]);
+            }
         }
     }
 }
@@ -996,7 +1014,7 @@ __device__ __forceinline__ void dyn_slot_small(const DynView& a, uint32_t k, con
 
 template <int KIND>
 __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, const ProgramHeader& h, uint32_t t,
-                                         uint32_t lane, const uint64_t* bufs) {
+                                         uint32_t lane, const uint64_t* bufs, bool stamp, uint64_t& ready) {
     const uint32_t d = uni(((const uint32_t*)(prog + h.off_tile_desc))[t]);
     const Desc* D = (const Desc*)(prog + h.off_desc) + d;
     const uint32_t op = uni(D->op);
@@ -1012,6 +1030,7 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
         const Dep* deps = (const Dep*)(prog + h.off_dep) + uni(D->dep);
         if (!wait_deps(deps, ndep, k, a.state, a.error, a.timeout, d, t)) return false;
     }
+    if (stamp) ready = wall_clock64();
 
     if (op == OP_DYN_COPY) {
         // the host runs programs with dynamic steps on these two kernels only
@@ -1074,6 +1093,44 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
         }
     }
     return true;
+}
+
+// Runs tile t and, when the launch is traced, records its times and place (lane 0 writes).
+// Only the generic kernel carries the trace code (the host runs traced launches on it): the
+// clock reads and the record stores in the tile loop of the specialised kernels, even when
+// skipped, measured 8 % slower copies.
+template <int KIND>
+__device__ __forceinline__ bool run_tile_traced(const Shared& a, const uint8_t* prog, const ProgramHeader& h,
+                                                uint32_t t, uint32_t lane, const uint64_t* bufs, TileStamp* trace,
+                                                uint32_t wave) {
+    if constexpr (KIND != kKindGeneric) {
+        uint64_t unused = 0;
+        return run_tile<KIND>(a, prog, h, t, lane, bufs, false, unused);
+    }
+    // one inlined copy of the tile code whether or not the launch is traced
+    const uint64_t t0 = trace ? wall_clock64() : 0;
+    uint64_t ready = t0;
+    const bool ok = run_tile<KIND>(a, prog, h, t, lane, bufs, trace != nullptr, ready);
+    if (trace && lane == 0) {
+        const uint64_t t2 = wall_clock64();
+        // HW_ID: SIMD [5:4], CU [11:8], shader engine [15:13]; XCC_ID [3:0]
+        const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);
+        const uint32_t xcc = __builtin_amdgcn_s_getreg((15 << 11) | 20) & 0xFu;
+        // two 16-byte stores straight from registers (a TileStamp temporary would live in scratch)
+        u32x4 lo, hi;
+        lo[0] = (uint32_t)t0;
+        lo[1] = (uint32_t)(t0 >> 32);
+        lo[2] = (uint32_t)(ready - t0);
+        lo[3] = (uint32_t)(t2 - t0);
+        hi[0] = wave;
+        hi[1] = (xcc << 24) | (((hw >> 13) & 7u) << 16) | (((hw >> 8) & 0xFu) << 8) | ((hw >> 4) & 3u);
+        hi[2] = 0;
+        hi[3] = 0;
+        u32x4* rec = (u32x4*)(trace + t);
+        rec[0] = lo;
+        rec[1] = hi;
+    }
+    return ok;
 }
 
 // ------------------------------------------------------------------ device trigger
@@ -1168,7 +1225,7 @@ hccl_executor(LaunchArgs a) {
         // with the whole grid resident the lowest unfinished tile is always running.
         for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
             if ((has_deps || triggered) && load_relaxed(&a.error->code) != 0u) break;
-            if (!run_tile<KIND>(sh, prog, h, t, lane, bufs)) break;
+            if (!run_tile_traced<KIND>(sh, prog, h, t, lane, bufs, a.trace, wave)) break;
         }
     } else if (started) {
         uint32_t* ticket = a.state + kStateTicket;
@@ -1180,7 +1237,7 @@ hccl_executor(LaunchArgs a) {
             // claim the next ticket now; its latency hides behind this tile's work
             uint32_t next = 0;
             if (lane == 0) next = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (!run_tile<KIND>(sh, prog, h, t, lane, bufs)) break;
+            if (!run_tile_traced<KIND>(sh, prog, h, t, lane, bufs, a.trace, wave)) break;
             t = uni(__shfl(next, 0));
         }
     }
@@ -1361,7 +1418,8 @@ hccl_resident(ResidentArgs r) {
         sh.timeout = r.timeout_ticks;
         for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
             if (has_deps && load_relaxed(&r.error->code) != 0u) break;
-            if (!run_tile<kKindGeneric>(sh, prog, h, t, lane, bufs)) break;
+            uint64_t unused = 0;
+            if (!run_tile<kKindGeneric>(sh, prog, h, t, lane, bufs, false, unused)) break;
         }
 
         // this workgroup's stores and counter updates are complete and visible device-wide

@@ -191,6 +191,18 @@ struct ErrorRecord {
     uint32_t pad;
 };
 
+// Per-tile trace record (work-packet counters, Section V-C): wall-clock times (the device's
+// constant-rate counter) of one tile, and where it ran.
+struct TileStamp {      // 32 bytes
+    uint64_t start;     // the wavefront took the tile
+    uint32_t ready;     // ticks from start until its dependencies were satisfied
+    uint32_t done;      // ticks from start until its data was moved and its signals set
+    uint32_t wave;      // executor wavefront that ran it
+    uint32_t where;     // XCC id << 24 | shader engine << 16 | CU << 8 | SIMD
+    uint64_t pad;
+};
+static_assert(sizeof(TileStamp) == 32, "trace record layout");
+
 // Kernel arguments of one executor launch.
 struct LaunchArgs {
     const uint8_t* prog;     // device image (ProgramHeader first)
@@ -206,6 +218,7 @@ struct LaunchArgs {
     uint64_t wait_value;
     uint32_t wait_cmp;       // TriggerCmp
     uint32_t pad;
+    TileStamp* trace;        // one record per tile of the program, or NULL (no trace)
     char* bufs[kMaxBuffers];
 };
 

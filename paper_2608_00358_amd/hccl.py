@@ -29,7 +29,7 @@ EXPORTS = [
     "hccl_get_last_error", "hccl_result_string", "hccl_get_async_error", "hccl_comm_last_program",
     "hccl_group_start", "hccl_group_end", "hccl_alltoallv_dynamic", "hccl_set_trigger",
     "hccl_resident_start", "hccl_resident_stop", "hccl_resident_wait", "hccl_resident_last_seq",
-    "hccl_allreduce_noalloc",
+    "hccl_allreduce_noalloc", "hccl_comm_trace",
 ]
 CMPS = {"eq": 0, "ne": 1, "ge": 2, "gt": 3, "le": 4, "lt": 5}
 
@@ -68,6 +68,13 @@ class hcclProgramInfo_t(ctypes.Structure):
     ]
 
 
+class hcclTileTrace_t(ctypes.Structure):
+    _fields_ = [
+        ("start", ctypes.c_uint64), ("ready", ctypes.c_uint32), ("done", ctypes.c_uint32),
+        ("wave", ctypes.c_uint32), ("where", ctypes.c_uint32), ("reserved", ctypes.c_uint64),
+    ]
+
+
 _lib = None
 
 
@@ -101,6 +108,8 @@ def load(path: str = LIB_PATH):
     lib.hccl_result_string.restype = ctypes.c_char_p
     lib.hccl_get_async_error.argtypes = [vp]
     lib.hccl_comm_last_program.argtypes = [vp, ctypes.POINTER(hcclProgramInfo_t)]
+    lib.hccl_comm_trace.argtypes = [vp, ctypes.POINTER(hcclTileTrace_t), sz, ctypes.POINTER(ctypes.c_size_t),
+                                    ctypes.POINTER(ctypes.c_uint64)]
     lib.hccl_group_start.argtypes = [vp]
     lib.hccl_group_end.argtypes = [vp]
     lib.hccl_resident_start.argtypes = [vp, ctypes.c_uint32, ctypes.c_uint32]
@@ -287,6 +296,23 @@ def hccl_comm_last_program(comm) -> dict:
     return {name: getattr(info, name) for name, _ in hcclProgramInfo_t._fields_}
 
 
+def hccl_comm_trace(comm):
+    """Records of the last traced launch as a numpy structured array (fields start, ready, done,
+    wave, where; times in wall-clock ticks) and the clock rate in kHz."""
+    import numpy as np
+
+    lib = load()
+    n = ctypes.c_size_t(0)
+    khz = ctypes.c_uint64(0)
+    _check(lib.hccl_comm_trace(comm, None, 0, ctypes.byref(n), ctypes.byref(khz)))
+    buf = (hcclTileTrace_t * max(1, n.value))()
+    _check(lib.hccl_comm_trace(comm, buf, n.value, ctypes.byref(n), ctypes.byref(khz)))
+    dt = np.dtype([("start", np.uint64), ("ready", np.uint32), ("done", np.uint32), ("wave", np.uint32),
+                   ("where", np.uint32), ("reserved", np.uint64)])
+    arr = np.frombuffer(bytes(buf), dtype=dt, count=n.value).copy()
+    return arr, int(khz.value)
+
+
 def _bound(fn, *args):
     def call():
         _check(fn(*args))
@@ -415,6 +441,9 @@ class Comm:
 
     def last_program(self) -> dict:
         return hccl_comm_last_program(self.handle)
+
+    def trace(self):
+        return hccl_comm_trace(self.handle)
 
     def async_error(self) -> int:
         return hccl_get_async_error(self.handle)

@@ -41,6 +41,14 @@ def test_comm_create_rejects_bad_rank_counts(n):
     assert e.value.code == 1
 
 
+def test_trace_of_a_host_only_communicator_is_empty():
+    with H.Comm(4, device=H.NO_DEVICE, trace=1) as c:
+        H.hccl_allreduce(c.handle, [1 << 40, 2 << 40, 3 << 40, 4 << 40], [5 << 40, 6 << 40, 7 << 40, 8 << 40], 1000,
+                         "fp32")
+        rec, khz = c.trace()
+    assert rec.shape == (0,)
+
+
 def test_resident_executor_host_only_rules():
     """A host-only communicator has no device to keep an executor on; stopping one that is not
     running is a no-op, and waiting on one is an error."""
