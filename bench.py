@@ -140,6 +140,13 @@ def run_headline(args, device):
         raise RuntimeError(H.hccl_get_last_error())
     ms_step = elapsed * 1e3 / args.steps
     launch_ms = first.elapsed_time(last) / args.steps
+    # host cost of re-enqueueing the cached work packet (group start, two calls, group end:
+    # four ctypes calls and one launch); the GPU is left to drain afterwards
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    host_us = (time.perf_counter() - t0) * 1e6 / args.steps
+    torch.cuda.synchronize()
 
     recv_counts = w["counts"].sum(axis=0)
     w.update({"send_ids": send_ids, "recv_rows": recv_rows, "recv_ids": recv_ids})
@@ -151,6 +158,7 @@ def run_headline(args, device):
         "recv_imbalance": float(recv_counts.max() / recv_counts.mean()),
         "program": info_step,
         "separate_calls": separate,
+        "host_enqueue_us": host_us,
     }
     comm.close()
     return result, w
@@ -203,7 +211,7 @@ def bench_allreduce_ring_c1(device, iters=200, cold_sets=40):
         ms = _time_events(c.bind_allreduce(send, recv), iters)
         out["unfused_warm_gbs"] = algo / (ms * 1e-3) / 1e9
     out.update({"workload": "allreduce ring P=4 N=2^20 fp32 chunk=64KiB", "algo_bytes": algo,
-                "descs": info["num_descs"], "tiles": info["num_tiles"]})
+                "descs": info["num_descs"], "tiles": info["num_tiles"], "compile_us": round(info["compile_us"], 1)})
     return out
 
 
@@ -225,9 +233,110 @@ def bench_reduce_scatter_c3(device, iters=20):
         info = c.last_program()
     res = {"workload": "reduce_scatter ring P=8 256MiB/rank bf16 chunk=1MiB", "us": ms * 1e3,
            "gbs": algo / (ms * 1e-3) / 1e9, "algo_bytes": algo, "descs": info["num_descs"],
+           "compile_us": round(info["compile_us"], 1),
            "tiles": info["num_tiles"], "workers": info["workers"]}
     res["frac"] = res["gbs"] / HBM_PEAK_GBS
     return res, send, recv
+
+
+def _bf16_ulp_distance(a, b):
+    """Elementwise distance in bf16 units in the last place between two bf16 tensors (the
+    encodings mapped to ordered integers: +0 and -0 coincide)."""
+    import torch
+
+    def ordered(t):
+        u = t.view(torch.int16).to(torch.int32) & 0xFFFF
+        mag = u & 0x7FFF
+        return torch.where(u >= 0x8000, -mag, mag)
+
+    return (ordered(a) - ordered(b)).abs()
+
+
+def bench_forwarded_partials(device, iters=10):
+    """The paper's forwarded-partial schedules (Section III-B-2 ring; recursive halving; Section
+    II-A-2 per-result re-quantisation) on the reduce-scatter configuration (P=8, 256 MiB bf16 per
+    rank, N(0, 0.02), 1 MiB chunks): time, effective GB/s, the schedule's own HBM bytes against
+    the algorithmic bytes, and the numeric drift of each fold order against the ascending one
+    (bf16 ulps; every schedule is bit-exact against the oracle in its own order)."""
+    import torch
+
+    import paper_2608_00358_amd as H
+    from workloads import device_normal_bf16
+
+    P = 8
+    M = (256 * MiB // 2) // P
+    send = device_normal_bf16(P, P * M, std=0.02, seed=0, device=device)
+    algo = (P + 1) * P * M * 2
+    variants = [
+        ("ascending_ring_fused", dict(algo="ring")),
+        ("ring_order_fused", dict(algo="ring", order="ring")),
+        ("ring_order_forwarded_partials", dict(algo="ring", order="ring", fuse=0)),
+        ("ring_order_forwarded_requantised", dict(algo="ring", order="ring", fuse=0, requantize=1)),
+        ("halving_rhd_fused", dict(algo="rhd", order="halving")),
+        ("halving_rhd_butterfly", dict(algo="rhd", order="halving", fuse=0)),
+        ("halving_rhd_butterfly_requantised", dict(algo="rhd", order="halving", fuse=0, requantize=1)),
+    ]
+    ref = None
+    out = {"workload": "reduce_scatter P=8 256MiB/rank bf16 N(0,0.02), 1 MiB chunks, fold orders and schedules",
+           "algo_bytes": algo}
+    for name, cfg in variants:
+        recv = [torch.empty(M, dtype=torch.bfloat16, device=device) for _ in range(P)]
+        with H.Comm(P, device=0, chunk_bytes=MiB, **cfg) as c:
+            c.reduce_scatter(send, recv)
+            ms = _time_events(lambda: c.reduce_scatter(send, recv), iters)
+            info = c.last_program()
+            if c.async_error() != 0:
+                raise RuntimeError(H.hccl_get_last_error())
+        sched = info["bytes_read"] + info["bytes_written"]
+        res = {"us": round(ms * 1e3, 1), "gbs": round(algo / (ms * 1e-3) / 1e9, 1),
+               "schedule_bytes": sched, "traffic_over_algorithmic": round(sched / algo, 4),
+               "descs": info["num_descs"], "deps": info["num_deps"], "scratch_bytes": info["scratch_bytes"],
+               "compile_us": round(info["compile_us"], 1)}
+        if ref is None:
+            ref = recv
+        else:
+            d = torch.cat([_bf16_ulp_distance(a, b) for a, b in zip(recv, ref)])
+            res.update({"differ_from_ascending": int((d > 0).sum()), "above_1ulp": int((d > 1).sum()),
+                        "max_ulp": int(d.max()), "mean_ulp": float(d.float().mean())})
+        out[name] = res
+        torch.cuda.synchronize()
+    out["elements"] = P * M
+    del send, ref
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_copy_ceiling(device, iters=20, nbytes=1 << 30):
+    """What plain HIP kernels reach on this device (bench_stream.hip): a contiguous copy, a
+    read-only and a write-only sweep of 1 GiB, each the best of four grid sizes; and the
+    library's own copy path on the same copy."""
+    import torch
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_00358_amd", "lib", "libbench_stream.so"))
+    lib.bench_stream.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
+                                 ctypes.c_int, ctypes.c_void_p]
+    a = torch.empty(nbytes, dtype=torch.uint8, device=device).fill_(7)
+    b = torch.empty_like(a)
+    st = torch.cuda.current_stream().cuda_stream
+    out = {"workload": "1 GiB contiguous copy / read / write, non-temporal 16-byte accesses, 8 KiB per wavefront step"}
+    for kind, name, moved in ((0, "copy", 2 * nbytes), (1, "read", nbytes), (2, "write", nbytes)):
+        best = (0.0, 0)
+        for blocks in (256, 512, 1024, 2048):
+            def run():
+                rc = lib.bench_stream(kind, a.data_ptr(), b.data_ptr(), nbytes, 8192, blocks, st)
+                if rc != 0:
+                    raise RuntimeError(f"bench_stream failed ({rc})")
+            for _ in range(3):
+                run()
+            ms = _time_events(run, iters)
+            best = max(best, (moved / (ms * 1e-3) / 1e9, blocks))
+        out[f"stream_{name}_gbs"], out[f"stream_{name}_blocks"] = round(best[0], 1), best[1]
+    torch.cuda.synchronize()
+    del a, b
+    ex = bench_executor_copy(device, iters=iters, nbytes=nbytes)
+    out["executor_copy_gbs"] = round(ex["gbs"], 1)
+    out["executor_copy_frac_of_stream_copy"] = round(ex["gbs"] / out["stream_copy_gbs"], 4)
+    return out
 
 
 def bench_executor_copy(device, iters=20, nbytes=1 << 30):
@@ -272,10 +381,22 @@ def bench_two_level_c4(device, iters=10, unfused=True):
         ms = _time_events(lambda: c.allreduce(send, recv), iters)
         info = c.last_program()
         out.update({"us": ms * 1e3, "gbs": algo / (ms * 1e-3) / 1e9, "descs": info["num_descs"],
+                    "compile_us": round(info["compile_us"], 1),
                     "tiles": info["num_tiles"], "workers": info["workers"]})
         if not unfused:
             out["frac"] = out["gbs"] / HBM_PEAK_GBS
             return out
+        # the same sum in the flat ascending order (one 64-source fold per element): its time,
+        # and how far the two-level tree order's results lie from it
+        flat = [torch.empty(N, dtype=torch.bfloat16, device=device) for _ in range(P)]
+        c.set_config(algo="ring")
+        c.allreduce(send, flat)
+        ms_flat = _time_events(lambda: c.allreduce(send, flat), iters)
+        d = _bf16_ulp_distance(recv[0], flat[0])
+        out.update({"flat_ascending_us": ms_flat * 1e3, "flat_ascending_gbs": algo / (ms_flat * 1e-3) / 1e9,
+                    "tree_vs_flat_differ": int((d > 0).sum()), "tree_vs_flat_above_1ulp": int((d > 1).sum()),
+                    "tree_vs_flat_max_ulp": int(d.max()), "elements": N})
+        del flat
         c.set_config(algo="two_level", group_size=L, fuse=0)
         c.allreduce(send, recv)
         ms = _time_events(lambda: c.allreduce(send, recv), iters)
@@ -322,6 +443,14 @@ def bench_latency_c5b(device, warmup=100, iters=1000, isolated=200):
             call()
             torch.cuda.synchronize()
             t_host.append((time.perf_counter() - t0) * 1e6)
+        # host cost of re-enqueueing the cached packet (one ctypes call and one launch; the
+        # paper keeps this under 10 us, Section V-B)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(200):
+            call()
+        enqueue_us = (time.perf_counter() - t0) * 1e6 / 200
+        torch.cuda.synchronize()
         info = c.last_program()
     # floor: a one-element torch fill launched back to back on the same stream
     tiny = torch.zeros(1, device=device)
@@ -330,8 +459,8 @@ def bench_latency_c5b(device, warmup=100, iters=1000, isolated=200):
             "back_to_back_with_python_marshalling_us": ms_marshal * 1e3,
             "tiny_torch_kernel_back_to_back_us": empty_ms * 1e3, "inline_launch": info["inline_launch"],
             "isolated_median_us": statistics.median(samples),
-            "host_roundtrip_median_us": statistics.median(t_host), "workers": info["workers"],
-            "tiles": info["num_tiles"]}
+            "host_roundtrip_median_us": statistics.median(t_host), "host_enqueue_us": enqueue_us,
+            "compile_us": round(info["compile_us"], 1), "workers": info["workers"], "tiles": info["num_tiles"]}
 
 
 def bench_resident_c5b(device, blocks=0, warmup=200, iters=1000):
@@ -900,6 +1029,8 @@ ONLY = {
     "c4": lambda d: bench_two_level_c4(d, unfused=False),
     "c4_both": bench_two_level_c4,
     "c5b": bench_latency_c5b,
+    "orders": bench_forwarded_partials,
+    "ceiling": bench_copy_ceiling,
 }
 
 
@@ -990,7 +1121,10 @@ def main():
                    "ranks": 8, "rows_per_rank": 1 << 18, "row_elems": 128,
                    "recv_imbalance_max_over_mean": round(head["recv_imbalance"], 3),
                    "descs": head["program"]["num_descs"], "tiles": head["program"]["num_tiles"],
-                   "workers": head["program"]["workers"]},
+                   "workers": head["program"]["workers"],
+                   "step_tiles_elems": [head["program"]["step_tile_min"], head["program"]["step_tile_max"]],
+                   "compile_us": round(head["program"]["compile_us"], 1),
+                   "host_enqueue_us_per_step": round(head["host_enqueue_us"], 2)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "hccl_executor<12> (copy-only executor; the grouped rows + ids launch)",
@@ -999,6 +1133,12 @@ def main():
     }
     if head["separate_calls"]:
         line["config"]["separate_calls"] = {k: round(v, 2) for k, v in head["separate_calls"].items()}
+    if not args.headline_only:
+        _log("copy ceiling")
+        ceil = _extra("ceiling", lambda: bench_copy_ceiling(device))
+        line["copy_ceiling"] = ceil
+        if "stream_copy_gbs" in ceil:
+            line["roofline"]["frac_of_stream_copy"] = round(achieved / ceil["stream_copy_gbs"], 4)
     if not args.headline_only:
         extras = {}
         _log("c1 ring all-reduce")
@@ -1012,6 +1152,8 @@ def main():
             extras["overlap_rs16cu_gemm"] = _extra("c5a overlap", lambda: bench_overlap_c5a(device, rs_send, rs_recv))
         del rs_send, rs_recv
         torch.cuda.empty_cache()
+        _log("forwarded-partial schedules and fold orders")
+        extras["forwarded_partial_schedules_rs_p8_bf16"] = _extra("orders", lambda: bench_forwarded_partials(device))
         _log("c4 two-level all-reduce")
         extras["allreduce_two_level_p64_bf16"] = _extra("c4", lambda: bench_two_level_c4(device))
         _log("c5b latency")

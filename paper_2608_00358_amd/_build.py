@@ -51,6 +51,23 @@ def _compile(src: str) -> str:
     return obj
 
 
+BENCH_STREAM_SRC = os.path.join(ROOT, "bench_stream.hip")
+BENCH_STREAM_LIB = os.path.join(LIBDIR, "libbench_stream.so")
+
+
+def build_bench_stream() -> str:
+    """The STREAM-style reference kernels bench.py times beside the collectives (not part of
+    libhccl.so)."""
+    os.makedirs(LIBDIR, exist_ok=True)
+    tmp = BENCH_STREAM_LIB + ".tmp"
+    cmd = [_hipcc(), *HIPCC_FLAGS, "-shared", "-x", "hip", BENCH_STREAM_SRC, "-o", tmp]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    os.replace(tmp, BENCH_STREAM_LIB)
+    return BENCH_STREAM_LIB
+
+
 def build() -> str:
     """Compiles every source and links lib/libhccl.so. Always rebuilds."""
     os.makedirs(OBJDIR, exist_ok=True)

@@ -11,9 +11,11 @@
 #include <atomic>
 #include <chrono>
 #include <thread>
+#include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <strings.h>
 #include <list>
 #include <memory>
 #include <string>
@@ -108,6 +110,10 @@ struct hcclComm {
     uint32_t* d_ctl = nullptr;
     hipStream_t resident_stream = nullptr;
     uint64_t resident_seq = 0;        // last packet published
+    // environment overrides (read at creation): HCCL_ALGO, HCCL_CHUNK_BYTES, HCCL_DEBUG
+    int env_algo = -1;                // hcclAlgo_t forced for every call, -1 = the configuration's
+    uint64_t env_chunk = 0;           // chunk bytes forced for every call, 0 = the configuration's
+    int log_level = 0;                // 0 off, 1 WARN, 2 INFO, 3 TRACE
     // per-tile trace of the last traced launch (cfg.trace)
     TileStamp* d_trace = nullptr;
     uint64_t trace_cap = 0;           // records the buffer holds
@@ -119,6 +125,45 @@ struct hcclComm {
 };
 
 namespace {
+
+// Log lines on stderr at HCCL_DEBUG=WARN (1), INFO (2) or TRACE (3).
+void hlog(const hcclComm* c, int level, const char* fmt, ...) __attribute__((format(printf, 3, 4)));
+void hlog(const hcclComm* c, int level, const char* fmt, ...) {
+    if (!c || c->log_level < level) return;
+    static const char* kNames[] = {"", "WARN", "INFO", "TRACE"};
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    std::fprintf(stderr, "[hccl %s] comm %p: %s\n", kNames[level], (const void*)c, buf);
+}
+
+const char* kCollNames[] = {"allreduce", "reduce_scatter", "allgather", "alltoallv", "alltoallv_dynamic"};
+const char* kAlgoNames[] = {"auto", "direct", "ring", "two_level", "rhd"};
+
+// The environment overrides of a new communicator. Unknown values are ignored with a warning.
+void read_env(hcclComm* c) {
+    if (const char* v = std::getenv("HCCL_DEBUG")) {
+        if (!strcasecmp(v, "WARN")) c->log_level = 1;
+        else if (!strcasecmp(v, "INFO")) c->log_level = 2;
+        else if (!strcasecmp(v, "TRACE")) c->log_level = 3;
+    }
+    if (const char* v = std::getenv("HCCL_ALGO")) {
+        for (int a = 0; a <= hcclAlgoRhd; ++a)
+            if (!strcasecmp(v, kAlgoNames[a])) c->env_algo = a;
+        if (c->env_algo < 0) hlog(c, 1, "HCCL_ALGO=%s is not a schedule (auto, direct, ring, two_level, rhd): ignored", v);
+    }
+    if (const char* v = std::getenv("HCCL_CHUNK_BYTES")) {
+        char* end = nullptr;
+        const unsigned long long n = std::strtoull(v, &end, 10);
+        uint64_t mul = 1;
+        if (end && (*end == 'K' || *end == 'k')) mul = 1024, ++end;
+        else if (end && (*end == 'M' || *end == 'm')) mul = 1024 * 1024, ++end;
+        if (end && *end == '\0' && n > 0 && n < (1ull << 40)) c->env_chunk = n * mul;
+        else hlog(c, 1, "HCCL_CHUNK_BYTES=%s is not a byte count: ignored", v);
+    }
+}
 
 bool env_flag(const char* name) {
     const char* v = std::getenv(name);
@@ -222,6 +267,12 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
     }
     if (!finalize(dp->prog, specs[0].tile_bytes, err)) return fail(hcclInternalError, err);
     dp->compile_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+    hlog(c, 2, "compiled %s%s: schedule %s%s, %zu steps, %u tiles, %u dependencies, %llu bytes read, %llu written, "
+               "%llu scratch, kernel kind %d, %.1f us",
+         specs.size() == 1 ? kCollNames[specs[0].coll] : "group of ", specs.size() == 1 ? "" : std::to_string(specs.size()).c_str(),
+         kAlgoNames[dp->prog.algo], dp->prog.fused ? " (fused)" : "", dp->prog.descs.size(), dp->prog.ntiles,
+         dp->prog.ndeps, (unsigned long long)dp->prog.bytes_read, (unsigned long long)dp->prog.bytes_written,
+         (unsigned long long)dp->prog.scratch_bytes, dp->prog.kind, dp->compile_us);
 
     if (c->device != HCCL_NO_DEVICE) {
         const auto& img = dp->prog.image;
@@ -441,7 +492,11 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         capturing = cs != hipStreamCaptureStatusNone;
     }
     hcclResult_t r = compile_program(c, specs, dp, hit, !capturing);
-    if (r != hcclSuccess) return r;
+    if (r != hcclSuccess) {
+        hlog(c, 1, "%s", g_last_error.c_str());
+        return r;
+    }
+    if (hit) hlog(c, 3, "cached program: %zu steps, %u tiles", dp->prog.descs.size(), dp->prog.ntiles);
 
     hcclProgramInfo_t& info = c->last;
     describe(info, specs, dp->prog, hit, dp->compile_us);
@@ -550,6 +605,8 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     }
     hipError_t e = launch_executor(a, blocks, kind, s);
     if (e != hipSuccess) return hip_fail(e, "executor launch");
+    hlog(c, 3, "launched kernel kind %d: %u workgroups, %u wavefronts, %s dispatch%s", kind, blocks, a.nworkers,
+         a.dynamic ? "ticket" : "static", a.trace ? ", traced" : "");
     if (signals) {
         e = launch_signal(trig.done_addr, trig.done_value, c->d_error, s);
         if (e != hipSuccess) return hip_fail(e, "completion word");
@@ -598,6 +655,8 @@ hcclResult_t fill_spec(hcclComm* c, CollectiveSpec& s, int coll, hcclDataType_t 
     s.tile_bytes = c->cfg.tile_bytes;
     s.order = c->cfg.order;
     s.requant = c->cfg.requantize != 0;
+    if (c->env_algo >= 0) s.algo = c->env_algo;
+    if (c->env_chunk) s.chunk_bytes = c->env_chunk;
     if (s.algo < hcclAlgoAuto || s.algo > hcclAlgoRhd) return fail(hcclInvalidArgument, "unknown algorithm");
     if (s.order < hcclOrderAscending || s.order > hcclOrderHalving) return fail(hcclInvalidArgument, "unknown order");
     return hcclSuccess;
@@ -634,6 +693,7 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
     c->device = device < 0 ? HCCL_NO_DEVICE : device;
     if (cfg) c->cfg = *cfg;
     else hccl_config_init(&c->cfg);
+    read_env(c.get());
     if (c->device != HCCL_NO_DEVICE) {
         int n = 0;
         hipError_t e = hipGetDeviceCount(&n);
@@ -666,6 +726,8 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
         if (e == hipSuccess) c->workspace = ws;
         else c->workspace_error = hipGetErrorString(e);
     }
+    hlog(c.get(), 2, "created: %d ranks on device %d (%d CUs)%s%s", c->nranks, c->device, c->cus,
+         c->env_algo >= 0 ? ", schedule forced by HCCL_ALGO" : "", c->env_chunk ? ", chunk forced by HCCL_CHUNK_BYTES" : "");
     *out = c.release();
     return hcclSuccess;
 }

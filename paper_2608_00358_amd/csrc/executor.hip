@@ -1056,7 +1056,7 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
                 else dyn_slot<KIND, true, true>(v, k, bufs, a.error, d, lane);
             }
         }
-    } else if (op != OP_NOOP) {
+    } else {
         TileOps ops;
         ops.nsrc = uni(D->nsrc);
         ops.ndst = uni(D->ndst);

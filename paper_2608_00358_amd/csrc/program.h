@@ -34,7 +34,9 @@ constexpr int kWaveSize = 64;
 enum Op : uint8_t {
     OP_COPY = 0,    // byte copy of src[0] to every destination (NMC "A = B")
     OP_REDUCE = 1,  // fold of all sources in list order, rounded once, to every destination
-    OP_NOOP = 2,    // carries only dependencies (a join)
+    // (2 is unused: the paper's NOOP WQE, a step that only carries dependencies so that a WQE
+    // can wait for several others, is not needed here: every step lists any number of
+    // dependency ids itself, so a join is the waiting step's own dependency list)
     // AllToAllvDynamic (device-resident layout): tile k ("slot" k) reads the count matrix from
     // device memory, checks the layout and moves its share of the rows. Names a DynA2A record.
     OP_DYN_COPY = 4,

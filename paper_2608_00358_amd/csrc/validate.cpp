@@ -2,7 +2,8 @@
 //
 // The paper's compiled model puts the whole dependency structure of a collective in the
 // host-generated graph (Section III-B-2: Fence, Sync, WQE Sync, Receive Sync, Send Sync and
-// NOOP joins). Here every ordering is an explicit dependency id, so the host can prove, before
+// NOOP joins). Here every ordering is an explicit dependency id (a join is a step's list of
+// several), so the host can prove, before
 // anything runs, that the program is well formed:
 //   * every dependency names an earlier step (the program is topologically ordered), and a
 //     per-tile dependency joins two steps with the same tiling;
@@ -69,9 +70,7 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
             err = fmt("step %llu has more than 64 sources or destinations", i);
             return false;
         }
-        if (d.op == OP_NOOP) {
-            if (!d.srcs.empty() || !d.dsts.empty()) { err = fmt("NOOP step %llu has operands", i); return false; }
-        } else if (d.op == OP_DYN_COPY) {
+        if (d.op == OP_DYN_COPY) {
             if (!d.srcs.empty() || !d.dsts.empty()) { err = fmt("dynamic step %llu has operands", i); return false; }
             if (d.aux >= p.aux.size()) { err = fmt("dynamic step %llu names record %llu", i, d.aux); return false; }
             const DynA2A& a = p.aux[d.aux];

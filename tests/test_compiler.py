@@ -456,3 +456,34 @@ def test_trigger_arguments_and_consumption():
         H.hccl_set_trigger(c.handle, (word, "lt", 3), (word + 8, 1))
         H.hccl_set_trigger(c.handle)                                                    # cleared
         H.hccl_allreduce(c.handle, s, r, 0, "fp32")
+
+
+# ------------------------------------------------------------------ environment overrides
+def test_hccl_algo_and_chunk_bytes_override_the_configuration(monkeypatch):
+    P, N = 4, 40000
+    monkeypatch.setenv("HCCL_ALGO", "direct")
+    monkeypatch.setenv("HCCL_CHUNK_BYTES", "16K")
+    with comm(P, algo="ring", chunk_bytes=1 << 20) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "fp32")
+        info = info_of(c)
+    assert info["algo"] == 1                               # direct, not the configured ring
+    assert info["num_descs"] == ceil_div(N, 16384 // 4)    # one step per 16 KiB chunk
+    monkeypatch.setenv("HCCL_ALGO", "no-such-schedule")
+    monkeypatch.delenv("HCCL_CHUNK_BYTES")
+    with comm(P, algo="ring", fuse=0) as c:              # an unknown value is ignored
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "fp32")
+        assert info_of(c)["algo"] == 2
+
+
+def test_hccl_debug_logs_creation_compiles_and_cache_hits(monkeypatch, capfd):
+    monkeypatch.setenv("HCCL_DEBUG", "TRACE")
+    with comm(2) as c:
+        for _ in range(2):
+            H.hccl_allgather(c.handle, fake_bufs(2, 1 << 40), fake_bufs(2, 1 << 44), 1000, "bf16")
+    err = capfd.readouterr().err
+    assert "[hccl INFO]" in err and "created: 2 ranks" in err
+    assert "compiled allgather" in err and "[hccl TRACE]" in err and "cached program" in err
+    monkeypatch.setenv("HCCL_DEBUG", "WARN")
+    with comm(2) as c:
+        H.hccl_allgather(c.handle, fake_bufs(2, 1 << 40), fake_bufs(2, 1 << 44), 1000, "bf16")
+    assert capfd.readouterr().err == ""
