@@ -26,6 +26,17 @@
  * Calls on one communicator must not run concurrently from several host threads. Calls
  * may be issued on different streams: the library orders a program's launches by itself.
  *
+ * Forward progress: a program whose steps wait for one another (unfused schedules) is launched
+ * with a grid sized to the CUs its stream may use. Handed out statically, its tiles need that
+ * whole grid resident at once; so while a kernel that waits for something still to come holds
+ * CUs of the device (a triggered packet of this process not yet released, a resident executor),
+ * such programs take their tiles by atomic ticket, which completes on whatever part of the
+ * grid is resident. Kernels of other processes that never finish are not known to the library.
+ * While a triggered packet waits, the library also makes no call that could wait for every
+ * stream of the device: programs are uploaded on a stream of the communicator that waits for
+ * no other, and memory it would free (evicted programs, outgrown scratch) is kept until
+ * hccl_comm_destroy.
+ *
  * Graph capture: a call (or group) whose program is already compiled enqueues kernel launches
  * only, so it may be made on a stream that is capturing a HIP graph. The first call of a given
  * shape compiles and uploads its program and may grow the communicator's scratch; made under
@@ -370,7 +381,8 @@ typedef struct {
     uint32_t workers;            /* wavefronts of the last launch (0 on host-only comms) */
     uint32_t max_srcs;           /* most sources of one step */
     uint32_t inline_launch;      /* 1 if the one-step program travelled in the launch packet */
-    uint32_t pad;
+    uint32_t tickets;            /* 1 if the last launch handed out tiles by atomic ticket (dependent
+                                    programs by default; see HCCL_DISPATCH), 0 if statically */
     uint64_t bytes_read;         /* bytes the program's steps read */
     uint64_t bytes_written;      /* bytes the program's steps write */
     uint64_t scratch_bytes;      /* FP32 scratch the program needs */

@@ -18,6 +18,7 @@
 #include <strings.h>
 #include <list>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -94,10 +95,13 @@ struct hcclComm {
     bool scratch_launched = false;
     bool scratch_captured = false;      // a graph holds d_scratch: growth keeps the old allocation
     std::vector<void*> retired_scratch;
+    hipStream_t setup_stream = nullptr;  // non-blocking: program uploads never wait for other streams
     std::list<std::unique_ptr<DeviceProgram>> cache;  // most recently used first
     std::vector<std::unique_ptr<DeviceProgram>> retired;  // evicted programs that a graph holds
     size_t cache_limit = 64;
-    bool dynamic_dispatch = false;  // tickets also for programs without dependencies
+    // tile dispatch (use_tickets): static, or by ticket for dependent programs while a waiting
+    // executor holds CUs; HCCL_DISPATCH=static / dynamic forces one for every program
+    int dispatch_mode = 0;           // 0 auto, 1 static, 2 tickets
     bool inline_single_step = true;  // one-step programs travel in the launch packet
     int group_depth = 0;             // > 0 between hccl_group_start and hccl_group_end
     std::vector<Call> pending;       // calls recorded inside a group
@@ -163,6 +167,67 @@ void read_env(hcclComm* c) {
         if (end && *end == '\0' && n > 0 && n < (1ull << 40)) c->env_chunk = n * mul;
         else hlog(c, 1, "HCCL_CHUNK_BYTES=%s is not a byte count: ignored", v);
     }
+}
+
+// Triggered packets still waiting on a device (any communicator of the process). While one is,
+// the library makes no call that could wait for every stream of that device (a free, a device
+// synchronisation): the host thread that would release the trigger might be the one waiting.
+struct PendingTrigger {
+    int device;
+    hipEvent_t done;  // recorded behind the packet (and its completion-word kernel)
+};
+std::mutex g_trigger_mu;
+std::vector<PendingTrigger> g_triggers;
+
+void note_trigger(int device, hipStream_t s) {
+    hipEvent_t ev = nullptr;
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return;
+    if (hipEventRecord(ev, s) != hipSuccess) {
+        (void)hipEventDestroy(ev);
+        return;
+    }
+    std::lock_guard<std::mutex> lock(g_trigger_mu);
+    g_triggers.push_back({device, ev});
+}
+
+// Resident executors running on each device (any communicator of the process).
+std::mutex g_resident_mu;
+std::vector<int> g_resident_devices;
+
+void note_resident(int device, bool running) {
+    std::lock_guard<std::mutex> lock(g_resident_mu);
+    if (running) {
+        g_resident_devices.push_back(device);
+        return;
+    }
+    for (size_t i = 0; i < g_resident_devices.size(); ++i)
+        if (g_resident_devices[i] == device) {
+            g_resident_devices.erase(g_resident_devices.begin() + (long)i);
+            return;
+        }
+}
+
+bool resident_running(int device) {
+    std::lock_guard<std::mutex> lock(g_resident_mu);
+    for (int d : g_resident_devices)
+        if (d == device) return true;
+    return false;
+}
+
+bool trigger_pending(int device) {
+    std::lock_guard<std::mutex> lock(g_trigger_mu);
+    bool any = false;
+    for (size_t i = 0; i < g_triggers.size();) {
+        if (hipEventQuery(g_triggers[i].done) == hipSuccess) {
+            (void)hipEventDestroy(g_triggers[i].done);
+            g_triggers[i] = g_triggers.back();
+            g_triggers.pop_back();
+            continue;
+        }
+        any |= g_triggers[i].device == device;
+        ++i;
+    }
+    return any;
 }
 
 bool env_flag(const char* name) {
@@ -278,7 +343,7 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
         const auto& img = dp->prog.image;
         hipError_t e = hipMalloc(&dp->d_image, img.size());
         if (e != hipSuccess) return fail(hcclOutOfMemory, "program image allocation failed");
-        e = hipMemcpy(dp->d_image, img.data(), img.size(), hipMemcpyHostToDevice);
+        e = hipMemcpyAsync(dp->d_image, img.data(), img.size(), hipMemcpyHostToDevice, c->setup_stream);
         if (e != hipSuccess) {
             free_program(dp.get());
             return hip_fail(e, "program upload");
@@ -288,9 +353,10 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
             free_program(dp.get());
             return fail(hcclOutOfMemory, "program state allocation failed");
         }
-        e = launch_fill_u32(dp->d_state, dp->prog.nstate, 0u, nullptr);
-        // only the fill is waited for: a resident executor on its own stream does not end by itself
-        if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+        e = launch_fill_u32(dp->d_state, dp->prog.nstate, 0u, c->setup_stream);
+        // only the upload and the fill are waited for, on a stream that waits for no other: a
+        // resident executor, or a triggered one whose release is still to come, may be running
+        if (e == hipSuccess) e = hipStreamSynchronize(c->setup_stream);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&dp->done, hipEventDisableTiming);
         if (e != hipSuccess) {
             free_program(dp.get());
@@ -299,8 +365,9 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
     }
     c->cache.push_front(std::move(dp));
     while (c->cache.size() > c->cache_limit) {
-        // (a free would also wait for a running resident executor, which ends only when stopped)
-        if (c->cache.back()->captured || c->resident)
+        // (a free could wait for a running resident executor, which ends only when stopped, or
+        // for a triggered one: those programs are kept until the communicator is destroyed)
+        if (c->cache.back()->captured || c->resident || trigger_pending(c->device))
             c->retired.push_back(std::move(c->cache.back()));
         else
             free_program(c->cache.back().get());
@@ -312,18 +379,26 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
 
 hcclResult_t ensure_scratch(hcclComm* c, uint64_t bytes) {
     if (bytes <= c->scratch_bytes) return hcclSuccess;
-    hipError_t e = hipDeviceSynchronize();  // the old scratch may still be in use
-    if (e != hipSuccess) return hip_fail(e, "synchronize before scratch growth");
-    if (c->d_scratch && c->scratch_captured)
+    // The old scratch may still be in use. A graph may hold it, and while a triggered packet
+    // waits a free could wait for it too: then it is kept until the communicator is destroyed.
+    // Otherwise the last launch that used it is waited for, and it is freed.
+    const bool keep = c->scratch_captured || trigger_pending(c->device);
+    if (c->d_scratch && !keep && c->scratch_launched) {
+        hipError_t e = hipEventSynchronize(c->scratch_done);
+        if (e != hipSuccess) return hip_fail(e, "wait before scratch growth");
+    }
+    if (c->d_scratch && keep)
         c->retired_scratch.push_back(c->d_scratch);
     else if (c->d_scratch)
         (void)hipFree(c->d_scratch);
+    hipError_t e;
     c->d_scratch = nullptr;
     c->scratch_captured = false;
     c->scratch_bytes = 0;
     e = hipMalloc(&c->d_scratch, bytes);
     if (e != hipSuccess) return fail(hcclOutOfMemory, "scratch allocation failed");
     c->scratch_bytes = bytes;
+    c->scratch_launched = false;
     return hcclSuccess;
 }
 
@@ -401,23 +476,41 @@ int launch_shape(hcclComm* c, const HostProgram& prog, LaunchArgs& a, uint32_t n
     return kind;
 }
 
+// How a launch hands out tiles. Static dispatch of a dependent program needs its whole grid
+// resident at once; that fails when a kernel that waits for something still to come holds CUs:
+// a triggered packet whose release is not enqueued yet, or a resident executor. While one of
+// those (of any communicator of the process) is on the device, dependent programs take their
+// tiles by ticket, which drains on whatever part of the grid is resident, at the price of one
+// same-address atomic per tile (the unfused ring all-reduce P=4 x 2^20 fp32: 86 -> 131 us).
+// HCCL_DISPATCH=static or =dynamic forces one way for every program.
+bool use_tickets(const hcclComm* c, const HostProgram& prog, bool triggered) {
+    if (c->dispatch_mode == 1) return false;
+    if (c->dispatch_mode == 2) return true;
+    if ((prog.flags & PF_HAS_DEPS) == 0) return false;
+    return triggered || trigger_pending(c->device) || resident_running(c->device);
+}
+
 // A program of one plain step without dependencies travels in the launch packet itself.
 bool inline_eligible(const hcclComm* c, const HostProgram& prog, bool triggered) {
     const bool plain_step = prog.descs.size() == 1 && (prog.descs[0].op == OP_COPY || prog.descs[0].op == OP_REDUCE);
-    return c->inline_single_step && plain_step && (prog.flags & PF_HAS_DEPS) == 0 && !c->dynamic_dispatch &&
+    return c->inline_single_step && plain_step && (prog.flags & PF_HAS_DEPS) == 0 && c->dispatch_mode != 2 &&
            !triggered && !c->cfg.trace;
 }
 
 // Trace buffer for `tiles` records (grown on demand; traced launches are a diagnostic mode).
 hcclResult_t ensure_trace(hcclComm* c, uint64_t tiles) {
     if (tiles <= c->trace_cap) return hcclSuccess;
-    hipError_t e = hipDeviceSynchronize();  // the old buffer may still be written
-    if (e != hipSuccess) return hip_fail(e, "synchronize before trace growth");
-    if (c->d_trace) (void)hipFree(c->d_trace);
+    if (trigger_pending(c->device)) {
+        if (c->d_trace) c->retired_scratch.push_back(c->d_trace);  // freed with the communicator
+    } else {
+        hipError_t e = hipDeviceSynchronize();  // the old buffer may still be written
+        if (e != hipSuccess) return hip_fail(e, "synchronize before trace growth");
+        if (c->d_trace) (void)hipFree(c->d_trace);
+    }
     c->d_trace = nullptr;
     c->trace_cap = 0;
     c->trace_tiles = 0;
-    e = hipMalloc(&c->d_trace, tiles * sizeof(TileStamp));
+    hipError_t e = hipMalloc(&c->d_trace, tiles * sizeof(TileStamp));
     if (e != hipSuccess) return fail(hcclOutOfMemory, "trace buffer allocation failed");
     c->trace_cap = tiles;
     return hcclSuccess;
@@ -558,7 +651,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     for (const Call& k : calls)
         for (void* m : k.meta) a.bufs[mb++] = (char*)m;
     const bool has_deps = (dp->prog.flags & PF_HAS_DEPS) != 0;
-    a.dynamic = c->dynamic_dispatch ? 1u : 0u;  // tickets only on request (HCCL_DISPATCH=dynamic)
+    a.dynamic = use_tickets(c, dp->prog, triggered) ? 1u : 0u;
     const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
     a.timeout_ticks = ms * c->wall_clock_khz;
     if (triggered) {
@@ -574,6 +667,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     uint32_t blocks = 0;
     const int kind = launch_shape(c, dp->prog, a, nuser, s, blocks);
     info.workers = a.nworkers;
+    info.tickets = a.dynamic;
 
     if (inline_eligible(c, dp->prog, triggered)) {
         info.inline_launch = 1;
@@ -611,6 +705,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         e = launch_signal(trig.done_addr, trig.done_value, c->d_error, s);
         if (e != hipSuccess) return hip_fail(e, "completion word");
     }
+    if (triggered) note_trigger(c->device, s);
     if (stateful) {
         e = hipEventRecord(dp->done, s);
         if (e != hipSuccess) return hip_fail(e, "completion event");
@@ -706,7 +801,7 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
             c->wall_clock_khz = (uint64_t)khz;
         c->inline_single_step = !(std::getenv("HCCL_INLINE") && std::strcmp(std::getenv("HCCL_INLINE"), "0") == 0);
         const char* disp = std::getenv("HCCL_DISPATCH");
-        c->dynamic_dispatch = disp && std::strcmp(disp, "dynamic") == 0;
+        c->dispatch_mode = !disp ? 0 : std::strcmp(disp, "static") == 0 ? 1 : std::strcmp(disp, "dynamic") == 0 ? 2 : 0;
         const char* bpc = std::getenv("HCCL_BLOCKS_PER_CU");
         for (int k = 0; k < kNumKinds; ++k) {
             if (k > SIG_INT32 && k < kKindCopyOnly) continue;  // no kernel of its own
@@ -716,6 +811,8 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
         }
         e = hipEventCreateWithFlags(&c->scratch_done, hipEventDisableTiming);
         if (e != hipSuccess) return hip_fail(e, "scratch event");
+        e = hipStreamCreateWithFlags(&c->setup_stream, hipStreamNonBlocking);
+        if (e != hipSuccess) return hip_fail(e, "setup stream");
         e = hipMalloc(&c->d_error, sizeof(ErrorRecord));
         if (e != hipSuccess) return fail(hcclOutOfMemory, "error record allocation failed");
         e = hipMemset(c->d_error, 0, sizeof(ErrorRecord));
@@ -747,6 +844,7 @@ hcclResult_t hccl_comm_destroy(hcclComm_t comm) {
         if (comm->d_error) (void)hipFree(comm->d_error);
         if (comm->d_trace) (void)hipFree(comm->d_trace);
         if (comm->scratch_done) (void)hipEventDestroy(comm->scratch_done);
+        if (comm->setup_stream) (void)hipStreamDestroy(comm->setup_stream);
     }
     delete comm;
     return hcclSuccess;
@@ -881,12 +979,13 @@ hcclResult_t hccl_allreduce_noalloc(hcclComm_t comm, const void* const* sendbufs
         a.bufs[recv_buf(P, i)] = (char*)recvbufs[i];
     }
     a.bufs[scratch_buf(P)] = ws + off_scratch;
-    a.dynamic = comm->dynamic_dispatch ? 1u : 0u;
+    a.dynamic = use_tickets(comm, *hp, false) ? 1u : 0u;
     const uint64_t ms = comm->cfg.timeout_ms ? comm->cfg.timeout_ms : 2000u;
     a.timeout_ticks = ms * comm->wall_clock_khz;
     uint32_t blocks = 0;
     const int kind = launch_shape(comm, *hp, a, 2u * (uint32_t)P, st, blocks);
     comm->last.workers = a.nworkers;
+    comm->last.tickets = a.dynamic;
     hipError_t e;
     if (inline_eligible(comm, *hp, false)) {
         comm->last.inline_launch = 1;
@@ -1208,6 +1307,7 @@ hcclResult_t hccl_resident_start(hcclComm_t comm, uint32_t blocks, uint32_t idle
     comm->resident_stream = st;
     comm->resident_seq = 0;
     comm->resident = true;
+    note_resident(comm->device, true);
     return hcclSuccess;
 }
 
@@ -1234,6 +1334,7 @@ hcclResult_t hccl_resident_stop(hcclComm_t comm) {
     comm->d_ctl = nullptr;
     comm->rq = nullptr;
     comm->resident = false;
+    note_resident(comm->device, false);
     if (e != hipSuccess) return hip_fail(e, "resident executor stop");
     return r;
 }

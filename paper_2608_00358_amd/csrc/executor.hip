@@ -1220,23 +1220,35 @@ hccl_executor(LaunchArgs a) {
     // a workgroup whose trigger wait failed runs no tile but still counts itself done below
     const bool started = !triggered || trigger_wait(a);
     if (started && !a.dynamic) {
-        // Wavefront w runs tiles w, w + W, w + 2W, ... in order. A tile waits only for tiles with
-        // lower numbers, and everything a wavefront ran before its current tile is lower too, so
-        // with the whole grid resident the lowest unfinished tile is always running.
+        // Wavefront w runs tiles w, w + W, w + 2W, ... in order. Without dependencies no tile
+        // waits for another, so any residency drains. A dependent program needs the whole grid
+        // resident (the host then sizes it to the CUs the stream may use and sends it here only
+        // while no waiting executor holds CUs): a tile waits only for lower tiles, everything
+        // a wavefront ran before is lower, and the lowest unfinished tile is always running.
         for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
             if ((has_deps || triggered) && load_relaxed(&a.error->code) != 0u) break;
             if (!run_tile_traced<KIND>(sh, prog, h, t, lane, bufs, a.trace, wave)) break;
         }
     } else if (started) {
+        // Tiles by ticket, in program order: a tile is only ever held by a running wavefront,
+        // and it waits only for lower tiles, which running wavefronts took before it; so the
+        // program drains whatever part of the grid is resident (a resident or a triggered
+        // executor may hold CUs). The first tiles are taken per workgroup, one atomic for its
+        // four wavefronts (the start is when every wavefront would hit the counter).
         uint32_t* ticket = a.state + kStateTicket;
-        uint32_t mine = 0;
-        if (lane == 0) mine = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        uint32_t t = uni(__shfl(mine, 0));
+        __shared__ uint32_t first;
+        if (threadIdx.x == 0)
+            first = __hip_atomic_fetch_add(ticket, (uint32_t)kWavesPerBlock, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+        uint32_t t = uni(first + threadIdx.x / kWaveSize);
+        // with at least as many wavefronts as tiles the first tickets cover every tile
+        const bool more = h.ntiles > nworkers;
         while (t < h.ntiles) {
             if (load_relaxed(&a.error->code) != 0u) break;
             // claim the next ticket now; its latency hides behind this tile's work
-            uint32_t next = 0;
-            if (lane == 0) next = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            uint32_t next = h.ntiles;
+            if (more && lane == 0)
+                next = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (!run_tile_traced<KIND>(sh, prog, h, t, lane, bufs, a.trace, wave)) break;
             t = uni(__shfl(next, 0));
         }

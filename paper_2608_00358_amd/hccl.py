@@ -61,7 +61,7 @@ class hcclProgramInfo_t(ctypes.Structure):
         ("collective", ctypes.c_int32), ("algo", ctypes.c_int32), ("fused", ctypes.c_int32),
         ("cache_hit", ctypes.c_int32), ("num_descs", ctypes.c_uint32), ("num_tiles", ctypes.c_uint32),
         ("num_deps", ctypes.c_uint32), ("num_operands", ctypes.c_uint32), ("workers", ctypes.c_uint32),
-        ("max_srcs", ctypes.c_uint32), ("inline_launch", ctypes.c_uint32), ("pad", ctypes.c_uint32),
+        ("max_srcs", ctypes.c_uint32), ("inline_launch", ctypes.c_uint32), ("tickets", ctypes.c_uint32),
         ("bytes_read", ctypes.c_uint64), ("bytes_written", ctypes.c_uint64),
         ("scratch_bytes", ctypes.c_uint64), ("program_bytes", ctypes.c_uint64), ("compile_us", ctypes.c_double),
         ("step_tile_min", ctypes.c_uint32), ("step_tile_max", ctypes.c_uint32),

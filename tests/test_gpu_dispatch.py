@@ -1,9 +1,11 @@
 """GPU parity of dependent programs under both ways of handing tiles to wavefronts.
 
-By default wavefront w runs tiles w, w + W, ...; HCCL_DISPATCH=dynamic makes every wavefront
-take tiles by atomic ticket instead, and HCCL_INLINE=0 sends one-step programs through the
-device image too. Each mode must give the oracle's bits, launch after launch (the counters are
-cleared at the end of every launch).
+By default programs take tiles statically (wavefront w runs tiles w, w + W, ...) and dependent
+ones by atomic ticket while a waiting executor holds CUs; HCCL_DISPATCH=static makes every
+program static, HCCL_DISPATCH=dynamic every program ticketed, and HCCL_INLINE=0 sends one-step
+programs through the device image too.
+Each mode must give the oracle's bits, launch after launch (the counters are cleared at the end
+of every launch).
 """
 import numpy as np
 import pytest
@@ -19,8 +21,10 @@ pytestmark = pytest.mark.gpu
 SMALL = dict(chunk_bytes=4096, tile_bytes=4096)
 
 
-@pytest.fixture(params=["static", "tickets", "no_inline"])
+@pytest.fixture(params=["auto", "static", "tickets", "no_inline"])
 def mode(request, monkeypatch):
+    if request.param == "static":
+        monkeypatch.setenv("HCCL_DISPATCH", "static")
     if request.param == "tickets":
         monkeypatch.setenv("HCCL_DISPATCH", "dynamic")
     if request.param == "no_inline":

@@ -18,8 +18,15 @@ def _check_records(rec, khz, info):
     assert rec.shape == (n,)
     assert (rec["start"] > 0).all(), "a tile left no record"
     assert (rec["done"] >= rec["ready"]).all()
-    # static dispatch: wavefront w runs tiles w, w + W, ...
-    assert np.array_equal(rec["wave"], np.arange(n, dtype=np.uint32) % info["workers"])
+    if not info["tickets"]:
+        # static dispatch: wavefront w runs tiles w, w + W, ...
+        assert np.array_equal(rec["wave"], np.arange(n, dtype=np.uint32) % info["workers"])
+    else:
+        # tickets: every wavefront takes its tiles in increasing order, one after the other
+        assert (rec["wave"] < info["workers"]).all()
+        for w in np.unique(rec["wave"]):
+            mine = np.nonzero(rec["wave"] == w)[0]
+            assert (np.diff(rec["start"][mine].astype(np.int64)) >= 0).all()
     assert ((rec["where"] >> 24) < 8).all()                   # XCC ids of the device
     span_us = (int((rec["start"] + rec["done"]).max()) - int(rec["start"].min())) * 1e3 / khz
     assert 0 < span_us < 1e6
@@ -44,9 +51,9 @@ def test_traced_ring_allreduce_records_every_tile(fuse):
     want = oracle.allreduce(x, "bf16")
     for r in range(P):
         assert same_bits(out[r].result(), want[r], "bf16") and out[r].guards_intact()
+    assert info["tickets"] == 0     # nothing else holds CUs: static dispatch
     if not fuse:
-        # a dependent step waits: some tiles are ready only after they were taken
-        assert (rec["ready"] > 0).any()
+        assert (rec["ready"] > 0).any()   # a dependent step waits
     print(f"trace: {info['num_tiles']} tiles over {span:.1f} us", flush=True)
 
 

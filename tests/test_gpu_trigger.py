@@ -173,3 +173,52 @@ def test_trigger_never_satisfied_times_out_and_moves_nothing():
     want = oracle.allreduce(x, "fp32")
     for r in range(P):
         assert same_bits(outs[r].result(), want[r], "fp32")
+
+
+def test_compile_and_scratch_growth_while_a_triggered_packet_waits():
+    """While a triggered all-reduce waits on its masked stream (holding those CUs), the same
+    communicator compiles a new program, grows its scratch and runs an unfused ring
+    reduce-scatter on another stream. That must finish before the trigger is released: nothing
+    the library does then waits for every stream of the device (the upload goes on a stream of
+    its own, the old scratch is kept instead of freed), and the dependent program drains on the
+    CUs left to it (its tiles go by ticket). Then the trigger is released."""
+    P, N, M = 8, 30011, 4001
+    x = inputs(P, N, "bf16", 33)
+    y = inputs(P, P * M, "bf16", 34)
+    send = [to_device(x[r], "bf16") for r in range(P)]
+    outs = [Guarded(N, "bf16") for _ in range(P)]
+    ysend = [to_device(y[r], "bf16") for r in range(P)]
+    small = [torch.empty(100, dtype=torch.bfloat16, device="cuda:0") for _ in range(P * 2)]
+    youts = [Guarded(M, "bf16") for _ in range(P)]
+    flag, done = words()
+    torch.cuda.synchronize()
+    print("trigger pending: compile, scratch growth and a dependent program on another stream", flush=True)
+    with MaskedStream(2) as s, SideStream() as cs, H.Comm(P, device=0, chunk_bytes=8192, timeout_ms=10000) as c:
+        c.set_config(algo="ring", fuse=0, chunk_bytes=8192, timeout_ms=10000)
+        H.hccl_allreduce(c.handle, small[:P], small[P:], 100, "bf16", stream=cs)   # a first, small scratch
+        cs.synchronize()
+        c.set_config(algo="ring", chunk_bytes=8192, timeout_ms=10000)
+        with c.triggered(wait=(flag, "ge", 1), done=(done, 7)):
+            H.hccl_allreduce(c.handle, send, [o.view for o in outs], N, "bf16", stream=s)
+        time.sleep(0.02)
+        c.set_config(algo="ring", fuse=0, chunk_bytes=8192, timeout_ms=10000)
+        t0 = time.perf_counter()
+        H.hccl_reduce_scatter(c.handle, ysend, [o.view for o in youts], M, "bf16", stream=cs)
+        tickets = c.last_program()["tickets"]
+        cs.synchronize()
+        elapsed = time.perf_counter() - t0
+        with torch.cuda.stream(cs):
+            before = int(done.cpu())          # the triggered packet has not run yet
+            flag.fill_(1)
+        cs.synchronize()
+        s.synchronize()
+        assert c.async_error() == 0
+    assert before == 0 and int(done.item()) == 7
+    assert tickets == 1    # a dependent program while a triggered packet waits takes tiles by ticket
+    assert elapsed < 2.0, f"the reduce-scatter took {elapsed:.2f} s while the trigger waited"
+    want = oracle.allreduce(x, "bf16")
+    for r in range(P):
+        assert same_bits(outs[r].result(), want[r], "bf16") and outs[r].guards_intact()
+    wrs = oracle.reduce_scatter(y, "bf16")
+    for r in range(P):
+        assert same_bits(youts[r].result(), wrs[r], "bf16") and youts[r].guards_intact()
