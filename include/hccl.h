@@ -395,6 +395,19 @@ typedef struct {
 hcclResult_t hccl_comm_last_program(hcclComm_t comm, hcclProgramInfo_t* info);
 
 /*
+ * The packed program image of the same program (Section III-B-2: the host builds the complete
+ * description of the work packet, its WQEs and their dependency metadata, before the device
+ * runs it), exactly as uploaded: a header, then 64-byte steps, 16-byte operands {buffer id,
+ * element type, byte offset}, 16-byte dependencies {step, kind, expected count, state word},
+ * one owning step per tile and the AllToAllvDynamic records (layout: csrc/program.h). Buffer
+ * ids, not addresses, name the operands: send buffers 0..P-1, receive buffers P..2P-1, the
+ * scratch 2P (in a group, each call's ids follow the previous calls'). For tools and tests,
+ * e.g. an interpreter that runs the steps in any order the dependencies allow. Copies
+ * min(capacity, *size) bytes; *size = 0 when the program was evicted or none was compiled.
+ */
+hcclResult_t hccl_comm_program_image(hcclComm_t comm, void* out, size_t capacity, size_t* size);
+
+/*
  * Per-tile trace (Section V-C: counters on every work packet and subgraph show when each
  * component handled it; the control-core overhead is read off them). With hcclConfig_t.trace
  * set, every launch records, for each tile of its program, the wall-clock time at which an

@@ -108,6 +108,7 @@ struct hcclComm {
     bool has_trigger = false;        // hccl_set_trigger for the next work packet
     hcclTrigger_t trigger{};
     hcclProgramInfo_t last{};
+    const HostProgram* last_prog = nullptr;  // the program `last` describes (NULL once evicted)
     // resident executor (hccl_resident_start .. hccl_resident_stop)
     bool resident = false;
     ResidentQueue* rq = nullptr;      // coherent pinned host memory, shared with the executor
@@ -369,8 +370,10 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
         // for a triggered one: those programs are kept until the communicator is destroyed)
         if (c->cache.back()->captured || c->resident || trigger_pending(c->device))
             c->retired.push_back(std::move(c->cache.back()));
-        else
+        else {
+            if (c->last_prog == &c->cache.back()->prog) c->last_prog = nullptr;
             free_program(c->cache.back().get());
+        }
         c->cache.pop_back();
     }
     out = c->cache.front().get();
@@ -593,6 +596,7 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
 
     hcclProgramInfo_t& info = c->last;
     describe(info, specs, dp->prog, hit, dp->compile_us);
+    c->last_prog = &dp->prog;
 
     if (triggered) {
         if (dp->prog.ntiles == 0) return fail(hcclInvalidArgument, "a triggered work packet has no work to run");
@@ -917,7 +921,10 @@ hcclResult_t host_program(hcclComm* c, const CollectiveSpec& s, const HostProgra
         return fail(hcclInternalError, "program validation failed: " + err);
     compile_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
     c->host_cache.emplace_front(s, std::move(hp));
-    while (c->host_cache.size() > 16) c->host_cache.pop_back();
+    while (c->host_cache.size() > 16) {
+        if (c->last_prog == c->host_cache.back().second.get()) c->last_prog = nullptr;
+        c->host_cache.pop_back();
+    }
     out = c->host_cache.front().second.get();
     return hcclSuccess;
 }
@@ -956,6 +963,7 @@ hcclResult_t hccl_allreduce_noalloc(hcclComm_t comm, const void* const* sendbufs
     double compile_us = 0;
     if ((r = host_program(comm, s, hp, hit, compile_us)) != hcclSuccess) return r;
     describe(comm->last, {s}, *hp, hit, compile_us);
+    comm->last_prog = hp;
     if (hp->ntiles == 0) return hcclSuccess;
 
     // workspace layout of this call: program image, counters, FP32 partials
@@ -1380,6 +1388,18 @@ hcclResult_t hccl_comm_trace(hcclComm_t comm, hcclTileTrace_t* out, size_t capac
         if (e != hipSuccess) return hip_fail(e, "read trace");
     }
     *count = comm->trace_tiles;
+    return hcclSuccess;
+}
+
+hcclResult_t hccl_comm_program_image(hcclComm_t comm, void* out, size_t capacity, size_t* size) {
+    if (check_comm(comm) != hcclSuccess) return hcclInvalidArgument;
+    if (!size) return fail(hcclInvalidArgument, "null size");
+    if (capacity && !out) return fail(hcclInvalidArgument, "null output");
+    *size = 0;
+    if (!comm->last_prog) return hcclSuccess;
+    const std::vector<uint8_t>& img = comm->last_prog->image;
+    *size = img.size();
+    if (capacity) std::memcpy(out, img.data(), std::min(capacity, img.size()));
     return hcclSuccess;
 }
 

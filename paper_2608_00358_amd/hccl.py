@@ -29,7 +29,7 @@ EXPORTS = [
     "hccl_get_last_error", "hccl_result_string", "hccl_get_async_error", "hccl_comm_last_program",
     "hccl_group_start", "hccl_group_end", "hccl_alltoallv_dynamic", "hccl_set_trigger",
     "hccl_resident_start", "hccl_resident_stop", "hccl_resident_wait", "hccl_resident_last_seq",
-    "hccl_allreduce_noalloc", "hccl_comm_trace",
+    "hccl_allreduce_noalloc", "hccl_comm_trace", "hccl_comm_program_image",
 ]
 CMPS = {"eq": 0, "ne": 1, "ge": 2, "gt": 3, "le": 4, "lt": 5}
 
@@ -108,6 +108,7 @@ def load(path: str = LIB_PATH):
     lib.hccl_result_string.restype = ctypes.c_char_p
     lib.hccl_get_async_error.argtypes = [vp]
     lib.hccl_comm_last_program.argtypes = [vp, ctypes.POINTER(hcclProgramInfo_t)]
+    lib.hccl_comm_program_image.argtypes = [vp, vp, sz, ctypes.POINTER(ctypes.c_size_t)]
     lib.hccl_comm_trace.argtypes = [vp, ctypes.POINTER(hcclTileTrace_t), sz, ctypes.POINTER(ctypes.c_size_t),
                                     ctypes.POINTER(ctypes.c_uint64)]
     lib.hccl_group_start.argtypes = [vp]
@@ -296,6 +297,16 @@ def hccl_comm_last_program(comm) -> dict:
     return {name: getattr(info, name) for name, _ in hcclProgramInfo_t._fields_}
 
 
+def hccl_comm_program_image(comm) -> bytes:
+    """The packed image of the communicator's last program (b"" if none)."""
+    lib = load()
+    n = ctypes.c_size_t(0)
+    _check(lib.hccl_comm_program_image(comm, None, 0, ctypes.byref(n)))
+    buf = ctypes.create_string_buffer(max(1, n.value))
+    _check(lib.hccl_comm_program_image(comm, buf, n.value, ctypes.byref(n)))
+    return buf.raw[: n.value]
+
+
 def hccl_comm_trace(comm):
     """Records of the last traced launch as a numpy structured array (fields start, ready, done,
     wave, where; times in wall-clock ticks) and the clock rate in kHz."""
@@ -444,6 +455,9 @@ class Comm:
 
     def trace(self):
         return hccl_comm_trace(self.handle)
+
+    def program_image(self) -> bytes:
+        return hccl_comm_program_image(self.handle)
 
     def async_error(self) -> int:
         return hccl_get_async_error(self.handle)
