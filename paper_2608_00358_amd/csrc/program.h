@@ -148,7 +148,7 @@ struct DynA2A {            // 72 bytes
     uint32_t sdispls;      // buffer id of explicit send offsets [s*P + d], or kNoBuffer (packed)
     uint32_t rdispls;      // buffer id of explicit receive offsets [d*P + s], or kNoBuffer (packed)
     uint32_t recvcounts;   // buffer id of the received-count output [d*P + s], or kNoBuffer
-    uint32_t slots;        // tiles of the step; slot k moves dynamic tiles [k*J/slots, (k+1)*J/slots)
+    uint32_t slots;        // tiles of the step; slot k moves dynamic tiles k, k + slots, k + 2 slots, ...
     uint32_t pad;
     uint64_t row_elems;
     uint64_t send_cap;     // rows per send buffer
