@@ -206,10 +206,15 @@ def bench_allreduce_ring_c1(device, iters=200, cold_sets=40):
         ms = _time_events(cold, iters)
         out["cold_us"] = ms * 1e3
         out["cold_gbs"] = algo / (ms * 1e-3) / 1e9
-        # the same program with every ring step as its own dependent descriptor
-        c.set_config(algo="ring", chunk_bytes=64 * 1024, fuse=0)
-        ms = _time_events(c.bind_allreduce(send, recv), iters)
-        out["unfused_warm_gbs"] = algo / (ms * 1e-3) / 1e9
+        # the same program with every ring step as its own dependent descriptor: one launch per
+        # hop (the default), and one launch whose steps wait for each other tile by tile
+        for phases in ("auto", "one"):
+            c.set_config(algo="ring", chunk_bytes=64 * 1024, fuse=0, phases=phases)
+            ms = _time_events(c.bind_allreduce(send, recv), iters)
+            key = "unfused" if phases == "auto" else "unfused_one_launch"
+            out[f"{key}_warm_us"] = ms * 1e3
+            out[f"{key}_warm_gbs"] = algo / (ms * 1e-3) / 1e9
+            out[f"{key}_launches"] = c.last_program()["num_phases"]
     out.update({"workload": "allreduce ring P=4 N=2^20 fp32 chunk=64KiB", "algo_bytes": algo,
                 "descs": info["num_descs"], "tiles": info["num_tiles"], "compile_us": round(info["compile_us"], 1)})
     return out
@@ -271,9 +276,11 @@ def bench_forwarded_partials(device, iters=10):
         ("ascending_ring_fused", dict(algo="ring")),
         ("ring_order_fused", dict(algo="ring", order="ring")),
         ("ring_order_forwarded_partials", dict(algo="ring", order="ring", fuse=0)),
+        ("ring_order_forwarded_partials_one_launch", dict(algo="ring", order="ring", fuse=0, phases="one")),
         ("ring_order_forwarded_requantised", dict(algo="ring", order="ring", fuse=0, requantize=1)),
         ("halving_rhd_fused", dict(algo="rhd", order="halving")),
         ("halving_rhd_butterfly", dict(algo="rhd", order="halving", fuse=0)),
+        ("halving_rhd_butterfly_one_launch", dict(algo="rhd", order="halving", fuse=0, phases="one")),
         ("halving_rhd_butterfly_requantised", dict(algo="rhd", order="halving", fuse=0, requantize=1)),
     ]
     ref = None
@@ -290,8 +297,8 @@ def bench_forwarded_partials(device, iters=10):
         sched = info["bytes_read"] + info["bytes_written"]
         res = {"us": round(ms * 1e3, 1), "gbs": round(algo / (ms * 1e-3) / 1e9, 1),
                "schedule_bytes": sched, "traffic_over_algorithmic": round(sched / algo, 4),
-               "descs": info["num_descs"], "deps": info["num_deps"], "scratch_bytes": info["scratch_bytes"],
-               "compile_us": round(info["compile_us"], 1)}
+               "descs": info["num_descs"], "deps": info["num_deps"], "launches": info["num_phases"],
+               "scratch_bytes": info["scratch_bytes"], "compile_us": round(info["compile_us"], 1)}
         if ref is None:
             ref = recv
         else:
@@ -381,11 +388,18 @@ def bench_two_level_c4(device, iters=10, unfused=True):
         ms = _time_events(lambda: c.allreduce(send, recv), iters)
         info = c.last_program()
         out.update({"us": ms * 1e3, "gbs": algo / (ms * 1e-3) / 1e9, "descs": info["num_descs"],
-                    "compile_us": round(info["compile_us"], 1),
+                    "compile_us": round(info["compile_us"], 1), "launches": info["num_phases"],
+                    "schedule_bytes": info["bytes_read"] + info["bytes_written"],
                     "tiles": info["num_tiles"], "workers": info["workers"]})
         if not unfused:
             out["frac"] = out["gbs"] / HBM_PEAK_GBS
             return out
+        # the same program as one launch: every reduction writes all 64 ranks itself
+        c.set_config(algo="two_level", group_size=L, phases="one")
+        c.allreduce(send, recv)
+        ms1 = _time_events(lambda: c.allreduce(send, recv), iters)
+        out.update({"one_launch_us": ms1 * 1e3, "one_launch_gbs": algo / (ms1 * 1e-3) / 1e9})
+        c.set_config(algo="two_level", group_size=L)
         # the same sum in the flat ascending order (one 64-source fold per element): its time,
         # and how far the two-level tree order's results lie from it
         flat = [torch.empty(N, dtype=torch.bfloat16, device=device) for _ in range(P)]
@@ -397,12 +411,15 @@ def bench_two_level_c4(device, iters=10, unfused=True):
                     "tree_vs_flat_differ": int((d > 0).sum()), "tree_vs_flat_above_1ulp": int((d > 1).sum()),
                     "tree_vs_flat_max_ulp": int(d.max()), "elements": N})
         del flat
-        c.set_config(algo="two_level", group_size=L, fuse=0)
-        c.allreduce(send, recv)
-        ms = _time_events(lambda: c.allreduce(send, recv), iters)
-        info = c.last_program()
-        out.update({"unfused_us": ms * 1e3, "unfused_gbs": algo / (ms * 1e-3) / 1e9,
-                    "unfused_schedule_bytes": info["bytes_read"] + info["bytes_written"]})
+        for phases in ("auto", "one"):
+            c.set_config(algo="two_level", group_size=L, fuse=0, phases=phases)
+            c.allreduce(send, recv)
+            ms = _time_events(lambda: c.allreduce(send, recv), iters)
+            info = c.last_program()
+            key = "unfused" if phases == "auto" else "unfused_one_launch"
+            out.update({f"{key}_us": ms * 1e3, f"{key}_gbs": algo / (ms * 1e-3) / 1e9,
+                        f"{key}_launches": info["num_phases"],
+                        f"{key}_schedule_bytes": info["bytes_read"] + info["bytes_written"]})
     out["frac"] = out["gbs"] / HBM_PEAK_GBS
     del send, recv
     torch.cuda.empty_cache()

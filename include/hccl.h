@@ -106,6 +106,23 @@ typedef enum {
 typedef enum { hcclOrderAscending = 0, hcclOrderRing = 1, hcclOrderHalving = 2 } hcclOrder_t;
 
 /*
+ * Phases (Section III-B-2: a WQE waits for the steps it depends on; Section II-A-2: the control
+ * core evaluates those dependencies as it unrolls the work). A compiled program runs as one or
+ * more executor launches on the caller's stream, its phases. A dependency between steps of
+ * different phases is met by the launch order (a launch ends with its results visible
+ * device-wide); only a dependency inside one phase is waited for on the device, tile by tile.
+ * AUTO: one launch per dependency level when the program has dependencies and at most 32
+ *   levels, otherwise one launch; and when the wide reductions (16 or more sources) of a call
+ *   read 256 MiB or more from the send buffers, their results are copied to the other ranks by a
+ *   later phase instead of being written to every rank by the reductions themselves.
+ * ONE: one launch; dependencies are waited for tile by tile on the device.
+ * LEVELS: one launch per dependency level (up to 64), and the copies of every wide reduction's
+ *   result run as a later phase.
+ * The results are the same in every mode (the same operations in the same order).
+ */
+typedef enum { hcclPhasesAuto = 0, hcclPhasesOne = 1, hcclPhasesLevels = 2 } hcclPhases_t;
+
+/*
  * Configuration of a communicator (Section V-D: topology-aware algorithm selection, here the
  * schedule, the fold order and the group size of the two-level schedule; Section III-B-2: the
  * work packet's chunking into WQEs, here the chunk and tile sizes). Fields left at zero take the
@@ -130,7 +147,8 @@ typedef struct {
     int32_t order;         /* hcclOrder_t */
     int32_t requantize;    /* 1 = round every partial to the buffer type */
     int32_t trace;         /* 1 = record times and place of every tile of every launch (hccl_comm_trace) */
-    int32_t reserved[2];
+    int32_t phases;        /* hcclPhases_t: how a program's steps are spread over launches */
+    int32_t reserved;
 } hcclConfig_t;
 
 typedef struct hcclComm* hcclComm_t;
@@ -330,7 +348,9 @@ hcclResult_t hccl_get_async_error(hcclComm_t comm);
  * and takes work packets through a doorbell: a ring of slots in coherent pinned host memory.
  * From then until hccl_resident_stop, every call (or group) on the communicator is handed to it
  * instead of being launched: the call writes the packet's arguments into the next slot and
- * then the slot's sequence number (1, 2, ...), and returns. No kernel is launched per call.
+ * then the slot's sequence number (1, 2, ...), and returns. No kernel is launched per call. A
+ * program of several phases (hcclPhases_t) is handed over as one packet per phase, each with
+ * its own sequence number, in phase order; hccl_resident_last_seq then names the last.
  *
  *   blocks   workgroups of 4 wavefronts (0 = 32); they must all fit on the device at once,
  *            else hcclInvalidArgument.
@@ -390,6 +410,8 @@ typedef struct {
     double compile_us;           /* host time to lower, fuse, validate and pack */
     uint32_t step_tile_min;      /* smallest and largest tile (elements) of the program's copy and */
     uint32_t step_tile_max;      /* reduce steps: steps of different element widths may differ */
+    uint32_t num_phases;         /* executor launches per call (see hcclPhases_t) */
+    uint32_t reserved;
 } hcclProgramInfo_t;
 
 hcclResult_t hccl_comm_last_program(hcclComm_t comm, hcclProgramInfo_t* info);

@@ -333,11 +333,11 @@ hcclResult_t compile_program(hcclComm* c, const std::vector<CollectiveSpec>& spe
     }
     if (!finalize(dp->prog, specs[0].tile_bytes, err)) return fail(hcclInternalError, err);
     dp->compile_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
-    hlog(c, 2, "compiled %s%s: schedule %s%s, %zu steps, %u tiles, %u dependencies, %llu bytes read, %llu written, "
-               "%llu scratch, kernel kind %d, %.1f us",
+    hlog(c, 2, "compiled %s%s: schedule %s%s, %zu steps, %u tiles, %u dependencies, %u phases, %llu bytes read, "
+               "%llu written, %llu scratch, kernel kind %d, %.1f us",
          specs.size() == 1 ? kCollNames[specs[0].coll] : "group of ", specs.size() == 1 ? "" : std::to_string(specs.size()).c_str(),
          kAlgoNames[dp->prog.algo], dp->prog.fused ? " (fused)" : "", dp->prog.descs.size(), dp->prog.ntiles,
-         dp->prog.ndeps, (unsigned long long)dp->prog.bytes_read, (unsigned long long)dp->prog.bytes_written,
+         dp->prog.ndeps, dp->prog.nphase(), (unsigned long long)dp->prog.bytes_read, (unsigned long long)dp->prog.bytes_written,
          (unsigned long long)dp->prog.scratch_bytes, dp->prog.kind, dp->compile_us);
 
     if (c->device != HCCL_NO_DEVICE) {
@@ -419,6 +419,15 @@ uint32_t stream_cu_count(hcclComm* c, hipStream_t s) {
 uint64_t resident_done(const hcclComm* c) { return __atomic_load_n(&c->rq->done_seq, __ATOMIC_ACQUIRE); }
 bool resident_exited(const hcclComm* c) { return __atomic_load_n(&c->rq->exited, __ATOMIC_ACQUIRE) != 0u; }
 
+// Why the resident executor ended, for messages.
+std::string resident_exit_reason(const hcclComm* c) {
+    const uint32_t why = __atomic_load_n(&c->rq->exited, __ATOMIC_ACQUIRE);
+    return why == RESIDENT_EXIT_IDLE         ? "no packet arrived within the idle limit"
+           : why == RESIDENT_EXIT_WORKGROUPS ? "its workgroups did not all finish a packet within the watchdog"
+           : why == RESIDENT_EXIT_STOP       ? "a stop request"
+                                             : "exit code " + std::to_string(why);
+}
+
 // Waits until packet `seq` has completed; fails if the executor stopped or `ms` passed first.
 hcclResult_t resident_wait_for(hcclComm* c, uint64_t seq, uint64_t ms) {
     if (resident_done(c) >= seq) return hcclSuccess;
@@ -426,8 +435,9 @@ hcclResult_t resident_wait_for(hcclComm* c, uint64_t seq, uint64_t ms) {
     for (uint32_t spin = 0;; ++spin) {
         if (resident_done(c) >= seq) return hcclSuccess;
         if (resident_exited(c) && resident_done(c) < seq)
-            return fail(hcclTimeout, "the resident executor stopped before the packet completed (idle limit "
-                                     "reached, or a workgroup gave up waiting for the others)");
+            return fail(hcclTimeout, "the resident executor stopped before packet " + std::to_string(seq) +
+                                         " completed (" + resident_exit_reason(c) + "; packets completed: " +
+                                         std::to_string(resident_done(c)) + ")");
         if ((spin & 1023u) == 1023u) {
             const double el = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
             if (el > (double)ms) return fail(hcclTimeout, "the resident executor did not complete the packet in time");
@@ -440,7 +450,8 @@ hcclResult_t resident_wait_for(hcclComm* c, uint64_t seq, uint64_t ms) {
 hcclResult_t resident_submit(hcclComm* c, const LaunchArgs& a, DeviceProgram* dp) {
     const uint64_t k = c->resident_seq + 1;
     const uint64_t ms = c->cfg.timeout_ms ? c->cfg.timeout_ms : 2000u;
-    if (resident_exited(c)) return fail(hcclTimeout, "the resident executor has stopped: restart it");
+    if (resident_exited(c))
+        return fail(hcclTimeout, "the resident executor has stopped (" + resident_exit_reason(c) + "): restart it");
     // the slot last held packet k - kResidentSlots, whose arguments every workgroup has read
     // once it has completed
     if (k > kResidentSlots) {
@@ -460,11 +471,13 @@ hcclResult_t resident_submit(hcclComm* c, const LaunchArgs& a, DeviceProgram* dp
 // copy kernel only if every user buffer is 16-byte aligned), sized to the resident capacity of
 // the CUs the stream may use, capped by the configuration and by the program's tiles.
 // Sets a.nworkers and `blocks`; returns the kernel kind.
-int launch_shape(hcclComm* c, const HostProgram& prog, LaunchArgs& a, uint32_t nuser, hipStream_t s,
+int launch_shape(hcclComm* c, const HostProgram& prog, uint32_t phase, LaunchArgs& a, uint32_t nuser, hipStream_t s,
                  uint32_t& blocks) {
     const uint32_t wpb = (uint32_t)executor_waves_per_block();
     uint32_t cus = stream_cu_count(c, s);
-    int kind = prog.kind;
+    int kind = prog.phase_kind.empty() ? prog.kind : prog.phase_kind[phase];
+    a.tile_begin = prog.phase_tile.empty() ? 0u : prog.phase_tile[phase];
+    a.tile_end = prog.phase_tile.empty() ? prog.ntiles : prog.phase_tile[phase + 1];
     if (a.trace) kind = kKindGeneric;  // the kernel that records the trace
     if (kind == kKindCopyAligned) {
         for (uint32_t i = 0; i < nuser; ++i)
@@ -472,7 +485,7 @@ int launch_shape(hcclComm* c, const HostProgram& prog, LaunchArgs& a, uint32_t n
     }
     uint32_t slots = cus * (uint32_t)std::max(1, c->blocks_per_cu[kind]) * wpb;
     if (c->cfg.max_workers > 0) slots = std::min<uint32_t>(slots, (uint32_t)c->cfg.max_workers);
-    uint32_t workers = std::min<uint32_t>(slots, prog.ntiles);
+    uint32_t workers = std::min<uint32_t>(slots, a.tile_end - a.tile_begin);
     blocks = (workers + wpb - 1) / wpb;
     if (blocks == 0) blocks = 1;
     a.nworkers = blocks * wpb;
@@ -563,6 +576,7 @@ void describe(hcclProgramInfo_t& info, const std::vector<CollectiveSpec>& specs,
     info.compile_us = compile_us;
     info.step_tile_min = prog.step_tile_min;
     info.step_tile_max = prog.step_tile_max;
+    info.num_phases = prog.nphase();
 }
 
 // Compiles and enqueues one work packet (a list of collective calls on one stream).
@@ -666,14 +680,23 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
     const bool signals = triggered && trig.done_addr != nullptr;
     if (traced) a.trace = c->d_trace;
 
-    if (c->resident) return resident_submit(c, a, dp);
+    const uint32_t nph = dp->prog.nphase();
+    if (c->resident) {
+        // one packet per phase: the executor finishes a packet everywhere before the next starts
+        for (uint32_t q = 0; q < nph; ++q) {
+            a.tile_begin = dp->prog.phase_tile[q];
+            a.tile_end = dp->prog.phase_tile[q + 1];
+            if ((r = resident_submit(c, a, dp)) != hcclSuccess) return r;
+        }
+        return hcclSuccess;
+    }
 
     uint32_t blocks = 0;
-    const int kind = launch_shape(c, dp->prog, a, nuser, s, blocks);
+    int kind = launch_shape(c, dp->prog, 0, a, nuser, s, blocks);
     info.workers = a.nworkers;
     info.tickets = a.dynamic;
 
-    if (inline_eligible(c, dp->prog, triggered)) {
+    if (nph == 1 && inline_eligible(c, dp->prog, triggered)) {
         info.inline_launch = 1;
         hipError_t e = launch_inline_step(dp->prog, a, blocks, kind, s);
         if (e != hipSuccess) return hip_fail(e, "inline executor launch");
@@ -701,10 +724,20 @@ hcclResult_t run_packet(hcclComm* c, const std::vector<Call>& calls) {
         hipError_t e = hipStreamWaitEvent(s, c->scratch_done, 0);
         if (e != hipSuccess) return hip_fail(e, "cross-stream ordering");
     }
-    hipError_t e = launch_executor(a, blocks, kind, s);
-    if (e != hipSuccess) return hip_fail(e, "executor launch");
-    hlog(c, 3, "launched kernel kind %d: %u workgroups, %u wavefronts, %s dispatch%s", kind, blocks, a.nworkers,
-         a.dynamic ? "ticket" : "static", a.trace ? ", traced" : "");
+    hipError_t e = hipSuccess;
+    for (uint32_t q = 0; q < nph; ++q) {
+        if (q > 0) {
+            // later phases follow the first on the stream: only the first waits for a trigger
+            a.wait_addr = nullptr;
+            kind = launch_shape(c, dp->prog, q, a, nuser, s, blocks);
+            info.workers = std::max(info.workers, a.nworkers);
+        }
+        e = launch_executor(a, blocks, kind, s);
+        if (e != hipSuccess) return hip_fail(e, "executor launch");
+        hlog(c, 3, "launched phase %u of %u, kernel kind %d: %u workgroups, %u wavefronts, tiles %u..%u, %s dispatch%s",
+             q + 1, nph, kind, blocks, a.nworkers, a.tile_begin, a.tile_end, a.dynamic ? "ticket" : "static",
+             a.trace ? ", traced" : "");
+    }
     if (signals) {
         e = launch_signal(trig.done_addr, trig.done_value, c->d_error, s);
         if (e != hipSuccess) return hip_fail(e, "completion word");
@@ -754,10 +787,12 @@ hcclResult_t fill_spec(hcclComm* c, CollectiveSpec& s, int coll, hcclDataType_t 
     s.tile_bytes = c->cfg.tile_bytes;
     s.order = c->cfg.order;
     s.requant = c->cfg.requantize != 0;
+    s.phases = c->cfg.phases;
     if (c->env_algo >= 0) s.algo = c->env_algo;
     if (c->env_chunk) s.chunk_bytes = c->env_chunk;
     if (s.algo < hcclAlgoAuto || s.algo > hcclAlgoRhd) return fail(hcclInvalidArgument, "unknown algorithm");
     if (s.order < hcclOrderAscending || s.order > hcclOrderHalving) return fail(hcclInvalidArgument, "unknown order");
+    if (s.phases < hcclPhasesAuto || s.phases > hcclPhasesLevels) return fail(hcclInvalidArgument, "unknown phase mode");
     return hcclSuccess;
 }
 
@@ -819,7 +854,10 @@ hcclResult_t hccl_comm_create(int nranks, int device, const hcclConfig_t* cfg, h
         if (e != hipSuccess) return hip_fail(e, "setup stream");
         e = hipMalloc(&c->d_error, sizeof(ErrorRecord));
         if (e != hipSuccess) return fail(hcclOutOfMemory, "error record allocation failed");
-        e = hipMemset(c->d_error, 0, sizeof(ErrorRecord));
+        // cleared on the communicator's own stream and waited for: launches go to the caller's
+        // streams, which need not be ordered after the null stream
+        e = launch_fill_u32((uint32_t*)c->d_error, sizeof(ErrorRecord) / sizeof(uint32_t), 0u, c->setup_stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(c->setup_stream);
         if (e != hipSuccess) return hip_fail(e, "error record init");
         // the device address of the static workspace, looked up once per device (allocation-free calls)
         void* ws = nullptr;
@@ -991,11 +1029,11 @@ hcclResult_t hccl_allreduce_noalloc(hcclComm_t comm, const void* const* sendbufs
     const uint64_t ms = comm->cfg.timeout_ms ? comm->cfg.timeout_ms : 2000u;
     a.timeout_ticks = ms * comm->wall_clock_khz;
     uint32_t blocks = 0;
-    const int kind = launch_shape(comm, *hp, a, 2u * (uint32_t)P, st, blocks);
+    int kind = launch_shape(comm, *hp, 0, a, 2u * (uint32_t)P, st, blocks);
     comm->last.workers = a.nworkers;
     comm->last.tickets = a.dynamic;
     hipError_t e;
-    if (inline_eligible(comm, *hp, false)) {
+    if (hp->nphase() == 1 && inline_eligible(comm, *hp, false)) {
         comm->last.inline_launch = 1;
         e = launch_inline_step(*hp, a, blocks, kind, st);
         if (e != hipSuccess) return hip_fail(e, "inline executor launch");
@@ -1007,8 +1045,14 @@ hcclResult_t hccl_allreduce_noalloc(hcclComm_t comm, const void* const* sendbufs
     if (e != hipSuccess) return hip_fail(e, "program copy into the static workspace");
     e = launch_fill_u32(a.state, hp->nstate, 0u, st);
     if (e != hipSuccess) return hip_fail(e, "counter clear in the static workspace");
-    e = launch_executor(a, blocks, kind, st);
-    if (e != hipSuccess) return hip_fail(e, "executor launch");
+    for (uint32_t q = 0; q < hp->nphase(); ++q) {
+        if (q > 0) {
+            kind = launch_shape(comm, *hp, q, a, 2u * (uint32_t)P, st, blocks);
+            comm->last.workers = std::max(comm->last.workers, a.nworkers);
+        }
+        e = launch_executor(a, blocks, kind, st);
+        if (e != hipSuccess) return hip_fail(e, "executor launch");
+    }
     return hcclSuccess;
 }
 
@@ -1260,9 +1304,11 @@ hcclResult_t hccl_get_async_error(hcclComm_t comm) {
     e = hipMemcpy(&rec, comm->d_error, sizeof rec, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "read error record");
     if (rec.code == 0) return hcclSuccess;
-    ErrorRecord cleared;
-    std::memset(&cleared, 0, sizeof cleared);
-    (void)hipMemcpy(comm->d_error, &cleared, sizeof cleared, hipMemcpyHostToDevice);
+    // cleared before anything else can be enqueued (the caller's streams need not follow the
+    // null stream)
+    e = launch_fill_u32((uint32_t*)comm->d_error, sizeof(ErrorRecord) / sizeof(uint32_t), 0u, comm->setup_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(comm->setup_stream);
+    if (e != hipSuccess) return hip_fail(e, "clear error record");
     return device_error(rec.code, rec.desc, rec.tile);
 }
 
@@ -1293,8 +1339,10 @@ hcclResult_t hccl_resident_start(hcclComm_t comm, uint32_t blocks, uint32_t idle
     // control words, then two device mirrors of packet arguments (one is filled ahead)
     const size_t ctl_bytes = 64 + 2 * sizeof(LaunchArgs);
     if (e == hipSuccess) e = hipMalloc(&ctl, ctl_bytes);
-    if (e == hipSuccess) e = hipMemset(ctl, 0, ctl_bytes);
     if (e == hipSuccess) e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
+    // cleared on the executor's own stream: a non-blocking stream is not ordered after work on
+    // the null stream, so a clear issued there could land after the executor has started
+    if (e == hipSuccess) e = launch_fill_u32(ctl, ctl_bytes / sizeof(uint32_t), 0u, st);
     ResidentArgs r;
     std::memset(&r, 0, sizeof r);
     r.q = (ResidentQueue*)qdev;

@@ -33,6 +33,12 @@ constexpr uint64_t kMinReduceTileElems = 1024;
 constexpr uint32_t kDefaultDependentTileBytes = 128u * 1024u;
 constexpr uint32_t kMinDependentTileBytes = 32u * 1024u;
 constexpr uint64_t kDependentMinTiles = 1024;
+// A copy to this many destinations or more reads up to 32 KiB per tile, as long as its phase
+// keeps about 1024 tiles (an all-gather of P = 64 x 512 KiB bf16 blocks: 8 KiB tiles 520 us,
+// 16 KiB 407 us, 32 KiB 367-380 us, 64 KiB 387 us, 128 KiB (256 tiles) 720 us).
+constexpr size_t kWideCopyDsts = 8;
+constexpr uint64_t kWideCopyTileBytes = 32u * 1024u;
+constexpr uint64_t kWideCopyTargetTiles = 1024;
 // Small collectives are latency bound: cut them into at least this many tiles (down to
 // one vector per lane) so that many wavefronts share the work.
 constexpr uint64_t kSmallTargetTiles = 2048;
@@ -383,11 +389,14 @@ void lower_rhd(const CollectiveSpec& s, HostProgram& p) {
 }
 
 // ------------------------------------------------------------------------- TWO_LEVEL
-// P = G groups x L consecutive ranks. Shard k of the vector is owned by local rank k of
-// every group. Phase 1 (inside each group): the L contributors of shard k are folded into
-// an FP32 partial per group. Phase 2 (across groups): the G partials of shard k are folded
-// in ascending group order, rounded, and written to local rank k of every group. Phase 3
-// (inside each group): local rank k forwards shard k to the other L-1 ranks of its group.
+// P = G groups x L consecutive ranks. Shard k of the vector belongs to local rank k of every
+// group and is cut into G sub-shards; sub-shard (k, g) is owned by local rank k of group g.
+// Phase 1 (inside each group, reduce-scatter): the L contributors of every element are folded
+// into an FP32 partial per group. Phase 2 (across groups, the all-reduce of shard k among the
+// local-k ranks as reduce-scatter + all-gather): the G partials of sub-shard (k, g) are folded
+// in ascending group order, rounded, and written to its owner; the owner forwards it to local
+// rank k of the other groups. Phase 3 (inside each group, all-gather): local rank k forwards
+// shard k to the other L-1 ranks of its group.
 void lower_two_level(const CollectiveSpec& s, HostProgram& p) {
     Builder b{p};
     const int P = s.P, L = s.group_size, G = P / L;
@@ -395,43 +404,57 @@ void lower_two_level(const CollectiveSpec& s, HostProgram& p) {
     const uint32_t dt = (uint32_t)s.dtype;
     const uint32_t acc = acc_dtype(s);
     const uint64_t q = shard_size(N, L);
-    struct Piece { int k; uint64_t o, n; };
+    struct Piece { int k, g; uint64_t o, n; };
     std::vector<Piece> pieces;
     for (int k = 0; k < L; ++k) {
-        uint64_t lo = std::min(N, (uint64_t)k * q), hi = std::min(N, lo + q);
-        for_chunks(lo, hi, C, [&](uint32_t, uint64_t o, uint64_t n) { pieces.push_back({k, o, n}); });
+        const uint64_t lo = std::min(N, (uint64_t)k * q), hi = std::min(N, lo + q);
+        const uint64_t qs = shard_size(hi - lo, G);
+        for (int g = 0; g < G; ++g) {
+            const uint64_t slo = std::min(hi, lo + (uint64_t)g * qs), shi = std::min(hi, slo + qs);
+            for_chunks(slo, shi, C, [&](uint32_t, uint64_t o, uint64_t n) { pieces.push_back({k, g, o, n}); });
+        }
     }
+    auto rank = [&](int g, int m) { return g * L + m; };
     std::vector<std::vector<uint32_t>> rs(pieces.size(), std::vector<uint32_t>(G));
-    for (int g = 0; g < G; ++g) {
+    for (int h = 0; h < G; ++h) {
         for (size_t i = 0; i < pieces.size(); ++i) {
             const Piece& pc = pieces[i];
             std::vector<Operand> src;
-            for (int m = 0; m < L; ++m) src.push_back(opnd(send_buf(g * L + m), dt, pc.o));
-            rs[i][g] = b.add(OP_REDUCE, (uint8_t)s.redop, pc.n, src,
-                             {opnd(scratch_buf(P), acc, (uint64_t)g * N + pc.o)});
+            for (int m = 0; m < L; ++m) src.push_back(opnd(send_buf(rank(h, m)), dt, pc.o));
+            rs[i][h] = b.add(OP_REDUCE, (uint8_t)s.redop, pc.n, src,
+                             {opnd(scratch_buf(P), acc, (uint64_t)h * N + pc.o)});
         }
     }
-    std::vector<uint32_t> inter(pieces.size());
+    std::vector<uint32_t> inter(pieces.size()), fwd(pieces.size());
     for (size_t i = 0; i < pieces.size(); ++i) {
         const Piece& pc = pieces[i];
-        std::vector<Operand> src, dst;
+        std::vector<Operand> src;
         std::vector<Dep> deps;
-        for (int g = 0; g < G; ++g) {
-            src.push_back(opnd(scratch_buf(P), acc, (uint64_t)g * N + pc.o));
-            deps.push_back(tile_dep(rs[i][g]));
+        for (int h = 0; h < G; ++h) {
+            src.push_back(opnd(scratch_buf(P), acc, (uint64_t)h * N + pc.o));
+            deps.push_back(tile_dep(rs[i][h]));
         }
-        for (int g = 0; g < G; ++g) dst.push_back(opnd(recv_buf(P, g * L + pc.k), dt, pc.o));
-        inter[i] = b.add(OP_REDUCE, (uint8_t)s.redop, pc.n, src, dst, deps);
+        inter[i] = b.add(OP_REDUCE, (uint8_t)s.redop, pc.n, src, {opnd(recv_buf(P, rank(pc.g, pc.k)), dt, pc.o)}, deps);
+    }
+    for (size_t i = 0; i < pieces.size(); ++i) {
+        const Piece& pc = pieces[i];
+        fwd[i] = inter[i];
+        if (G == 1) continue;
+        std::vector<Operand> dst;
+        for (int h = 0; h < G; ++h)
+            if (h != pc.g) dst.push_back(opnd(recv_buf(P, rank(h, pc.k)), dt, pc.o));
+        fwd[i] = b.add(OP_COPY, RO_SUM, pc.n, {opnd(recv_buf(P, rank(pc.g, pc.k)), dt, pc.o)}, dst,
+                       {tile_dep(inter[i])});
     }
     if (L > 1) {
-        for (int g = 0; g < G; ++g) {
+        for (int h = 0; h < G; ++h) {
             for (size_t i = 0; i < pieces.size(); ++i) {
                 const Piece& pc = pieces[i];
                 std::vector<Operand> dst;
                 for (int m = 0; m < L; ++m)
-                    if (m != pc.k) dst.push_back(opnd(recv_buf(P, g * L + m), dt, pc.o));
-                b.add(OP_COPY, RO_SUM, pc.n, {opnd(recv_buf(P, g * L + pc.k), dt, pc.o)}, dst,
-                      {tile_dep(inter[i])});
+                    if (m != pc.k) dst.push_back(opnd(recv_buf(P, rank(h, m)), dt, pc.o));
+                b.add(OP_COPY, RO_SUM, pc.n, {opnd(recv_buf(P, rank(h, pc.k)), dt, pc.o)}, dst,
+                      {tile_dep(h == pc.g ? inter[i] : fwd[i])});
             }
         }
     }
@@ -534,7 +557,7 @@ bool CollectiveSpec::operator==(const CollectiveSpec& o) const {
            sendcounts == o.sendcounts && sdispls == o.sdispls && recvcounts == o.recvcounts &&
            rdispls == o.rdispls && in_place == o.in_place && algo == o.algo && group_size == o.group_size &&
            chunk_bytes == o.chunk_bytes && fuse == o.fuse && tile_bytes == o.tile_bytes && order == o.order &&
-           requant == o.requant && row_elems == o.row_elems && send_cap == o.send_cap && recv_cap == o.recv_cap &&
+           requant == o.requant && phases == o.phases && row_elems == o.row_elems && send_cap == o.send_cap && recv_cap == o.recv_cap &&
            dyn_sdispls == o.dyn_sdispls && dyn_rdispls == o.dyn_rdispls && dyn_recvcounts == o.dyn_recvcounts;
 }
 
@@ -593,6 +616,7 @@ BufferSizes buffer_sizes(const CollectiveSpec& s, uint64_t scratch_bytes) {
 bool lower(const CollectiveSpec& s, HostProgram& p, std::string& err) {
     p = HostProgram();
     p.P = s.P;
+    p.phase_mode = s.phases;
     if (s.coll == COLL_ALLTOALLV) {
         lower_alltoallv(s, p);
         return true;
@@ -666,7 +690,13 @@ bool lower(const CollectiveSpec& s, HostProgram& p, std::string& err) {
 //   flat REDUCE D_g of L sources that only E reads  ->  E = REDUCE(all D_g sources,
 //   group = L): fold each run of L into a partial, then fold the partials, as before.
 // Rule 3 (forwarding): F = COPY(x -> y...) where x is the value a step E wrote (same
-//   location and element count) and F waits for E  ->  E also writes y... .
+//   location and element count) and F waits for E  ->  E also writes y... . Except when E is a
+//   wide reduction (kSplitMinSources or more sources) and the program splits them (by its phase
+//   mode and size): then F stays a step of its own, a later phase that copies E's result once
+//   it is complete, and a second such copy of the same value joins the first (F also writes
+//   its destinations). Measured on the two-level all-reduce P = 64 x 32 MiB bf16: one step of
+//   64 sources and 64 destinations 860 us; 64 sources to one destination, then one source to 63
+//   destinations in a second launch, about 770 us.
 // Rule 4 (trees): E = REDUCE(a, b) where a and b are the private partials of two binary-tree
 //   reductions over equally many sources  ->  E = binary tree over both source lists. This
 //   is what a recursive-halving level does; the tree, and so every operation, is unchanged.
@@ -680,6 +710,16 @@ void fuse(HostProgram& p) {
     const uint32_t D = (uint32_t)p.descs.size();
     std::vector<uint32_t> fwd(D);
     for (uint32_t i = 0; i < D; ++i) fwd[i] = i;
+    // whether the forwarding copies of wide reductions stay separate steps (by the bytes the
+    // reductions read from the send buffers)
+    uint64_t reduce_bytes = 0;
+    for (const auto& d : p.descs)
+        if (d.op == OP_REDUCE)
+            for (const Operand& o : d.srcs)
+                if (o.buf < (uint32_t)p.P) reduce_bytes += d.nelem * dtype_size(o.dtype);
+    const bool split = p.phase_mode == PHASE_LEVELS || (p.phase_mode == PHASE_AUTO && reduce_bytes >= kSplitMinBytes);
+    // split copies, by the value they read: a second copy of that value joins the first
+    std::unordered_map<OperandKey, uint32_t, OperandKeyHash> split_copy;
     auto find = [&](uint32_t x) {
         while (fwd[x] != x) {
             fwd[x] = fwd[fwd[x]];
@@ -812,8 +852,32 @@ void fuse(HostProgram& p) {
         if (B.op == OP_COPY && B.srcs.size() == 1 && prod[i][0] >= 0) {
             // Rule 3: a forwarding copy of a value becomes more destinations of its producer.
             uint32_t e = find((uint32_t)prod[i][0]);
-            HostDesc& E = p.descs[e];
-            if (!E.alive || E.nelem != B.nelem || !depends_on(B, e)) continue;
+            HostDesc& E0 = p.descs[e];
+            if (!E0.alive || E0.nelem != B.nelem || !depends_on(B, e)) continue;
+            if (split && E0.op == OP_REDUCE && E0.srcs.size() >= kSplitMinSources) {
+                // the copy of a wide reduction's result stays a step; an earlier copy of the
+                // same value that waits only for that reduction takes its destinations
+                bool only_e = true;
+                for (const Dep& d : B.deps) only_e &= find(d.desc) == e;
+                const OperandKey key{B.srcs[0].buf, B.srcs[0].offset};
+                auto it = split_copy.find(key);
+                if (only_e && it != split_copy.end()) {
+                    HostDesc& S = p.descs[it->second];
+                    bool s_only_e = true;
+                    for (const Dep& d : S.deps) s_only_e &= find(d.desc) == e;
+                    if (S.alive && S.nelem == B.nelem && S.srcs[0].dtype == B.srcs[0].dtype && s_only_e &&
+                        S.dsts.size() + B.dsts.size() <= (size_t)kMaxOperands) {
+                        S.dsts.insert(S.dsts.end(), B.dsts.begin(), B.dsts.end());
+                        nread[it->second].resize(S.dsts.size(), 0);
+                        B.alive = false;
+                        fwd[i] = it->second;
+                        continue;
+                    }
+                }
+                if (only_e) split_copy[key] = i;
+                continue;
+            }
+            HostDesc& E = E0;
             if (E.dsts.size() + B.dsts.size() > (size_t)kMaxOperands) continue;
             bool deps_ok = true;
             for (const Dep& d : B.deps) {
@@ -930,6 +994,7 @@ bool merge(std::vector<HostProgram>& parts, const std::vector<CollectiveSpec>& s
         }
     }
     out.nmeta = nmeta;
+    out.phase_mode = specs[0].phases;
     out.algo = parts[order[0]].algo;
     out.fused = fused;
     out.scratch_bytes = scratch;
@@ -958,18 +1023,56 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     }
     p.descs = std::move(live);
 
+    // Phases. A step's level is 0 without dependencies, else one more than the highest level it
+    // waits for. Run level by level, one launch each, every dependency is met by the launch
+    // order: the steps are laid out level by level (program order inside a level) and carry no
+    // dependencies on the device. Otherwise the whole program is one launch and its
+    // dependencies are waited for tile by tile.
+    {
+        const uint32_t n = (uint32_t)p.descs.size();
+        std::vector<uint32_t> level(n, 0);
+        uint32_t nlev = 1;
+        bool deps_here = false;
+        for (uint32_t i = 0; i < n; ++i) {
+            for (const Dep& d : p.descs[i].deps) level[i] = std::max(level[i], level[d.desc] + 1);
+            deps_here |= !p.descs[i].deps.empty();
+            nlev = std::max(nlev, level[i] + 1);
+        }
+        const bool by_level = deps_here && nlev <= kMaxPhases &&
+                              (p.phase_mode == PHASE_LEVELS || (p.phase_mode == PHASE_AUTO && nlev <= kAutoMaxPhases));
+        p.desc_phase.assign(n, 0);
+        if (by_level) {
+            std::vector<uint32_t> order(n);
+            for (uint32_t i = 0; i < n; ++i) order[i] = i;
+            std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return level[a] < level[b]; });
+            std::vector<HostDesc> sorted;
+            sorted.reserve(n);
+            for (uint32_t k = 0; k < n; ++k) {
+                sorted.push_back(std::move(p.descs[order[k]]));
+                sorted.back().deps.clear();  // met by the launch order
+                p.desc_phase[k] = level[order[k]];
+            }
+            p.descs = std::move(sorted);
+        }
+    }
+    const uint32_t nphase = p.descs.empty() ? 1u : p.desc_phase.back() + 1;
+
     // One tile size for a program with dependencies, so per-tile dependencies line up; without
     // them every step gets the tile size for its own element width (the bf16 rows of a group
     // with int32 ids keep 8 KiB tiles instead of taking the ids' element count).
     uint64_t max_bpe = 1, total_elems = 0;
+    std::vector<uint64_t> phase_elems(nphase, 0), phase_wide_copy_bytes(nphase, 0);
     bool any_reduce = false, any_deps = false;
-    for (const auto& d : p.descs) {
+    for (size_t i = 0; i < p.descs.size(); ++i) {
+        const auto& d = p.descs[i];
         uint64_t bpe = 0;
         for (const Operand& o : d.srcs) bpe += dtype_size(o.dtype);
         max_bpe = std::max(max_bpe, bpe);
         any_reduce |= d.op == OP_REDUCE;
         any_deps |= !d.deps.empty();
         total_elems += d.nelem;
+        phase_elems[p.desc_phase[i]] += d.nelem;
+        if (d.op == OP_COPY && d.dsts.size() >= kWideCopyDsts) phase_wide_copy_bytes[p.desc_phase[i]] += d.nelem * bpe;
     }
     uint64_t tb = tile_bytes;
     if (!tb) tb = any_deps ? kDefaultDependentTileBytes : any_reduce ? kDefaultReduceTileBytes : kDefaultCopyTileBytes;
@@ -990,14 +1093,20 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     te = std::max<uint64_t>(te, kWaveStepElems);
     te = std::min<uint64_t>(te, 1ull << 30);
     p.tile_elems = (uint32_t)te;
-    auto step_tile = [&](const HostDesc& h) -> uint64_t {
+    auto step_tile = [&](const HostDesc& h, uint32_t phase) -> uint64_t {
         if (any_deps || tile_bytes) return te;
         uint64_t bpe = 0;
         for (const Operand& o : h.srcs) bpe += dtype_size(o.dtype);
         if (bpe == 0) return te;
-        uint64_t t = (tb / bpe) / kWaveStepElems * kWaveStepElems;
-        if (any_reduce) t = std::max<uint64_t>(t, kMinReduceTileElems);
-        t = std::min<uint64_t>(t, total_elems / kSmallTargetTiles / kWaveStepElems * kWaveStepElems);
+        // a copy to many destinations writes its tile to each of them: longer runs per
+        // destination, and enough work per tile without cutting it for parallelism
+        const bool wide_copy = h.op == OP_COPY && h.dsts.size() >= kWideCopyDsts;
+        const uint64_t wide_tb = std::max<uint64_t>(
+            kDefaultCopyTileBytes, std::min<uint64_t>(kWideCopyTileBytes, phase_wide_copy_bytes[phase] / kWideCopyTargetTiles));
+        uint64_t t = ((wide_copy ? wide_tb : tb) / bpe) / kWaveStepElems * kWaveStepElems;
+        if (any_reduce && !wide_copy) t = std::max<uint64_t>(t, kMinReduceTileElems);
+        if (!wide_copy)
+            t = std::min<uint64_t>(t, phase_elems[phase] / kSmallTargetTiles / kWaveStepElems * kWaveStepElems);
         return std::min<uint64_t>(std::max<uint64_t>(t, kWaveStepElems), 1ull << 30);
     };
 
@@ -1023,7 +1132,7 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
         d.nelem = h.nelem;
         d.fold = h.fold;
         d.requant = h.requant ? 1u : 0u;
-        const uint64_t dte = step_tile(h);
+        const uint64_t dte = step_tile(h, p.desc_phase[i]);
         d.tile_elems = (uint32_t)dte;
         if (h.op == OP_COPY || h.op == OP_REDUCE) {
             p.step_tile_min = p.step_tile_min ? std::min<uint32_t>(p.step_tile_min, (uint32_t)dte) : (uint32_t)dte;
@@ -1086,25 +1195,37 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     p.ndeps = (uint32_t)deps.size();
     p.noperands = (uint32_t)ops.size();
 
-    // the leanest executor kernel that covers every step
-    int kind = kKindCopyOnly;
-    bool dynamic = false;
-    for (uint32_t i = 0; i < nd; ++i) dynamic |= out[i].op == OP_DYN_COPY;
-    for (uint32_t i = 0; i < nd; ++i) {
-        if (out[i].op != OP_REDUCE) continue;
-        const bool plain = out[i].sig <= SIG_INT32 && out[i].redop == RO_SUM && out[i].fold == FOLD_LIST &&
-                           !out[i].requant;
-        if (!plain) { kind = kKindGeneric; break; }
-        if (kind == kKindCopyOnly) kind = out[i].sig;
-        else if (kind != out[i].sig) { kind = kKindGeneric; break; }
+    // the leanest executor kernel that covers every step of [d0, d1)
+    auto kernel_for = [&](uint32_t d0, uint32_t d1) {
+        int kind = kKindCopyOnly;
+        bool dynamic = false;
+        for (uint32_t i = d0; i < d1; ++i) dynamic |= out[i].op == OP_DYN_COPY;
+        for (uint32_t i = d0; i < d1; ++i) {
+            if (out[i].op != OP_REDUCE) continue;
+            const bool plain = out[i].sig <= SIG_INT32 && out[i].redop == RO_SUM && out[i].fold == FOLD_LIST &&
+                               !out[i].requant;
+            if (!plain) { kind = kKindGeneric; break; }
+            if (kind == kKindCopyOnly) kind = out[i].sig;
+            else if (kind != out[i].sig) { kind = kKindGeneric; break; }
+        }
+        if (dynamic) kind = (kind == kKindCopyOnly) ? kKindDynamic : kKindGeneric;  // the two that run them
+        if (kind == kKindCopyOnly) {
+            bool aligned = true;
+            for (uint32_t i = d0; i < d1; ++i)
+                for (uint32_t k = 0; k < (uint32_t)out[i].nsrc + out[i].ndst; ++k) aligned &= (ops[out[i].src + k].offset % 16) == 0;
+            if (aligned) kind = kKindCopyAligned;  // the launch falls back if a buffer is not aligned
+        }
+        return kind;
+    };
+    p.kind = kernel_for(0, nd);
+    p.phase_tile.assign(1, 0);
+    p.phase_kind.clear();
+    for (uint32_t q = 0, i = 0; q < nphase; ++q) {
+        const uint32_t d0 = i;
+        while (i < nd && p.desc_phase[i] == q) ++i;
+        p.phase_kind.push_back(kernel_for(d0, i));
+        p.phase_tile.push_back(i < nd ? out[i].tile0 : p.ntiles);
     }
-    if (dynamic) kind = (kind == kKindCopyOnly) ? kKindDynamic : kKindGeneric;  // the two that run them
-    if (kind == kKindCopyOnly) {
-        bool aligned = true;
-        for (const Operand& o : ops) aligned &= (o.offset % 16) == 0;
-        if (aligned) kind = kKindCopyAligned;  // the launch falls back if a buffer is not aligned
-    }
-    p.kind = kind;
 
     auto align16 = [](uint64_t x) { return (x + 15) & ~uint64_t(15); };
     ProgramHeader hdr;
@@ -1123,7 +1244,9 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     hdr.off_tile_desc = align16(hdr.off_dep + deps.size() * sizeof(Dep));
     hdr.off_aux = align16(hdr.off_tile_desc + tile_owner.size() * sizeof(uint32_t));
     hdr.naux = (uint32_t)p.aux.size();
-    hdr.total_bytes = align16(hdr.off_aux + p.aux.size() * sizeof(DynA2A));
+    hdr.nphase = nphase;
+    hdr.off_phase = align16(hdr.off_aux + p.aux.size() * sizeof(DynA2A));
+    hdr.total_bytes = align16(hdr.off_phase + p.phase_tile.size() * sizeof(uint32_t));
     hdr.scratch_bytes = p.scratch_bytes;
     p.image.assign(hdr.total_bytes, 0);
     std::memcpy(p.image.data(), &hdr, sizeof hdr);
@@ -1133,6 +1256,7 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     if (!tile_owner.empty())
         std::memcpy(p.image.data() + hdr.off_tile_desc, tile_owner.data(), tile_owner.size() * sizeof(uint32_t));
     if (!p.aux.empty()) std::memcpy(p.image.data() + hdr.off_aux, p.aux.data(), p.aux.size() * sizeof(DynA2A));
+    std::memcpy(p.image.data() + hdr.off_phase, p.phase_tile.data(), p.phase_tile.size() * sizeof(uint32_t));
     return true;
 }
 

@@ -26,6 +26,20 @@ enum Collective : int {
 };
 enum Algo : int { ALGO_AUTO = 0, ALGO_DIRECT = 1, ALGO_RING = 2, ALGO_TWO_LEVEL = 3, ALGO_RHD = 4 };
 enum Order : int { ORDER_ASCENDING = 0, ORDER_RING = 1, ORDER_HALVING = 2 };
+// How the steps of a program are spread over launches (phases).
+//   PHASE_AUTO: one launch per dependency level when the program has dependencies and at most
+//     kAutoMaxPhases levels, else one launch; the forwarding copies of wide, large reductions
+//     stay separate steps (a second phase) instead of becoming extra destinations.
+//   PHASE_ONE: one launch; dependencies are waited for on the device, tile by tile.
+//   PHASE_LEVELS: one launch per dependency level, and the forwarding copies of every
+//     reduction of kSplitMinSources or more sources stay separate steps.
+enum PhaseMode : int { PHASE_AUTO = 0, PHASE_ONE = 1, PHASE_LEVELS = 2 };
+constexpr uint32_t kAutoMaxPhases = 32;
+constexpr uint32_t kSplitMinSources = 16;
+// bytes the wide reductions read from the send buffers, from which PHASE_AUTO splits (the
+// two-level all-reduce of 64 ranks, one launch against two: 2 MiB per rank 44-48 / 67 us,
+// 4 MiB 98-101 / 90 us, 8 MiB 224 / 203 us, 32 MiB 875-881 / 781-784 us)
+constexpr uint64_t kSplitMinBytes = 256ull << 20;
 
 struct CollectiveSpec {
     int coll = COLL_ALLREDUCE;
@@ -42,6 +56,7 @@ struct CollectiveSpec {
     uint32_t tile_bytes = 0;
     int order = ORDER_ASCENDING;
     bool requant = false;        // round every partial to the buffer type
+    int phases = PHASE_AUTO;     // PhaseMode
     // alltoallv_dynamic: rows of row_elems elements; buffers hold send_cap / recv_cap rows;
     // which optional metadata arrays the call passes
     uint64_t row_elems = 0, send_cap = 0, recv_cap = 0;
@@ -68,6 +83,7 @@ struct HostProgram {
     int P = 0;
     int algo = ALGO_DIRECT;      // schedule actually lowered
     bool fused = false;
+    int phase_mode = PHASE_AUTO; // PhaseMode: read by fuse() and finalize()
     uint64_t scratch_bytes = 0;
     std::vector<HostDesc> descs;
     std::vector<DynA2A> aux;     // records of the dynamic steps
@@ -86,7 +102,13 @@ struct HostProgram {
     std::vector<uint8_t> image;  // ProgramHeader + arrays, uploaded to the device as is
     uint32_t nstate = 0;
     uint32_t flags = 0;
-    int kind = kKindGeneric;     // executor specialisation that can run this program
+    int kind = kKindGeneric;     // executor specialisation that can run every step
+    // phases: descriptor p of the packed program belongs to phase desc_phase[p]; phase q runs
+    // tiles [phase_tile[q], phase_tile[q + 1]) with kernel phase_kind[q]
+    std::vector<uint32_t> desc_phase;
+    std::vector<uint32_t> phase_tile;
+    std::vector<int> phase_kind;
+    uint32_t nphase() const { return phase_kind.empty() ? 1u : (uint32_t)phase_kind.size(); }
 };
 
 // Buffer ids used by lowerings.
@@ -123,7 +145,8 @@ uint64_t shard_size(uint64_t count, int parts);
 bool lower(const CollectiveSpec& spec, HostProgram& prog, std::string& err);
 
 // Merges chained steps: reduce chains into multi-source reductions, group partial folds into
-// grouped reductions, forwarding copies into extra destinations of their producer.
+// grouped reductions, forwarding copies into extra destinations of their producer (except, by
+// prog.phase_mode, the copies of wide reductions, which then run as a later phase).
 void fuse(HostProgram& prog);
 
 // Merges the (lowered, possibly fused) programs of the collectives of one group into one
@@ -134,8 +157,9 @@ void fuse(HostProgram& prog);
 bool merge(std::vector<HostProgram>& parts, const std::vector<CollectiveSpec>& specs, HostProgram& out,
            std::string& err);
 
-// Removes dead descriptors, renumbers dependencies, cuts tiles, sets signal flags and packs
-// the device image. tile_bytes = 0 selects the default.
+// Removes dead descriptors, assigns phases (prog.phase_mode), renumbers dependencies, cuts
+// tiles, sets signal flags, picks each phase's kernel and packs the device image.
+// tile_bytes = 0 selects the default.
 bool finalize(HostProgram& prog, uint32_t tile_bytes, std::string& err);
 
 // Structural checks of a finalized program: dependency order, operand bounds, per-tile

@@ -1222,13 +1222,16 @@ hccl_executor(LaunchArgs a) {
     const bool triggered = a.wait_addr != nullptr;
     // a workgroup whose trigger wait failed runs no tile but still counts itself done below
     const bool started = !triggered || trigger_wait(a);
+    // this launch runs one phase of the program: tiles [tile_begin, tile_end)
+    const uint32_t tb = a.tile_begin, te = a.tile_end;
     if (started && !a.dynamic) {
-        // Wavefront w runs tiles w, w + W, w + 2W, ... in order. Without dependencies no tile
-        // waits for another, so any residency drains. A dependent program needs the whole grid
-        // resident (the host then sizes it to the CUs the stream may use and sends it here only
-        // while no waiting executor holds CUs): a tile waits only for lower tiles, everything
-        // a wavefront ran before is lower, and the lowest unfinished tile is always running.
-        for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
+        // Wavefront w runs tiles w, w + W, w + 2W, ... of the phase in order. Without
+        // dependencies no tile waits for another, so any residency drains. A dependent program
+        // needs the whole grid resident (the host then sizes it to the CUs the stream may use and
+        // sends it here only while no waiting executor holds CUs): a tile waits only for lower
+        // tiles, everything a wavefront ran before is lower, and the lowest unfinished tile is
+        // always running.
+        for (uint32_t t = tb + wave; t < te; t += nworkers) {
             if ((has_deps || triggered) && load_relaxed(&a.error->code) != 0u) break;
             if (!run_tile_traced<KIND>(sh, prog, h, t, lane, bufs, a.trace, wave)) break;
         }
@@ -1243,15 +1246,15 @@ hccl_executor(LaunchArgs a) {
         if (threadIdx.x == 0)
             first = __hip_atomic_fetch_add(ticket, (uint32_t)kWavesPerBlock, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __syncthreads();
-        uint32_t t = uni(first + threadIdx.x / kWaveSize);
+        uint32_t t = uni(tb + first + threadIdx.x / kWaveSize);
         // with at least as many wavefronts as tiles the first tickets cover every tile
-        const bool more = h.ntiles > nworkers;
-        while (t < h.ntiles) {
+        const bool more = te - tb > nworkers;
+        while (t < te) {
             if (load_relaxed(&a.error->code) != 0u) break;
             // claim the next ticket now; its latency hides behind this tile's work
-            uint32_t next = h.ntiles;
+            uint32_t next = te;
             if (more && lane == 0)
-                next = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                next = tb + __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (!run_tile_traced<KIND>(sh, prog, h, t, lane, bufs, a.trace, wave)) break;
             t = uni(__shfl(next, 0));
         }
@@ -1336,6 +1339,7 @@ hccl_resident(ResidentArgs r) {
     __shared__ uint32_t ahead;       // relay: the next packet is already in pk and its mirror
     __shared__ uint32_t ahead_stop;  // relay: ... and it is the stop request
     __shared__ uint32_t sig, fetch;  // relay: decisions of thread 0 while it waits
+    __shared__ uint32_t why;         // relay: why it stopped (ResidentExit)
     const uint32_t lane = __lane_id();
     const uint32_t wave = uni(blockIdx.x * kWavesPerBlock + (threadIdx.x / kWaveSize));
     const uint32_t nworkers = gridDim.x * kWavesPerBlock;
@@ -1349,6 +1353,7 @@ hccl_resident(ResidentArgs r) {
     if (threadIdx.x == 0) {
         ahead = 0;
         ahead_stop = 0;
+        why = RESIDENT_EXIT_STOP;
     }
     __syncthreads();
 
@@ -1371,6 +1376,7 @@ hccl_resident(ResidentArgs r) {
                         }
                         if (wall_clock64() - t0 > r.idle_ticks) {
                             end = 1;
+                            why = RESIDENT_EXIT_IDLE;
                             break;
                         }
                         backoff(nap, 4);
@@ -1431,7 +1437,7 @@ hccl_resident(ResidentArgs r) {
         sh.state = state;
         sh.error = r.error;
         sh.timeout = r.timeout_ticks;
-        for (uint32_t t = wave; t < h.ntiles; t += nworkers) {
+        for (uint32_t t = a.tile_begin + wave; t < a.tile_end; t += nworkers) {
             if (has_deps && load_relaxed(&r.error->code) != 0u) break;
             uint64_t unused = 0;
             if (!run_tile<kKindGeneric>(sh, prog, h, t, lane, bufs, false, unused)) break;
@@ -1517,7 +1523,10 @@ hccl_resident(ResidentArgs r) {
                         ahead = 1;
                         ahead_stop = f == 2u ? 1u : 0u;
                     }
-                    if (g == 2u) stop = 1;
+                    if (g == 2u) {
+                        stop = 1;
+                        why = RESIDENT_EXIT_WORKGROUPS;
+                    }
                     if (g == 0u) backoff(nap, 4);
                 }
                 if (g != 0u) break;
@@ -1534,7 +1543,7 @@ hccl_resident(ResidentArgs r) {
             }
         }
     }
-    if (threadIdx.x == 0 && relay) __hip_atomic_store(&r.q->exited, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (threadIdx.x == 0 && relay) __hip_atomic_store(&r.q->exited, why, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // A program of one step needs no device image: its step travels inside the launch packet

@@ -13,6 +13,12 @@
 // in descriptor order. Wavefront w of a grid of W runs tiles w, w + W, ... in order (or, on
 // request, takes tiles by atomic ticket). A tile only waits for tiles with lower numbers, so
 // the lowest unfinished tile can always run.
+//
+// A program is run as one or more phases: consecutive ranges of tiles, each its own executor
+// launch on the stream, so that everything a phase wrote is visible to the next (the end of a
+// kernel is a device-wide release, the start of the next an acquire). A dependency between
+// steps of different phases is therefore met by the launch order and is not in the image;
+// only dependencies inside one phase are waited for on the device.
 #pragma once
 
 #include <stddef.h>
@@ -21,7 +27,8 @@
 namespace hccl {
 
 constexpr uint32_t kProgramMagic = 0x4C434348u;  // "HCCL"
-constexpr uint32_t kProgramVersion = 1;
+constexpr uint32_t kProgramVersion = 2;
+constexpr uint32_t kMaxPhases = 64;  // launches of one program
 constexpr int kMaxOperands = 64;   // sources or destinations of one descriptor (one per lane)
 constexpr int kMaxRanks = 64;
 constexpr int kMaxMetaBuffers = 8;      // metadata arrays of the dynamic calls of one program
@@ -175,8 +182,11 @@ struct ProgramHeader {
     uint64_t scratch_bytes;
     uint64_t off_aux;      // DynA2A records
     uint32_t naux;
-    uint32_t pad;
+    uint32_t nphase;       // phases (launches) of the program, 1 .. kMaxPhases
+    uint64_t off_phase;    // nphase + 1 u32 tile numbers: phase p runs tiles [t[p], t[p+1])
+    uint64_t pad;
 };
+static_assert(sizeof(ProgramHeader) % 16 == 0, "arrays follow the header 16-byte aligned");
 
 // Device state words: [0] ticket counter, [1] finished-wavefront counter, then one tile
 // counter per descriptor, then one flag per tile. All zero between launches.
@@ -220,6 +230,8 @@ struct LaunchArgs {
     uint64_t wait_value;
     uint32_t wait_cmp;       // TriggerCmp
     uint32_t pad;
+    uint32_t tile_begin;     // the tiles of this launch (one phase of the program):
+    uint32_t tile_end;       // [tile_begin, tile_end)
     TileStamp* trace;        // one record per tile of the program, or NULL (no trace)
     char* bufs[kMaxBuffers];
 };
@@ -232,6 +244,13 @@ constexpr uint32_t kResidentSlots = 64;
 
 constexpr uint64_t kResidentStop = 1ull << 63;  // set in a slot's seq: no packet, the executor ends
 
+// Why a resident executor ended.
+enum ResidentExit : uint32_t {
+    RESIDENT_EXIT_STOP = 1,        // the host's stop request
+    RESIDENT_EXIT_IDLE = 2,        // no packet arrived within the idle limit
+    RESIDENT_EXIT_WORKGROUPS = 3,  // the workgroups did not all finish a packet within the watchdog
+};
+
 struct ResidentSlot {
     uint64_t seq;      // written last by the host: the packet's sequence number (1, 2, ...),
                        // with kResidentStop set for the stop request (one read gives both)
@@ -242,7 +261,8 @@ struct ResidentSlot {
 struct ResidentQueue {
     uint64_t done_seq;   // written by the device: every packet up to this number has completed
     uint32_t error;      // first error code of any completed packet (ErrorRecord codes), sticky
-    uint32_t exited;     // written by the device when the executor has stopped taking packets
+    uint32_t exited;     // written by the device when the executor has stopped taking packets:
+                         // why (ResidentExit, never 0)
     uint32_t err_desc;
     uint32_t err_tile;
     uint64_t pad[5];

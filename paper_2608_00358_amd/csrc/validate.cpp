@@ -9,7 +9,8 @@
 //     per-tile dependency joins two steps with the same tiling;
 //   * every operand lies inside its buffer;
 //   * two steps that touch overlapping bytes, one of them writing, are ordered by the
-//     dependency closure (per tile only when both walk the bytes with the same tiling);
+//     dependency closure (per tile only when both walk the bytes with the same tiling) or by
+//     running in different phases (launches), the earlier phase first;
 //   * every scratch byte a step reads was written by a step ordered before it;
 //   * the steps write exactly the bytes the collective defines as its output (for a dynamic
 //     exchange, whose bytes depend on the counts: one dynamic step inside the capacities).
@@ -137,8 +138,16 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
                 }
             }
         }
+        if (p.desc_phase.size() == D && i > 0 && p.desc_phase[i] < p.desc_phase[i - 1]) {
+            err = fmt("step %llu is in an earlier phase than step %llu", i, i - 1);
+            return false;
+        }
         for (const Dep& e : d.deps) {
             if (e.desc >= i) { err = fmt("step %llu depends on step %llu, which is not earlier", i, e.desc); return false; }
+            if (p.desc_phase.size() == D && p.desc_phase[e.desc] != p.desc_phase[i]) {
+                err = fmt("step %llu waits on the device for step %llu of another phase", i, e.desc);
+                return false;
+            }
             if (e.kind == DEP_TILE && p.descs[e.desc].nelem != d.nelem) {
                 err = fmt("step %llu waits per tile on step %llu with a different size", i, e.desc);
                 return false;
@@ -174,8 +183,11 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
             }
         }
     }
+    // steps of an earlier phase (launch) complete before any step of a later one starts
+    const bool phased = p.desc_phase.size() == D;
     auto ordered = [&](const Access& a, const Access& b) {
         // a.desc < b.desc
+        if (phased && p.desc_phase[a.desc] < p.desc_phase[b.desc]) return true;
         if (!closure) return false;
         if (all.test(b.desc, a.desc)) return true;
         // per-tile order is enough when both walk identical bytes with the same tiling

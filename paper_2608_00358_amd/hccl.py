@@ -17,6 +17,7 @@ DTYPES = {"bf16": 0, "fp16": 1, "fp32": 2, "int32": 3}
 OPS = {"sum": 0, "max": 1, "min": 2}
 ALGOS = {"auto": 0, "direct": 1, "ring": 2, "two_level": 3, "rhd": 4}
 ORDERS = {"ascending": 0, "ring": 1, "halving": 2}
+PHASES = {"auto": 0, "one": 1, "levels": 2}
 RESULTS = {0: "hcclSuccess", 1: "hcclInvalidArgument", 2: "hcclUnsupported", 3: "hcclHipError",
            4: "hcclOutOfMemory", 5: "hcclTimeout", 6: "hcclInternalError"}
 NO_DEVICE = -1
@@ -45,7 +46,8 @@ class hcclConfig_t(ctypes.Structure):
         ("algo", ctypes.c_int32), ("group_size", ctypes.c_int32), ("chunk_bytes", ctypes.c_uint64),
         ("fuse", ctypes.c_int32), ("max_workers", ctypes.c_int32), ("tile_bytes", ctypes.c_uint32),
         ("timeout_ms", ctypes.c_uint32), ("validate", ctypes.c_int32), ("order", ctypes.c_int32),
-        ("requantize", ctypes.c_int32), ("trace", ctypes.c_int32), ("reserved", ctypes.c_int32 * 2),
+        ("requantize", ctypes.c_int32), ("trace", ctypes.c_int32), ("phases", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 
@@ -65,6 +67,7 @@ class hcclProgramInfo_t(ctypes.Structure):
         ("bytes_read", ctypes.c_uint64), ("bytes_written", ctypes.c_uint64),
         ("scratch_bytes", ctypes.c_uint64), ("program_bytes", ctypes.c_uint64), ("compile_us", ctypes.c_double),
         ("step_tile_min", ctypes.c_uint32), ("step_tile_max", ctypes.c_uint32),
+        ("num_phases", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
     ]
 
 
@@ -181,6 +184,8 @@ def hccl_config_init(**kw) -> hcclConfig_t:
             v = ALGOS[v]
         if k == "order" and isinstance(v, str):
             v = ORDERS[v]
+        if k == "phases" and isinstance(v, str):
+            v = PHASES[v]
         setattr(cfg, k, int(v))
     return cfg
 

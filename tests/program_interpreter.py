@@ -3,7 +3,8 @@
 It decodes the packed image the library uploads (hccl_comm_program_image) and runs its tiles on
 host buffers in an order drawn at random among those the program's dependencies allow: a tile
 starts only when every tile it waits for has finished (DEP_TILE: the tile with the same index
-of the named step; DEP_ALL: every tile of it). So it checks what the compiler promises, that
+of the named step; DEP_ALL: every tile of it) and every tile of the earlier phases (launches)
+has finished. So it checks what the compiler promises, that
 the program computes the collective under any schedule the executor may produce, with the
 arithmetic written out here once more from the step semantics:
 
@@ -31,17 +32,20 @@ ES = {DT_BF16: 2, DT_FP16: 2, DT_FP32: 4, DT_INT32: 4}
 HEADER = np.dtype([("magic", "<u4"), ("version", "<u4"), ("ndesc", "<u4"), ("ntiles", "<u4"), ("noperand", "<u4"),
                    ("ndep", "<u4"), ("flags", "<u4"), ("nstate", "<u4"), ("off_desc", "<u8"), ("off_operand", "<u8"),
                    ("off_dep", "<u8"), ("off_tile_desc", "<u8"), ("total_bytes", "<u8"), ("scratch_bytes", "<u8"),
-                   ("off_aux", "<u8"), ("naux", "<u4"), ("pad", "<u4")])
+                   ("off_aux", "<u8"), ("naux", "<u4"), ("nphase", "<u4"), ("off_phase", "<u8"), ("pad", "<u8")])
 DESC = np.dtype([("op", "u1"), ("redop", "u1"), ("flags", "u1"), ("sig", "u1"), ("nsrc", "<u2"), ("ndst", "<u2"),
                  ("group", "<u2"), ("ndep", "<u2"), ("src", "<u4"), ("dst", "<u4"), ("dep", "<u4"), ("tile0", "<u4"),
                  ("ntiles", "<u4"), ("tile_elems", "<u4"), ("pad0", "<u4"), ("nelem", "<u8"), ("fold", "<u4"),
                  ("requant", "<u4"), ("aux", "<u4"), ("pad1", "<u4")])
 OPERAND = np.dtype([("buf", "<u4"), ("dtype", "<u4"), ("offset", "<u8")])
 DEP = np.dtype([("desc", "<u4"), ("kind", "<u4"), ("expected", "<u4"), ("state", "<u4")])
-assert HEADER.itemsize == 96 and DESC.itemsize == 64 and OPERAND.itemsize == 16 and DEP.itemsize == 16
+assert HEADER.itemsize == 112 and DESC.itemsize == 64 and OPERAND.itemsize == 16 and DEP.itemsize == 16
 
 
 class Program:
+    def phase_of(self, tile: int) -> int:
+        return int(np.searchsorted(self.phase_tile, tile, side="right")) - 1
+
     def __init__(self, image: bytes):
         raw = np.frombuffer(image, dtype=np.uint8).copy()
         self.h = np.frombuffer(image, dtype=HEADER, count=1)[0]
@@ -52,6 +56,11 @@ class Program:
         self.deps = raw[int(self.h["off_dep"]):][: ndep * 16].view(DEP)
         self.tile_desc = raw[int(self.h["off_tile_desc"]):][: int(self.h["ntiles"]) * 4].view("<u4")
         self.scratch_bytes = int(self.h["scratch_bytes"])
+        nph = int(self.h["nphase"])
+        # phase q runs tiles [phase_tile[q], phase_tile[q + 1])
+        self.phase_tile = raw[int(self.h["off_phase"]):][: (nph + 1) * 4].view("<u4").astype(np.int64)
+        assert nph >= 1 and self.phase_tile[0] == 0 and self.phase_tile[-1] == int(self.h["ntiles"])
+        assert (np.diff(self.phase_tile) >= 0).all()
 
 
 # ------------------------------------------------------------------------ element types
@@ -149,7 +158,7 @@ class Interpreter:
             self._view(o, first, n)[:] = out
 
     def run(self, rng: np.random.Generator):
-        """Every tile once, in a random order the dependencies allow."""
+        """Every tile once, phase after phase, in a random order the dependencies allow."""
         p = self.p
         ntiles = len(p.tile_desc)
         nd = len(p.descs)
@@ -166,6 +175,7 @@ class Interpreter:
             for e in p.deps[int(D["dep"]): int(D["dep"]) + int(D["ndep"])]:
                 src = int(e["desc"])
                 assert src < d, "a step waits for a later step"
+                assert p.phase_of(int(p.descs[src]["tile0"])) == p.phase_of(t), "a wait across phases"
                 if int(e["kind"]) == DEP_TILE:
                     st = int(p.descs[src]["tile0"]) + k
                     assert k < int(p.descs[src]["ntiles"]), "per-tile wait on a missing tile"
@@ -175,23 +185,26 @@ class Interpreter:
                     waits[t].append(("d", src))
                     waiters_desc[src].append(t)
         missing = np.array([len(w) for w in waits])
-        ready = [t for t in range(ntiles) if missing[t] == 0]
         order = []
-        while ready:
-            i = int(rng.integers(len(ready)))
-            ready[i], ready[-1] = ready[-1], ready[i]
-            t = ready.pop()
-            self.run_tile(t)
-            order.append(t)
-            done_tiles[t] = True
-            d = int(p.tile_desc[t])
-            done_count[d] += 1
-            woken = list(waiters_tile[t])
-            if done_count[d] == int(p.descs[d]["ntiles"]):
-                woken += waiters_desc[d]
-            for w in woken:
-                missing[w] -= 1
-                if missing[w] == 0:
-                    ready.append(w)
-        assert done_tiles.all(), "some tiles never became ready (a dependency cycle or a missing producer)"
+        for q in range(len(p.phase_tile) - 1):
+            lo, hi = int(p.phase_tile[q]), int(p.phase_tile[q + 1])
+            ready = [t for t in range(lo, hi) if missing[t] == 0]
+            while ready:
+                i = int(rng.integers(len(ready)))
+                ready[i], ready[-1] = ready[-1], ready[i]
+                t = ready.pop()
+                self.run_tile(t)
+                order.append(t)
+                done_tiles[t] = True
+                d = int(p.tile_desc[t])
+                done_count[d] += 1
+                woken = list(waiters_tile[t])
+                if done_count[d] == int(p.descs[d]["ntiles"]):
+                    woken += waiters_desc[d]
+                for w in woken:
+                    missing[w] -= 1
+                    if missing[w] == 0:
+                        ready.append(w)
+            assert done_tiles[lo:hi].all(), "some tiles never became ready (a dependency cycle or a missing producer)"
+        assert done_tiles.all()
         return order

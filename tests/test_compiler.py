@@ -57,17 +57,24 @@ def test_reduce_scatter_ring_structure(dt, P, fuse):
 @pytest.mark.parametrize("algo", ["direct", "ring"])
 @pytest.mark.parametrize("P", [1, 2, 4, 5])
 @pytest.mark.parametrize("fuse", [0, 1])
-def test_allreduce_structure_and_minimal_traffic_when_fused(algo, P, fuse):
+@pytest.mark.parametrize("phases", ["auto", "one"])
+def test_allreduce_structure_and_minimal_traffic_when_fused(algo, P, fuse, phases):
     N = 100003
     dt = "bf16"
-    with comm(P, algo=algo, fuse=fuse, chunk_bytes=65536) as c:
+    with comm(P, algo=algo, fuse=fuse, chunk_bytes=65536, phases=phases) as c:
         H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, dt)
         info = info_of(c)
     if fuse or algo == "direct":
-        assert info["num_deps"] == 0
+        assert info["num_deps"] == 0 and info["num_phases"] == 1
         assert info["bytes_read"] == P * N * 2 and info["bytes_written"] == P * N * 2
     elif P > 1:
-        assert info["num_deps"] > 0 and info["bytes_read"] > P * N * 2
+        assert info["bytes_read"] > P * N * 2
+        if phases == "one":
+            # one launch: the ring's hops wait for each other tile by tile on the device
+            assert info["num_deps"] > 0 and info["num_phases"] == 1
+        else:
+            # one launch per hop: P-2 reduce hops after the first, P-1 forwarding hops
+            assert info["num_deps"] == 0 and info["num_phases"] == max(1, P - 1) + (P - 1)
 
 
 def test_allreduce_in_place_is_validated_with_aliasing():
@@ -288,7 +295,7 @@ def test_empty_group_is_a_no_op():
 @pytest.mark.parametrize("fuse", [0, 1])
 def test_rhd_reduce_scatter_structure(P, fuse):
     M, chunk = 5000, 4096
-    with comm(P, algo="rhd", order="halving", fuse=fuse, chunk_bytes=chunk) as c:
+    with comm(P, algo="rhd", order="halving", fuse=fuse, chunk_bytes=chunk, phases="one") as c:
         H.hccl_reduce_scatter(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), M, "bf16")
         info = info_of(c)
     chunks = ceil_div(M, chunk // 2)
@@ -302,6 +309,13 @@ def test_rhd_reduce_scatter_structure(P, fuse):
         # P ranks x (P-1) kept blocks summed over the levels, per chunk
         assert info["num_descs"] == P * (P - 1) * chunks
         assert (info["num_deps"] > 0) == (P > 2)     # one level has nothing to wait for
+        assert info["num_phases"] == 1
+    # by default the butterfly levels are launches of their own and wait for nothing on the device
+    with comm(P, algo="rhd", order="halving", fuse=fuse, chunk_bytes=chunk) as c:
+        H.hccl_reduce_scatter(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), M, "bf16")
+        auto = info_of(c)
+    assert auto["num_deps"] == 0 and auto["num_descs"] == info["num_descs"]
+    assert auto["num_phases"] == (1 if fuse or P == 1 else P.bit_length() - 1)
 
 
 @pytest.mark.parametrize("P", [2, 4, 8])
@@ -487,3 +501,66 @@ def test_hccl_debug_logs_creation_compiles_and_cache_hits(monkeypatch, capfd):
     with comm(2) as c:
         H.hccl_allgather(c.handle, fake_bufs(2, 1 << 40), fake_bufs(2, 1 << 44), 1000, "bf16")
     assert capfd.readouterr().err == ""
+
+
+# ------------------------------------------------------------------------------ phases
+@pytest.mark.parametrize("kib,split", [(32 * 1024, True), (4 * 1024, True), (2 * 1024, False), (256, False)])
+def test_wide_allreduce_splits_its_copies_only_when_large(kib, split):
+    """The two-level all-reduce of 64 ranks: at 32 MiB per rank the 64-source reductions write
+    one destination each and a second launch copies every result to the other 63 ranks (from 4 MiB
+    per rank); at 2 MiB or 256 KiB per rank the fused one-launch program is kept."""
+    P, N = 64, kib * 1024 // 2
+    with comm(P, algo="two_level", group_size=8, validate=1) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "bf16")
+        info = info_of(c)
+    assert info["num_deps"] == 0 and info["max_srcs"] == P
+    if split:
+        assert info["num_phases"] == 2
+        assert info["bytes_read"] == (P + 1) * N * 2 and info["bytes_written"] == P * N * 2
+        # the wide copies read up to 32 KiB per tile, in about 1024 tiles
+        assert info["step_tile_max"] == max(8192, min(32768, N * 2 // 1024)) // 2
+    else:
+        assert info["num_phases"] == 1
+        assert info["bytes_read"] == P * N * 2 and info["bytes_written"] == P * N * 2
+    with comm(P, algo="two_level", group_size=8, phases="one") as c:
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "bf16")
+        assert info_of(c)["num_phases"] == 1 and info_of(c)["bytes_read"] == P * N * 2
+
+
+@pytest.mark.parametrize("phases,launches", [("auto", 3), ("levels", 3), ("one", 1)])
+def test_unfused_two_level_runs_level_by_level(phases, launches):
+    """Unfused two-level schedule: group reductions, the reduction of the group partials, then
+    the forwarding copies (the inter-group copy and the intra-group copies it feeds are merged
+    by nothing, fusion being off: three dependency levels, plus one for copies of copies)."""
+    P, N = 16, 100000
+    with comm(P, algo="two_level", group_size=4, fuse=0, phases=phases, validate=1) as c:
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "fp32")
+        info = info_of(c)
+    if phases == "one":
+        assert info["num_phases"] == 1 and info["num_deps"] > 0
+    else:
+        assert info["num_phases"] == 4 and info["num_deps"] == 0
+
+
+def test_phase_mode_is_part_of_the_cached_program():
+    P, N = 4, 50000
+    with comm(P, algo="ring", fuse=0) as c:
+        s, r = fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44)
+        H.hccl_allreduce(c.handle, s, r, N, "fp32")
+        assert info_of(c)["num_phases"] > 1
+        c.set_config(algo="ring", fuse=0, phases="one")
+        H.hccl_allreduce(c.handle, s, r, N, "fp32")
+        assert info_of(c)["num_phases"] == 1 and info_of(c)["cache_hit"] == 0
+        with pytest.raises(H.HcclError):
+            c.set_config(algo="ring", phases=7)
+            H.hccl_allreduce(c.handle, s, r, N, "fp32")
+
+
+def test_wide_copies_keep_about_1024_tiles():
+    """Forced split (phases=levels) at 4 MiB per rank: the wide copies shrink their tiles to keep
+    the copy phase parallel (8 KiB at the least)."""
+    P, N = 64, 4 * (1 << 20) // 2
+    with comm(P, algo="two_level", group_size=8, phases="levels") as c:
+        H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "bf16")
+        info = info_of(c)
+    assert info["num_phases"] == 2 and info["step_tile_max"] == 8192 // 2

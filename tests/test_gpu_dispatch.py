@@ -32,11 +32,13 @@ def mode(request, monkeypatch):
     return request.param
 
 
+@pytest.mark.parametrize("phases", ["one", "auto"])
 @pytest.mark.parametrize("algo,cfg", [("ring", dict(fuse=0)), ("two_level", dict(group_size=4, fuse=0)),
                                       ("rhd", dict(order="halving", fuse=0)), ("direct", {})])
-def test_allreduce_repeated_launches(mode, algo, cfg):
+def test_allreduce_repeated_launches(mode, algo, cfg, phases):
     P, N = 8, 12345
     x = inputs(P, N, "bf16", 21)
+    cfg = dict(cfg, phases=phases)
     print(f"dispatch={mode} allreduce algo={algo} cfg={cfg}", flush=True)
     want = oracle.allreduce_ordered(x, "bf16", order=cfg.get("order", "two_level" if algo == "two_level" else
                                                            "ascending"), group=cfg.get("group_size", 0))
@@ -80,9 +82,10 @@ def test_dynamic_alltoallv_repeated_launches(mode):
                 assert np.array_equal(to_host(recv[d], "int32"), want[d]), f"launch {it} destination {d}"
 
 
-def test_triggered_dependent_program(mode):
-    """A pre-launched unfused ring all-reduce (dependent steps) released by a device word, in
-    every dispatch mode."""
+@pytest.mark.parametrize("phases", ["one", "auto"])
+def test_triggered_dependent_program(mode, phases):
+    """A pre-launched unfused ring all-reduce (dependent steps, waited for on the device or run
+    as one launch per level behind the first) released by a device word, in every dispatch mode."""
     import time
 
     from gpu_helpers import MaskedStream, SideStream
@@ -95,8 +98,9 @@ def test_triggered_dependent_program(mode):
     flag = torch.zeros(1, dtype=torch.int64, device="cuda:0")
     done = torch.zeros(1, dtype=torch.int64, device="cuda:0")
     torch.cuda.synchronize()
-    print(f"dispatch={mode} triggered unfused ring", flush=True)
-    with MaskedStream(2) as s, SideStream() as cs, H.Comm(P, device=0, algo="ring", fuse=0, **SMALL) as c:
+    print(f"dispatch={mode} triggered unfused ring phases={phases}", flush=True)
+    with MaskedStream(2) as s, SideStream() as cs, H.Comm(P, device=0, algo="ring", fuse=0, phases=phases,
+                                                          **SMALL) as c:
         with c.triggered(wait=(flag, "eq", 3), done=(done, 4)):
             H.hccl_allreduce(c.handle, send, recv, N, "fp32", stream=s)
         time.sleep(0.01)

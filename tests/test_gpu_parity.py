@@ -224,10 +224,10 @@ def test_fp16_rounding_boundaries_of_the_hardware_conversion():
 
 
 def test_repeated_launches_of_a_dependent_program_reset_their_counters():
-    # the unfused ring uses per-tile counters; ten launches in a row must all be right
+    # the unfused ring in one launch uses per-tile counters; ten launches in a row must all be right
     P, N = 8, 65536
     x = inputs(P, N, "bf16", 21)
-    with H.Comm(P, device=0, algo="ring", fuse=0, chunk_bytes=16384, tile_bytes=8192) as c:
+    with H.Comm(P, device=0, algo="ring", fuse=0, chunk_bytes=16384, tile_bytes=8192, phases="one") as c:
         send = [to_device(x[r], "bf16") for r in range(P)]
         outs = [Guarded(N, "bf16") for _ in range(P)]
         want = oracle.allreduce(x, "bf16")
@@ -241,12 +241,13 @@ def test_repeated_launches_of_a_dependent_program_reset_their_counters():
                 assert same_bits(outs[r].result(), want[r], "bf16"), f"launch {it} rank {r}"
 
 
-def test_launches_on_two_streams_are_ordered():
+@pytest.mark.parametrize("phases", ["one", "auto"])
+def test_launches_on_two_streams_are_ordered(phases):
     P, N = 4, 100000
     x = inputs(P, N, "fp32", 22)
     want = oracle.allreduce(x, "fp32")
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
-    with H.Comm(P, device=0, algo="ring", fuse=0, chunk_bytes=16384, tile_bytes=8192) as c:
+    with H.Comm(P, device=0, algo="ring", fuse=0, chunk_bytes=16384, tile_bytes=8192, phases=phases) as c:
         send = [to_device(x[r], "fp32") for r in range(P)]
         o1 = [Guarded(N, "fp32") for _ in range(P)]
         o2 = [Guarded(N, "fp32") for _ in range(P)]

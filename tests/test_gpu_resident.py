@@ -26,7 +26,9 @@ def put(dst, bits, dt):
 
 
 @pytest.mark.parametrize("algo,cfg,N", [("direct", {}, 16384), ("ring", dict(fuse=1), 100003),
-                                        ("ring", dict(fuse=0), 50000), ("two_level", dict(group_size=4, fuse=0), 40000)])
+                                        ("ring", dict(fuse=0), 50000), ("ring", dict(fuse=0, phases="one"), 50000),
+                                        ("two_level", dict(group_size=4, fuse=0), 40000),
+                                        ("two_level", dict(group_size=4, fuse=0, phases="one"), 40000)])
 def test_resident_allreduce_packets_match_the_oracle(algo, cfg, N):
     P = 8
     print(f"resident allreduce algo={algo} cfg={cfg} N={N}", flush=True)
@@ -40,6 +42,7 @@ def test_resident_allreduce_packets_match_the_oracle(algo, cfg, N):
         c.allreduce(send, recv)                  # compiles the program and sizes the scratch
         torch.cuda.synchronize()
         assert c.async_error() == 0
+        phases = c.last_program()["num_phases"]
         with c.resident(idle_ms=IDLE_MS):
             for k in range(3):
                 for r in range(P):
@@ -47,7 +50,7 @@ def test_resident_allreduce_packets_match_the_oracle(algo, cfg, N):
                     recv[r].fill_(-1.0)
                 torch.cuda.current_stream().synchronize()
                 c.allreduce(send, recv)
-                assert c.resident_seq() == k + 1
+                assert c.resident_seq() == (k + 1) * phases     # one packet per phase
                 c.resident_wait()
                 want = oracle.allreduce_ordered(xs[k], "fp32", order=order, group=cfg.get("group_size", 0))
                 for r in range(P):
@@ -55,26 +58,31 @@ def test_resident_allreduce_packets_match_the_oracle(algo, cfg, N):
                     assert same_bits(got, want[r], "fp32"), f"packet {k} rank {r}: {first_mismatch(got, want[r])}"
 
 
-def test_resident_burst_wraps_the_doorbell_ring():
-    """150 packets submitted without waiting (more than the 64 slots: the call waits for a free
-    slot), alternating two programs; a dependent program's counters must be clear for the next."""
+@pytest.mark.parametrize("phases", ["one", "auto"])
+def test_resident_burst_wraps_the_doorbell_ring(phases):
+    """150 calls submitted without waiting (more than the 64 slots: the call waits for a free
+    slot), alternating two programs; a dependent program's counters must be clear for the next
+    (in one launch), or every phase is a packet of its own."""
     P, N = 4, 30000
     x = inputs(P, N, "fp32", 110)
     send = [to_device(x[r], "fp32") for r in range(P)]
     out_a = [torch.zeros(N, dtype=torch.float32, device="cuda:0") for _ in range(P)]
     out_b = [torch.zeros(N // P, dtype=torch.float32, device="cuda:0") for _ in range(P)]
-    print("resident burst of 150 packets", flush=True)
-    with H.Comm(P, device=0, algo="ring", fuse=0, chunk_bytes=8192) as c:
+    print(f"resident burst of 150 calls, phases={phases}", flush=True)
+    with H.Comm(P, device=0, algo="ring", fuse=0, chunk_bytes=8192, phases=phases) as c:
         c.allreduce(send, out_a)
+        n_a = c.last_program()["num_phases"]
         c.reduce_scatter(send, out_b)
+        n_b = c.last_program()["num_phases"]
         torch.cuda.synchronize()
+        assert (n_a, n_b) == ((1, 1) if phases == "one" else (2 * (P - 1), P - 1))
         with c.resident(idle_ms=IDLE_MS):
             for k in range(150):
                 if k % 2 == 0:
                     c.allreduce(send, out_a)
                 else:
                     c.reduce_scatter(send, out_b)
-            assert c.resident_seq() == 150
+            assert c.resident_seq() == 75 * (n_a + n_b)
             c.resident_wait(timeout_ms=10000)
         want = oracle.allreduce(x, "fp32")
         want_rs = oracle.reduce_scatter(x, "fp32")
@@ -230,7 +238,7 @@ def test_resident_large_packets_where_the_relay_runs_tiles(blocks):
     out_b = [torch.zeros(N, dtype=torch.bfloat16, device="cuda:0") for _ in range(P)]
     print(f"resident large packets blocks={blocks}", flush=True)
     with H.Comm(P, device=0, algo="direct") as ca, H.Comm(P, device=0, algo="ring", fuse=0,
-                                                          chunk_bytes=65536) as cb:
+                                                          chunk_bytes=65536, phases="one") as cb:
         ca.allreduce(send, out_a)
         cb.allreduce(send, out_b)
         torch.cuda.synchronize()

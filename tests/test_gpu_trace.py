@@ -8,17 +8,29 @@ import torch
 import oracle
 import paper_2608_00358_amd as H
 from gpu_helpers import Guarded, same_bits, to_device
+from program_interpreter import Program
 from workloads import alltoallv_layout, normal_bf16, zipf_counts
 
 pytestmark = pytest.mark.gpu
 
 
-def _check_records(rec, khz, info):
+def _check_records(rec, khz, info, phase_tile=None):
     n = info["num_tiles"]
     assert rec.shape == (n,)
     assert (rec["start"] > 0).all(), "a tile left no record"
     assert (rec["done"] >= rec["ready"]).all()
-    if not info["tickets"]:
+    if not info["tickets"] and info["num_phases"] > 1:
+        # one launch per phase, each static: wavefront w runs tiles b + w, b + w + W, ... of its
+        # phase, and a phase starts after the previous one has ended
+        for q in range(info["num_phases"]):
+            lo, hi = int(phase_tile[q]), int(phase_tile[q + 1])
+            W = int(rec["wave"][lo:hi].max()) + 1
+            assert W <= info["workers"]
+            assert np.array_equal(rec["wave"][lo:hi], np.arange(hi - lo, dtype=np.uint32) % W)
+            if q:
+                prev_end = (rec["start"][:lo].astype(np.int64) + rec["done"][:lo]).max()
+                assert int(rec["start"][lo:hi].min()) >= prev_end
+    elif not info["tickets"]:
         # static dispatch: wavefront w runs tiles w, w + W, ...
         assert np.array_equal(rec["wave"], np.arange(n, dtype=np.uint32) % info["workers"])
     else:
@@ -33,12 +45,12 @@ def _check_records(rec, khz, info):
     return span_us
 
 
-@pytest.mark.parametrize("fuse", [0, 1])
-def test_traced_ring_allreduce_records_every_tile(fuse):
+@pytest.mark.parametrize("fuse,phases", [(0, "one"), (0, "auto"), (1, "auto")])
+def test_traced_ring_allreduce_records_every_tile(fuse, phases):
     P, N = 4, 300_001
-    print(f"trace: ring allreduce P={P} N={N} fuse={fuse}", flush=True)
+    print(f"trace: ring allreduce P={P} N={N} fuse={fuse} phases={phases}", flush=True)
     x = normal_bf16(P, N, seed=900 + fuse)
-    with H.Comm(P, device=0, algo="ring", fuse=fuse, chunk_bytes=16384, trace=1) as c:
+    with H.Comm(P, device=0, algo="ring", fuse=fuse, chunk_bytes=16384, trace=1, phases=phases) as c:
         send = [to_device(x[r], "bf16") for r in range(P)]
         out = [Guarded(N, "bf16") for _ in range(P)]
         c.allreduce(send, [o.view for o in out])
@@ -46,14 +58,17 @@ def test_traced_ring_allreduce_records_every_tile(fuse):
         assert c.async_error() == 0
         info = c.last_program()
         rec, khz = c.trace()
+        phase_tile = Program(c.program_image()).phase_tile
     assert info["inline_launch"] == 0
-    span = _check_records(rec, khz, info)
+    span = _check_records(rec, khz, info, phase_tile)
     want = oracle.allreduce(x, "bf16")
     for r in range(P):
         assert same_bits(out[r].result(), want[r], "bf16") and out[r].guards_intact()
     assert info["tickets"] == 0     # nothing else holds CUs: static dispatch
-    if not fuse:
+    if not fuse and phases == "one":
         assert (rec["ready"] > 0).any()   # a dependent step waits
+    if not fuse and phases == "auto":
+        assert info["num_phases"] == 2 * (P - 1) and info["num_deps"] == 0
     print(f"trace: {info['num_tiles']} tiles over {span:.1f} us", flush=True)
 
 

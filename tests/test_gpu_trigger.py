@@ -194,14 +194,14 @@ def test_compile_and_scratch_growth_while_a_triggered_packet_waits():
     torch.cuda.synchronize()
     print("trigger pending: compile, scratch growth and a dependent program on another stream", flush=True)
     with MaskedStream(2) as s, SideStream() as cs, H.Comm(P, device=0, chunk_bytes=8192, timeout_ms=10000) as c:
-        c.set_config(algo="ring", fuse=0, chunk_bytes=8192, timeout_ms=10000)
+        c.set_config(algo="ring", fuse=0, chunk_bytes=8192, timeout_ms=10000, phases="one")
         H.hccl_allreduce(c.handle, small[:P], small[P:], 100, "bf16", stream=cs)   # a first, small scratch
         cs.synchronize()
         c.set_config(algo="ring", chunk_bytes=8192, timeout_ms=10000)
         with c.triggered(wait=(flag, "ge", 1), done=(done, 7)):
             H.hccl_allreduce(c.handle, send, [o.view for o in outs], N, "bf16", stream=s)
         time.sleep(0.02)
-        c.set_config(algo="ring", fuse=0, chunk_bytes=8192, timeout_ms=10000)
+        c.set_config(algo="ring", fuse=0, chunk_bytes=8192, timeout_ms=10000, phases="one")
         t0 = time.perf_counter()
         H.hccl_reduce_scatter(c.handle, ysend, [o.view for o in youts], M, "bf16", stream=cs)
         tickets = c.last_program()["tickets"]

@@ -66,6 +66,10 @@ def check(got_bytes, want, dt):
 
 ALLREDUCE = [
     ("ring", dict(algo="ring", fuse=0), "ascending"),
+    ("ring one launch", dict(algo="ring", fuse=0, phases="one"), "ascending"),
+    ("two-level one launch", dict(algo="two_level", group_size=4, fuse=0, phases="one"), "two_level"),
+    ("rhd butterfly one launch", dict(algo="rhd", order="halving", fuse=0, phases="one"), "halving"),
+    ("two-level fused, copies split", dict(algo="two_level", group_size=2, phases="levels"), "two_level"),
     ("ring fused", dict(algo="ring"), "ascending"),
     ("direct", dict(algo="direct"), "ascending"),
     ("ring rotated", dict(algo="ring", fuse=0, order="ring"), "ring"),
@@ -169,18 +173,24 @@ def test_alltoallv_program_with_split_pieces_in_random_orders():
         check(got, want, "bf16")
 
 
-def test_group_of_dependent_programs_in_random_orders():
+@pytest.mark.parametrize("phases", ["one", "auto"])
+def test_group_of_dependent_programs_in_random_orders(phases):
     P = 4
     xa = inputs(P, 2000, "bf16", seed=17)
     xb = inputs(P, P * 600, "fp32", seed=18)
     xc = inputs(P, 333, "bf16", seed=19)
-    with H.Comm(P, device=H.NO_DEVICE, algo="ring", fuse=0, **SMALL) as c:
+    with H.Comm(P, device=H.NO_DEVICE, algo="ring", fuse=0, phases=phases, **SMALL) as c:
         with c.group():
             H.hccl_allreduce(c.handle, fake(P, 1 << 40), fake(P, 2 << 40), 2000, "bf16")
             H.hccl_reduce_scatter(c.handle, fake(P, 3 << 40), fake(P, 4 << 40), 600, "fp32")
             H.hccl_allgather(c.handle, fake(P, 5 << 40), fake(P, 6 << 40), 333, "bf16")
         image = c.program_image()
-        assert c.last_program()["collective"] == -1 and c.last_program()["num_deps"] > 0
+        info = c.last_program()
+        assert info["collective"] == -1
+        # one launch waiting tile by tile, or the three calls' hops level by level (the
+        # all-reduce has the most: 2 reduce hops + 3 forwarding hops after its first step)
+        assert (info["num_deps"] > 0 and info["num_phases"] == 1) if phases == "one" else \
+            (info["num_deps"] == 0 and info["num_phases"] == 6)
     layout = [(P, list(xa), [2000 * 2] * P), (P, list(xb), [600 * 4] * P), (P, list(xc), [P * 333 * 2] * P)]
     for seed in SEEDS:
         ga, gb, gc = run_program(image, None, None, seed, group_layout=layout)
@@ -192,3 +202,24 @@ def test_group_of_dependent_programs_in_random_orders():
 def test_image_is_empty_before_any_program():
     with H.Comm(2, device=H.NO_DEVICE) as c:
         assert c.program_image() == b""
+
+
+@pytest.mark.parametrize("cfg,order", [(dict(algo="two_level", group_size=4), "two_level"),
+                                       (dict(algo="ring"), "ascending"),
+                                       (dict(algo="two_level", group_size=16), "two_level")],
+                         ids=["two-level 4x4", "ring", "two-level 1x16"])
+def test_wide_reduction_with_split_copies_in_random_orders(cfg, order):
+    """16 ranks: every reduction has 16 sources, so under phases=levels its result is written
+    once and copied to the other 15 ranks by a second phase."""
+    P, N = 16, 2500
+    x = inputs(P, N, "bf16", seed=21)
+    with H.Comm(P, device=H.NO_DEVICE, phases="levels", **cfg, **SMALL) as c:
+        H.hccl_allreduce(c.handle, fake(P, 1 << 40), fake(P, 1 << 44), N, "bf16")
+        image = c.program_image()
+        info = c.last_program()
+    assert info["num_phases"] == 2 and info["num_deps"] == 0
+    assert info["bytes_read"] == P * N * 2 + N * 2 and info["bytes_written"] == P * N * 2
+    want = oracle.allreduce_ordered(x, "bf16", order=order, group=cfg.get("group_size", 0), shard=shard(N, P))
+    for seed in SEEDS:
+        (got,) = run_program(image, list(x), [N * 2] * P, seed)
+        check(got, want, "bf16")

@@ -20,11 +20,15 @@ pytestmark = pytest.mark.gpu
 
 # label, ranks, element type, configuration, first and second element count, oracle order
 CASES = [
-    ("ring unfused bf16", 4, "bf16", dict(algo="ring", fuse=0, chunk_bytes=8192), 300_001, 70_003, {}),
-    ("two-level unfused bf16", 16, "bf16", dict(algo="two_level", group_size=4, fuse=0, chunk_bytes=16384),
-     200_000, 33_333, {"group": 4}),
-    ("recursive halving unfused bf16", 8, "bf16", dict(algo="rhd", order="halving", fuse=0), 100_000, 4_097,
-     {"order": "halving"}),
+    ("ring unfused bf16", 4, "bf16", dict(algo="ring", fuse=0, chunk_bytes=8192, phases="one"), 300_001, 70_003, {}),
+    ("ring unfused bf16, a launch per level", 4, "bf16", dict(algo="ring", fuse=0, chunk_bytes=8192), 300_001,
+     70_003, {}),
+    ("two-level unfused bf16", 16, "bf16", dict(algo="two_level", group_size=4, fuse=0, chunk_bytes=16384,
+                                                phases="one"), 200_000, 33_333, {"group": 4}),
+    ("two-level fused bf16, copies in a second launch", 16, "bf16", dict(algo="two_level", group_size=4,
+                                                                        phases="levels"), 200_000, 33_333, {"group": 4}),
+    ("recursive halving unfused bf16", 8, "bf16", dict(algo="rhd", order="halving", fuse=0, phases="one"), 100_000,
+     4_097, {"order": "halving"}),
     ("ring fused fp32", 8, "fp32", dict(algo="ring", chunk_bytes=65536), 1 << 20, 12_345, {}),
     ("one-step direct fp32", 8, "fp32", dict(algo="direct"), 1 << 14, 1000, {}),
 ]
@@ -58,7 +62,10 @@ def test_noalloc_matches_allreduce_on_two_calls_second_smaller(case):
             torch.cuda.synchronize()
             assert c.async_error() == 0
             if cfg.get("fuse") == 0 and P > 2:
-                assert info["scratch_bytes"] > 0 and info["num_deps"] > 0, info   # partials and counters used
+                assert info["scratch_bytes"] > 0, info                            # partials used
+                assert (info["num_deps"] > 0) == (cfg.get("phases") == "one"), info  # counters used
+            if cfg.get("phases") == "levels" or (cfg.get("fuse") == 0 and "phases" not in cfg):
+                assert info["num_phases"] > 1, info
             want = _want(x, dt, order)
             for r in range(P):
                 a, b = got[r].result(), ref[r].result()
