@@ -315,8 +315,9 @@ def bench_forwarded_partials(device, iters=10):
 
 def bench_copy_ceiling(device, iters=20, nbytes=1 << 30):
     """What plain HIP kernels reach on this device (bench_stream.hip): a contiguous copy, a
-    read-only and a write-only sweep of 1 GiB, each the best of four grid sizes; and the
-    library's own copy path on the same copy."""
+    read-only and a write-only sweep of 1 GiB, and read-only sweeps of 8 and 64 regions at the
+    same offset (the reductions' pattern), each the best of four grid sizes; and the library's
+    own copy path on the same copy."""
     import torch
 
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_00358_amd", "lib", "libbench_stream.so"))
@@ -338,6 +339,21 @@ def bench_copy_ceiling(device, iters=20, nbytes=1 << 30):
             ms = _time_events(run, iters)
             best = max(best, (moved / (ms * 1e-3) / 1e9, blocks))
         out[f"stream_{name}_gbs"], out[f"stream_{name}_blocks"] = round(best[0], 1), best[1]
+    # the reductions' access pattern: the same offset of 8 or 64 regions in turn, 4 KiB each
+    lib.bench_stream_multi.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
+                                       ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p]
+    for streams in (8, 64):
+        best = (0.0, 0)
+        for blocks in (256, 512, 1024, 2048):
+            def run():
+                rc = lib.bench_stream_multi(a.data_ptr(), b.data_ptr(), nbytes, streams, 4096, blocks, st)
+                if rc != 0:
+                    raise RuntimeError(f"bench_stream_multi failed ({rc})")
+            for _ in range(3):
+                run()
+            ms = _time_events(run, iters)
+            best = max(best, (nbytes / (ms * 1e-3) / 1e9, blocks))
+        out[f"stream_read_{streams}_regions_gbs"], out[f"stream_read_{streams}_regions_blocks"] = round(best[0], 1), best[1]
     torch.cuda.synchronize()
     del a, b
     ex = bench_executor_copy(device, iters=iters, nbytes=nbytes)
