@@ -478,6 +478,7 @@ int launch_shape(hcclComm* c, const HostProgram& prog, uint32_t phase, LaunchArg
     int kind = prog.phase_kind.empty() ? prog.kind : prog.phase_kind[phase];
     a.tile_begin = prog.phase_tile.empty() ? 0u : prog.phase_tile[phase];
     a.tile_end = prog.phase_tile.empty() ? prog.ntiles : prog.phase_tile[phase + 1];
+    a.xcd_order = prog.phase_xcd.empty() ? 0u : prog.phase_xcd[phase];
     if (a.trace) kind = kKindGeneric;  // the kernel that records the trace
     if (kind == kKindCopyAligned) {
         for (uint32_t i = 0; i < nuser; ++i)

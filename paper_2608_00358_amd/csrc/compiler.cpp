@@ -1223,10 +1223,16 @@ bool finalize(HostProgram& p, uint32_t tile_bytes, std::string& err) {
     p.kind = kernel_for(0, nd);
     p.phase_tile.assign(1, 0);
     p.phase_kind.clear();
+    p.phase_xcd.clear();
     for (uint32_t q = 0, i = 0; q < nphase; ++q) {
         const uint32_t d0 = i;
         while (i < nd && p.desc_phase[i] == q) ++i;
         p.phase_kind.push_back(kernel_for(d0, i));
+        // A phase of wide reductions reads many buffers per wavefront; numbered XCD by XCD, each
+        // XCD works on one stretch of them at a time.
+        bool wide = i > d0;
+        for (uint32_t k = d0; k < i; ++k) wide &= out[k].op == OP_REDUCE && out[k].nsrc >= kSplitMinSources;
+        p.phase_xcd.push_back(wide ? 1 : 0);
         p.phase_tile.push_back(i < nd ? out[i].tile0 : p.ntiles);
     }
 

@@ -108,6 +108,7 @@ struct HostProgram {
     std::vector<uint32_t> desc_phase;
     std::vector<uint32_t> phase_tile;
     std::vector<int> phase_kind;
+    std::vector<uint8_t> phase_xcd;  // 1 = the phase's wavefronts are numbered XCD by XCD
     uint32_t nphase() const { return phase_kind.empty() ? 1u : (uint32_t)phase_kind.size(); }
 };
 

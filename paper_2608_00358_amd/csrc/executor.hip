@@ -38,6 +38,7 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWavesPerBlock = 4;
+constexpr uint32_t kXcds = 8;  // XCDs of an MI355X
 constexpr int kBlockThreads = kWavesPerBlock * kWaveSize;
 #ifndef HCCL_SRC_BATCH
 #define HCCL_SRC_BATCH 4
@@ -1197,7 +1198,15 @@ template <int KIND>
 __global__ void __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(KIND == kKindGeneric ? 3 : 4)))
 hccl_executor(LaunchArgs a) {
     const uint32_t lane = __lane_id();
-    const uint32_t wave = uni(blockIdx.x * kWavesPerBlock + (threadIdx.x / kWaveSize));
+    // The hardware deals workgroups to the XCDs in turn (block b to XCD b mod 8). With xcd_order
+    // the blocks of one XCD take consecutive numbers, so at any moment each XCD (its L2 and its
+    // address-translation caches) works on one contiguous stretch of the tiles.
+    uint32_t block = blockIdx.x;
+    if (a.xcd_order) {
+        const uint32_t B = gridDim.x, x = block % kXcds, j = block / kXcds;
+        block = x * (B / kXcds) + (x < B % kXcds ? x : B % kXcds) + j;
+    }
+    const uint32_t wave = uni(block * kWavesPerBlock + (threadIdx.x / kWaveSize));
     const uint8_t* prog = a.prog;
     ProgramHeader h;
     h.ndesc = uni(((const ProgramHeader*)prog)->ndesc);

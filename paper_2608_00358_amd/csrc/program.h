@@ -229,7 +229,7 @@ struct LaunchArgs {
     const uint64_t* wait_addr;
     uint64_t wait_value;
     uint32_t wait_cmp;       // TriggerCmp
-    uint32_t pad;
+    uint32_t xcd_order;      // 1 = wavefront numbers grouped by XCD (see the kernel), 0 = in block order
     uint32_t tile_begin;     // the tiles of this launch (one phase of the program):
     uint32_t tile_end;       // [tile_begin, tile_end)
     TileStamp* trace;        // one record per tile of the program, or NULL (no trace)
