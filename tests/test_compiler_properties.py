@@ -3,7 +3,7 @@ that the validator proves well formed (dependency order, operand bounds, no unor
 conflicting accesses, scratch read after write, exact output coverage).
 
 Host-only communicators compile and validate without touching memory, so the search covers
-schedules, orders, fusion, chunk and tile sizes, groups and dynamic exchanges on the CPU.
+schedules, orders, fusion, phase modes, chunk and tile sizes, groups and dynamic exchanges on the CPU.
 """
 import numpy as np
 import pytest
@@ -25,10 +25,10 @@ def reduction_case(draw):
     coll = draw(st.sampled_from(["allreduce", "reduce_scatter", "allgather"]))
     order = draw(st.sampled_from(["ascending", "ring", "halving"]))
     if order == "halving":
-        P = draw(st.sampled_from([1, 2, 4, 8, 16]))
+        P = draw(st.sampled_from([1, 2, 4, 8, 16, 32]))
         algo = draw(st.sampled_from(["direct", "rhd", "auto"]))
     else:
-        P = draw(st.integers(1, 12))
+        P = draw(st.sampled_from([draw(st.integers(1, 12)), 16, 20, 32]))
         algos = ["direct", "ring", "auto"]
         if coll == "allreduce" and order == "ascending":
             algos.append("two_level")
@@ -46,7 +46,8 @@ def reduction_case(draw):
                 fuse=draw(st.integers(0, 1)),
                 requant=draw(st.integers(0, 1)),
                 chunk=draw(st.sampled_from([0, 512, 4096, 65536])),
-                tile=draw(st.sampled_from([0, 1024, 8192])))
+                tile=draw(st.sampled_from([0, 1024, 8192])),
+                phases=draw(st.sampled_from(["auto", "one", "levels"])))
 
 
 @SETTINGS
@@ -54,7 +55,8 @@ def reduction_case(draw):
 def test_every_accepted_reduction_validates(case):
     P = case["P"]
     cfg = dict(algo=case["algo"], order=case["order"], group_size=case["group"], fuse=case["fuse"],
-               requantize=case["requant"], chunk_bytes=case["chunk"], tile_bytes=case["tile"], validate=1)
+               requantize=case["requant"], chunk_bytes=case["chunk"], tile_bytes=case["tile"], validate=1,
+               phases=case["phases"])
     if case["algo"] == "rhd" and case["coll"] != "allgather":
         cfg["order"] = "halving"
     with H.Comm(P, device=H.NO_DEVICE, **cfg) as c:
@@ -76,6 +78,11 @@ def test_every_accepted_reduction_validates(case):
             return
         info = c.last_program()
         assert info["num_descs"] >= 0
+        # a launch per level waits for nothing on the device; one launch keeps every wait
+        if case["phases"] == "levels" or (case["phases"] == "auto" and info["num_phases"] > 1):
+            assert info["num_deps"] == 0
+        if case["phases"] == "one":
+            assert info["num_phases"] == 1
 
 
 @st.composite
