@@ -140,7 +140,9 @@ typedef struct {
     uint64_t chunk_bytes;  /* pipeline chunk, bytes of the input type per rank (0 = 1 MiB) */
     int32_t fuse;          /* 1 = fuse chained steps into multi-operand steps (default);
                               0 = run every lowered step as its own dependent descriptor */
-    int32_t max_workers;   /* upper bound on executor wavefronts (0 = size from the device) */
+    int32_t max_workers;   /* upper bound on executor wavefronts (0 = no bound: one wavefront per
+                              tile for a launch whose tiles never wait, else as many as the
+                              stream's CUs hold at once) */
     uint32_t tile_bytes;   /* work claimed per ticket, bytes read per tile (0 = default) */
     uint32_t timeout_ms;   /* watchdog for one dependency or trigger wait on the device (0 = 2000) */
     int32_t validate;      /* 1 = run the program validator on every compile */

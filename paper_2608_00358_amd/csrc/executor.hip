@@ -67,21 +67,32 @@ constexpr int kSrcBatch = HCCL_SRC_BATCH;  // sources whose loads are issued tog
 #define HCCL_REDUCE_UNROLL16 2
 #endif
 
+// Collective buffers are device memory (or pinned host memory), never LDS or scratch, so every
+// data access goes through a global-address-space pointer. Through a generic pointer the same
+// access compiles to a flat instruction, which also counts on the counter that scalar and LDS
+// accesses use (a wait for a program-image read then waits for the data in flight as well)
+// and needs a full 64-bit address per lane.
+#define HCCL_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ const HCCL_GLOBAL T* gp(const char* p) { return (const HCCL_GLOBAL T*)p; }
+template <typename T>
+__device__ __forceinline__ HCCL_GLOBAL T* gp(char* p) { return (HCCL_GLOBAL T*)p; }
+
 __device__ __forceinline__ u32x4 vld(const char* p) {
-    if constexpr (HCCL_NT_LOAD) return __builtin_nontemporal_load((const u32x4*)p);
-    else return *(const u32x4*)p;
+    if constexpr (HCCL_NT_LOAD) return __builtin_nontemporal_load(gp<u32x4>(p));
+    else return *gp<u32x4>(p);
 }
 // store of reduction results (NT: a step with many destinations)
 template <bool NT = false>
 __device__ __forceinline__ void vst(char* p, u32x4 v) {
-    if constexpr (HCCL_NT_STORE_REDUCE || NT) __builtin_nontemporal_store(v, (u32x4*)p);
-    else *(u32x4*)p = v;
+    if constexpr (HCCL_NT_STORE_REDUCE || NT) __builtin_nontemporal_store(v, gp<u32x4>(p));
+    else *gp<u32x4>(p) = v;
 }
 constexpr uint32_t kWideStoreDsts = 8;  // destinations from which reduction results stream
 // store of copied data
 __device__ __forceinline__ void vst_copy(char* p, u32x4 v) {
-    if constexpr (HCCL_NT_STORE_COPY) __builtin_nontemporal_store(v, (u32x4*)p);
-    else *(u32x4*)p = v;
+    if constexpr (HCCL_NT_STORE_COPY) __builtin_nontemporal_store(v, gp<u32x4>(p));
+    else *gp<u32x4>(p) = v;
 }
 
 template <int DT> struct DtInfo;
@@ -213,18 +224,18 @@ __device__ __forceinline__ void store8(char* p, const A (&x)[8]) {
 // single elements (tails and misaligned operands)
 template <int DT, typename A>
 __device__ __forceinline__ A load1(const char* p) {
-    if constexpr (DT == DT_BF16) return bf16_lo(*(const uint16_t*)p);
-    else if constexpr (DT == DT_FP16) return f16_lo(*(const uint16_t*)p);
-    else if constexpr (DT == DT_FP32) return *(const float*)p;
-    else return *(const int32_t*)p;
+    if constexpr (DT == DT_BF16) return bf16_lo(*gp<uint16_t>(p));
+    else if constexpr (DT == DT_FP16) return f16_lo(*gp<uint16_t>(p));
+    else if constexpr (DT == DT_FP32) return *gp<float>(p);
+    else return *gp<int32_t>(p);
 }
 
 template <int DT, typename A>
 __device__ __forceinline__ void store1(char* p, A v) {
-    if constexpr (DT == DT_BF16) *(uint16_t*)p = (uint16_t)bf16_bits(v);
-    else if constexpr (DT == DT_FP16) *(uint16_t*)p = (uint16_t)f16_bits(v);
-    else if constexpr (DT == DT_FP32) *(float*)p = v;
-    else *(int32_t*)p = v;
+    if constexpr (DT == DT_BF16) *gp<uint16_t>(p) = (uint16_t)bf16_bits(v);
+    else if constexpr (DT == DT_FP16) *gp<uint16_t>(p) = (uint16_t)f16_bits(v);
+    else if constexpr (DT == DT_FP32) *gp<float>(p) = v;
+    else *gp<int32_t>(p) = v;
 }
 
 // ---------------------------------------------------------------------------- REDUCE
@@ -572,18 +583,18 @@ __device__ __forceinline__ void copy_elems(const char* src, const TileOps& t, ui
     for (; e + (uint64_t)U * kWaveSize <= first + count; e += (uint64_t)U * kWaveSize) {
         W v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = *(const W*)(src + (e + (uint64_t)u * kWaveSize + lane) * ES);
+        for (int u = 0; u < U; ++u) v[u] = *gp<W>(src + (e + (uint64_t)u * kWaveSize + lane) * ES);
         for (uint32_t j = 0; j < t.ndst; ++j) {
             char* d = (char*)from_lane(t.dst, j);
 #pragma unroll
-            for (int u = 0; u < U; ++u) *(W*)(d + (e + (uint64_t)u * kWaveSize + lane) * ES) = v[u];
+            for (int u = 0; u < U; ++u) *gp<W>(d + (e + (uint64_t)u * kWaveSize + lane) * ES) = v[u];
         }
     }
     for (uint64_t x = e + lane; x < first + count; x += kWaveSize) {
-        W v = *(const W*)(src + x * ES);
+        W v = *gp<W>(src + x * ES);
         for (uint32_t j = 0; j < t.ndst; ++j) {
             char* d = (char*)from_lane(t.dst, j);
-            *(W*)(d + x * ES) = v;
+            *gp<W>(d + x * ES) = v;
         }
     }
 }
@@ -1234,7 +1245,8 @@ hccl_executor(LaunchArgs a) {
     // this launch runs one phase of the program: tiles [tile_begin, tile_end)
     const uint32_t tb = a.tile_begin, te = a.tile_end;
     if (started && !a.dynamic) {
-        // Wavefront w runs tiles w, w + W, w + 2W, ... of the phase in order. Without
+        // Wavefront w runs tiles w, w + W, w + 2W, ... of the phase in order (only tile w when
+        // the host gave the launch one wavefront per tile, as it does when no tile waits). Without
         // dependencies no tile waits for another, so any residency drains. A dependent program
         // needs the whole grid resident (the host then sizes it to the CUs the stream may use and
         // sends it here only while no waiting executor holds CUs): a tile waits only for lower

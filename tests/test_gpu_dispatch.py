@@ -115,3 +115,22 @@ def test_triggered_dependent_program(mode, phases):
     want = oracle.allreduce(x, "fp32")
     for r in range(P):
         assert same_bits(to_host(recv[r], "fp32"), want[r], "fp32")
+
+
+@pytest.mark.parametrize("max_workers", [0, 4, 100])
+@pytest.mark.parametrize("algo", ["direct", "ring"])
+def test_grid_of_programs_that_never_wait(algo, max_workers):
+    """A launch with no dependency inside it gets one wavefront per tile (max_workers = 0);
+    a capped grid makes every wavefront run many tiles in turn. Same bits either way."""
+    from test_gpu_parity import run_allreduce, run_alltoallv, run_reduce_scatter
+    from workloads import zipf_counts
+
+    cfg = dict(algo=algo, fuse=1, chunk_bytes=65536, tile_bytes=4096, max_workers=max_workers)
+    info = run_allreduce(8, 300001, "bf16", **cfg)
+    assert info["num_phases"] == 1
+    if max_workers == 0:
+        assert info["num_tiles"] <= info["workers"] < info["num_tiles"] + 4
+    else:
+        assert info["workers"] == max_workers
+    run_reduce_scatter(8, 70001, "fp32", **cfg)
+    run_alltoallv(8, zipf_counts(8, 3000, 1.1, seed=5), 129, "bf16", max_workers=max_workers)
