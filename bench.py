@@ -315,45 +315,54 @@ def bench_forwarded_partials(device, iters=10):
 
 def bench_copy_ceiling(device, iters=20, nbytes=1 << 30):
     """What plain HIP kernels reach on this device (bench_stream.hip): a contiguous copy, a
-    read-only and a write-only sweep of 1 GiB, and read-only sweeps of 8 and 64 regions at the
-    same offset (the reductions' pattern), each the best of four grid sizes; and the library's
-    own copy path on the same copy."""
+    read-only and a write-only sweep of 1 GiB, read-only sweeps of 8 and 64 regions at the same
+    offset, and a bf16 sum of 8 regions of 128 MiB into one (the reductions' patterns), each the
+    best over grids of 1 024 and 2 048 workgroups and of one wavefront per chunk, chunks of 8 and
+    32 KiB (4 KiB per region for the multi-region kernels) and 4 or 8 vectors per lane per step;
+    and the library's own copy path on the same copy."""
     import torch
 
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_00358_amd", "lib", "libbench_stream.so"))
-    lib.bench_stream.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
-                                 ctypes.c_int, ctypes.c_void_p]
+    lib.bench_stream.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
+                                 ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p]
+    lib.bench_stream_multi.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
+                                       ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p]
+    lib.bench_stream_reduce.argtypes = lib.bench_stream_multi.argtypes
     a = torch.empty(nbytes, dtype=torch.uint8, device=device).fill_(7)
     b = torch.empty_like(a)
     st = torch.cuda.current_stream().cuda_stream
-    out = {"workload": "1 GiB contiguous copy / read / write, non-temporal 16-byte accesses, 8 KiB per wavefront step"}
+    out = {"workload": "1 GiB contiguous copy / read / write, 8 or 64 regions read, 8 x 128 MiB bf16 summed "
+                       "into 128 MiB; non-temporal 16-byte loads"}
+
+    def best_of(shapes, moved, launch, name):
+        best = (0.0, None)
+        for shape in shapes:
+            def run():
+                rc = launch(*shape)
+                if rc != 0:
+                    raise RuntimeError(f"{name} failed ({rc})")
+            for _ in range(3):
+                run()
+            ms = _time_events(run, iters)
+            best = max(best, (moved / (ms * 1e-3) / 1e9, shape), key=lambda x: x[0])
+        return best
+
     for kind, name, moved in ((0, "copy", 2 * nbytes), (1, "read", nbytes), (2, "write", nbytes)):
-        best = (0.0, 0)
-        for blocks in (256, 512, 1024, 2048):
-            def run():
-                rc = lib.bench_stream(kind, a.data_ptr(), b.data_ptr(), nbytes, 8192, blocks, st)
-                if rc != 0:
-                    raise RuntimeError(f"bench_stream failed ({rc})")
-            for _ in range(3):
-                run()
-            ms = _time_events(run, iters)
-            best = max(best, (moved / (ms * 1e-3) / 1e9, blocks))
-        out[f"stream_{name}_gbs"], out[f"stream_{name}_blocks"] = round(best[0], 1), best[1]
-    # the reductions' access pattern: the same offset of 8 or 64 regions in turn, 4 KiB each
-    lib.bench_stream_multi.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
-                                       ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p]
+        shapes = [(u, ch, bl) for u in (4, 8) for ch in (8192, 32768) for bl in (1024, 2048, nbytes // ch // 4)]
+        gbs, (u, ch, bl) = best_of(shapes, moved, lambda u, ch, bl: lib.bench_stream(
+            kind, u, a.data_ptr(), b.data_ptr(), nbytes, ch, bl, st), name)
+        out[f"stream_{name}_gbs"] = round(gbs, 1)
+        out[f"stream_{name}_shape"] = {"unroll": u, "chunk_bytes": ch, "blocks": bl}
     for streams in (8, 64):
-        best = (0.0, 0)
-        for blocks in (256, 512, 1024, 2048):
-            def run():
-                rc = lib.bench_stream_multi(a.data_ptr(), b.data_ptr(), nbytes, streams, 4096, blocks, st)
-                if rc != 0:
-                    raise RuntimeError(f"bench_stream_multi failed ({rc})")
-            for _ in range(3):
-                run()
-            ms = _time_events(run, iters)
-            best = max(best, (nbytes / (ms * 1e-3) / 1e9, blocks))
-        out[f"stream_read_{streams}_regions_gbs"], out[f"stream_read_{streams}_regions_blocks"] = round(best[0], 1), best[1]
+        shapes = [(bl,) for bl in (256, 512, 1024, 2048, nbytes // streams // 4096 // 4)]
+        gbs, (bl,) = best_of(shapes, nbytes, lambda bl: lib.bench_stream_multi(
+            a.data_ptr(), b.data_ptr(), nbytes, streams, 4096, bl, st), f"read of {streams} regions")
+        out[f"stream_read_{streams}_regions_gbs"], out[f"stream_read_{streams}_regions_blocks"] = round(gbs, 1), bl
+    region = nbytes // 8
+    shapes = [(bl,) for bl in (1024, 2048, 4096, region // 4096 // 4)]
+    gbs, (bl,) = best_of(shapes, 9 * region, lambda bl: lib.bench_stream_reduce(
+        a.data_ptr(), b.data_ptr(), region, 8, 4096, bl, st), "reduce of 8 regions")
+    out["stream_reduce_8_regions_gbs"], out["stream_reduce_8_regions_blocks"] = round(gbs, 1), bl
     torch.cuda.synchronize()
     del a, b
     ex = bench_executor_copy(device, iters=iters, nbytes=nbytes)
@@ -1179,6 +1188,8 @@ def main():
         _log("c3 ring reduce-scatter")
         c3, rs_send, rs_recv = bench_reduce_scatter_c3(device)
         extras["reduce_scatter_ring_p8_bf16"] = c3
+        if not args.headline_only and "stream_reduce_8_regions_gbs" in line.get("copy_ceiling", {}):
+            c3["frac_of_stream_reduce"] = round(c3["gbs"] / line["copy_ceiling"]["stream_reduce_8_regions_gbs"], 4)
         _log(f"c3 {c3['gbs']:.1f} GB/s")
         if not args.no_overlap:
             _log("c5a overlap")

@@ -34,11 +34,16 @@ constexpr uint32_t kDefaultDependentTileBytes = 128u * 1024u;
 constexpr uint32_t kMinDependentTileBytes = 32u * 1024u;
 constexpr uint64_t kDependentMinTiles = 1024;
 // A copy to this many destinations or more reads up to 32 KiB per tile, as long as its phase
-// keeps about 1024 tiles (an all-gather of P = 64 x 512 KiB bf16 blocks: 8 KiB tiles 520 us,
-// 16 KiB 407 us, 32 KiB 367-380 us, 64 KiB 387 us, 128 KiB (256 tiles) 720 us).
+// keeps about 256 tiles: each tile writes its bytes to every destination, so a few long tiles
+// beat many short ones. Measured with one wavefront per tile on the copy phase of the two-level
+// all-reduce of 64 ranks (every 1/64 sub-shard to 63 ranks): tiles of the phase's bytes / 1024
+// -> / 256 took 8 MiB per rank 222 -> 183 us, 4 MiB 109 -> 102 us; at 32 MiB per rank 32 KiB
+// tiles (1 024) 736-754 us against 64 KiB 745-762 us and 128 KiB 819-836 us; the all-gather of
+// P = 64 x 512 KiB bf16 blocks 396-400 us with 32 KiB tiles, 418-424 with 64 KiB, 543-550 with
+// 128 KiB, 515-525 with 8 KiB.
 constexpr size_t kWideCopyDsts = 8;
 constexpr uint64_t kWideCopyTileBytes = 32u * 1024u;
-constexpr uint64_t kWideCopyTargetTiles = 1024;
+constexpr uint64_t kWideCopyTargetTiles = 256;
 // Small collectives are latency bound: cut them into at least this many tiles (down to
 // one vector per lane) so that many wavefronts share the work.
 constexpr uint64_t kSmallTargetTiles = 2048;

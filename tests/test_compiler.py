@@ -517,8 +517,8 @@ def test_wide_allreduce_splits_its_copies_only_when_large(kib, split):
     if split:
         assert info["num_phases"] == 2
         assert info["bytes_read"] == (P + 1) * N * 2 and info["bytes_written"] == P * N * 2
-        # the wide copies read up to 32 KiB per tile, in about 1024 tiles
-        assert info["step_tile_max"] == max(8192, min(32768, N * 2 // 1024)) // 2
+        # the wide copies read up to 32 KiB per tile, in at least about 256 tiles
+        assert info["step_tile_max"] == max(8192, min(32768, N * 2 // 256)) // 2
     else:
         assert info["num_phases"] == 1
         assert info["bytes_read"] == P * N * 2 and info["bytes_written"] == P * N * 2
@@ -556,11 +556,12 @@ def test_phase_mode_is_part_of_the_cached_program():
             H.hccl_allreduce(c.handle, s, r, N, "fp32")
 
 
-def test_wide_copies_keep_about_1024_tiles():
-    """Forced split (phases=levels) at 4 MiB per rank: the wide copies shrink their tiles to keep
-    the copy phase parallel (8 KiB at the least)."""
-    P, N = 64, 4 * (1 << 20) // 2
+@pytest.mark.parametrize("mib,tile_kib", [(1, 8), (4, 16), (8, 32), (32, 32)])
+def test_wide_copies_keep_about_256_tiles(mib, tile_kib):
+    """Forced split (phases=levels): the wide copies read the phase's copy bytes / 256 per tile,
+    at least 8 KiB and at most 32 KiB."""
+    P, N = 64, mib * (1 << 20) // 2
     with comm(P, algo="two_level", group_size=8, phases="levels") as c:
         H.hccl_allreduce(c.handle, fake_bufs(P, 1 << 40), fake_bufs(P, 1 << 44), N, "bf16")
         info = info_of(c)
-    assert info["num_phases"] == 2 and info["step_tile_max"] == 8192 // 2
+    assert info["num_phases"] == 2 and info["step_tile_max"] == tile_kib * 1024 // 2
