@@ -50,11 +50,12 @@ constexpr uint64_t kSmallTargetTiles = 2048;
 constexpr uint32_t kWaveStepElems = kWaveSize * kVecElems;  // 512: one vector per lane
 constexpr uint64_t kShardAlignElems = 64;                      // 128 B of bf16, 256 B of fp32
 // Static tiles (slots) of the copy step of an AllToAllvDynamic: slot k moves dynamic tiles k,
-// k + slots, ... Every slot plans the exchange once, so the slots of a launch should fit in
-// one round of its wavefronts (7 168 for the dynamic kernel on a whole MI355X): rows + ids of
-// the 8-rank 2^18-row exchange took 201-203 us with 8 192 + 1 088 slots, 197-198 us with
-// 4 096 + 1 088 or 6 080 + 1 088, and 203-205 us with 7 168 + 1 088 (two rounds again).
-constexpr uint32_t kDynamicSlots = 4096;
+// k + slots, ... Every slot plans the exchange itself, so more slots cost more for an exchange
+// far below its capacities, while fewer leave each slot a longer run of tiles. The launch has
+// one wavefront per slot; rows + ids of the 8-rank 2^18-row exchange, full / all counts zero:
+// 4 096 + 1 088 slots 197-198 / 8 us, 16 384 + 1 088 194 / 14 us, 32 768 + 1 088 192-193 /
+// 23-24 us, 65 536 + 1 088 190 / 44 us.
+constexpr uint32_t kDynamicSlots = 32768;
 
 // Type of partials that leave registers: FP32 for floating sums (one rounding at the end),
 // the buffer type when every partial is re-quantised, or for MAX / MIN (exact in any type).

@@ -371,7 +371,7 @@ def test_incompatible_orders_and_schedules_are_rejected():
 def dyn_slots(P, send_cap, R, es, tile_bytes=8192):
     te = max(512, (tile_bytes // es) // 512 * 512)
     bound = P * (ceil_div(send_cap * R, te) + P)
-    return max(1, min(4096, bound))
+    return max(1, min(32768, bound))
 
 
 META = 1 << 47   # fake device metadata arrays, far from the data buffers
