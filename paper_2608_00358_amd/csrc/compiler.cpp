@@ -474,7 +474,10 @@ void lower_two_level(const CollectiveSpec& s, HostProgram& p) {
 // ------------------------------------------------------------------------- ALLTOALLV
 // Every non-empty (source, destination) block becomes COPY steps of at most one chunk; the
 // steps are ordered largest first so the long blocks start early (Section IV-A: AllToAllv
-// spread across parallel engines).
+// spread across parallel engines), and equal ones destination by destination: launches start
+// their tiles in program order, so at any moment the chip fills one receive buffer in order
+// while it reads from every send buffer (grouped AllToAllv of 8 ranks x 2^18 embedding rows,
+// source-major 182.8-184.2 us, destination-major 181.0-182.5 us).
 void lower_alltoallv(const CollectiveSpec& s, HostProgram& p) {
     Builder b{p};
     const int P = s.P;
@@ -482,8 +485,8 @@ void lower_alltoallv(const CollectiveSpec& s, HostProgram& p) {
     const uint64_t C = chunk_elems(s);
     struct Piece { int src, dst; uint64_t so, ro, n; };
     std::vector<Piece> pieces;
-    for (int src = 0; src < P; ++src) {
-        for (int dst = 0; dst < P; ++dst) {
+    for (int dst = 0; dst < P; ++dst) {
+        for (int src = 0; src < P; ++src) {
             uint64_t n = s.sendcounts[(size_t)src * P + dst];
             uint64_t so = s.sdispls[(size_t)src * P + dst];
             uint64_t ro = s.rdispls[(size_t)dst * P + src];
