@@ -467,6 +467,10 @@ hcclResult_t resident_submit(hcclComm* c, const LaunchArgs& a, DeviceProgram* dp
     return hcclSuccess;
 }
 
+// Largest grid of one wavefront per tile: a program has under 2^31 tiles, so the kernel's tile
+// numbers (t + W, 32 bits) cannot wrap; larger phases loop as a resident grid does.
+constexpr uint32_t kMaxGridWorkers = 1u << 24;
+
 // Executor kernel and grid of a launch: the leanest kernel that covers the program (the aligned
 // copy kernel only if every user buffer is 16-byte aligned), and its grid, capped by the
 // configuration and by the tiles of the phase.
@@ -481,8 +485,6 @@ hcclResult_t resident_submit(hcclComm* c, const LaunchArgs& a, DeviceProgram* dp
 //    waits for lower tiles, and static dispatch relies on the whole grid being resident; a
 //    triggered launch holds its CUs while it waits; a traced launch records wavefront numbers.
 // Sets a.nworkers and `blocks`; returns the kernel kind.
-constexpr uint32_t kMaxGridWorkers = 1u << 24;
-
 int launch_shape(hcclComm* c, const HostProgram& prog, uint32_t phase, LaunchArgs& a, uint32_t nuser, hipStream_t s,
                  uint32_t& blocks) {
     const uint32_t wpb = (uint32_t)executor_waves_per_block();
@@ -499,8 +501,6 @@ int launch_shape(hcclComm* c, const HostProgram& prog, uint32_t phase, LaunchArg
     const uint32_t tiles = a.tile_end - a.tile_begin;
     uint32_t slots = cus * (uint32_t)std::max(1, c->blocks_per_cu[kind]) * wpb;
     const bool never_waits = (prog.flags & PF_HAS_DEPS) == 0 && a.wait_addr == nullptr && !a.dynamic && !a.trace;
-    // at most 2^24 wavefronts: a program has under 2^31 tiles, so the kernel's tile numbers
-    // (t + W, 32 bits) cannot wrap; larger phases loop as a resident grid does
     if (never_waits) slots = std::max(slots, std::min<uint32_t>(tiles, kMaxGridWorkers));
     if (c->cfg.max_workers > 0) slots = std::min<uint32_t>(slots, (uint32_t)c->cfg.max_workers);
     uint32_t workers = std::min<uint32_t>(slots, tiles);
