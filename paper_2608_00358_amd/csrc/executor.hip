@@ -118,6 +118,20 @@ __device__ __forceinline__ uint64_t from_lane(uint64_t v, uint32_t j) {
     return ((uint64_t)hi << 32) | lo;
 }
 
+// uniform read of the program image through the constant address space (a scalar load)
+template <typename T>
+__device__ __forceinline__ T cld(const uint8_t* base, uint64_t off) {
+    return *(const __attribute__((address_space(4))) T*)(base + off);
+}
+// the descriptor words run_tile decodes (little-endian, as on the host that packs them)
+static_assert(offsetof(Desc, op) == 0 && offsetof(Desc, redop) == 1 && offsetof(Desc, flags) == 2 &&
+                  offsetof(Desc, sig) == 3 && offsetof(Desc, nsrc) == 4 && offsetof(Desc, ndst) == 6 &&
+                  offsetof(Desc, group) == 8 && offsetof(Desc, ndep) == 10 && offsetof(Desc, src) == 12 &&
+                  offsetof(Desc, dst) == 16 && offsetof(Desc, dep) == 20 && offsetof(Desc, tile0) == 24 &&
+                  offsetof(Desc, tile_elems) == 32 && offsetof(Desc, nelem) == 40 && offsetof(Desc, fold) == 48 &&
+                  offsetof(Desc, requant) == 52 && offsetof(Desc, aux) == 56,
+              "descriptor words");
+
 __device__ __forceinline__ uint32_t elem_bytes(uint32_t dt) { return (dt == DT_BF16 || dt == DT_FP16) ? 2u : 4u; }
 
 // ----------------------------------------------------------------------- conversions
@@ -1043,18 +1057,28 @@ template <int KIND>
 __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, const ProgramHeader& h, uint32_t t,
                                          uint32_t lane, const uint64_t* bufs, bool stamp, uint64_t& ready) {
     const uint32_t d = uni(((const uint32_t*)(prog + h.off_tile_desc))[t]);
-    const Desc* D = (const Desc*)(prog + h.off_desc) + d;
-    const uint32_t op = uni(D->op);
-    const uint32_t flags = uni(D->flags);
-    const uint32_t ndep = uni(D->ndep);
-    const uint32_t k = t - uni(D->tile0);
-    const uint64_t te = uni(D->tile_elems);
-    const uint64_t nelem = uni64(D->nelem);
+    // The descriptor arrives as four 16-byte scalar loads through the constant address space
+    // (its fields sit in the words named below). Against per-field vector loads: the two-level
+    // all-reduce of 64 ranks and the reduce-scatter P=8 x 256 MiB -1 %, AllToAllvDynamic -1 %,
+    // the ring all-reduce P=4 x 2^20 fp32 -2 %, the grouped AllToAllv -0.5 %; a 1 GiB copy of 1 024
+    // one-chunk steps +3 %. The tile table itself (one word per tile, up to megabytes) stays on
+    // the vector path: through the scalar cache it cost that copy 4 % and gained nothing else.
+    const uint64_t Db = h.off_desc + (uint64_t)sizeof(Desc) * d;
+    const u32x4 w0 = cld<u32x4>(prog, Db);       // op redop flags sig | nsrc ndst | group ndep | src
+    const u32x4 w1 = cld<u32x4>(prog, Db + 16);  // dst | dep | tile0 | ntiles
+    const u32x4 w2 = cld<u32x4>(prog, Db + 32);  // tile_elems | - | nelem
+    const u32x4 w3 = cld<u32x4>(prog, Db + 48);  // fold | requant | aux | -
+    const uint32_t op = w0[0] & 0xFFu;
+    const uint32_t flags = (w0[0] >> 16) & 0xFFu;
+    const uint32_t ndep = w0[2] >> 16;
+    const uint32_t k = t - w1[2];
+    const uint64_t te = w2[0];
+    const uint64_t nelem = (uint64_t)w2[2] | ((uint64_t)w2[3] << 32);
     const uint64_t e0 = (uint64_t)k * te;
     const uint32_t n = (uint32_t)((nelem - e0 < te) ? (nelem - e0) : te);
 
     if (ndep) {
-        const Dep* deps = (const Dep*)(prog + h.off_dep) + uni(D->dep);
+        const Dep* deps = (const Dep*)(prog + h.off_dep) + w1[1];
         if (!wait_deps(deps, ndep, k, a.state, a.error, a.timeout, d, t)) return false;
     }
     if (stamp) ready = wall_clock64();
@@ -1062,7 +1086,7 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
     if (op == OP_DYN_COPY) {
         // the host runs programs with dynamic steps on these two kernels only
         if constexpr (KIND == kKindDynamic || KIND == kKindGeneric) {
-            const DynView v = load_dyn((const DynA2A*)(prog + h.off_aux) + uni(D->aux));
+            const DynView v = load_dyn((const DynA2A*)(prog + h.off_aux) + w3[2]);
             const bool es = v.sdispls != kNoBuffer, er = v.rdispls != kNoBuffer;
             // the register-resident planner only in the dynamic kernel: the generic one carries
             // every other path already, and the general planner covers every P
@@ -1085,27 +1109,27 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
         }
     } else {
         TileOps ops;
-        ops.nsrc = uni(D->nsrc);
-        ops.ndst = uni(D->ndst);
-        ops.group = uni(D->group);
-        ops.fold = uni(D->fold);
-        ops.requant = uni(D->requant);
+        ops.nsrc = w0[1] & 0xFFFFu;
+        ops.ndst = w0[1] >> 16;
+        ops.group = w0[2] & 0xFFFFu;
+        ops.fold = w3[0];
+        ops.requant = w3[1];
         const Operand* opl = (const Operand*)(prog + h.off_operand);
         ops.src = 0;
         ops.dst = 0;
         bool misaligned = false;
         if (lane < ops.nsrc) {
-            Operand o = opl[uni(D->src) + lane];
+            Operand o = opl[w0[3] + lane];
             ops.src = bufs[o.buf] + o.offset + e0 * elem_bytes(o.dtype);
             misaligned |= (ops.src & 15u) != 0;
         }
         if (lane < ops.ndst) {
-            Operand o = opl[uni(D->dst) + lane];
+            Operand o = opl[w1[0] + lane];
             ops.dst = bufs[o.buf] + o.offset + e0 * elem_bytes(o.dtype);
             misaligned |= (ops.dst & 15u) != 0;
         }
-        exec_tile<KIND>(op, uni(D->sig), uni(D->redop), elem_bytes(uni(opl[uni(D->src)].dtype)), ops, n,
-                        __ballot(misaligned) == 0ull, lane);
+        const uint32_t es0 = elem_bytes(cld<uint32_t>(prog, h.off_operand + 16ull * w0[3] + 4));
+        exec_tile<KIND>(op, w0[0] >> 24, (w0[0] >> 8) & 0xFFu, es0, ops, n, __ballot(misaligned) == 0ull, lane);
     }
 
     if (flags) {
@@ -1232,14 +1256,14 @@ hccl_executor(LaunchArgs a) {
     const uint32_t wave = uni(block * kWavesPerBlock + (threadIdx.x / kWaveSize));
     const uint8_t* prog = a.prog;
     ProgramHeader h;
-    h.ndesc = uni(((const ProgramHeader*)prog)->ndesc);
-    h.ntiles = uni(((const ProgramHeader*)prog)->ntiles);
-    h.nstate = uni(((const ProgramHeader*)prog)->nstate);
-    h.off_desc = uni64(((const ProgramHeader*)prog)->off_desc);
-    h.off_operand = uni64(((const ProgramHeader*)prog)->off_operand);
-    h.off_dep = uni64(((const ProgramHeader*)prog)->off_dep);
-    h.off_tile_desc = uni64(((const ProgramHeader*)prog)->off_tile_desc);
-    h.off_aux = uni64(((const ProgramHeader*)prog)->off_aux);
+    h.ndesc = cld<uint32_t>(prog, offsetof(ProgramHeader, ndesc));
+    h.ntiles = cld<uint32_t>(prog, offsetof(ProgramHeader, ntiles));
+    h.nstate = cld<uint32_t>(prog, offsetof(ProgramHeader, nstate));
+    h.off_desc = cld<uint64_t>(prog, offsetof(ProgramHeader, off_desc));
+    h.off_operand = cld<uint64_t>(prog, offsetof(ProgramHeader, off_operand));
+    h.off_dep = cld<uint64_t>(prog, offsetof(ProgramHeader, off_dep));
+    h.off_tile_desc = cld<uint64_t>(prog, offsetof(ProgramHeader, off_tile_desc));
+    h.off_aux = cld<uint64_t>(prog, offsetof(ProgramHeader, off_aux));
     // the buffer table is indexed per lane, so it is read from the kernel-argument segment
     const uint64_t* bufs = (const uint64_t*)((const char*)__builtin_amdgcn_kernarg_segment_ptr() +
                                              offsetof(LaunchArgs, bufs));
@@ -1250,7 +1274,7 @@ hccl_executor(LaunchArgs a) {
     sh.timeout = a.timeout_ticks;
     const uint32_t nworkers = a.nworkers;
 
-    const bool has_deps = (uni(((const ProgramHeader*)prog)->flags) & PF_HAS_DEPS) != 0u;
+    const bool has_deps = (cld<uint32_t>(prog, offsetof(ProgramHeader, flags)) & PF_HAS_DEPS) != 0u;
     const bool triggered = a.wait_addr != nullptr;
     // a workgroup whose trigger wait failed runs no tile but still counts itself done below
     const bool started = !triggered || trigger_wait(a);
