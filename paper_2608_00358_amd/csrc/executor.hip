@@ -1239,10 +1239,15 @@ __device__ __forceinline__ bool trigger_wait(const LaunchArgs& a) {
     return go != 0u;
 }
 
-// Four waves per SIMD for the specialised kernels; the generic kernel (every fold, mixed types)
-// may use more registers rather than spill.
+// At least four waves per SIMD for the specialised kernels, five for the 16-bit SUM reductions
+// (they fit in 96 VGPRs without spilling: the reduce-scatter P=8 x 256 MiB bf16 confined to 16
+// CUs, where few wavefronts carry every tile, 2.85 -> 2.70 ms; on the whole chip no change);
+// the generic kernel (every fold, mixed types) may use more registers rather than spill.
 template <int KIND>
-__global__ void __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(KIND == kKindGeneric ? 3 : 4)))
+constexpr int kMinWavesPerEu = KIND == kKindGeneric ? 3 : (KIND == SIG_BF16 || KIND == SIG_FP16) ? 5 : 4;
+
+template <int KIND>
+__global__ void __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(kMinWavesPerEu<KIND>)))
 hccl_executor(LaunchArgs a) {
     const uint32_t lane = __lane_id();
     // The hardware deals workgroups to the XCDs in turn (block b to XCD b mod 8). With xcd_order
