@@ -1,13 +1,14 @@
-// executor.hip -- the persistent descriptor executor for gfx950 (MI355X).
+// executor.hip -- the descriptor executor for gfx950 (MI355X).
 //
-// One launch runs one program (the single-GPU form of a work packet; paper, Section III-B-2).
-// Every wavefront is an independent worker, the analogue of a message engine's control core
-// (Section II-A-2: fetch the graph, evaluate dependencies, issue the work): it runs tiles w,
-// w + W, ... of the program (or takes them by ticket on request), waits for each tile's
-// dependencies, performs the copy or reduction of the tile with 128-bit coalesced loads and
-// stores (the near-memory-compute analogue: FP32 arithmetic, one rounding to the buffer type),
-// and signals completion with monotonically growing counters (the signal pairs of Section
-// III-B-2). A launch may first wait on a trigger word (Section IV-B-3), and an AllToAllvDynamic
+// One launch runs one phase of a program (the single-GPU form of a work packet; paper, Section
+// III-B-2). Every wavefront is an independent worker, the analogue of a message engine's
+// control core (Section II-A-2: fetch the graph, evaluate dependencies, issue the work): it
+// runs tile w of the phase when the grid has one wavefront per tile (a launch in which no tile
+// waits), else tiles w, w + W, ... of a grid the CUs hold at once (or takes them by ticket on
+// request), waits for each tile's dependencies, performs the copy or reduction of the tile
+// with 128-bit coalesced loads and stores (the near-memory-compute analogue: FP32 arithmetic,
+// one rounding to the buffer type), and signals completion with monotonically growing
+// counters (the signal pairs of Section III-B-2). A launch may first wait on a trigger word (Section IV-B-3), and an AllToAllvDynamic
 // step plans its layout on the device (Section IV-B-2).
 //
 // Memory model: dependency counters are written with agent-scope release and read with
