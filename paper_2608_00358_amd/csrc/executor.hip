@@ -804,21 +804,23 @@ struct DynView {     // a DynA2A record loaded into scalar registers
     uint64_t row_elems, send_cap, recv_cap, tile_elems;
 };
 
-__device__ __forceinline__ DynView load_dyn(const DynA2A* r) {
+// The record at byte `off` of the program image, read through the constant address space
+// (scalar loads; records are 8-byte aligned, so 4- and 8-byte fields).
+__device__ __forceinline__ DynView load_dyn(const uint8_t* prog, uint64_t off) {
     DynView v;
-    v.P = uni(r->P);
-    v.es = uni(r->elem_bytes);
-    v.send0 = uni(r->send0);
-    v.recv0 = uni(r->recv0);
-    v.counts = uni(r->counts);
-    v.sdispls = uni(r->sdispls);
-    v.rdispls = uni(r->rdispls);
-    v.recvcounts = uni(r->recvcounts);
-    v.slots = uni(r->slots);
-    v.row_elems = uni64(r->row_elems);
-    v.send_cap = uni64(r->send_cap);
-    v.recv_cap = uni64(r->recv_cap);
-    v.tile_elems = uni64(r->tile_elems);
+    v.P = cld<uint32_t>(prog, off + offsetof(DynA2A, P));
+    v.es = cld<uint32_t>(prog, off + offsetof(DynA2A, elem_bytes));
+    v.send0 = cld<uint32_t>(prog, off + offsetof(DynA2A, send0));
+    v.recv0 = cld<uint32_t>(prog, off + offsetof(DynA2A, recv0));
+    v.counts = cld<uint32_t>(prog, off + offsetof(DynA2A, counts));
+    v.sdispls = cld<uint32_t>(prog, off + offsetof(DynA2A, sdispls));
+    v.rdispls = cld<uint32_t>(prog, off + offsetof(DynA2A, rdispls));
+    v.recvcounts = cld<uint32_t>(prog, off + offsetof(DynA2A, recvcounts));
+    v.slots = cld<uint32_t>(prog, off + offsetof(DynA2A, slots));
+    v.row_elems = cld<uint64_t>(prog, off + offsetof(DynA2A, row_elems));
+    v.send_cap = cld<uint64_t>(prog, off + offsetof(DynA2A, send_cap));
+    v.recv_cap = cld<uint64_t>(prog, off + offsetof(DynA2A, recv_cap));
+    v.tile_elems = cld<uint64_t>(prog, off + offsetof(DynA2A, tile_elems));
     return v;
 }
 
@@ -1088,7 +1090,7 @@ __device__ __forceinline__ bool run_tile(const Shared& a, const uint8_t* prog, c
     if (op == OP_DYN_COPY) {
         // the host runs programs with dynamic steps on these two kernels only
         if constexpr (KIND == kKindDynamic || KIND == kKindGeneric) {
-            const DynView v = load_dyn((const DynA2A*)(prog + h.off_aux) + w3[2]);
+            const DynView v = load_dyn(prog, h.off_aux + (uint64_t)sizeof(DynA2A) * w3[2]);
             const bool es = v.sdispls != kNoBuffer, er = v.rdispls != kNoBuffer;
             // the register-resident planner only in the dynamic kernel: the generic one carries
             // every other path already, and the general planner covers every P
@@ -1486,15 +1488,15 @@ hccl_resident(ResidentArgs r) {
         const LaunchArgs& a = *(const LaunchArgs*)pk;
         const uint8_t* prog = a.prog;
         ProgramHeader h;
-        h.ndesc = uni(((const ProgramHeader*)prog)->ndesc);
-        h.ntiles = uni(((const ProgramHeader*)prog)->ntiles);
-        h.nstate = uni(((const ProgramHeader*)prog)->nstate);
-        h.off_desc = uni64(((const ProgramHeader*)prog)->off_desc);
-        h.off_operand = uni64(((const ProgramHeader*)prog)->off_operand);
-        h.off_dep = uni64(((const ProgramHeader*)prog)->off_dep);
-        h.off_tile_desc = uni64(((const ProgramHeader*)prog)->off_tile_desc);
-        h.off_aux = uni64(((const ProgramHeader*)prog)->off_aux);
-        const bool has_deps = (uni(((const ProgramHeader*)prog)->flags) & PF_HAS_DEPS) != 0u;
+        h.ndesc = cld<uint32_t>(prog, offsetof(ProgramHeader, ndesc));
+        h.ntiles = cld<uint32_t>(prog, offsetof(ProgramHeader, ntiles));
+        h.nstate = cld<uint32_t>(prog, offsetof(ProgramHeader, nstate));
+        h.off_desc = cld<uint64_t>(prog, offsetof(ProgramHeader, off_desc));
+        h.off_operand = cld<uint64_t>(prog, offsetof(ProgramHeader, off_operand));
+        h.off_dep = cld<uint64_t>(prog, offsetof(ProgramHeader, off_dep));
+        h.off_tile_desc = cld<uint64_t>(prog, offsetof(ProgramHeader, off_tile_desc));
+        h.off_aux = cld<uint64_t>(prog, offsetof(ProgramHeader, off_aux));
+        const bool has_deps = (cld<uint32_t>(prog, offsetof(ProgramHeader, flags)) & PF_HAS_DEPS) != 0u;
         uint32_t* const state = a.state;
         const uint64_t* bufs = pk + offsetof(LaunchArgs, bufs) / 8;
         Shared sh;

@@ -11,6 +11,7 @@ from hypothesis import HealthCheck, given, settings
 from hypothesis import strategies as st
 
 import paper_2608_00358_amd as H
+from program_interpreter import Program
 
 ES = {"bf16": 2, "fp16": 2, "fp32": 4, "int32": 4}
 SETTINGS = settings(max_examples=120, deadline=None, suppress_health_check=[HealthCheck.too_slow])
@@ -83,6 +84,26 @@ def test_every_accepted_reduction_validates(case):
             assert info["num_deps"] == 0
         if case["phases"] == "one":
             assert info["num_phases"] == 1
+        check_tile_layout(Program(H.hccl_comm_program_image(c.handle)))
+
+
+def check_tile_layout(prog):
+    """Inside each phase the descriptors own consecutive runs of tiles, in descriptor order, each
+    run starting at the descriptor's tile0 and as long as its ntiles (so in a phase whose
+    descriptors all have K tiles, tile t belongs to descriptor d0 + (t - t0) // K)."""
+    for q in range(len(prog.phase_tile) - 1):
+        t0, t1 = int(prog.phase_tile[q]), int(prog.phase_tile[q + 1])
+        if t0 == t1:
+            continue
+        owners = prog.tile_desc[t0:t1].astype(np.int64)
+        d0, d1 = int(owners[0]), int(owners[-1]) + 1
+        assert (np.diff(owners) >= 0).all() and (np.diff(owners) <= 1).all()
+        for d in range(d0, d1):
+            assert int(prog.descs[d]["tile0"]) == t0 + int(np.searchsorted(owners, d))
+            assert int(prog.descs[d]["ntiles"]) == int((owners == d).sum())
+        K = prog.descs[d0:d1]["ntiles"]
+        if (K == K[0]).all():
+            assert np.array_equal(owners, d0 + (np.arange(t1 - t0) // int(K[0])))
 
 
 @st.composite
