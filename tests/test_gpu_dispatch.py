@@ -134,3 +134,33 @@ def test_grid_of_programs_that_never_wait(algo, max_workers):
         assert info["workers"] == max_workers
     run_reduce_scatter(8, 70001, "fp32", **cfg)
     run_alltoallv(8, zipf_counts(8, 3000, 1.1, seed=5), 129, "bf16", max_workers=max_workers)
+
+
+def test_triggered_launch_keeps_a_grid_the_cus_hold():
+    """A triggered launch holds its workgroups at the trigger, so its grid stays within what the
+    CUs hold at once; the same program launched untriggered gets one wavefront per tile. Both
+    give the oracle's bits (the trigger word is already set: nothing waits)."""
+    P, N = 8, 1 << 22  # 4 KiB tiles: 8 192 tiles, more than the chip holds at once
+    x = inputs(P, N, "bf16", 24)
+    want = oracle.allreduce(x, "bf16")
+    flag = torch.ones(1, dtype=torch.int64, device="cuda:0")
+    print("dispatch: triggered against untriggered grid", flush=True)
+    with H.Comm(P, device=0, algo="direct", tile_bytes=4096) as c:
+        send = [to_device(x[r], "bf16") for r in range(P)]
+        for triggered in (False, True):
+            recv = [torch.empty(N, dtype=torch.bfloat16, device="cuda:0") for _ in range(P)]
+            if triggered:
+                with c.triggered(wait=(flag, "eq", 1)):
+                    c.allreduce(send, recv)
+            else:
+                c.allreduce(send, recv)
+            torch.cuda.synchronize()
+            assert c.async_error() == 0
+            info = c.last_program()
+            if triggered:
+                assert 0 < info["workers"] < info["num_tiles"]
+            else:
+                assert info["workers"] >= info["num_tiles"]
+            for r in range(P):
+                got = to_host(recv[r], "bf16")
+                assert same_bits(got, want[r], "bf16"), f"triggered={triggered} rank {r}: {first_mismatch(got, want[r])}"
