@@ -165,6 +165,13 @@ struct DynA2A {            // 72 bytes
 static_assert(sizeof(DynA2A) == 72, "auxiliary record layout");
 
 // Device image: header, then the arrays at the offsets the header records (16-byte aligned).
+// An image never changes while a kernel that may read it runs: the executor reads the header,
+// the descriptors and the AllToAllvDynamic records through the constant address space, whose
+// scalar cache is not kept coherent with writes made during a kernel (each launch starts with
+// it invalidated). A launched executor reads only the image it was given; the resident executor,
+// which outlives many packets, reads images uploaded before their packets were published, and
+// those images are kept until the communicator is destroyed, so no address it has read is
+// reused for another image while it runs.
 struct ProgramHeader {
     uint32_t magic;
     uint32_t version;
