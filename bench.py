@@ -1065,6 +1065,21 @@ def _only_c3(device):
     return res
 
 
+def _only_c5a(device):
+    """The overlap measurement alone: the c3 inputs, every reduce-scatter on the masked stream."""
+    import torch
+
+    from workloads import device_normal_bf16
+
+    P = 8
+    M = (256 * MiB // 2) // P
+    send = device_normal_bf16(P, P * M, std=0.02, seed=0, device=device)
+    recv = [torch.empty(M, dtype=torch.bfloat16, device=device) for _ in range(P)]
+    res = bench_overlap_c5a(device, send, recv)
+    del send, recv
+    return res
+
+
 # single measurements for profiling runs (bench.py --only NAME)
 ONLY = {
     "copy": bench_executor_copy,
@@ -1072,6 +1087,7 @@ ONLY = {
     "c3": _only_c3,
     "c4": lambda d: bench_two_level_c4(d, unfused=False),
     "c4_both": bench_two_level_c4,
+    "c5a": _only_c5a,
     "c5b": bench_latency_c5b,
     "orders": bench_forwarded_partials,
     "ceiling": bench_copy_ceiling,
