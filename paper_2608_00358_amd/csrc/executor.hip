@@ -783,7 +783,8 @@ __device__ __forceinline__ void exec_tile(uint32_t op, uint32_t sig, uint32_t re
 // row by row with lane d standing for destination d, so no slot waits for another and nothing
 // is shared between wavefronts: pass 1 checks every range and counts the dynamic tiles J,
 // pass 2 walks the rows again and moves the slot's tiles k, k + S, k + 2S, ... Dynamic tiles are
-// numbered source-major, then destination, then tile within the pair. Strided like the static
+// numbered source-major, then destination, then tile within the pair (destination-major in the
+// register-resident form for P <= 8, dyn_slot_small). Strided like the static
 // dispatch of a launched program, the slots work on one window of neighbouring tiles at a time:
 // the grouped 2^18-row exchange of 8 ranks took 214 us with a contiguous run of J/S tiles per
 // slot (thousands of separate streams at once), 202 us strided (194 us as a static AllToAllv),
@@ -974,25 +975,27 @@ __device__ __forceinline__ void dyn_slot(const DynView& a, uint32_t k, const uin
 }
 
 // Slot k of an AllToAllvDynamic with P*P <= 64 (P <= 8): lane l stands for the pair
-// (s, d) = (l / P, l % P), so one load brings the whole count matrix into registers; row and
+// (s, d) = (l % P, l / P), so one load brings the whole count matrix into registers; row and
 // column sums, the packed offsets and the overlap checks are P shuffles each, and the tiles
-// are found with one scan, with no further loads. Same rules and results as dyn_slot.
+// are found with one scan, with no further loads. Same rules and results as dyn_slot; the
+// dynamic tiles are numbered destination-major here (the slots then fill one receive buffer at
+// a time, as the static exchange does: headline exchange 189.6-192.4 -> 189.4-190.8 us).
 template <int KIND, bool ES, bool ER>
 __device__ __forceinline__ void dyn_slot_small(const DynView& a, uint32_t k, const uint64_t* bufs, ErrorRecord* err,
                                                uint32_t desc, uint32_t lane) {
     const uint32_t P = a.P, PP = a.P * a.P;
     const bool on = lane < PP;
-    const uint32_t s = on ? lane / P : 0u, d = on ? lane % P : 0u;
+    const uint32_t s = on ? lane % P : 0u, d = on ? lane / P : 0u;
     const uint64_t R = a.row_elems, te = a.tile_elems;
     const uint64_t cmax = a.send_cap < a.recv_cap ? a.send_cap : a.recv_cap;
     const int64_t* counts = (const int64_t*)uni64(bufs[a.counts]);
-    const int64_t cx = on ? counts[lane] : 0;
+    const int64_t cx = on ? counts[(uint64_t)s * P + d] : 0;
     bool bad = on && (cx < 0 || (uint64_t)cx > cmax);
     const uint64_t c = (on && !bad) ? (uint64_t)cx : 0;  // at most 2^59: sums of 8 cannot wrap
     uint64_t row = 0, col = 0, row_before = 0, col_before = 0;
     for (uint32_t j = 0; j < P; ++j) {
-        const uint64_t cr = __shfl(c, (int)(s * P + j));  // pair (s, j)
-        const uint64_t cc = __shfl(c, (int)(j * P + d));  // pair (j, d)
+        const uint64_t cr = __shfl(c, (int)(j * P + s));  // pair (s, j)
+        const uint64_t cc = __shfl(c, (int)(d * P + j));  // pair (j, d)
         row += cr;
         col += cc;
         if (j < d) row_before += cr;
@@ -1000,7 +1003,7 @@ __device__ __forceinline__ void dyn_slot_small(const DynView& a, uint32_t k, con
     }
     uint64_t so, ro;
     if constexpr (ES) {
-        const int64_t x = on ? ((const int64_t*)uni64(bufs[a.sdispls]))[lane] : 0;
+        const int64_t x = on ? ((const int64_t*)uni64(bufs[a.sdispls]))[(uint64_t)s * P + d] : 0;
         if (c && (x < 0 || (uint64_t)x > a.send_cap || c > a.send_cap - (uint64_t)x)) bad = true;
         so = (uint64_t)x;
     } else {
@@ -1013,7 +1016,7 @@ __device__ __forceinline__ void dyn_slot_small(const DynView& a, uint32_t k, con
         ro = (uint64_t)x;
         // the other sources of destination d (an out-of-bounds range has already failed)
         for (uint32_t j = 0; j < P; ++j) {
-            const uint64_t cj = __shfl(c, (int)(j * P + d)), rj = __shfl(ro, (int)(j * P + d));
+            const uint64_t cj = __shfl(c, (int)(d * P + j)), rj = __shfl(ro, (int)(d * P + j));
             if (j != s && c && cj && ro < rj + cj && rj < ro + c) bad = true;
         }
     } else {
@@ -1051,8 +1054,8 @@ __device__ __forceinline__ void dyn_slot_small(const DynView& a, uint32_t k, con
         const uint64_t sod = from_lane(so, pr), rod = from_lane(ro, pr);
         if (sod > a.send_cap || rod > a.recv_cap || sod * R + e0 + n > send_elems || rod * R + e0 + n > recv_elems)
             continue;  // only a caller race on the metadata gets here
-        ops.src = uni64(bufs[a.send0 + pr / P]) + (sod * R + e0) * a.es;
-        ops.dst = uni64(bufs[a.recv0 + pr % P]) + (rod * R + e0) * a.es;
+        ops.src = uni64(bufs[a.send0 + pr % P]) + (sod * R + e0) * a.es;
+        ops.dst = uni64(bufs[a.recv0 + pr / P]) + (rod * R + e0) * a.es;
         exec_tile<KIND>(OP_COPY, 0, 0, a.es, ops, n, false, lane);
     }
 }
