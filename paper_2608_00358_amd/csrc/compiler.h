@@ -166,6 +166,9 @@ bool finalize(HostProgram& prog, uint32_t tile_bytes, std::string& err);
 // Structural checks of a finalized program: dependency order, operand bounds, per-tile
 // dependency shape, data races between steps not ordered by dependencies (with send and
 // receive buffers aliased when in_place), and exact coverage of the collective's output.
-bool validate(const HostProgram& prog, const CollectiveSpec& spec, std::string& err);
+// Programs of at most max_bitset_steps steps keep the dependency closure as bit matrices, larger
+// ones search it pair by pair; both give the same answers.
+bool validate(const HostProgram& prog, const CollectiveSpec& spec, std::string& err,
+              uint32_t max_bitset_steps = 24000);
 
 }  // namespace hccl

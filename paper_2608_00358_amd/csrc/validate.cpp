@@ -57,7 +57,7 @@ std::string fmt(const char* f, unsigned long long a = 0, unsigned long long b = 
 
 }  // namespace
 
-bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err) {
+bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err, uint32_t max_bitset_steps) {
     const int P = p.P;
     const uint32_t D = (uint32_t)p.descs.size();
     const uint32_t nbuf = (uint32_t)(2 * P + 1);
@@ -158,10 +158,36 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
     // ---------------------------------------------------------- dependency closure
     // all[y] has x when every tile of x completes before any tile of y starts; tile[y] has x
     // when tile k of x completes before tile k of y starts (chains of per-tile waits).
+    // Up to max_bitset_steps steps both relations are D x D bit matrices (144 MB at 24 000).
+    // Beyond that a pair is decided by a backward search from the later step over its waits: a
+    // path of per-tile waits alone puts x in tile[y], a path with at least one whole-step wait
+    // puts it in all[y]; the search visits only steps after x, since every wait names an
+    // earlier step.
     bool any_deps = false;
     for (const auto& d : p.descs) any_deps |= !d.deps.empty();
-    const bool closure = any_deps && D <= 24000;
+    const bool closure = any_deps && D <= max_bitset_steps;
     Bits all, tile;
+    std::vector<uint32_t> seen;  // search stamp of (step, whether a whole-step wait was crossed)
+    uint32_t stamp = 0;
+    std::vector<std::pair<uint32_t, bool>> todo;
+    auto search = [&](uint32_t from, uint32_t x, bool& via_all, bool& via_tile) {
+        if (seen.empty()) seen.assign((size_t)2 * D, 0);
+        ++stamp;
+        todo.assign(1, {from, false});
+        while (!todo.empty() && !via_all) {
+            const auto [y, crossed] = todo.back();
+            todo.pop_back();
+            for (const Dep& e : p.descs[y].deps) {
+                const bool c = crossed || e.kind == DEP_ALL;
+                if (e.desc == x) {
+                    (c ? via_all : via_tile) = true;
+                } else if (e.desc > x && seen[(size_t)2 * e.desc + c] != stamp) {
+                    seen[(size_t)2 * e.desc + c] = stamp;
+                    todo.push_back({e.desc, c});
+                }
+            }
+        }
+    };
     if (closure) {
         all.init(D, D);
         tile.init(D, D);
@@ -188,10 +214,17 @@ bool validate(const HostProgram& p, const CollectiveSpec& spec, std::string& err
     auto ordered = [&](const Access& a, const Access& b) {
         // a.desc < b.desc
         if (phased && p.desc_phase[a.desc] < p.desc_phase[b.desc]) return true;
-        if (!closure) return false;
-        if (all.test(b.desc, a.desc)) return true;
+        if (!any_deps) return false;
+        bool via_all, via_tile;
+        if (closure) {
+            via_all = all.test(b.desc, a.desc);
+            via_tile = tile.test(b.desc, a.desc);
+        } else {
+            via_all = via_tile = false;
+            search(b.desc, a.desc, via_all, via_tile);
+        }
         // per-tile order is enough when both walk identical bytes with the same tiling
-        return tile.test(b.desc, a.desc) && a.lo == b.lo && a.es == b.es && a.es != 0;
+        return via_all || (via_tile && a.lo == b.lo && a.es == b.es && a.es != 0);
     };
 
     // ------------------------------------------------------------------ races
