@@ -21,7 +21,8 @@
  *
  * Limits: 1 <= nranks <= HCCL_MAX_RANKS. Element counts are in elements of `dtype`.
  * Buffers must be aligned to their element size; 16-byte aligned buffers take the
- * 128-bit vector path, other alignments are handled element by element.
+ * 128-bit vector path, other alignments a vector path with a head and tail of single
+ * elements where the destinations allow it, else element by element.
  *
  * Calls on one communicator must not run concurrently from several host threads. Calls
  * may be issued on different streams: the library orders a program's launches by itself.

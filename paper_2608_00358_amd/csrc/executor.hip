@@ -615,37 +615,45 @@ __device__ __forceinline__ void copy_elems(const char* src, const TileOps& t, ui
     }
 }
 
-// 16 bytes at a 4-byte-aligned address: one global_load_dwordx4 (global accesses of the HSA
-// target may be unaligned)
+// 16 bytes at an address aligned only to 4 or 2 bytes: one global_load_dwordx4 (global accesses
+// of the HSA target may be unaligned)
 typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+typedef uint32_t u32x4_a2 __attribute__((ext_vector_type(4), aligned(2)));
 
-// Copy of 4-byte elements to one destination whose offset modulo 16 differs from the source's
-// (the int32 row ids of an AllToAllv): after a head of at most three elements the destination is
-// 16-byte aligned, and every lane loads the 16 source bytes of its destination vector at their
-// 4-byte alignment, one instruction instead of four element loads (grouped AllToAllv of rows +
-// ids 180.9-181.4 -> 179.6-180.0 us). A form that built each vector from two aligned loads and
-// lane shuffles compiled to packed 32-bit moves, which the build rejects.
-__device__ __forceinline__ void copy_tile_misaligned4(const char* src, const TileOps& t, uint32_t n, uint32_t lane) {
-    char* dst = (char*)from_lane(t.dst, 0);
-    const uint64_t nbytes = (uint64_t)n * 4;
-    uint64_t head = (16u - ((uint64_t)dst & 15u)) & 15u;
+// Copy to destinations that share one offset modulo 16 that is not the source's (the int32 row
+// ids of an AllToAllv, an AllGather of a count that is not a multiple of 16 bytes): after a head
+// of fewer than 16 bytes every destination is 16-byte aligned, and every lane loads the 16 source
+// bytes of its destination vector at the source's element alignment, one instruction instead of
+// 16 / ES element loads (grouped AllToAllv of rows + ids 180.9-181.4 -> 179.6-180.0 us). A form
+// that built each vector from two aligned loads and lane shuffles compiled to packed 32-bit
+// moves, which the build rejects.
+template <int ES>
+__device__ __forceinline__ void copy_tile_shifted(const char* src, const TileOps& t, uint32_t n, uint32_t lane) {
+    typedef typename std::conditional<ES == 2, u32x4_a2, u32x4_a4>::type VU;
+    const uint64_t nbytes = (uint64_t)n * ES;
+    uint64_t head = (16u - (from_lane(t.dst, 0) & 15u)) & 15u;
     if (head > nbytes) head = nbytes;
-    if (head) copy_elems<4>(src, t, 0, head / 4, lane);
+    if (head) copy_elems<ES>(src, t, 0, head / ES, lane);
     const char* s1 = src + head;
-    char* d1 = dst + head;
     const uint64_t nvec = (nbytes - head) / 16;
     constexpr int U = HCCL_COPY_UNROLL;
     uint64_t v0 = 0;
     for (; v0 + (uint64_t)U * kWaveSize <= nvec; v0 += (uint64_t)U * kWaveSize) {
         u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = *gp<u32x4_a4>(s1 + 16 * (v0 + (uint64_t)u * kWaveSize + lane));
+        for (int u = 0; u < U; ++u) v[u] = *gp<VU>(s1 + 16 * (v0 + (uint64_t)u * kWaveSize + lane));
+        for (uint32_t j = 0; j < t.ndst; ++j) {
+            char* d1 = (char*)from_lane(t.dst, j) + head;
 #pragma unroll
-        for (int u = 0; u < U; ++u) vst_copy(d1 + 16 * (v0 + (uint64_t)u * kWaveSize + lane), v[u]);
+            for (int u = 0; u < U; ++u) vst_copy(d1 + 16 * (v0 + (uint64_t)u * kWaveSize + lane), v[u]);
+        }
     }
-    for (uint64_t v = v0 + lane; v < nvec; v += kWaveSize) vst_copy(d1 + 16 * v, *gp<u32x4_a4>(s1 + 16 * v));
+    for (uint64_t v = v0 + lane; v < nvec; v += kWaveSize) {
+        const u32x4 x = *gp<VU>(s1 + 16 * v);
+        for (uint32_t j = 0; j < t.ndst; ++j) vst_copy((char*)from_lane(t.dst, j) + head + 16 * v, x);
+    }
     const uint64_t done = head + nvec * 16;
-    if (done < nbytes) copy_elems<4>(src, t, done / 4, (nbytes - done) / 4, lane);
+    if (done < nbytes) copy_elems<ES>(src, t, done / ES, (nbytes - done) / ES, lane);
 }
 
 template <int ES>
@@ -656,13 +664,14 @@ __device__ __forceinline__ void copy_tile(const TileOps& t, uint32_t n, uint32_t
     const bool congruent =
         __ballot(lane < t.ndst && (uint32_t)(t.dst & 15u) != mis) == 0ull;
     if (!congruent) {
-        if constexpr (ES == 4) {
-            if (t.ndst == 1) {
-                copy_tile_misaligned4(src, t, n, lane);
-                return;
-            }
-        }
-        copy_elems<ES>(src, t, 0, n, lane);
+        // Destinations that agree among themselves modulo 16 still store whole vectors, except
+        // 4-byte elements to several destinations: there element loads kept pace (all-gather of
+        // 8 x (4 MiB + 4 B) int32 60 us element-wise, 73 us shifted; of 8 x (512 KiB + 2 B) bf16
+        // 22.7 -> 13.5 us shifted).
+        const uint32_t dmis = (uint32_t)(from_lane(t.dst, 0) & 15u);
+        const bool agree = __ballot(lane < t.ndst && (uint32_t)(t.dst & 15u) != dmis) == 0ull;
+        if (agree && (ES == 2 || t.ndst == 1)) copy_tile_shifted<ES>(src, t, n, lane);
+        else copy_elems<ES>(src, t, 0, n, lane);
         return;
     }
     const uint64_t nbytes = (uint64_t)n * ES;
