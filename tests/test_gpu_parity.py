@@ -362,6 +362,41 @@ def test_group_of_dependent_programs_with_scratch(fuse):
 
 
 @pytest.mark.parametrize("es_dt", ["bf16", "int32"])
+@pytest.mark.parametrize("algo", ["direct", "ring"])
+def test_allgather_every_source_and_receive_alignment(es_dt, algo):
+    """All-gathers of 4 ranks whose send blocks start at every offset modulo 16 and whose blocks
+    land at every offset modulo 16: every rank's receive buffer at the same offset (the
+    destinations of a direct copy agree among themselves but not with the source) or at offsets
+    that differ by rank; counts around the 16-byte and wavefront boundaries."""
+    es = 2 if es_dt == "bf16" else 4
+    per = 16 // es
+    P = 4
+    rng = np.random.default_rng(40 + es)
+    print(f"allgather alignments dt={es_dt} algo={algo}", flush=True)
+    with H.Comm(P, device=0, algo=algo, tile_bytes=2048) as c:
+        for n in [1, per - 1, per + 1, 64 * per + 3, 131 * per + 5]:
+            for so in range(per):
+                for ro in range(per):
+                    for mixed in (False, True):
+                        roff = [(ro + (r if mixed else 0)) % per for r in range(P)]
+                        src = [rng.integers(0, 1 << 15, size=so + n).astype(np.uint16 if es == 2 else np.int32)
+                               for _ in range(P)]
+                        send = [to_device(x, es_dt)[so:] for x in src]
+                        outs = [Guarded(roff[r] + P * n + per, es_dt) for r in range(P)]
+                        H.hccl_allgather(c.handle, send, [o.view[roff[r]:roff[r] + P * n] for r, o in enumerate(outs)],
+                                         n, es_dt)
+                        torch.cuda.synchronize()
+                        gathered = oracle.allgather(np.stack([x[so:] for x in src]))
+                        for r in range(P):
+                            want = outs[r].host_init[GUARD:GUARD + outs[r].n].copy()
+                            want[roff[r]:roff[r] + P * n] = gathered[r]
+                            got = outs[r].result()
+                            assert np.array_equal(got.view(np.uint8), want.view(np.uint8)), (n, so, ro, mixed, r)
+                            assert outs[r].guards_intact(), (n, so, ro, mixed, r)
+        assert c.async_error() == 0
+
+
+@pytest.mark.parametrize("es_dt", ["bf16", "int32"])
 def test_copy_every_source_and_destination_alignment(es_dt):
     """Every (source, destination) byte offset modulo 16 and lengths around the 16-byte and
     wavefront boundaries, as one-rank AllToAllv copies (the offsets set the alignments)."""
