@@ -313,6 +313,37 @@ def bench_forwarded_partials(device, iters=10):
     return out
 
 
+def _stream_lib():
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_00358_amd", "lib", "libbench_stream.so"))
+    lib.bench_stream.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
+                                 ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p]
+    lib.bench_stream_multi.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
+                                       ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p]
+    lib.bench_stream_reduce.argtypes = lib.bench_stream_multi.argtypes
+    return lib
+
+
+def _plain_reduce_ms(device, stream, region, streams=8, iters=3):
+    """A plain bf16 sum of `streams` regions of `region` bytes into one (bench_stream.hip), on
+    `stream`: the reduce-scatter's access pattern without the library, best of two grids (256
+    workgroups, one wavefront per 4 KiB chunk)."""
+    import torch
+
+    lib = _stream_lib()
+    a = torch.zeros(streams * region, dtype=torch.uint8, device=device)
+    b = torch.empty(region, dtype=torch.uint8, device=device)
+    best = float("inf")
+    for bl in (256, region // 4096 // 4):
+        def run():
+            rc = lib.bench_stream_reduce(a.data_ptr(), b.data_ptr(), region, streams, 4096, bl, stream.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"bench_stream_reduce failed ({rc})")
+        run()
+        best = min(best, _time_events(run, iters, stream))
+    del a, b
+    return best
+
+
 def bench_copy_ceiling(device, iters=20, nbytes=1 << 30):
     """What plain HIP kernels reach on this device (bench_stream.hip): a contiguous copy, a
     read-only and a write-only sweep of 1 GiB, read-only sweeps of 8 and 64 regions at the same
@@ -322,12 +353,7 @@ def bench_copy_ceiling(device, iters=20, nbytes=1 << 30):
     and the library's own copy path on the same copy."""
     import torch
 
-    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_00358_amd", "lib", "libbench_stream.so"))
-    lib.bench_stream.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
-                                 ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p]
-    lib.bench_stream_multi.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
-                                       ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p]
-    lib.bench_stream_reduce.argtypes = lib.bench_stream_multi.argtypes
+    lib = _stream_lib()
     a = torch.empty(nbytes, dtype=torch.uint8, device=device).fill_(7)
     b = torch.empty_like(a)
     st = torch.cuda.current_stream().cuda_stream
@@ -648,8 +674,13 @@ def _overlap_c5a(device, rs_send, rs_recv, n_rs, rs_stream, rest_stream):
     M = rs_recv[0].numel()
     algo = (P + 1) * P * M * 2
     comm = H.Comm(P, device=0, algo="ring", chunk_bytes=MiB)
-    rs_ms = _time_events(lambda: comm.reduce_scatter(rs_send, rs_recv, stream=rs_stream), 3, rs_stream)
+    comm.reduce_scatter(rs_send, rs_recv, stream=rs_stream)  # compile and upload outside the timing
+    rs_stream.synchronize()
+    rs_ms = _time_events(lambda: comm.reduce_scatter(rs_send, rs_recv, stream=rs_stream), 5, rs_stream)
     workers = comm.last_program()["workers"]
+    # on a few CUs the bound is what those CUs move, not HBM: the plain 8-region sum on the
+    # same masked stream is this case's ceiling
+    plain_ms = _plain_reduce_ms(device, rs_stream, P * M * 2, streams=P)
     # overlap: n_rs back-to-back reduce-scatters on the masked stream, GEMMs alongside
     n_gemm = max(5, int(0.9 * n_rs * rs_ms / t_all))
     results = {}
@@ -679,6 +710,8 @@ def _overlap_c5a(device, rs_send, rs_recv, n_rs, rs_stream, rest_stream):
             "gemm_alone_all_cus_ms": t_all, "gemm_alone_all_cus_tflops": flop / (t_all * 1e-3) / 1e12,
             "gemm_alone_240_cus_ms": t_240, "rs_alone_16cu_ms": rs_ms,
             "rs_alone_16cu_gbs": algo / (rs_ms * 1e-3) / 1e9, "rs_workers": workers,
+            "plain_reduce_16cu_ms": plain_ms, "plain_reduce_16cu_gbs": algo / (plain_ms * 1e-3) / 1e9,
+            "rs_alone_16cu_frac_of_plain_reduce": plain_ms / rs_ms,
             "n_rs": n_rs, "n_gemm": n_gemm, "overlap": results}
 
 
