@@ -83,6 +83,16 @@ __device__ __forceinline__ u32x4 vld(const char* p) {
     if constexpr (HCCL_NT_LOAD) return __builtin_nontemporal_load(gp<u32x4>(p));
     else return *gp<u32x4>(p);
 }
+// 16 bytes at an address aligned only to 4 or 2 bytes: one global_load_dwordx4 (global accesses
+// of the HSA target may be unaligned)
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+typedef uint32_t u32x4_a2 __attribute__((ext_vector_type(4), aligned(2)));
+template <int ES>
+__device__ __forceinline__ u32x4 vld_shifted(const char* p) {
+    typedef typename std::conditional<ES == 2, u32x4_a2, u32x4_a4>::type VU;
+    if constexpr (HCCL_NT_LOAD) return __builtin_nontemporal_load(gp<VU>(p));
+    else return *gp<VU>(p);
+}
 // store of reduction results (NT: a step with many destinations)
 template <bool NT = false>
 __device__ __forceinline__ void vst(char* p, u32x4 v) {
@@ -182,11 +192,13 @@ __device__ __forceinline__ int32_t comb(int32_t a, int32_t x) {
 // ------------------------------------------------------- 8-element vectors per lane
 template <int DT> struct Raw8 { u32x4 v[DtInfo<DT>::size / 2]; };
 
-template <int DT>
+// SHIFT: p is aligned only to the element size
+template <int DT, bool SHIFT = false>
 __device__ __forceinline__ Raw8<DT> load8(const char* p) {
     Raw8<DT> r;
 #pragma unroll
-    for (int q = 0; q < DtInfo<DT>::size / 2; ++q) r.v[q] = vld(p + 16 * q);
+    for (int q = 0; q < DtInfo<DT>::size / 2; ++q)
+        r.v[q] = SHIFT ? vld_shifted<DtInfo<DT>::size>(p + 16 * q) : vld(p + 16 * q);
     return r;
 }
 
@@ -305,7 +317,8 @@ __device__ __forceinline__ void reduce_elems(const TileOps& t, uint32_t first, u
 }
 
 // U vectors of 8 elements per lane: elements [base, base + U*512) of the tile, all in range.
-template <int T0, int TR, int TO, int OPR, int U, bool REQ = false>
+// The destinations are 16-byte aligned at element base; SHIFT: the sources need not be.
+template <int T0, int TR, int TO, int OPR, int U, bool REQ = false, bool SHIFT = false>
 __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, uint32_t lane) {
     typedef typename DtInfo<TO>::acc A;
     // a first source of another type (a chained step's FP32 partial) needs its own registers
@@ -327,7 +340,7 @@ __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, ui
 #pragma unroll
                     for (int u = 0; u < U; ++u) {
                         uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
-                        raw0[u] = load8<T0>(b + (uint64_t)e * DtInfo<T0>::size);
+                        raw0[u] = load8<T0, SHIFT>(b + (uint64_t)e * DtInfo<T0>::size);
                     }
                 }
             }
@@ -338,7 +351,7 @@ __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, ui
 #pragma unroll
                     for (int u = 0; u < U; ++u) {
                         uint32_t e = base + ((uint32_t)u * kWaveSize + lane) * kVecElems;
-                        raw[j][u] = load8<TR>(b + (uint64_t)e * DtInfo<TR>::size);
+                        raw[j][u] = load8<TR, SHIFT>(b + (uint64_t)e * DtInfo<TR>::size);
                     }
                 }
             }
@@ -393,26 +406,45 @@ __device__ __forceinline__ void reduce_block(const TileOps& t, uint32_t base, ui
     }
 }
 
-template <int T0, int TR, int TO, int OPR, bool REQ = false>
-__device__ __forceinline__ void reduce_tile(const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
-    if (!aligned) {
-        reduce_elems<T0, TR, TO, OPR, REQ>(t, 0, n, lane);
-        return;
-    }
+// Elements [base, n) of the tile in vector steps (destinations 16-byte aligned at base), then
+// single elements.
+template <int T0, int TR, int TO, int OPR, bool REQ, bool SHIFT>
+__device__ __forceinline__ void reduce_vectors(const TileOps& t, uint32_t base, uint32_t n, uint32_t lane) {
     constexpr int U = (DtInfo<TR>::size == 2) ? HCCL_REDUCE_UNROLL16 : 1;
     constexpr uint32_t kBlock = (uint32_t)U * kWaveSize * kVecElems;
-    uint32_t base = 0;
-    for (; base + kBlock <= n; base += kBlock) reduce_block<T0, TR, TO, OPR, U, REQ>(t, base, lane);
+    for (; base + kBlock <= n; base += kBlock) reduce_block<T0, TR, TO, OPR, U, REQ, SHIFT>(t, base, lane);
     // remaining whole 512-element steps, then single elements
     for (; base + kWaveSize * kVecElems <= n; base += kWaveSize * kVecElems)
-        reduce_block<T0, TR, TO, OPR, 1, REQ>(t, base, lane);
+        reduce_block<T0, TR, TO, OPR, 1, REQ, SHIFT>(t, base, lane);
     if (base < n) {
         // lanes whose 8 elements are all in range take one more vector step
         const uint32_t whole = (n - base) / kVecElems;
-        if (lane < whole) reduce_block<T0, TR, TO, OPR, 1, REQ>(t, base, lane);
+        if (lane < whole) reduce_block<T0, TR, TO, OPR, 1, REQ, SHIFT>(t, base, lane);
         base += whole * kVecElems;
     }
     if (base < n) reduce_elems<T0, TR, TO, OPR, REQ>(t, base, n - base, lane);
+}
+
+// A tile whose operands are not all 16-byte aligned keeps the vector steps when its
+// destinations agree modulo 16 (a reduce-scatter of a count that is not a multiple of 16 bytes:
+// every source of a block at one offset, the output at another): after a head of single
+// elements the destinations are aligned, and the sources are read with 16-byte loads at their
+// element alignment, folded in the same order. Otherwise element by element.
+template <int T0, int TR, int TO, int OPR, bool REQ = false>
+__device__ __forceinline__ void reduce_tile(const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
+    if (aligned) {
+        reduce_vectors<T0, TR, TO, OPR, REQ, false>(t, 0, n, lane);
+        return;
+    }
+    const uint32_t dmis = (uint32_t)(from_lane(t.dst, 0) & 15u);
+    if (__ballot(lane < t.ndst && (uint32_t)(t.dst & 15u) != dmis) != 0ull) {
+        reduce_elems<T0, TR, TO, OPR, REQ>(t, 0, n, lane);
+        return;
+    }
+    uint32_t head = ((16u - dmis) & 15u) / DtInfo<TO>::size;
+    if (head > n) head = n;
+    if (head) reduce_elems<T0, TR, TO, OPR, REQ>(t, 0, head, lane);
+    reduce_vectors<T0, TR, TO, OPR, REQ, true>(t, head, n, lane);
 }
 
 // ------------------------------------------------------------- binary-tree (pairwise) fold
@@ -614,11 +646,6 @@ __device__ __forceinline__ void copy_elems(const char* src, const TileOps& t, ui
         }
     }
 }
-
-// 16 bytes at an address aligned only to 4 or 2 bytes: one global_load_dwordx4 (global accesses
-// of the HSA target may be unaligned)
-typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
-typedef uint32_t u32x4_a2 __attribute__((ext_vector_type(4), aligned(2)));
 
 // Copy to destinations that share one offset modulo 16 that is not the source's (the int32 row
 // ids of an AllToAllv, an AllGather of a count that is not a multiple of 16 bytes): after a head

@@ -361,6 +361,49 @@ def test_group_of_dependent_programs_with_scratch(fuse):
         assert np.array_equal(oc[r].result().view(np.uint8), wc[r].view(np.uint8)) and oc[r].guards_intact()
 
 
+@pytest.mark.parametrize("dt", ["bf16", "fp32"])
+@pytest.mark.parametrize("algo", ["direct", "ring"])
+@pytest.mark.parametrize("coll", ["reduce_scatter", "allreduce"])
+def test_reduction_every_source_and_receive_alignment(dt, algo, coll):
+    """Reductions of 4 ranks whose send and receive buffers start at every offset modulo 16, at
+    one offset for every rank or at offsets that differ by rank (a reduce-scatter block's sources
+    then agree with each other but not with the output, or disagree too); counts around the
+    16-byte and wavefront boundaries. Bit-exact against the oracle's ascending fold."""
+    es = DT_ES[dt]
+    per = 16 // es
+    P = 4
+    print(f"reduction alignments {coll} dt={dt} algo={algo}", flush=True)
+    with H.Comm(P, device=0, algo=algo, tile_bytes=2048) as c:
+        for k, n in enumerate([1, per - 1, per + 1, 64 * per + 3, 131 * per + 5]):
+            n_in = P * n if coll == "reduce_scatter" else n
+            x = inputs(P, n_in, dt, seed=100 + k)
+            want = oracle.reduce_scatter(x, dt) if coll == "reduce_scatter" else oracle.allreduce(x, dt)
+            for so in range(per):
+                for ro in range(per):
+                    for mixed in (False, True):
+                        soff = [(so + (r if mixed else 0)) % per for r in range(P)]
+                        roff = [(ro + (2 * r if mixed else 0)) % per for r in range(P)]
+                        send = [to_device(np.concatenate([np.zeros(soff[r], x.dtype), x[r]]), dt)[soff[r]:]
+                                for r in range(P)]
+                        outs = [Guarded(roff[r] + n + per, dt) for r in range(P)]
+                        views = [o.view[roff[r]:roff[r] + n] for r, o in enumerate(outs)]
+                        if coll == "reduce_scatter":
+                            H.hccl_reduce_scatter(c.handle, send, views, n, dt)
+                        else:
+                            H.hccl_allreduce(c.handle, send, views, n, dt)
+                        torch.cuda.synchronize()
+                        for r in range(P):
+                            got = outs[r].result()
+                            where = (n, so, ro, mixed, r)
+                            assert same_bits(got[roff[r]:roff[r] + n], want[r], dt), \
+                                f"{where}: {first_mismatch(got[roff[r]:roff[r] + n], want[r])}"
+                            init = outs[r].host_init[GUARD:GUARD + outs[r].n]
+                            assert np.array_equal(got[:roff[r]].view(np.uint8), init[:roff[r]].view(np.uint8)), where
+                            assert np.array_equal(got[roff[r] + n:].view(np.uint8), init[roff[r] + n:].view(np.uint8)), where
+                            assert outs[r].guards_intact(), where
+        assert c.async_error() == 0
+
+
 @pytest.mark.parametrize("es_dt", ["bf16", "int32"])
 @pytest.mark.parametrize("algo", ["direct", "ring"])
 def test_allgather_every_source_and_receive_alignment(es_dt, algo):
