@@ -404,6 +404,56 @@ def test_reduction_every_source_and_receive_alignment(dt, algo, coll):
         assert c.async_error() == 0
 
 
+@pytest.mark.parametrize("case", [
+    ("reduce_scatter", "fp16", "max", dict(algo="direct"), "ascending", 0),
+    ("reduce_scatter", "int32", "sum", dict(algo="ring"), "ascending", 0),
+    ("reduce_scatter", "bf16", "min", dict(algo="ring"), "ascending", 0),
+    ("reduce_scatter", "bf16", "sum", dict(algo="ring", fuse=0, requantize=1), "ascending", 0),
+    ("allreduce", "bf16", "sum", dict(algo="two_level", group_size=2), "two_level", 2),
+    ("allreduce", "fp16", "sum", dict(algo="two_level", group_size=2, fuse=0, requantize=1), "two_level", 2),
+    ("allreduce", "fp32", "sum", dict(algo="two_level", group_size=2, fuse=0), "two_level", 2),
+], ids=lambda c: f"{c[0]}-{c[1]}-{c[2]}-{'-'.join(f'{k}{v}' for k, v in c[3].items())}")
+def test_reduction_variants_at_shifted_offsets(case):
+    """Grouped, re-quantised, unfused, MAX / MIN, fp16 and int32 reductions of 4 ranks with send
+    and receive buffers at offsets modulo 16 that differ by rank and from each other, counts
+    around the 16-byte and wavefront boundaries; against the oracle in the schedule's order."""
+    coll, dt, op, cfg, order, group = case
+    es = DT_ES[dt]
+    per = 16 // es
+    P = 4
+    requant = bool(cfg.get("requantize", 0))
+    print(f"shifted reductions {case}", flush=True)
+    with H.Comm(P, device=0, tile_bytes=2048, chunk_bytes=4096, **cfg) as c:
+        for k, n in enumerate([1, per + 1, 64 * per + 3, 131 * per + 5, 1500]):
+            n_in = P * n if coll == "reduce_scatter" else n
+            x = inputs(P, n_in, dt, seed=200 + k)
+            if coll == "reduce_scatter":
+                want = oracle.reduce_scatter_ordered(x, dt, order=order, op=op, group=group, requant=requant)
+            else:
+                want = oracle.allreduce_ordered(x, dt, order=order, op=op, group=group, requant=requant)
+            for so, ro in [(0, 1), (1, 0), (per - 1, 2), (3 % per, per - 1)]:
+                soff = [(so + r) % per for r in range(P)]
+                roff = [(ro + 3 * r) % per for r in range(P)]
+                send = [to_device(np.concatenate([np.zeros(soff[r], x.dtype), x[r]]), dt)[soff[r]:] for r in range(P)]
+                outs = [Guarded(roff[r] + n + per, dt) for r in range(P)]
+                views = [o.view[roff[r]:roff[r] + n] for r, o in enumerate(outs)]
+                if coll == "reduce_scatter":
+                    H.hccl_reduce_scatter(c.handle, send, views, n, dt, op)
+                else:
+                    H.hccl_allreduce(c.handle, send, views, n, dt, op)
+                torch.cuda.synchronize()
+                for r in range(P):
+                    got = outs[r].result()
+                    where = (n, so, ro, r)
+                    assert same_bits(got[roff[r]:roff[r] + n], want[r], dt), \
+                        f"{where}: {first_mismatch(got[roff[r]:roff[r] + n], want[r])}"
+                    init = outs[r].host_init[GUARD:GUARD + outs[r].n]
+                    assert np.array_equal(got[:roff[r]].view(np.uint8), init[:roff[r]].view(np.uint8)), where
+                    assert np.array_equal(got[roff[r] + n:].view(np.uint8), init[roff[r] + n:].view(np.uint8)), where
+                    assert outs[r].guards_intact(), where
+        assert c.async_error() == 0
+
+
 @pytest.mark.parametrize("es_dt", ["bf16", "int32"])
 @pytest.mark.parametrize("algo", ["direct", "ring"])
 def test_allgather_every_source_and_receive_alignment(es_dt, algo):
