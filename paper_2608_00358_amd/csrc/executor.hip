@@ -487,7 +487,7 @@ __device__ __forceinline__ void reduce_elems_tree(const TileOps& t, uint32_t fir
     }
 }
 
-template <int T, int OPR, bool REQ>
+template <int T, int OPR, bool REQ, bool SHIFT = false>
 __device__ __forceinline__ void reduce_block_tree(const TileOps& t, uint32_t base, uint32_t lane) {
     typedef typename DtInfo<T>::acc A;
     A stk[kTreeLevels][8], root[8];
@@ -498,7 +498,7 @@ __device__ __forceinline__ void reduce_block_tree(const TileOps& t, uint32_t bas
         for (int j = 0; j < kTreeBatch; ++j) {
             if (s + j < t.nsrc) {
                 const char* b = (const char*)from_lane(t.src, s + j);
-                raw[j] = load8<T>(b + (uint64_t)e * DtInfo<T>::size);
+                raw[j] = load8<T, SHIFT>(b + (uint64_t)e * DtInfo<T>::size);
             }
         }
 #pragma unroll
@@ -539,19 +539,35 @@ __device__ __forceinline__ void reduce_block_tree(const TileOps& t, uint32_t bas
     }
 }
 
-template <int T, int OPR, bool REQ>
-__device__ __forceinline__ void reduce_tile_tree(const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
-    uint32_t base = 0;
-    if (aligned) {
-        for (; base + kWaveSize * kVecElems <= n; base += kWaveSize * kVecElems)
-            reduce_block_tree<T, OPR, REQ>(t, base, lane);
-        if (base < n) {
-            const uint32_t whole = (n - base) / kVecElems;
-            if (lane < whole) reduce_block_tree<T, OPR, REQ>(t, base, lane);
-            base += whole * kVecElems;
-        }
+template <int T, int OPR, bool REQ, bool SHIFT>
+__device__ __forceinline__ void tree_vectors(const TileOps& t, uint32_t base, uint32_t n, uint32_t lane) {
+    for (; base + kWaveSize * kVecElems <= n; base += kWaveSize * kVecElems)
+        reduce_block_tree<T, OPR, REQ, SHIFT>(t, base, lane);
+    if (base < n) {
+        const uint32_t whole = (n - base) / kVecElems;
+        if (lane < whole) reduce_block_tree<T, OPR, REQ, SHIFT>(t, base, lane);
+        base += whole * kVecElems;
     }
     if (base < n) reduce_elems_tree<T, OPR, REQ>(t, base, n - base, lane);
+}
+
+// Operands not all 16-byte aligned: as reduce_tile, shifted source loads after a head of single
+// elements when the destinations agree modulo 16, else element by element.
+template <int T, int OPR, bool REQ>
+__device__ __forceinline__ void reduce_tile_tree(const TileOps& t, uint32_t n, bool aligned, uint32_t lane) {
+    if (aligned) {
+        tree_vectors<T, OPR, REQ, false>(t, 0, n, lane);
+        return;
+    }
+    const uint32_t dmis = (uint32_t)(from_lane(t.dst, 0) & 15u);
+    if (__ballot(lane < t.ndst && (uint32_t)(t.dst & 15u) != dmis) != 0ull) {
+        reduce_elems_tree<T, OPR, REQ>(t, 0, n, lane);
+        return;
+    }
+    uint32_t head = ((16u - dmis) & 15u) / DtInfo<T>::size;
+    if (head > n) head = n;
+    if (head) reduce_elems_tree<T, OPR, REQ>(t, 0, head, lane);
+    tree_vectors<T, OPR, REQ, true>(t, head, n, lane);
 }
 
 template <int T0, int TR, int TO>

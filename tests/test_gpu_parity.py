@@ -412,6 +412,9 @@ def test_reduction_every_source_and_receive_alignment(dt, algo, coll):
     ("allreduce", "bf16", "sum", dict(algo="two_level", group_size=2), "two_level", 2),
     ("allreduce", "fp16", "sum", dict(algo="two_level", group_size=2, fuse=0, requantize=1), "two_level", 2),
     ("allreduce", "fp32", "sum", dict(algo="two_level", group_size=2, fuse=0), "two_level", 2),
+    ("reduce_scatter", "bf16", "sum", dict(algo="rhd", order="halving"), "halving", 0),
+    ("allreduce", "fp32", "max", dict(algo="direct", order="halving"), "halving", 0),
+    ("allreduce", "fp16", "sum", dict(algo="rhd", order="halving", fuse=0, requantize=1), "halving", 0),
 ], ids=lambda c: f"{c[0]}-{c[1]}-{c[2]}-{'-'.join(f'{k}{v}' for k, v in c[3].items())}")
 def test_reduction_variants_at_shifted_offsets(case):
     """Grouped, re-quantised, unfused, MAX / MIN, fp16 and int32 reductions of 4 ranks with send
