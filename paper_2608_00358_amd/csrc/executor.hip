@@ -84,14 +84,17 @@ __device__ __forceinline__ u32x4 vld(const char* p) {
     else return *gp<u32x4>(p);
 }
 // 16 bytes at an address aligned only to 4 or 2 bytes: one global_load_dwordx4 (global accesses
-// of the HSA target may be unaligned)
+// of the HSA target may be unaligned). An ordinary load, not a non-temporal one: for these the
+// non-temporal hint cost more than it saved (reduce-scatter of 8 ranks with a count that is not
+// a multiple of 16 bytes: bf16 (2 Mi + 1) 63 -> 48 us, fp32 (1 Mi + 1) 68 -> 46 us while the
+// inputs stay in the 256 MiB last-level cache; at 2 GiB of input bf16 462 -> 467 us, fp32
+// 510 -> 467 us; AllToAllv of rows of 4 095 bf16 57 -> 46 us).
 typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
 typedef uint32_t u32x4_a2 __attribute__((ext_vector_type(4), aligned(2)));
 template <int ES>
 __device__ __forceinline__ u32x4 vld_shifted(const char* p) {
     typedef typename std::conditional<ES == 2, u32x4_a2, u32x4_a4>::type VU;
-    if constexpr (HCCL_NT_LOAD) return __builtin_nontemporal_load(gp<VU>(p));
-    else return *gp<VU>(p);
+    return *gp<VU>(p);
 }
 // store of reduction results (NT: a step with many destinations)
 template <bool NT = false>
@@ -672,7 +675,6 @@ __device__ __forceinline__ void copy_elems(const char* src, const TileOps& t, ui
 // moves, which the build rejects.
 template <int ES>
 __device__ __forceinline__ void copy_tile_shifted(const char* src, const TileOps& t, uint32_t n, uint32_t lane) {
-    typedef typename std::conditional<ES == 2, u32x4_a2, u32x4_a4>::type VU;
     const uint64_t nbytes = (uint64_t)n * ES;
     uint64_t head = (16u - (from_lane(t.dst, 0) & 15u)) & 15u;
     if (head > nbytes) head = nbytes;
@@ -684,7 +686,7 @@ __device__ __forceinline__ void copy_tile_shifted(const char* src, const TileOps
     for (; v0 + (uint64_t)U * kWaveSize <= nvec; v0 += (uint64_t)U * kWaveSize) {
         u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = *gp<VU>(s1 + 16 * (v0 + (uint64_t)u * kWaveSize + lane));
+        for (int u = 0; u < U; ++u) v[u] = vld_shifted<ES>(s1 + 16 * (v0 + (uint64_t)u * kWaveSize + lane));
         for (uint32_t j = 0; j < t.ndst; ++j) {
             char* d1 = (char*)from_lane(t.dst, j) + head;
 #pragma unroll
@@ -692,7 +694,7 @@ __device__ __forceinline__ void copy_tile_shifted(const char* src, const TileOps
         }
     }
     for (uint64_t v = v0 + lane; v < nvec; v += kWaveSize) {
-        const u32x4 x = *gp<VU>(s1 + 16 * v);
+        const u32x4 x = vld_shifted<ES>(s1 + 16 * v);
         for (uint32_t j = 0; j < t.ndst; ++j) vst_copy((char*)from_lane(t.dst, j) + head + 16 * v, x);
     }
     const uint64_t done = head + nvec * 16;
